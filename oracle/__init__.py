@@ -1,0 +1,25 @@
+"""CPU oracle for the rolling denoise step -- TEST INFRASTRUCTURE ONLY.
+
+A plain, slow, obviously correct numpy definition of what the GPU library
+computes, written from the paper (Sec. 3.1 Eq. 1/3, Sec. 3.2 Eq. 4, App. A.1)
+plus the readings listed in each module's header.  It shares no code with the
+HIP path: only the tests, ``__graft_entry__.smoke()`` and the bench's
+CPU-baseline leg may import it.  Product code never does.
+
+Modules:
+  philox   -- Philox4x32-10 + Box-Muller ring noise (pinned by published
+              known-answer vectors).
+  expert   -- the action expert v_theta (conditioning, adaptive RMSNorm,
+              grouped-query attention over [prefix ; buffer], FOP adapters,
+              gated-GeLU MLP, output head) and the FOP stand-in encoder.
+  rolling  -- the rolling buffer: Euler update, release, noise append,
+              context publication and temporal offset.
+
+Parity status: model output beyond the pins in tests/test_oracle_*.py is
+"parity unpinned" -- no trained weights or worked numeric example exist, so
+the oracle is the definition (see the pins for what is fixed independently).
+"""
+
+from .expert import Expert, fop_encode  # noqa: F401
+from .philox import philox4x32_10, ring_noise  # noqa: F401
+from .rolling import OracleRavel  # noqa: F401
