@@ -1,0 +1,210 @@
+/*
+ * ravel.h -- C ABI of the MI355X rolling-denoise-step library (libravel.so).
+ *
+ * One call of ravel_step performs one control step of rolling flow denoising
+ * for B independent environments:
+ *   - one pass of the flow-matching action expert over every env's H-slot
+ *     action buffer, each slot at its own flow time, conditioned on the
+ *     env's latest VLM context (layer-wise prefix K/V caches) and its age,
+ *     and on Fast-Observation-Pathway tokens (paper Sec. 3.1 Eq. 3, Sec. 3.2
+ *     Eq. 4, App. A.1);
+ *   - a per-slot Euler update, release of the now-clean first slot as the
+ *     env's action, and a fresh N(0, I) action appended in its place by
+ *     advancing a ring index (the rule stated right after Eq. 3).
+ *
+ * Time convention: logical slot i = 0..H-1 holds the action executed i+1
+ * steps from now at flow time tau_i = (i+1)/H (1 = noise, 0 = clean), and a
+ * step applies a_i <- a_i - (1/H) v_i.  This is the paper's Eq. 3 mirrored
+ * (tau_paper = 1 - tau, v_paper = -v, K = H).
+ *
+ * Threading: ravel_set_context / ravel_context_acquire (the VLM worker, paper
+ * Sec. 3.2 and Sec. 4.3's separate workers) may run on another host thread
+ * concurrently with ravel_step (the control loop).  Two ravel_step calls on
+ * one buffer must not overlap, and consecutive steps must be ordered (same
+ * stream, or the caller orders them).
+ *
+ * Errors: every entry point returns a ravel_status and never throws; the
+ * message of the calling thread's last failure is in ravel_last_error().
+ * Shape and argument errors are returned synchronously.  Asynchronous device
+ * faults surface as RAVEL_E_HIP on a later call that synchronises.
+ *
+ * Streams are hipStream_t values passed as void* (NULL = the default stream).
+ */
+#ifndef RAVEL_H
+#define RAVEL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  RAVEL_OK = 0,
+  RAVEL_E_INVALID = -1, /* bad argument (null pointer, out-of-range value)   */
+  RAVEL_E_NOMEM = -2,   /* device or host allocation failed                   */
+  RAVEL_E_HIP = -3,     /* a HIP runtime call or kernel failed                */
+  RAVEL_E_SHAPE = -4,   /* tensor shape or config inconsistent                */
+  RAVEL_E_STATE = -5    /* call not valid in the current state (no context,
+                           t_obs going backwards, missing weight, ...)        */
+} ravel_status;
+
+enum { RAVEL_F32 = 0, RAVEL_BF16 = 1 };
+
+/* Velocity model.  TRANSFORMER is the action expert.  The two analytic fields
+ * need no weights beyond one tensor and exist to pin the rolling scheduler:
+ *   ANALYTIC_OT:     v_i = (x_i - a*) / tau_i      weight "analytic.target" [D_a]
+ *   ANALYTIC_LINEAR: v_i = lambda * x_i            weight "analytic.lambda" [1]   */
+enum { RAVEL_TRANSFORMER = 0, RAVEL_ANALYTIC_OT = 1, RAVEL_ANALYTIC_LINEAR = 2 };
+
+typedef struct {
+  int32_t layers;      /* L transformer blocks                                  */
+  int32_t width;       /* w residual width (even, multiple of 8)                */
+  int32_t n_q_heads;   /* query heads                                           */
+  int32_t n_kv_heads;  /* KV heads (divides n_q_heads), grouped-query attention */
+  int32_t head_dim;    /* hd (multiple of 32, <= 256)                           */
+  int32_t mlp_dim;     /* F gated-GeLU hidden size (multiple of 16)             */
+  int32_t horizon;     /* H buffer slots (the paper's K), 1..128                 */
+  int32_t action_dim;  /* D_a per slot (the paper's h low-level actions folded)  */
+  int32_t prefix_len;  /* P prefix tokens of the VLM context per layer (>= 0)    */
+  int32_t n_fop;       /* FOP tokens per env (0 disables adapters)              */
+  int32_t fop_obs_dim; /* observation size of the FOP stand-in encoder          */
+  int32_t fop_stride;  /* adapter in layers l with l % stride == stride - 1     */
+  int32_t dtype;       /* RAVEL_F32 or RAVEL_BF16 (bf16 weights/activations,
+                          fp32 accumulation, fp32 residual stream and ring)     */
+  int32_t model_kind;  /* RAVEL_TRANSFORMER / RAVEL_ANALYTIC_OT / _LINEAR        */
+  float delta_bias;    /* delta_0 added to the offset p/H (Sec. 4.4, App. B.1)   */
+  float rms_eps;       /* RMSNorm epsilon (1e-6)                                 */
+} ravel_config;
+
+/* A named host or device tensor, row-major, [out, in] for linear layers.
+ * dtype RAVEL_F32 or RAVEL_BF16 (raw bf16 bits).  Names and shapes:
+ *   in.w [w,D_a]  in.b [w]  time.w1 [w,w] time.b1 [w] time.w2 [w,w] time.b2 [w]
+ *   delta.w1 [w,1] delta.b1 [w] delta.w2 [w,w] delta.b2 [w]
+ *   layers.<l>.mod.w [6w,w] .mod.b [6w] .qkv.w [(nq+2nkv)hd,w] .o.w [w,nq hd]
+ *   layers.<l>.gate.w [F,w] .up.w [F,w] .down.w [w,F]
+ *   adapter layers: layers.<l>.fop.gamma [w] .fop.q.w [nq hd,w]
+ *                   .fop.kv.w [2 nkv hd,w] .fop.o.w [w,nq hd] .fop.alpha [1]
+ *   final.mod.w [3w,w] final.mod.b [3w] (third chunk unused)  out.w [D_a,w] out.b [D_a]
+ *   FOP encoder (optional): fop.w1 [w,d_obs] fop.b1 [w] fop.w2 [n_fop w,w] fop.b2 [n_fop w]
+ * The modulation rows of layers.<l>.mod are the chunks (s1,b1,g1,s2,b2,g2) of
+ * w rows each: attention-norm scale/shift/gate, MLP-norm scale/shift/gate.  */
+typedef struct {
+  const char* name;
+  int32_t dtype;
+  int32_t rank;
+  int64_t dims[4];
+  const void* data;
+} ravel_tensor;
+
+typedef struct ravel_model ravel_model;
+typedef struct ravel_buffer ravel_buffer;
+
+/* Build a model on the current HIP device.  Copies every tensor (the caller
+ * keeps ownership), converts to the model dtype (bf16 round-to-nearest-even)
+ * and lays weights out for the kernels; precomputes each slot's flow-time
+ * conditioning c_tau(i), fixed because tau_i is fixed (Sec. 3.1 after Eq. 1).
+ * Synchronous.  Errors: E_SHAPE (config or tensor shape), E_STATE (missing
+ * weight), E_NOMEM, E_HIP. */
+ravel_status ravel_create(const ravel_config* cfg, const ravel_tensor* weights, int32_t n_weights,
+                          ravel_model** out);
+void ravel_destroy(ravel_model* model);
+
+/* Bytes of device memory held by the model's weights (for roofline accounting). */
+int64_t ravel_model_weight_bytes(const ravel_model* model);
+
+/* Create the rolling state of `batch` environments.  Every slot starts as
+ * pure N(0, I) noise: initial action r = 0..H-1 of env e sits in physical
+ * slot r mod H and is Philox noise for (seed, e, r) (App. A.1: no additional
+ * initialisation).  Noise is Philox4x32-10 (Salmon et al., SC'11) keyed by
+ * (seed lo, seed hi) with counter (j/4, env, r lo, r hi) and Box-Muller in
+ * float64 rounded to float32.  Synchronous. */
+ravel_status ravel_buffer_create(ravel_model* model, int32_t batch, uint64_t seed, ravel_buffer** out);
+void ravel_buffer_destroy(ravel_buffer* buf);
+
+/* Options (ravel_buffer_set_option):
+ *   RAVEL_OPT_SYNC_CONTEXT  1: a published context is applied at the very next
+ *                           step, which waits on the GPU (not the host) for its
+ *                           data; 0 (default): applied at the first step whose
+ *                           host-side event query finds the data ready.
+ *   RAVEL_OPT_USE_GRAPH     1 (default): replay a captured hipGraph per step.
+ *   RAVEL_OPT_DEBUG         1: synchronise and check for NaN/Inf after each kernel. */
+enum { RAVEL_OPT_SYNC_CONTEXT = 1, RAVEL_OPT_USE_GRAPH = 2, RAVEL_OPT_DEBUG = 3 };
+ravel_status ravel_buffer_set_option(ravel_buffer* buf, int32_t option, int64_t value);
+
+/* Context plane (paper Sec. 3.2: the latest available context is reused
+ * across steps until a newer one is ready; refreshing never blocks a step).
+ *
+ * Each env owns two device context slots; steps read the active one.
+ * ravel_context_acquire returns device pointers to the env's inactive slot,
+ * K and V each [L, P, n_kv, hd] in the model dtype, after making `producer`
+ * wait (on the GPU) until no enqueued step still reads that slot.  The
+ * producer writes the new context there (e.g. its own kernels), then calls
+ * ravel_set_context with k = v = NULL.  Acquiring cancels a publish of this
+ * env that has not yet been applied.
+ *
+ * ravel_set_context publishes a context for env (0..B-1) computed from the
+ * observation of control step t_obs.  With non-NULL k and v (host or device,
+ * [L, P, n_kv, hd] model dtype) it first copies them into the inactive slot
+ * on `producer` (acquire + copy); the sources must stay valid until that copy
+ * has run.  The swap happens at a later ravel_step: the slot index flips in
+ * device memory and the step's offset becomes p = t - t_obs.  t_obs must not
+ * decrease per env (E_STATE).  Never blocks on the GPU. */
+ravel_status ravel_context_acquire(ravel_buffer* buf, int32_t env, void** k_slot, void** v_slot,
+                                   void* producer_stream);
+ravel_status ravel_set_context(ravel_buffer* buf, int32_t env, const void* k, const void* v,
+                               int64_t t_obs, void* producer_stream);
+
+/* One rolling denoise step for all envs, enqueued on `stream` (asynchronous).
+ *   fop_tokens: device [B, n_fop, w] in the model dtype (NULL only when the
+ *               model has no adapters);
+ *   action_out: device float [B, D_a], the action released by this step.
+ * The step number t lives in device memory (starts at 0, +1 per step).
+ * Errors: E_STATE if some env has no context yet (transformer model). */
+ravel_status ravel_step(ravel_buffer* buf, const void* fop_tokens, float* action_out, void* stream);
+
+/* FOP stand-in encoder z = reshape(W_f2 gelu_tanh(W_f1 obs + b_f1) + b_f2)
+ * (paper Eq. 4 with a 2-layer MLP in place of the image encoder).
+ *   obs: device float [B, d_obs]; fop_tokens: device [B, n_fop, w] model dtype. */
+ravel_status ravel_fop_encode(ravel_buffer* buf, const float* obs, void* fop_tokens, void* stream);
+
+/* Wait until every enqueued step and context copy of this buffer finished. */
+ravel_status ravel_buffer_sync(ravel_buffer* buf);
+
+/* Synchronises, then copies the state out (any pointer may be NULL):
+ *   X_host float [B, H, D_a] ring in PHYSICAL slot order (slot (t+i) mod H is
+ *   logical slot i); t = step counter; t_obs_host int64 [B]. */
+ravel_status ravel_debug_state(ravel_buffer* buf, float* X_host, int64_t* t, int64_t* t_obs_host);
+
+/* Publish log: entries (env, t_apply, t_obs) as int64 triples, oldest first.
+ * On input *n is the capacity in entries; on output the number written. */
+ravel_status ravel_publish_log(ravel_buffer* buf, int64_t* entries, int32_t* n);
+
+/* Bit-exact checkpoint of the rolling state (ring, t, seed, per-env t_obs and
+ * active context).  Call with host_blob = NULL to get the size in *n.
+ * Synchronises.  Load requires a buffer of the same model and batch. */
+ravel_status ravel_buffer_save(ravel_buffer* buf, void* host_blob, size_t* n);
+ravel_status ravel_buffer_load(ravel_buffer* buf, const void* host_blob, size_t n);
+
+/* Per-kernel timing of one eagerly launched step (HIP events around every
+ * launch on `stream`; synchronises).  Each record: kernel class name,
+ * algorithmic bytes and flops of that launch, and its duration.  On input
+ * *n is the capacity; on output the number of records. */
+typedef struct {
+  char name[48];
+  double bytes;
+  double flops;
+  float ms;
+} ravel_kernel_record;
+ravel_status ravel_profile_step(ravel_buffer* buf, const void* fop_tokens, float* action_out,
+                                void* stream, ravel_kernel_record* records, int32_t* n);
+
+/* Message of the calling thread's last non-OK status ("" if none). */
+const char* ravel_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RAVEL_H */

@@ -42,8 +42,12 @@ ANALYTIC_LINEAR = 2
 
 
 class OracleRavel:
-    def __init__(self, shape, weights: dict, batch: int, seed: int, dtype=np.float64):
+    def __init__(self, shape, weights: dict, batch: int, seed: int, dtype=np.float64, env_ids=None):
+        """env_ids: environment index of each row for its noise stream (default
+        0..batch-1); lets a few sampled environments of a large batch be rolled."""
         self.s = shape
+        self.env_ids = list(range(batch)) if env_ids is None else [int(e) for e in env_ids]
+        assert len(self.env_ids) == batch
         self.B = batch
         self.seed = int(seed)
         self.dt = dtype
@@ -59,7 +63,7 @@ class OracleRavel:
         self.X = np.zeros((batch, H, D), dtype=dtype)
         for e in range(batch):
             for r in range(H):
-                self.X[e, r % H] = ring_noise(self.seed, e, r, D)
+                self.X[e, r % H] = ring_noise(self.seed, self.env_ids[e], r, D)
         self.t = 0
         self.ctx = [None] * batch  # (K, V) per env
         self.t_obs = np.zeros(batch, dtype=np.int64)
@@ -118,7 +122,7 @@ class OracleRavel:
             vel = np.asarray(self.velocity(e, a, fop_tokens, hooks), dtype=self.dt)
             self.X[e, phys] = a - dtau * vel
             out[e] = self.X[e, t % H]
-            self.X[e, t % H] = ring_noise(self.seed, e, t + H, self.s.action_dim)
+            self.X[e, t % H] = ring_noise(self.seed, self.env_ids[e], t + H, self.s.action_dim)
         self.t += 1
         return out
 

@@ -1,0 +1,321 @@
+// Attention of the buffer tokens over [prefix tokens ; buffer tokens] (and of
+// the FOP adapters over FOP tokens), bidirectional, grouped-query heads.
+//
+// bf16 path (MFMA, wave64): one block per (key split, query head, env); each
+// of the 4 waves owns 16-query blocks.  Key/value tiles of 32 keys are staged
+// in LDS (V stored transposed) and shared by the waves.  Scores are computed
+// transposed, S^T = K Q^T, so that each lane owns one query: the online
+// softmax statistics stay in registers and P^T feeds the second MFMA
+// O^T += V^T P^T directly, without an LDS round trip.  With several key
+// splits, each block writes (m, l, unnormalised O) and the last block of the
+// (env, head) merges the splits in fixed order.
+//
+// fp32 path: one wavefront per (query, head, env), lanes over head dims.
+#include "kernels.h"
+
+namespace ravel {
+
+static constexpr float kLog2e = 1.4426950408889634f;
+
+template <typename T>
+RAVEL_DEV const T* key_base(const AttnArgs& a, const T* pbase, const T* sbase, int e, int kidx, int g,
+                            int hd) {
+  if (kidx < a.P) return pbase + (long long)kidx * a.p_ld + g * hd;
+  return sbase + (long long)(e * a.S + (kidx - a.P)) * a.s_ld + g * hd;
+}
+
+template <int HD, int MAXQB>
+__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
+  constexpr int TK = 32;
+  constexpr int KS = HD / 32;  // k-steps of the score MFMA
+  constexpr int DT = HD / 16;  // 16-row tiles of O^T
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[TK][HD + 8];
+  __shared__ __attribute__((aligned(16))) bf16_t Vt[HD][TK + 8];
+  __shared__ int s_last;
+
+  const int split = blockIdx.x, j = blockIdx.y, e = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, grp = lane >> 4;
+  const int g = (j * a.nkv) / a.nq;
+  const int QB = (a.Hq + 15) / 16;
+  const int nkeys = a.P + a.S;
+  const int kbeg = split * a.keys_per_split;
+  const int kend = min(nkeys, kbeg + a.keys_per_split);
+
+  const bf16_t* q = (const bf16_t*)a.q;
+  const int slot = a.slot ? a.slot[e] : 0;
+  const bf16_t* pk = (const bf16_t*)a.pk + slot * a.p_slot_stride + e * a.p_env_stride;
+  const bf16_t* pv = (const bf16_t*)a.pv + slot * a.p_slot_stride + e * a.p_env_stride;
+  const bf16_t* sk = (const bf16_t*)a.sk;
+  const bf16_t* sv = (const bf16_t*)a.sv;
+
+  bf16x8_t qf[MAXQB][KS];
+  f32x4_t o[MAXQB][DT];
+  float mrow[MAXQB], lrow[MAXQB];
+#pragma unroll
+  for (int qi = 0; qi < MAXQB; ++qi) {
+    const int qb = wave + 4 * qi;
+    const int query = qb * 16 + l16;
+    mrow[qi] = -INFINITY;
+    lrow[qi] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[qi][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (qb < QB && query < a.Hq)
+        qf[qi][ks] = *(const bf16x8_t*)(q + (size_t)(e * a.Hq + query) * a.ldq + j * HD + ks * 32 + grp * 8);
+      else
+        qf[qi][ks] = bf16x8_t{};
+    }
+  }
+  const float sl2 = a.scale * kLog2e;
+
+  for (int k0 = kbeg; k0 < kend; k0 += TK) {
+    __syncthreads();
+    // K tile: TK rows x HD, 16-byte chunks
+    for (int c = tid; c < TK * (HD / 8); c += 256) {
+      const int row = c / (HD / 8), dc = (c % (HD / 8)) * 8;
+      const int kidx = k0 + row;
+      u32x4_t val = {0, 0, 0, 0};
+      if (kidx < kend) val = *(const u32x4_t*)(key_base(a, pk, sk, e, kidx, g, HD) + dc);
+      *(u32x4_t*)&Ks[row][dc] = val;
+    }
+    // V tile transposed: Vt[d][key]; item = (quad of keys, 8 dims)
+    for (int c = tid; c < (TK / 4) * (HD / 8); c += 256) {
+      const int kq = c / (HD / 8), dc = (c % (HD / 8)) * 8;
+      u32x4_t r4[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int kidx = k0 + kq * 4 + i;
+        r4[i] = u32x4_t{0, 0, 0, 0};
+        if (kidx < kend) r4[i] = *(const u32x4_t*)(key_base(a, pv, sv, e, kidx, g, HD) + dc);
+      }
+      const bf16_t* h0 = (const bf16_t*)&r4[0];
+      const bf16_t* h1 = (const bf16_t*)&r4[1];
+      const bf16_t* h2 = (const bf16_t*)&r4[2];
+      const bf16_t* h3 = (const bf16_t*)&r4[3];
+#pragma unroll
+      for (int dd = 0; dd < 8; ++dd) {
+        u32x2_t w;
+        w[0] = (uint32_t)h0[dd] | ((uint32_t)h1[dd] << 16);
+        w[1] = (uint32_t)h2[dd] | ((uint32_t)h3[dd] << 16);
+        *(u32x2_t*)&Vt[dc + dd][kq * 4] = w;
+      }
+    }
+    __syncthreads();
+
+#pragma unroll
+    for (int qi = 0; qi < MAXQB; ++qi) {
+      const int qb = wave + 4 * qi;
+      if (qb >= QB) continue;  // wave-uniform
+      // S^T[key][query] for two 16-key sub-tiles
+      f32x4_t s[2];
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+        s[st] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8_t kf = *(const bf16x8_t*)&Ks[st * 16 + l16][ks * 32 + grp * 8];
+          s[st] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qi][ks], s[st], 0, 0, 0);
+        }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int kidx = k0 + st * 16 + grp * 4 + r;
+          float x = s[st][r] * sl2;
+          if (kidx >= kend) x = -INFINITY;
+          s[st][r] = x;
+          mx = fmaxf(mx, x);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mnew = fmaxf(mrow[qi], mx);
+      const float corr = (mnew == -INFINITY) ? 1.f : exp2f(mrow[qi] - mnew);
+      float psum = 0.f;
+      float p[2][4];
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          p[st][r] = (s[st][r] == -INFINITY) ? 0.f : exp2f(s[st][r] - mnew);
+          psum += p[st][r];
+        }
+      psum += __shfl_xor(psum, 16, 64);
+      psum += __shfl_xor(psum, 32, 64);
+      lrow[qi] = lrow[qi] * corr + psum;
+      mrow[qi] = mnew;
+      // P^T as the B operand: slot jj of group grp is key (jj<4 ? 4grp+jj : 16+4grp+jj-4)
+      bf16x8_t pf;
+      {
+        bf16_t pb[8];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          pb[r] = f32_to_bf16(p[0][r]);
+          pb[4 + r] = f32_to_bf16(p[1][r]);
+        }
+        pf = *(const bf16x8_t*)pb;
+      }
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        o[qi][dt][0] *= corr;
+        o[qi][dt][1] *= corr;
+        o[qi][dt][2] *= corr;
+        o[qi][dt][3] *= corr;
+        const bf16_t* vrow = &Vt[dt * 16 + l16][0];
+        u32x4_t vv;
+        const u32x2_t lo = *(const u32x2_t*)(vrow + grp * 4);
+        const u32x2_t hi = *(const u32x2_t*)(vrow + 16 + grp * 4);
+        vv[0] = lo[0];
+        vv[1] = lo[1];
+        vv[2] = hi[0];
+        vv[3] = hi[1];
+        o[qi][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8_t*)&vv, pf, o[qi][dt], 0, 0, 0);
+      }
+    }
+  }
+
+  // o[qi][dt][r] = O^T[d = dt*16 + 4grp + r][query = qb*16 + l16]
+  bf16_t* out = (bf16_t*)a.out;
+  if (a.nsplit == 1) {
+#pragma unroll
+    for (int qi = 0; qi < MAXQB; ++qi) {
+      const int qb = wave + 4 * qi;
+      const int query = qb * 16 + l16;
+      if (qb >= QB || query >= a.Hq) continue;
+      const float inv = 1.f / lrow[qi];
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        u32x2_t w;
+        w[0] = (uint32_t)f32_to_bf16(o[qi][dt][0] * inv) | ((uint32_t)f32_to_bf16(o[qi][dt][1] * inv) << 16);
+        w[1] = (uint32_t)f32_to_bf16(o[qi][dt][2] * inv) | ((uint32_t)f32_to_bf16(o[qi][dt][3] * inv) << 16);
+        *(u32x2_t*)(out + (size_t)(e * a.Hq + query) * a.ldo + j * HD + dt * 16 + grp * 4) = w;
+      }
+    }
+    return;
+  }
+
+  const int Hp = QB * 16;
+  const size_t pidx = ((size_t)e * a.nq + j) * a.nsplit + split;
+#pragma unroll
+  for (int qi = 0; qi < MAXQB; ++qi) {
+    const int qb = wave + 4 * qi;
+    const int query = qb * 16 + l16;
+    if (qb >= QB) continue;
+    float* po = a.part_o + (pidx * Hp + query) * HD;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) *(f32x4_t*)(po + dt * 16 + grp * 4) = o[qi][dt];
+    if (grp == 0) {
+      a.part_ml[(pidx * Hp + query) * 2 + 0] = mrow[qi];
+      a.part_ml[(pidx * Hp + query) * 2 + 1] = lrow[qi];
+    }
+  }
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) {
+    unsigned prev = __hip_atomic_fetch_add(&a.counters[e * a.nq + j], 1u, __ATOMIC_ACQ_REL,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+    s_last = (prev == (unsigned)(a.nsplit - 1));
+  }
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  const size_t pbase = ((size_t)e * a.nq + j) * a.nsplit;
+  for (int idx = tid; idx < a.Hq * HD; idx += 256) {
+    const int query = idx / HD, d = idx % HD;
+    float mmax = -INFINITY;
+    for (int sp = 0; sp < a.nsplit; ++sp) mmax = fmaxf(mmax, a.part_ml[((pbase + sp) * Hp + query) * 2]);
+    float num = 0.f, den = 0.f;
+    for (int sp = 0; sp < a.nsplit; ++sp) {
+      const float ms = a.part_ml[((pbase + sp) * Hp + query) * 2];
+      const float w = (ms == -INFINITY) ? 0.f : exp2f(ms - mmax);
+      num += w * a.part_o[((pbase + sp) * Hp + query) * HD + d];
+      den += w * a.part_ml[((pbase + sp) * Hp + query) * 2 + 1];
+    }
+    out[(size_t)(e * a.Hq + query) * a.ldo + j * HD + d] = f32_to_bf16(num / den);
+  }
+  if (tid == 0) a.counters[e * a.nq + j] = 0u;
+}
+
+template <int HD, int MAXQB>
+static hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
+  dim3 grid(a.nsplit, a.nq, a.B);
+  hipLaunchKernelGGL((attn_bf16_kernel<HD, MAXQB>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s) {
+  const int QB = (a.Hq + 15) / 16;
+  if (QB > 8) return hipErrorInvalidValue;
+  const bool two = QB > 4;
+  switch (a.hd) {
+    case 32: return two ? launch_hd<32, 2>(a, s) : launch_hd<32, 1>(a, s);
+    case 64: return two ? launch_hd<64, 2>(a, s) : launch_hd<64, 1>(a, s);
+    case 128: return two ? launch_hd<128, 2>(a, s) : launch_hd<128, 1>(a, s);
+    case 256: return two ? launch_hd<256, 2>(a, s) : launch_hd<256, 1>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// fp32 path
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
+  const int query = blockIdx.x, j = blockIdx.y, e = blockIdx.z;
+  const int lane = threadIdx.x;
+  const int hd = a.hd;
+  const int g = (j * a.nkv) / a.nq;
+  const int slot = a.slot ? a.slot[e] : 0;
+  const float* pk = (const float*)a.pk + slot * a.p_slot_stride + e * a.p_env_stride;
+  const float* pv = (const float*)a.pv + slot * a.p_slot_stride + e * a.p_env_stride;
+  const float* sk = (const float*)a.sk;
+  const float* sv = (const float*)a.sv;
+  const float* q = (const float*)a.q + (size_t)(e * a.Hq + query) * a.ldq + j * hd;
+  float qv[4], ov[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int d = lane + 64 * c;
+    qv[c] = d < hd ? q[d] : 0.f;
+    ov[c] = 0.f;
+  }
+  float m = -INFINITY, l = 0.f;
+  const int nkeys = a.P + a.S;
+  for (int kidx = 0; kidx < nkeys; ++kidx) {
+    const float* kr = key_base(a, pk, sk, e, kidx, g, hd);
+    const float* vr = key_base(a, pv, sv, e, kidx, g, hd);
+    float part = 0.f;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int d = lane + 64 * c;
+      if (d < hd) part += qv[c] * kr[d];
+    }
+    const float sc = wave_sum(part) * a.scale;
+    const float mnew = fmaxf(m, sc);
+    const float corr = expf(m - mnew);
+    const float p = expf(sc - mnew);
+    l = l * corr + p;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int d = lane + 64 * c;
+      ov[c] = ov[c] * corr + (d < hd ? p * vr[d] : 0.f);
+    }
+    m = mnew;
+  }
+  float* out = (float*)a.out + (size_t)(e * a.Hq + query) * a.ldo + j * hd;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int d = lane + 64 * c;
+    if (d < hd) out[d] = ov[c] / l;
+  }
+}
+
+hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t s) {
+  if (a.hd > 256) return hipErrorInvalidValue;
+  dim3 grid(a.Hq, a.nq, a.B);
+  hipLaunchKernelGGL(attn_f32_kernel, grid, dim3(64), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace ravel

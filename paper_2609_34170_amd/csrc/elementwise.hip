@@ -1,0 +1,336 @@
+// Row and element-wise kernels of the rolling step: adaptive RMSNorm (one
+// wavefront per row), offset conditioning, input projection in logical slot
+// order, analytic velocity fields, the fused Euler / release / Philox-append
+// kernel, ring initialisation, the flow-time embedding and small utilities.
+#include "kernels.h"
+
+namespace ravel {
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11) and Box-Muller.
+// ---------------------------------------------------------------------------
+RAVEL_DEV void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t lo0 = 0xD2511F53u * c[0];
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c[0]);
+    const uint32_t lo1 = 0xCD9E8D57u * c[2];
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c[2]);
+    const uint32_t n0 = hi1 ^ c[1] ^ k0;
+    const uint32_t n2 = hi0 ^ c[3] ^ k1;
+    c[0] = n0;
+    c[1] = lo1;
+    c[2] = n2;
+    c[3] = lo0;
+  }
+}
+
+// Two normals from a (radius word, angle word) pair: float64, rounded to float32.
+RAVEL_DEV void box_muller(uint32_t xr, uint32_t xa, float* z0, float* z1) {
+  const double ua = ((double)(xr >> 8) + 1.0) * 5.9604644775390625e-08;  // 2^-24
+  const double ub = (double)(xa >> 8) * 5.9604644775390625e-08;
+  const double rad = sqrt(-2.0 * log(ua));
+  const double ang = 6.283185307179586 * ub;
+  *z0 = (float)(rad * cos(ang));
+  *z1 = (float)(rad * sin(ang));
+}
+
+// Noise of action r for env e, elements 4c .. 4c+3.
+RAVEL_DEV void ring_noise4(uint64_t seed, int e, int64_t r, int c, float z[4]) {
+  uint32_t ctr[4] = {(uint32_t)c, (uint32_t)e, (uint32_t)((uint64_t)r & 0xFFFFFFFFu),
+                     (uint32_t)((uint64_t)r >> 32)};
+  philox4x32_10(ctr, (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32));
+  box_muller(ctr[0], ctr[1], &z[0], &z[1]);
+  box_muller(ctr[2], ctr[3], &z[2], &z[3]);
+}
+
+// ---------------------------------------------------------------------------
+// Adaptive RMSNorm
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void adarms_kernel(const float* __restrict__ x, int ldx, int M, int w,
+                                                     const float* __restrict__ scale,
+                                                     const float* __restrict__ shift, int ldm, int mode,
+                                                     float eps, T* __restrict__ y, int ldy) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= M) return;
+  const float* xr = x + (size_t)row * ldx;
+  float ss = 0.f;
+  for (int n = lane * 4; n < w; n += 256) {
+    const f32x4_t v = *(const f32x4_t*)(xr + n);
+    ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+  }
+  ss = wave_sum(ss);
+  const float r = 1.0f / sqrtf(ss / (float)w + eps);
+  T* yr = y + (size_t)row * ldy;
+  for (int n = lane * 4; n < w; n += 256) {
+    const f32x4_t v = *(const f32x4_t*)(xr + n);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float o;
+      if (mode == 0)
+        o = v[i] * r * (1.0f + scale[(size_t)row * ldm + n + i]) + shift[(size_t)row * ldm + n + i];
+      else
+        o = v[i] * r * (1.0f + scale[n + i]);
+      yr[n + i] = act<T>::from_f(o);
+    }
+  }
+}
+
+template <typename T>
+hipError_t launch_adarms(const float* x, int ldx, int M, int w, const float* scale, const float* shift,
+                         int ldm, int mode, float eps, T* y, int ldy, hipStream_t s) {
+  if (w % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(adarms_kernel<T>, dim3((M + 3) / 4), dim3(256), 0, s, x, ldx, M, w, scale, shift,
+                     ldm, mode, eps, y, ldy);
+  return hipGetLastError();
+}
+template hipError_t launch_adarms<float>(const float*, int, int, int, const float*, const float*, int, int,
+                                         float, float*, int, hipStream_t);
+template hipError_t launch_adarms<bf16_t>(const float*, int, int, int, const float*, const float*, int,
+                                          int, float, bf16_t*, int, hipStream_t);
+
+// ---------------------------------------------------------------------------
+// Offset conditioning hidden layer
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void delta_hidden_kernel(const int64_t* t, const int64_t* t_obs, int B, int H, float delta_bias,
+                                    const float* wd1, const float* bd1, int w, T* h1) {
+  const int e = blockIdx.y;
+  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= w || e >= B) return;
+  const float p = (float)(*t - t_obs[e]);
+  const float delta = p / (float)H + delta_bias;
+  h1[(size_t)e * w + n] = act<T>::from_f(silu_f(wd1[n] * delta + bd1[n]));
+}
+
+template <typename T>
+hipError_t launch_delta_hidden(const int64_t* t, const int64_t* t_obs, int B, int H, float delta_bias,
+                               const float* wd1, const float* bd1, int w, T* h1, hipStream_t s) {
+  hipLaunchKernelGGL(delta_hidden_kernel<T>, dim3((w + 255) / 256, B), dim3(256), 0, s, t, t_obs, B, H,
+                     delta_bias, wd1, bd1, w, h1);
+  return hipGetLastError();
+}
+template hipError_t launch_delta_hidden<float>(const int64_t*, const int64_t*, int, int, float, const float*,
+                                               const float*, int, float*, hipStream_t);
+template hipError_t launch_delta_hidden<bf16_t>(const int64_t*, const int64_t*, int, int, float, const float*,
+                                                const float*, int, bf16_t*, hipStream_t);
+
+// ---------------------------------------------------------------------------
+// Input projection (logical slot order)
+// ---------------------------------------------------------------------------
+__global__ void in_proj_kernel(const float* __restrict__ X, const int64_t* t, int B, int H, int D,
+                               const float* __restrict__ w_in, const float* __restrict__ b_in, int w,
+                               float* __restrict__ x) {
+  const int row = blockIdx.y;  // e*H + i
+  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= w) return;
+  const int e = row / H, i = row % H;
+  const int ph = (int)((*t + i) % H);
+  const float* a = X + ((size_t)e * H + ph) * D;
+  const float* wr = w_in + (size_t)n * D;
+  float acc = 0.f;
+  for (int d = 0; d < D; ++d) acc += wr[d] * a[d];
+  x[(size_t)row * w + n] = acc + b_in[n];
+}
+
+hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D, const float* w_in,
+                          const float* b_in, int w, float* x, hipStream_t s) {
+  hipLaunchKernelGGL(in_proj_kernel, dim3((w + 255) / 256, B * H), dim3(256), 0, s, X, t, B, H, D, w_in,
+                     b_in, w, x);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Analytic velocity fields
+// ---------------------------------------------------------------------------
+__global__ void analytic_velocity_kernel(int kind, const float* __restrict__ X, const int64_t* t, int B,
+                                         int H, int D, const float* __restrict__ param,
+                                         float* __restrict__ v) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= B * H * D) return;
+  const int d = idx % D, i = (idx / D) % H, e = idx / (D * H);
+  const int ph = (int)((*t + i) % H);
+  const float x = X[((size_t)e * H + ph) * D + d];
+  float out;
+  if (kind == 1) {  // OT: (x - a*) / tau_i, tau_i = (i+1)/H
+    const float tau = (float)(i + 1) / (float)H;
+    out = (x - param[d]) / tau;
+  } else {  // LINEAR: lambda * x
+    out = param[0] * x;
+  }
+  v[idx] = out;
+}
+
+hipError_t launch_analytic_velocity(int kind, const float* X, const int64_t* t, int B, int H, int D,
+                                    const float* param, float* v, hipStream_t s) {
+  const int n = B * H * D;
+  hipLaunchKernelGGL(analytic_velocity_kernel, dim3((n + 255) / 256), dim3(256), 0, s, kind, X, t, B, H, D,
+                     param, v);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Euler update + release + noise append + step counter
+// ---------------------------------------------------------------------------
+// x <- x - dt * v with a separately rounded product (no fused multiply-add), the
+// exact operation order of the reference definition.
+RAVEL_DEV float euler_sub(float x, float dt, float v) {
+#pragma clang fp contract(off)
+  const float step = dt * v;
+  return x - step;
+}
+
+__global__ __launch_bounds__(64) void euler_release_kernel(float* __restrict__ X, const float* __restrict__ v,
+                                                           int64_t* t, int B, int H, int D, uint64_t seed,
+                                                           float* __restrict__ action, unsigned* ticket) {
+  __shared__ int s_last;
+  const int64_t tt = *t;
+  const int NG = (D + 3) / 4;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx < B * NG) {
+    const int e = idx / NG, c = idx % NG;
+    const float dt = 1.0f / (float)H;
+    const int h0 = (int)(tt % H);
+    float* Xe = X + (size_t)e * H * D;
+    const float* ve = v + (size_t)e * H * D;
+    for (int q = 0; q < 4; ++q) {
+      const int d = c * 4 + q;
+      if (d >= D) break;
+      for (int i = 0; i < H; ++i) {
+        int ph = h0 + i;
+        if (ph >= H) ph -= H;
+        Xe[(size_t)ph * D + d] = euler_sub(Xe[(size_t)ph * D + d], dt, ve[(size_t)i * D + d]);
+      }
+      action[(size_t)e * D + d] = Xe[(size_t)h0 * D + d];
+    }
+    float z[4];
+    ring_noise4(seed, e, tt + H, c, z);
+    for (int q = 0; q < 4; ++q) {
+      const int d = c * 4 + q;
+      if (d < D) Xe[(size_t)h0 * D + d] = z[q];
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned prev = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = (prev == gridDim.x - 1);
+  }
+  __syncthreads();
+  if (s_last && threadIdx.x == 0) {
+    *t = tt + 1;
+    *ticket = 0u;
+  }
+}
+
+hipError_t launch_euler_release(float* X, const float* v, int64_t* t, int B, int H, int D, uint64_t seed,
+                                float* action, unsigned* ticket, hipStream_t s) {
+  const int n = B * ((D + 3) / 4);
+  hipLaunchKernelGGL(euler_release_kernel, dim3((n + 63) / 64), dim3(64), 0, s, X, v, t, B, H, D, seed,
+                     action, ticket);
+  return hipGetLastError();
+}
+
+__global__ void ring_init_kernel(float* X, int B, int H, int D, uint64_t seed) {
+  const int NG = (D + 3) / 4;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= B * H * NG) return;
+  const int c = idx % NG, r = (idx / NG) % H, e = idx / (NG * H);
+  float z[4];
+  ring_noise4(seed, e, r, c, z);
+  for (int q = 0; q < 4; ++q) {
+    const int d = c * 4 + q;
+    if (d < D) X[((size_t)e * H + (r % H)) * D + d] = z[q];
+  }
+}
+
+hipError_t launch_ring_init(float* X, int B, int H, int D, uint64_t seed, hipStream_t s) {
+  const int n = B * H * ((D + 3) / 4);
+  hipLaunchKernelGGL(ring_init_kernel, dim3((n + 255) / 256), dim3(256), 0, s, X, B, H, D, seed);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Flow-time embedding (float64)
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void time_embedding_kernel(int H, int w, T* emb) {
+  const int half = w / 2;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= H * half) return;
+  const int i = idx / half, jj = idx % half;
+  const double tau = (double)(i + 1) / (double)H;
+  const double omega = pow(10000.0, -(double)jj / (double)half);
+  const double arg = 1000.0 * tau * omega;
+  emb[(size_t)i * w + jj] = act<T>::from_f((float)sin(arg));
+  emb[(size_t)i * w + half + jj] = act<T>::from_f((float)cos(arg));
+}
+
+template <typename T>
+hipError_t launch_time_embedding(int H, int w, T* emb, hipStream_t s) {
+  const int n = H * (w / 2);
+  hipLaunchKernelGGL(time_embedding_kernel<T>, dim3((n + 255) / 256), dim3(256), 0, s, H, w, emb);
+  return hipGetLastError();
+}
+template hipError_t launch_time_embedding<float>(int, int, float*, hipStream_t);
+template hipError_t launch_time_embedding<bf16_t>(int, int, bf16_t*, hipStream_t);
+
+// ---------------------------------------------------------------------------
+// Utilities
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void convert_kernel(const float* __restrict__ src, T* __restrict__ dst, long long n) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = act<T>::from_f(src[i]);
+}
+
+template <typename T>
+hipError_t launch_convert(const float* src, T* dst, long long n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(convert_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src, dst, n);
+  return hipGetLastError();
+}
+template hipError_t launch_convert<float>(const float*, float*, long long, hipStream_t);
+template hipError_t launch_convert<bf16_t>(const float*, bf16_t*, long long, hipStream_t);
+
+__global__ void publish_kernel(PublishBatch pb, int* slot, int64_t* t_obs) {
+  const int i = threadIdx.x;
+  if (i < pb.n) {
+    slot[pb.env[i]] = pb.new_slot[i];
+    t_obs[pb.env[i]] = pb.tobs[i];
+  }
+}
+
+hipError_t launch_publish(const PublishBatch& pb, int* slot, int64_t* t_obs, hipStream_t s) {
+  hipLaunchKernelGGL(publish_kernel, dim3(1), dim3(32), 0, s, pb, slot, t_obs);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ void check_finite_kernel(const T* p, long long n, int* flag) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) {
+    const float v = act<T>::to_f(p[i]);
+    if (!isfinite(v)) atomicOr(flag, 1);
+  }
+}
+
+hipError_t launch_check_finite(const float* p, long long n, int* flag, hipStream_t s) {
+  return launch_check_finite_t<float>(p, n, flag, s);
+}
+
+template <typename T>
+hipError_t launch_check_finite_t(const T* p, long long n, int* flag, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(check_finite_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, p, n, flag);
+  return hipGetLastError();
+}
+template hipError_t launch_check_finite_t<float>(const float*, long long, int*, hipStream_t);
+template hipError_t launch_check_finite_t<bf16_t>(const bf16_t*, long long, int*, hipStream_t);
+
+}  // namespace ravel

@@ -1,0 +1,130 @@
+// Kernel launch interface of libravel (internal; not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace ravel {
+
+// ---------------------------------------------------------------------------
+// GEMM  C[M,N] = A[M,K] . B[N,K]^T  (both operands K-contiguous), fp32 accumulate,
+// followed by a fused epilogue.
+// ---------------------------------------------------------------------------
+enum EpiMode {
+  EPI_F32 = 0,        // out_f[m,n]  = acc + bias[n]
+  EPI_T = 1,          // out_t[m,n]  = T(acc + bias[n])
+  EPI_RESID = 2,      // out_f[m,n] += gate[m,n] * acc            (gated residual)
+  EPI_RESID_TANH = 3, // out_f[m,n] += tanh(*gate_scalar) * acc    (adapter gate)
+  EPI_GEGLU = 4,      // out_t[m,f]  = T(gelu_tanh(acc_gate) * acc_up), columns interleaved
+                      //               in blocks of 16 gate / 16 up (N = 2F)
+  EPI_COND = 5,       // out_t[m*H+i, n] = T(silu(ctau[i,n] + acc + bias[n])) for i < H
+  EPI_GELU_T = 6,     // out_t[m,n]  = T(gelu_tanh(acc + bias[n]))
+  EPI_SILU_T = 7,     // out_t[m,n]  = T(silu(acc + bias[n]))
+};
+
+struct GemmArgs {
+  const void* A; int lda;
+  const void* B; int ldb;
+  int M, N, K;
+  int ksplit;          // number of K ranges (grid.z); 1 = no split
+  int kchunk;          // K elements per range (multiple of 64)
+  float* partial;      // [ksplit][M][N] fp32 workspace (ksplit > 1)
+  unsigned* counters;  // one per output tile, zero; the reducing block re-zeroes it
+  int mode;
+  const float* bias;
+  float* out_f; int ldo_f;
+  void* out_t; int ldo_t;
+  const float* gate; int ldg;
+  const float* gate_scalar;
+  const float* ctau; int H;
+};
+
+// Tile configurations of the bf16 MFMA GEMM.
+enum GemmTile { TILE_64x64 = 0, TILE_128x128 = 1, TILE_64x128 = 2, TILE_128x64 = 3, TILE_32x64 = 4 };
+
+hipError_t launch_gemm_bf16(const GemmArgs& a, int tile, hipStream_t s);
+hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Attention: per env e and query head j, softmax(q K^T * scale) V over the keys
+// [prefix tokens of env e ; S self tokens of env e], no mask, GQA head map
+// g = j * nkv / nq.
+// ---------------------------------------------------------------------------
+struct AttnArgs {
+  const void* q; int ldq;          // q[(e*Hq + i)*ldq + j*hd + d]
+  int Hq;                          // queries per env
+  const void* pk; const void* pv;  // prefix rows: base + slot*slot_stride + e*env_stride + p*p_ld + g*hd
+  long long p_env_stride, p_slot_stride;
+  const int* slot;                 // [B] active context slot or null
+  int P, p_ld;
+  const void* sk; const void* sv;  // self rows: base + (e*S + s)*s_ld + g*hd
+  int S, s_ld;
+  int B, nq, nkv, hd;
+  float scale;
+  void* out; int ldo;              // out[(e*Hq + i)*ldo + j*hd + d]
+  int nsplit, keys_per_split;      // split of the key range (multiple of 32)
+  float* part_o;                   // [B*nq*nsplit][Hq_pad][hd]
+  float* part_ml;                  // [B*nq*nsplit][Hq_pad][2]
+  unsigned* counters;              // [B*nq]
+};
+
+hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s);
+hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Element-wise / row kernels
+// ---------------------------------------------------------------------------
+// y[m,:] = T( x/rms(x) * (1 + scale) + shift ), per-row modulation rows of stride ldm
+// (mode 0) or a per-feature scale without shift (mode 1: scale[n], shift ignored).
+template <typename T>
+hipError_t launch_adarms(const float* x, int ldx, int M, int w, const float* scale,
+                         const float* shift, int ldm, int mode, float eps, T* y, int ldy,
+                         hipStream_t s);
+
+// Offset conditioning hidden layer: h1[e,n] = T(silu(wd1[n]*delta_e + bd1[n])),
+// delta_e = (t - t_obs[e]) / H + delta_bias.
+template <typename T>
+hipError_t launch_delta_hidden(const int64_t* t, const int64_t* t_obs, int B, int H, float delta_bias,
+                               const float* wd1, const float* bd1, int w, T* h1, hipStream_t s);
+
+// Input projection in logical slot order: x[e*H+i, n] = W_in[n,:] . X[e, (t+i) mod H, :] + b_in[n].
+hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D, const float* w_in,
+                          const float* b_in, int w, float* x, hipStream_t s);
+
+// Analytic velocity fields (logical order): OT v = (x - a*)/tau_i, LINEAR v = lambda x.
+hipError_t launch_analytic_velocity(int kind, const float* X, const int64_t* t, int B, int H, int D,
+                                    const float* param, float* v, hipStream_t s);
+
+// Euler update of every slot, release of logical slot 0 into action[e,:], Philox
+// noise for action index r = t + H into the released physical slot, t += 1.
+hipError_t launch_euler_release(float* X, const float* v, int64_t* t, int B, int H, int D,
+                                uint64_t seed, float* action, unsigned* ticket, hipStream_t s);
+
+// Fill X[e, r mod H, :] with the Philox noise of action r, for r = 0..H-1.
+hipError_t launch_ring_init(float* X, int B, int H, int D, uint64_t seed, hipStream_t s);
+
+// Sinusoidal flow-time embedding of tau_i = (i+1)/H: emb[i, j] = sin(1000 tau w_j),
+// emb[i, w/2 + j] = cos(1000 tau w_j), w_j = 10000^(-j/(w/2)); evaluated in float64.
+template <typename T>
+hipError_t launch_time_embedding(int H, int w, T* emb, hipStream_t s);
+
+template <typename T>
+hipError_t launch_convert(const float* src, T* dst, long long n, hipStream_t s);
+
+// Context publication: for i < n: slot[env[i]] = new_slot[i]; t_obs[env[i]] = tobs[i].
+struct PublishBatch {
+  int n;
+  int env[32];
+  int new_slot[32];
+  long long tobs[32];
+};
+hipError_t launch_publish(const PublishBatch& pb, int* slot, int64_t* t_obs, hipStream_t s);
+
+// NaN/Inf scan used by the debug mode: flag[0] |= any non-finite value.
+hipError_t launch_check_finite(const float* p, long long n, int* flag, hipStream_t s);
+template <typename T>
+hipError_t launch_check_finite_t(const T* p, long long n, int* flag, hipStream_t s);
+
+}  // namespace ravel

@@ -1,0 +1,1353 @@
+// libravel runtime: model creation, rolling buffers, the asynchronous context
+// plane, step orchestration and hipGraph replay behind the C ABI of ravel.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <array>
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "ravel.h"
+
+using namespace ravel;
+
+namespace {
+
+thread_local std::string g_err;
+
+ravel_status fail(ravel_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+#define HIP_TRY(expr)                                                                        \
+  do {                                                                                       \
+    hipError_t e_ = (expr);                                                                  \
+    if (e_ != hipSuccess) return fail(RAVEL_E_HIP, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+#define RV_TRY(expr)                      \
+  do {                                    \
+    ravel_status s_ = (expr);             \
+    if (s_ != RAVEL_OK) return s_;        \
+  } while (0)
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Simple bump allocator over one device allocation.
+struct Arena {
+  size_t off = 0;
+  std::vector<std::pair<void**, size_t>> pending;
+  void want(void** p, size_t bytes) {
+    pending.push_back({p, off});
+    off = align_up(off + std::max<size_t>(bytes, 1), 256);
+  }
+  ravel_status commit(void** base) {
+    if (hipMalloc(base, std::max<size_t>(off, 256)) != hipSuccess)
+      return fail(RAVEL_E_NOMEM, "hipMalloc of " + std::to_string(off) + " bytes failed");
+    for (auto& pr : pending) *pr.first = (char*)*base + pr.second;
+    pending.clear();
+    return RAVEL_OK;
+  }
+};
+
+struct KernelRecorder {
+  hipStream_t stream;
+  struct Rec {
+    std::string name;
+    double bytes, flops;
+    hipEvent_t a, b;
+  };
+  std::vector<Rec> recs;
+  void begin(const char* name, double bytes, double flops) {
+    Rec r{name, bytes, flops, nullptr, nullptr};
+    (void)hipEventCreate(&r.a);
+    (void)hipEventCreate(&r.b);
+    (void)hipEventRecord(r.a, stream);
+    recs.push_back(r);
+  }
+  void end() { (void)hipEventRecord(recs.back().b, stream); }
+};
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Model
+// ---------------------------------------------------------------------------
+struct LayerW {
+  void* mod_w = nullptr;
+  float* mod_b = nullptr;
+  void* qkv_w = nullptr;
+  void* o_w = nullptr;
+  void* gu_w = nullptr;  // [2F, w], gate/up interleaved in blocks of 16 rows
+  void* down_w = nullptr;
+  int adapter = -1;  // index into the adapter list, -1 = none
+  float* gamma = nullptr;
+  void* qa_w = nullptr;
+  void* oa_w = nullptr;
+  float* alpha = nullptr;
+};
+
+struct ravel_model {
+  ravel_config cfg;
+  bool bf16 = true;
+  size_t elt = 2;
+  int device = 0;
+  void* arena = nullptr;
+  size_t arena_bytes = 0;
+  int64_t weight_bytes = 0;
+  float *in_w = nullptr, *in_b = nullptr;
+  float* ctau = nullptr;  // [H, w]
+  float *d_w1 = nullptr, *d_b1 = nullptr, *d_b2 = nullptr;
+  void* d_w2 = nullptr;
+  std::vector<LayerW> layers;
+  int n_ad = 0;
+  void* kva_w = nullptr;  // [n_ad * 2 kvd, w]
+  void* fmod_w = nullptr;  // [2w, w]
+  float* fmod_b = nullptr;
+  void* out_w = nullptr;
+  float* out_b = nullptr;
+  bool has_fop_encoder = false;
+  void* f_w1 = nullptr;
+  float* f_b1 = nullptr;
+  void* f_w2 = nullptr;
+  float* f_b2 = nullptr;
+  float* analytic = nullptr;
+};
+
+namespace {
+
+struct TensorMap {
+  std::map<std::string, const ravel_tensor*> m;
+  const ravel_tensor* get(const std::string& n) const {
+    auto it = m.find(n);
+    return it == m.end() ? nullptr : it->second;
+  }
+};
+
+ravel_status check_shape(const ravel_tensor* t, const std::string& name, std::vector<int64_t> dims) {
+  if (!t) return fail(RAVEL_E_STATE, "missing weight '" + name + "'");
+  if (t->rank != (int)dims.size()) return fail(RAVEL_E_SHAPE, "weight '" + name + "': wrong rank");
+  for (size_t i = 0; i < dims.size(); ++i)
+    if (t->dims[i] != dims[i])
+      return fail(RAVEL_E_SHAPE, "weight '" + name + "': dim " + std::to_string(i) + " is " +
+                                     std::to_string(t->dims[i]) + ", expected " + std::to_string(dims[i]));
+  if (!t->data) return fail(RAVEL_E_INVALID, "weight '" + name + "': null data");
+  if (t->dtype != RAVEL_F32 && t->dtype != RAVEL_BF16)
+    return fail(RAVEL_E_INVALID, "weight '" + name + "': unknown dtype");
+  return RAVEL_OK;
+}
+
+int64_t numel(const ravel_tensor* t) {
+  int64_t n = 1;
+  for (int i = 0; i < t->rank; ++i) n *= t->dims[i];
+  return n;
+}
+
+// Device staging for uploads: an fp32 region and a bf16 region of S elements each.
+struct Staging {
+  float* f = nullptr;
+  bf16_t* h = nullptr;
+  size_t S = 0;
+};
+
+// Upload rows [row0, row0+nrows) of a [*, cols] tensor, converting to the model
+// dtype, placing source row r at destination row dst_row(r) (runs of consecutive
+// destination rows are copied at once).
+template <typename MapFn>
+ravel_status upload_rows(const ravel_tensor* t, int64_t row0, int64_t nrows, int64_t cols, bool to_bf16,
+                         void* dst, MapFn dst_row, const Staging& stg) {
+  const size_t src_elt = t->dtype == RAVEL_BF16 ? 2 : 4;
+  const size_t dst_elt = to_bf16 ? 2 : 4;
+  if (t->dtype == RAVEL_BF16 && !to_bf16)
+    return fail(RAVEL_E_INVALID, std::string(t->name) + ": bf16 source for an fp32 model");
+  const int64_t chunk_rows = std::max<int64_t>(1, (int64_t)(stg.S / std::max<int64_t>(cols, 1)));
+  for (int64_t r = 0; r < nrows; r += chunk_rows) {
+    const int64_t nr = std::min(chunk_rows, nrows - r);
+    const char* src = (const char*)t->data + (size_t)(row0 + r) * cols * src_elt;
+    const void* tmp = stg.f;
+    if (t->dtype == RAVEL_F32 && to_bf16) {
+      HIP_TRY(hipMemcpy(stg.f, src, (size_t)nr * cols * 4, hipMemcpyDefault));
+      HIP_TRY(launch_convert<bf16_t>(stg.f, stg.h, nr * cols, 0));
+      tmp = stg.h;
+    } else {
+      HIP_TRY(hipMemcpy(stg.f, src, (size_t)nr * cols * src_elt, hipMemcpyDefault));
+    }
+    int64_t i = 0;
+    while (i < nr) {
+      int64_t j = i + 1;
+      while (j < nr && dst_row(r + j) == dst_row(r + i) + (j - i)) ++j;
+      HIP_TRY(hipMemcpy((char*)dst + (size_t)dst_row(r + i) * cols * dst_elt,
+                        (const char*)tmp + (size_t)i * cols * dst_elt, (size_t)(j - i) * cols * dst_elt,
+                        hipMemcpyDeviceToDevice));
+      i = j;
+    }
+  }
+  return RAVEL_OK;
+}
+
+ravel_status upload_all(const ravel_tensor* t, bool to_bf16, void* dst, const Staging& stg) {
+  const int64_t n = numel(t);
+  if (t->dtype == RAVEL_BF16 && !to_bf16)
+    return fail(RAVEL_E_INVALID, std::string(t->name) + ": bf16 source for an fp32 model");
+  if (!(t->dtype == RAVEL_F32 && to_bf16)) {
+    HIP_TRY(hipMemcpy(dst, t->data, (size_t)n * (t->dtype == RAVEL_BF16 ? 2 : 4), hipMemcpyDefault));
+    return RAVEL_OK;
+  }
+  if ((size_t)n <= stg.S) {
+    HIP_TRY(hipMemcpy(stg.f, t->data, (size_t)n * 4, hipMemcpyDefault));
+    HIP_TRY(launch_convert<bf16_t>(stg.f, (bf16_t*)dst, n, 0));
+    return RAVEL_OK;
+  }
+  const int64_t cols = t->rank >= 2 ? t->dims[t->rank - 1] : n;
+  return upload_rows(t, 0, n / cols, cols, to_bf16, dst, [](int64_t r) { return r; }, stg);
+}
+
+// GEMM dispatch ---------------------------------------------------------------
+struct GemmPlan {
+  int tile;
+  int ksplit;
+  int kchunk;
+  int tiles;
+};
+
+GemmPlan plan_gemm(int M, int N, int K, bool geglu) {
+  GemmPlan p;
+  int bm, bn;
+  if (M <= 32 && !geglu) {
+    p.tile = TILE_32x64; bm = 32; bn = 64;
+  } else if (M <= 64) {
+    p.tile = TILE_64x64; bm = 64; bn = 64;
+  } else if (M <= 256) {
+    p.tile = TILE_64x128; bm = 64; bn = 128;
+  } else {
+    p.tile = TILE_128x128; bm = 128; bn = 128;
+  }
+  p.tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+  // split K until the grid has about 2 blocks per CU, keeping >= 128 K per range
+  int ks = 1;
+  const int target = 512;
+  while (p.tiles * ks * 2 <= target && (K / (ks * 2)) >= 128 && ks < 64) ks *= 2;
+  int kchunk = (K + ks - 1) / ks;
+  kchunk = (kchunk + 63) / 64 * 64;
+  ks = (K + kchunk - 1) / kchunk;
+  p.ksplit = ks;
+  p.kchunk = kchunk;
+  return p;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Buffer
+// ---------------------------------------------------------------------------
+struct PendingCtx {
+  bool valid = false;
+  int64_t t_obs = 0;
+  hipEvent_t ready = nullptr;
+};
+
+struct GraphEntry {
+  const void* fop;
+  float* action;
+  hipGraph_t graph;
+  hipGraphExec_t exec;
+};
+
+struct ravel_buffer {
+  ravel_model* m = nullptr;
+  int B = 0;
+  uint64_t seed = 0;
+  void* arena = nullptr;
+  // device state
+  float* X = nullptr;
+  int64_t* t = nullptr;
+  int64_t* t_obs = nullptr;
+  int* slot = nullptr;
+  unsigned* ticket = nullptr;
+  void* ctx_k = nullptr;
+  void* ctx_v = nullptr;
+  size_t ctx_elems = 0;  // per env per slot: L * P * nkv * hd
+  // activations
+  float* x = nullptr;
+  void* cond = nullptr;
+  void* h1 = nullptr;
+  float* mod = nullptr;
+  void* y = nullptr;
+  void* qkv = nullptr;
+  void* att = nullptr;
+  void* qa = nullptr;
+  void* kva = nullptr;
+  void* u = nullptr;
+  float* v = nullptr;
+  float* fmod = nullptr;
+  void* fhid = nullptr;
+  void* obs_t = nullptr;
+  float* gpart = nullptr;
+  unsigned* gcnt = nullptr;
+  float* apart_o = nullptr;
+  float* apart_ml = nullptr;
+  unsigned* acnt = nullptr;
+  int* dbg_flag = nullptr;
+  int attn_nsplit = 1, attn_kps = 0;
+  // host
+  int64_t t_host = 0;
+  std::vector<int> active;
+  std::vector<int> has_ctx;
+  std::vector<int64_t> tobs_host;
+  std::vector<PendingCtx> pending;
+  std::vector<hipEvent_t> retire;
+  std::vector<int> retire_valid;
+  std::vector<std::array<int64_t, 3>> log;
+  std::mutex mu;
+  bool sync_ctx = false, use_graph = true, debug = false;
+  hipStream_t cap_stream = nullptr;
+  std::vector<GraphEntry> graphs;
+};
+
+namespace {
+
+template <typename T>
+ravel_status run_gemm(ravel_buffer* b, hipStream_t s, KernelRecorder* rec, const char* name, const void* A,
+                      int lda, const void* W, int ldb, int M, int N, int K, GemmArgs epi) {
+  ravel_model* m = b->m;
+  epi.A = A;
+  epi.lda = lda;
+  epi.B = W;
+  epi.ldb = ldb;
+  epi.M = M;
+  epi.N = N;
+  epi.K = K;
+  const double elt = (double)m->elt;
+  double obytes = (double)M * N * (epi.mode == EPI_F32 ? 4 : elt);
+  if (epi.mode == EPI_RESID) obytes = (double)M * N * 12;  // read x, gate; write x
+  if (epi.mode == EPI_RESID_TANH) obytes = (double)M * N * 8;
+  if (epi.mode == EPI_GEGLU) obytes = (double)M * (N / 2) * elt;
+  if (epi.mode == EPI_COND) obytes = (double)M * m->cfg.horizon * N * elt;
+  const double bytes = ((double)M * K + (double)N * K) * elt + obytes;
+  const double flops = 2.0 * M * N * K;
+  if (!m->bf16) {
+    epi.ksplit = 1;
+    epi.kchunk = K;
+    if (rec) rec->begin(name, bytes, flops);
+    HIP_TRY(launch_gemm_f32(epi, s));
+    if (rec) rec->end();
+    return RAVEL_OK;
+  }
+  if ((K % 8) || (lda % 8) || (ldb % 8)) return fail(RAVEL_E_SHAPE, std::string(name) + ": K and strides must be multiples of 8");
+  const GemmPlan p = plan_gemm(M, N, K, epi.mode == EPI_GEGLU);
+  epi.ksplit = p.ksplit;
+  epi.kchunk = p.kchunk;
+  epi.partial = b->gpart;
+  epi.counters = b->gcnt;
+  if (rec) {
+    static const char* tn[] = {"64x64", "128x128", "64x128", "128x64", "32x64"};
+    char full[48];
+    snprintf(full, sizeof full, "gemm%s:%s", tn[p.tile], name);
+    rec->begin(full, bytes, flops);
+  }
+  HIP_TRY(launch_gemm_bf16(epi, p.tile, s));
+  if (rec) rec->end();
+  return RAVEL_OK;
+}
+
+GemmArgs epi_args(int mode) {
+  GemmArgs a;
+  memset(&a, 0, sizeof a);
+  a.mode = mode;
+  a.ksplit = 1;
+  return a;
+}
+
+template <typename T>
+ravel_status run_attn(ravel_buffer* b, hipStream_t s, KernelRecorder* rec, const char* name, AttnArgs a) {
+  ravel_model* m = b->m;
+  const ravel_config& c = m->cfg;
+  a.B = b->B;
+  a.nq = c.n_q_heads;
+  a.nkv = c.n_kv_heads;
+  a.hd = c.head_dim;
+  a.scale = 1.0f / sqrtf((float)c.head_dim);
+  const int nkeys = a.P + a.S;
+  if (m->bf16 && a.S > 0 && b->attn_nsplit > 1) {
+    a.nsplit = b->attn_nsplit;
+    a.keys_per_split = b->attn_kps;
+  } else {
+    a.nsplit = 1;
+    a.keys_per_split = ((nkeys + 31) / 32) * 32;
+  }
+  a.part_o = b->apart_o;
+  a.part_ml = b->apart_ml;
+  a.counters = b->acnt;
+  const double elt = (double)m->elt;
+  const double bytes = (double)b->B * (a.Hq * (double)c.n_q_heads * c.head_dim * 2 * elt +
+                                       (double)nkeys * c.n_kv_heads * c.head_dim * 2 * elt);
+  const double flops = 4.0 * b->B * c.n_q_heads * (double)a.Hq * nkeys * c.head_dim;
+  if (rec) rec->begin(name, bytes, flops);
+  if (m->bf16)
+    HIP_TRY(launch_attn_bf16(a, s));
+  else
+    HIP_TRY(launch_attn_f32(a, s));
+  if (rec) rec->end();
+  return RAVEL_OK;
+}
+
+#define REC_BEGIN(nm, by, fl) \
+  if (rec) rec->begin(nm, by, fl)
+#define REC_END() \
+  if (rec) rec->end()
+
+template <typename T>
+ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s, KernelRecorder* rec) {
+  ravel_model* m = b->m;
+  const ravel_config& c = m->cfg;
+  const int B = b->B, H = c.horizon, w = c.width, D = c.action_dim;
+  const int BH = B * H;
+  const int qd = c.n_q_heads * c.head_dim, kvd = c.n_kv_heads * c.head_dim;
+  const int qkvd = qd + 2 * kvd;
+  const int F = c.mlp_dim;
+  const double elt = (double)m->elt;
+
+  // 1. offset conditioning: delta_e = p/H + delta_0, d = W_d2 silu(W_d1 delta + b_d1) + b_d2,
+  //    cond[e,i] = silu(c_tau(i) + d)
+  REC_BEGIN("delta_hidden", (double)B * w * (8 + elt), (double)B * w * 4);
+  HIP_TRY(launch_delta_hidden<T>(b->t, b->t_obs, B, H, c.delta_bias, m->d_w1, m->d_b1, w, (T*)b->h1, s));
+  REC_END();
+  {
+    GemmArgs e = epi_args(EPI_COND);
+    e.bias = m->d_b2;
+    e.out_t = b->cond;
+    e.ldo_t = w;
+    e.ctau = m->ctau;
+    e.H = H;
+    RV_TRY(run_gemm<T>(b, s, rec, "cond", b->h1, w, m->d_w2, w, B, w, w, e));
+  }
+  // 2. input projection of the buffer in logical order
+  REC_BEGIN("in_proj", (double)BH * (D + w) * 4, 2.0 * BH * w * D);
+  HIP_TRY(launch_in_proj(b->X, b->t, B, H, D, m->in_w, m->in_b, w, b->x, s));
+  REC_END();
+  // FOP adapter keys/values of every adapter layer at once
+  if (m->n_ad > 0) {
+    GemmArgs e = epi_args(EPI_T);
+    e.out_t = b->kva;
+    e.ldo_t = m->n_ad * 2 * kvd;
+    RV_TRY(run_gemm<T>(b, s, rec, "fop_kv", fop, w, m->kva_w, w, B * c.n_fop, m->n_ad * 2 * kvd, w, e));
+  }
+  const size_t ctx_layer = (size_t)c.prefix_len * kvd;
+  for (int l = 0; l < c.layers; ++l) {
+    const LayerW& L = m->layers[l];
+    // modulation chunks (s1, b1, g1, s2, b2, g2)
+    {
+      GemmArgs e = epi_args(EPI_F32);
+      e.bias = L.mod_b;
+      e.out_f = b->mod;
+      e.ldo_f = 6 * w;
+      RV_TRY(run_gemm<T>(b, s, rec, "mod", b->cond, w, L.mod_w, w, BH, 6 * w, w, e));
+    }
+    REC_BEGIN("adarms", (double)BH * w * (12 + elt), (double)BH * w * 5);
+    HIP_TRY(launch_adarms<T>(b->x, w, BH, w, b->mod, b->mod + w, 6 * w, 0, c.rms_eps, (T*)b->y, w, s));
+    REC_END();
+    {
+      GemmArgs e = epi_args(EPI_T);
+      e.out_t = b->qkv;
+      e.ldo_t = qkvd;
+      RV_TRY(run_gemm<T>(b, s, rec, "qkv", b->y, w, L.qkv_w, w, BH, qkvd, w, e));
+    }
+    {
+      AttnArgs a;
+      memset(&a, 0, sizeof a);
+      a.q = b->qkv;
+      a.ldq = qkvd;
+      a.Hq = H;
+      a.pk = (const char*)b->ctx_k + l * ctx_layer * m->elt;
+      a.pv = (const char*)b->ctx_v + l * ctx_layer * m->elt;
+      a.p_env_stride = (long long)b->ctx_elems;
+      a.p_slot_stride = (long long)b->ctx_elems * B;
+      a.slot = b->slot;
+      a.P = c.prefix_len;
+      a.p_ld = kvd;
+      a.sk = (const char*)b->qkv + (size_t)qd * m->elt;
+      a.sv = (const char*)b->qkv + (size_t)(qd + kvd) * m->elt;
+      a.S = H;
+      a.s_ld = qkvd;
+      a.out = b->att;
+      a.ldo = qd;
+      RV_TRY(run_attn<T>(b, s, rec, "attn", a));
+    }
+    {
+      GemmArgs e = epi_args(EPI_RESID);
+      e.out_f = b->x;
+      e.ldo_f = w;
+      e.gate = b->mod + 2 * w;
+      e.ldg = 6 * w;
+      RV_TRY(run_gemm<T>(b, s, rec, "o", b->att, qd, L.o_w, qd, BH, w, qd, e));
+    }
+    if (L.adapter >= 0 && fop) {
+      REC_BEGIN("adarms", (double)BH * w * (8 + elt), (double)BH * w * 4);
+      HIP_TRY(launch_adarms<T>(b->x, w, BH, w, L.gamma, nullptr, 0, 1, c.rms_eps, (T*)b->y, w, s));
+      REC_END();
+      {
+        GemmArgs e = epi_args(EPI_T);
+        e.out_t = b->qa;
+        e.ldo_t = qd;
+        RV_TRY(run_gemm<T>(b, s, rec, "fop_q", b->y, w, L.qa_w, w, BH, qd, w, e));
+      }
+      {
+        AttnArgs a;
+        memset(&a, 0, sizeof a);
+        const int ld = m->n_ad * 2 * kvd;
+        a.q = b->qa;
+        a.ldq = qd;
+        a.Hq = H;
+        a.pk = (const char*)b->kva + (size_t)L.adapter * 2 * kvd * m->elt;
+        a.pv = (const char*)b->kva + (size_t)(L.adapter * 2 * kvd + kvd) * m->elt;
+        a.p_env_stride = (long long)c.n_fop * ld;
+        a.p_slot_stride = 0;
+        a.slot = nullptr;
+        a.P = c.n_fop;
+        a.p_ld = ld;
+        a.sk = nullptr;
+        a.sv = nullptr;
+        a.S = 0;
+        a.s_ld = 0;
+        a.out = b->att;
+        a.ldo = qd;
+        RV_TRY(run_attn<T>(b, s, rec, "fop_attn", a));
+      }
+      {
+        GemmArgs e = epi_args(EPI_RESID_TANH);
+        e.out_f = b->x;
+        e.ldo_f = w;
+        e.gate_scalar = L.alpha;
+        RV_TRY(run_gemm<T>(b, s, rec, "fop_o", b->att, qd, L.oa_w, qd, BH, w, qd, e));
+      }
+    }
+    REC_BEGIN("adarms", (double)BH * w * (12 + elt), (double)BH * w * 5);
+    HIP_TRY(launch_adarms<T>(b->x, w, BH, w, b->mod + 3 * w, b->mod + 4 * w, 6 * w, 0, c.rms_eps, (T*)b->y, w, s));
+    REC_END();
+    {
+      GemmArgs e = epi_args(EPI_GEGLU);
+      e.out_t = b->u;
+      e.ldo_t = F;
+      RV_TRY(run_gemm<T>(b, s, rec, "gate_up", b->y, w, L.gu_w, w, BH, 2 * F, w, e));
+    }
+    {
+      GemmArgs e = epi_args(EPI_RESID);
+      e.out_f = b->x;
+      e.ldo_f = w;
+      e.gate = b->mod + 5 * w;
+      e.ldg = 6 * w;
+      RV_TRY(run_gemm<T>(b, s, rec, "down", b->u, F, L.down_w, F, BH, w, F, e));
+    }
+  }
+  // final adaptive norm and output head
+  {
+    GemmArgs e = epi_args(EPI_F32);
+    e.bias = m->fmod_b;
+    e.out_f = b->fmod;
+    e.ldo_f = 2 * w;
+    RV_TRY(run_gemm<T>(b, s, rec, "final_mod", b->cond, w, m->fmod_w, w, BH, 2 * w, w, e));
+  }
+  REC_BEGIN("adarms", (double)BH * w * (12 + elt), (double)BH * w * 5);
+  HIP_TRY(launch_adarms<T>(b->x, w, BH, w, b->fmod, b->fmod + w, 2 * w, 0, c.rms_eps, (T*)b->y, w, s));
+  REC_END();
+  {
+    GemmArgs e = epi_args(EPI_F32);
+    e.bias = m->out_b;
+    e.out_f = b->v;
+    e.ldo_f = D;
+    RV_TRY(run_gemm<T>(b, s, rec, "out", b->y, w, m->out_w, w, BH, D, w, e));
+  }
+  return RAVEL_OK;
+}
+
+ravel_status enqueue_step(ravel_buffer* b, const void* fop, float* action, hipStream_t s, KernelRecorder* rec) {
+  ravel_model* m = b->m;
+  const ravel_config& c = m->cfg;
+  const int B = b->B, H = c.horizon, D = c.action_dim;
+  if (c.model_kind == RAVEL_TRANSFORMER) {
+    if (m->bf16)
+      RV_TRY(enqueue_transformer<bf16_t>(b, fop, s, rec));
+    else
+      RV_TRY(enqueue_transformer<float>(b, fop, s, rec));
+  } else {
+    REC_BEGIN("analytic_velocity", (double)B * H * D * 8, (double)B * H * D * 2);
+    HIP_TRY(launch_analytic_velocity(c.model_kind, b->X, b->t, B, H, D, m->analytic, b->v, s));
+    REC_END();
+  }
+  REC_BEGIN("euler_release", (double)B * H * D * 12 + (double)B * D * 4, (double)B * H * D * 2);
+  HIP_TRY(launch_euler_release(b->X, b->v, b->t, B, H, D, b->seed, action, b->ticket, s));
+  REC_END();
+  return RAVEL_OK;
+}
+
+// Apply ready context publishes on the step stream (caller holds the mutex).
+ravel_status apply_publishes(ravel_buffer* b, hipStream_t s) {
+  PublishBatch pb;
+  memset(&pb, 0, sizeof pb);
+  for (int e = 0; e < b->B; ++e) {
+    PendingCtx& p = b->pending[e];
+    if (!p.valid) continue;
+    if (b->sync_ctx) {
+      HIP_TRY(hipStreamWaitEvent(s, p.ready, 0));
+    } else {
+      const hipError_t q = hipEventQuery(p.ready);
+      if (q == hipErrorNotReady) continue;
+      if (q != hipSuccess) return fail(RAVEL_E_HIP, std::string("hipEventQuery: ") + hipGetErrorString(q));
+    }
+    // the slot that stops being read: free once the steps enqueued so far are done
+    HIP_TRY(hipEventRecord(b->retire[e], s));
+    b->retire_valid[e] = 1;
+    const int ns = b->has_ctx[e] ? 1 - b->active[e] : b->active[e] ^ 1;
+    b->active[e] = ns;
+    b->has_ctx[e] = 1;
+    b->tobs_host[e] = p.t_obs;
+    b->log.push_back({(int64_t)e, b->t_host, p.t_obs});
+    p.valid = false;
+    pb.env[pb.n] = e;
+    pb.new_slot[pb.n] = ns;
+    pb.tobs[pb.n] = p.t_obs;
+    if (++pb.n == 32) {
+      HIP_TRY(launch_publish(pb, b->slot, b->t_obs, s));
+      pb.n = 0;
+    }
+  }
+  if (pb.n) HIP_TRY(launch_publish(pb, b->slot, b->t_obs, s));
+  return RAVEL_OK;
+}
+
+ravel_status acquire_locked(ravel_buffer* b, int env, void** k, void** v, hipStream_t producer) {
+  ravel_model* m = b->m;
+  b->pending[env].valid = false;  // a not-yet-applied publish of this env is superseded
+  const int inactive = b->has_ctx[env] ? 1 - b->active[env] : (b->active[env] ^ 1);
+  if (b->retire_valid[env]) HIP_TRY(hipStreamWaitEvent(producer, b->retire[env], 0));
+  const size_t off = ((size_t)inactive * b->B + env) * b->ctx_elems * m->elt;
+  *k = (char*)b->ctx_k + off;
+  *v = (char*)b->ctx_v + off;
+  return RAVEL_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C ABI
+// ---------------------------------------------------------------------------
+extern "C" {
+
+const char* ravel_last_error(void) { return g_err.c_str(); }
+
+int64_t ravel_model_weight_bytes(const ravel_model* m) { return m ? m->weight_bytes : 0; }
+
+ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights, int32_t n_weights,
+                          ravel_model** out) {
+  if (!cfgp || !out || (n_weights > 0 && !weights)) return fail(RAVEL_E_INVALID, "null argument");
+  *out = nullptr;
+  const ravel_config c = *cfgp;
+  if (c.dtype != RAVEL_F32 && c.dtype != RAVEL_BF16) return fail(RAVEL_E_INVALID, "dtype");
+  if (c.horizon < 1 || c.horizon > 128) return fail(RAVEL_E_SHAPE, "horizon must be in 1..128");
+  if (c.action_dim < 1) return fail(RAVEL_E_SHAPE, "action_dim must be >= 1");
+  TensorMap tm;
+  for (int i = 0; i < n_weights; ++i) {
+    if (!weights[i].name) return fail(RAVEL_E_INVALID, "weight without a name");
+    tm.m[weights[i].name] = &weights[i];
+  }
+  ravel_model* m = new ravel_model();
+  m->cfg = c;
+  m->bf16 = c.dtype == RAVEL_BF16;
+  m->elt = m->bf16 ? 2 : 4;
+  (void)hipGetDevice(&m->device);
+  auto bail = [&](ravel_status s) {
+    if (m->arena) (void)hipFree(m->arena);
+    delete m;
+    return s;
+  };
+  const int w = c.width, D = c.action_dim, H = c.horizon;
+  if (c.model_kind == RAVEL_ANALYTIC_OT || c.model_kind == RAVEL_ANALYTIC_LINEAR) {
+    const char* nm = c.model_kind == RAVEL_ANALYTIC_OT ? "analytic.target" : "analytic.lambda";
+    const int64_t n = c.model_kind == RAVEL_ANALYTIC_OT ? D : 1;
+    const ravel_tensor* t = tm.get(nm);
+    ravel_status st = check_shape(t, nm, {n});
+    if (st != RAVEL_OK) return bail(st);
+    if (t->dtype != RAVEL_F32) return bail(fail(RAVEL_E_INVALID, "analytic parameter must be fp32"));
+    Arena ar;
+    ar.want((void**)&m->analytic, n * 4);
+    if ((st = ar.commit(&m->arena)) != RAVEL_OK) return bail(st);
+    if (hipMemcpy(m->analytic, t->data, n * 4, hipMemcpyDefault) != hipSuccess)
+      return bail(fail(RAVEL_E_HIP, "upload analytic parameter"));
+    m->weight_bytes = n * 4;
+    *out = m;
+    return RAVEL_OK;
+  }
+  if (c.model_kind != RAVEL_TRANSFORMER) return bail(fail(RAVEL_E_INVALID, "model_kind"));
+  const int nq = c.n_q_heads, nkv = c.n_kv_heads, hd = c.head_dim, F = c.mlp_dim, L = c.layers;
+  if (w <= 0 || w % 8 || nq <= 0 || nkv <= 0 || nq % nkv || hd % 32 || hd > 256 || F <= 0 || F % 16 ||
+      L <= 0 || c.prefix_len < 0 || c.n_fop < 0)
+    return bail(fail(RAVEL_E_SHAPE, "invalid transformer config (w%8, hd%32<=256, F%16, nq%nkv)"));
+  if (m->bf16 && (H + 15) / 16 > 8) return bail(fail(RAVEL_E_SHAPE, "bf16 attention supports H <= 128"));
+  const int qd = nq * hd, kvd = nkv * hd, qkvd = qd + 2 * kvd;
+  const int stride = c.fop_stride;
+  std::vector<int> ad_of(L, -1);
+  int n_ad = 0;
+  if (c.n_fop > 0 && stride > 0)
+    for (int l = 0; l < L; ++l)
+      if (l % stride == stride - 1) ad_of[l] = n_ad++;
+  m->n_ad = n_ad;
+  m->layers.resize(L);
+
+  // shape checks
+  ravel_status st;
+#define CHK(name, ...)                                             \
+  do {                                                             \
+    if ((st = check_shape(tm.get(name), name, {__VA_ARGS__})) != RAVEL_OK) return bail(st); \
+  } while (0)
+  CHK("in.w", w, D);
+  CHK("in.b", w);
+  CHK("time.w1", w, w);
+  CHK("time.b1", w);
+  CHK("time.w2", w, w);
+  CHK("time.b2", w);
+  CHK("delta.w1", w, 1);
+  CHK("delta.b1", w);
+  CHK("delta.w2", w, w);
+  CHK("delta.b2", w);
+  CHK("final.mod.w", 3 * w, w);
+  CHK("final.mod.b", 3 * w);
+  CHK("out.w", D, w);
+  CHK("out.b", D);
+  for (int l = 0; l < L; ++l) {
+    const std::string p = "layers." + std::to_string(l) + ".";
+    CHK((p + "mod.w").c_str(), 6 * w, w);
+    CHK((p + "mod.b").c_str(), 6 * w);
+    CHK((p + "qkv.w").c_str(), qkvd, w);
+    CHK((p + "o.w").c_str(), w, qd);
+    CHK((p + "gate.w").c_str(), F, w);
+    CHK((p + "up.w").c_str(), F, w);
+    CHK((p + "down.w").c_str(), w, F);
+    if (ad_of[l] >= 0) {
+      CHK((p + "fop.gamma").c_str(), w);
+      CHK((p + "fop.q.w").c_str(), qd, w);
+      CHK((p + "fop.kv.w").c_str(), 2 * kvd, w);
+      CHK((p + "fop.o.w").c_str(), w, qd);
+      CHK((p + "fop.alpha").c_str(), 1);
+    }
+  }
+  m->has_fop_encoder = c.n_fop > 0 && tm.get("fop.w1") != nullptr;
+  if (m->has_fop_encoder) {
+    CHK("fop.w1", w, c.fop_obs_dim);
+    CHK("fop.b1", w);
+    CHK("fop.w2", (int64_t)c.n_fop * w, w);
+    CHK("fop.b2", (int64_t)c.n_fop * w);
+  }
+#undef CHK
+
+  // device layout
+  const size_t E = m->elt;
+  Arena ar;
+  ar.want((void**)&m->in_w, (size_t)w * D * 4);
+  ar.want((void**)&m->in_b, (size_t)w * 4);
+  ar.want((void**)&m->ctau, (size_t)H * w * 4);
+  ar.want((void**)&m->d_w1, (size_t)w * 4);
+  ar.want((void**)&m->d_b1, (size_t)w * 4);
+  ar.want((void**)&m->d_w2, (size_t)w * w * E);
+  ar.want((void**)&m->d_b2, (size_t)w * 4);
+  for (int l = 0; l < L; ++l) {
+    LayerW& Lw = m->layers[l];
+    ar.want(&Lw.mod_w, (size_t)6 * w * w * E);
+    ar.want((void**)&Lw.mod_b, (size_t)6 * w * 4);
+    ar.want(&Lw.qkv_w, (size_t)qkvd * w * E);
+    ar.want(&Lw.o_w, (size_t)w * qd * E);
+    ar.want(&Lw.gu_w, (size_t)2 * F * w * E);
+    ar.want(&Lw.down_w, (size_t)w * F * E);
+    Lw.adapter = ad_of[l];
+    if (ad_of[l] >= 0) {
+      ar.want((void**)&Lw.gamma, (size_t)w * 4);
+      ar.want(&Lw.qa_w, (size_t)qd * w * E);
+      ar.want(&Lw.oa_w, (size_t)w * qd * E);
+      ar.want((void**)&Lw.alpha, 4);
+    }
+  }
+  if (n_ad > 0) ar.want(&m->kva_w, (size_t)n_ad * 2 * kvd * w * E);
+  ar.want(&m->fmod_w, (size_t)2 * w * w * E);
+  ar.want((void**)&m->fmod_b, (size_t)2 * w * 4);
+  ar.want(&m->out_w, (size_t)D * w * E);
+  ar.want((void**)&m->out_b, (size_t)D * 4);
+  if (m->has_fop_encoder) {
+    ar.want(&m->f_w1, (size_t)w * c.fop_obs_dim * E);
+    ar.want((void**)&m->f_b1, (size_t)w * 4);
+    ar.want(&m->f_w2, (size_t)c.n_fop * w * w * E);
+    ar.want((void**)&m->f_b2, (size_t)c.n_fop * w * 4);
+  }
+  m->arena_bytes = ar.off;
+  if ((st = ar.commit(&m->arena)) != RAVEL_OK) return bail(st);
+
+  // staging (fp32 + converted bf16) for uploads
+  Staging stg;
+  stg.S = (size_t)std::max<int64_t>((int64_t)6 * w * w, (int64_t)c.n_fop * w * w);
+  stg.S = std::min<size_t>(stg.S, (size_t)64 << 20);
+  stg.S = std::max<size_t>(stg.S, (size_t)2 * F * w);
+  void* staging = nullptr;
+  if (hipMalloc(&staging, stg.S * 6 + 512) != hipSuccess) return bail(fail(RAVEL_E_NOMEM, "staging"));
+  stg.f = (float*)staging;
+  stg.h = (bf16_t*)((char*)staging + align_up(stg.S * 4, 256));
+  auto up = [&](const char* name, void* dst, bool model_dtype) {
+    return upload_all(tm.get(name), model_dtype && m->bf16, dst, stg);
+  };
+  auto done = [&](ravel_status s2) {
+    (void)hipFree(staging);
+    return s2;
+  };
+#define UP(name, dst, md)                                     \
+  do {                                                        \
+    if ((st = up(name, dst, md)) != RAVEL_OK) return bail(done(st)); \
+  } while (0)
+  UP("in.w", m->in_w, false);
+  UP("in.b", m->in_b, false);
+  UP("delta.w1", m->d_w1, false);
+  UP("delta.b1", m->d_b1, false);
+  UP("delta.w2", m->d_w2, true);
+  UP("delta.b2", m->d_b2, false);
+  for (int l = 0; l < L; ++l) {
+    LayerW& Lw = m->layers[l];
+    const std::string p = "layers." + std::to_string(l) + ".";
+    UP((p + "mod.w").c_str(), Lw.mod_w, true);
+    UP((p + "mod.b").c_str(), Lw.mod_b, false);
+    UP((p + "qkv.w").c_str(), Lw.qkv_w, true);
+    UP((p + "o.w").c_str(), Lw.o_w, true);
+    UP((p + "down.w").c_str(), Lw.down_w, true);
+    // gate/up interleave: dst row 32b + j <- gate row 16b + j, dst row 32b + 16 + j <- up row 16b + j
+    {
+      const ravel_tensor* g = tm.get(p + "gate.w");
+      const ravel_tensor* u = tm.get(p + "up.w");
+      if ((st = upload_rows(g, 0, F, w, m->bf16, Lw.gu_w, [](int64_t r) { return (r / 16) * 32 + (r % 16); },
+                            stg)) != RAVEL_OK)
+        return bail(done(st));
+      if ((st = upload_rows(u, 0, F, w, m->bf16, Lw.gu_w,
+                            [](int64_t r) { return (r / 16) * 32 + 16 + (r % 16); }, stg)) != RAVEL_OK)
+        return bail(done(st));
+    }
+    if (Lw.adapter >= 0) {
+      UP((p + "fop.gamma").c_str(), Lw.gamma, false);
+      UP((p + "fop.q.w").c_str(), Lw.qa_w, true);
+      UP((p + "fop.o.w").c_str(), Lw.oa_w, true);
+      UP((p + "fop.alpha").c_str(), Lw.alpha, false);
+      void* dst = (char*)m->kva_w + (size_t)Lw.adapter * 2 * kvd * w * E;
+      UP((p + "fop.kv.w").c_str(), dst, true);
+    }
+  }
+  {
+    // final modulation: only the scale and shift chunks (rows 0 .. 2w) are used
+    const ravel_tensor* fw = tm.get("final.mod.w");
+    if ((st = upload_rows(fw, 0, 2 * w, w, m->bf16, m->fmod_w, [](int64_t r) { return r; }, stg)) !=
+        RAVEL_OK)
+      return bail(done(st));
+    const ravel_tensor* fb = tm.get("final.mod.b");
+    if (hipMemcpy(m->fmod_b, fb->data, (size_t)2 * w * 4, hipMemcpyDefault) != hipSuccess)
+      return bail(done(fail(RAVEL_E_HIP, "final.mod.b")));
+  }
+  UP("out.w", m->out_w, true);
+  UP("out.b", m->out_b, false);
+  if (m->has_fop_encoder) {
+    UP("fop.w1", m->f_w1, true);
+    UP("fop.b1", m->f_b1, false);
+    UP("fop.w2", m->f_w2, true);
+    UP("fop.b2", m->f_b2, false);
+  }
+
+  // flow-time conditioning c_tau(i) = W_t2 silu(W_t1 emb(tau_i) + b_t1) + b_t2, once per model
+  {
+    void *emb = nullptr, *hid = nullptr, *tw1 = nullptr, *tw2 = nullptr;
+    float *tb1 = nullptr, *tb2 = nullptr;
+    Arena ta;
+    void* tarena = nullptr;
+    ta.want(&emb, (size_t)H * w * E);
+    ta.want(&hid, (size_t)H * w * E);
+    ta.want(&tw1, (size_t)w * w * E);
+    ta.want(&tw2, (size_t)w * w * E);
+    ta.want((void**)&tb1, (size_t)w * 4);
+    ta.want((void**)&tb2, (size_t)w * 4);
+    if ((st = ta.commit(&tarena)) != RAVEL_OK) return bail(done(st));
+    auto tdone = [&](ravel_status s2) {
+      (void)hipFree(tarena);
+      return done(s2);
+    };
+    if ((st = up("time.w1", tw1, true)) != RAVEL_OK) return bail(tdone(st));
+    if ((st = up("time.w2", tw2, true)) != RAVEL_OK) return bail(tdone(st));
+    if ((st = up("time.b1", tb1, false)) != RAVEL_OK) return bail(tdone(st));
+    if ((st = up("time.b2", tb2, false)) != RAVEL_OK) return bail(tdone(st));
+    // a throwaway buffer-like context for the GEMM workspace
+    ravel_buffer tmp;
+    tmp.m = m;
+    tmp.B = 1;
+    const GemmPlan p1 = plan_gemm(H, w, w, false);
+    const size_t part = (size_t)p1.ksplit * H * w;
+    Arena wa;
+    void* warena = nullptr;
+    wa.want((void**)&tmp.gpart, part * 4);
+    wa.want((void**)&tmp.gcnt, (size_t)std::max(p1.tiles, 1) * 4);
+    if ((st = wa.commit(&warena)) != RAVEL_OK) return bail(tdone(st));
+    (void)hipMemset(tmp.gcnt, 0, (size_t)std::max(p1.tiles, 1) * 4);
+    hipError_t he = m->bf16 ? launch_time_embedding<bf16_t>(H, w, (bf16_t*)emb, 0)
+                            : launch_time_embedding<float>(H, w, (float*)emb, 0);
+    if (he != hipSuccess) {
+      (void)hipFree(warena);
+      return bail(tdone(fail(RAVEL_E_HIP, hipGetErrorString(he))));
+    }
+    GemmArgs e1 = epi_args(EPI_SILU_T);
+    e1.bias = tb1;
+    e1.out_t = hid;
+    e1.ldo_t = w;
+    GemmArgs e2 = epi_args(EPI_F32);
+    e2.bias = tb2;
+    e2.out_f = m->ctau;
+    e2.ldo_f = w;
+    if (m->bf16) {
+      st = run_gemm<bf16_t>(&tmp, 0, nullptr, "time1", emb, w, tw1, w, H, w, w, e1);
+      if (st == RAVEL_OK) st = run_gemm<bf16_t>(&tmp, 0, nullptr, "time2", hid, w, tw2, w, H, w, w, e2);
+    } else {
+      st = run_gemm<float>(&tmp, 0, nullptr, "time1", emb, w, tw1, w, H, w, w, e1);
+      if (st == RAVEL_OK) st = run_gemm<float>(&tmp, 0, nullptr, "time2", hid, w, tw2, w, H, w, w, e2);
+    }
+    hipError_t se = hipDeviceSynchronize();
+    (void)hipFree(warena);
+    if (st != RAVEL_OK) return bail(tdone(st));
+    if (se != hipSuccess) return bail(tdone(fail(RAVEL_E_HIP, hipGetErrorString(se))));
+    (void)hipFree(tarena);
+  }
+  (void)hipFree(staging);
+#undef UP
+  if (hipDeviceSynchronize() != hipSuccess) return bail(fail(RAVEL_E_HIP, "create sync"));
+  // algorithmic weight bytes streamed by one step (time MLP excluded: precomputed)
+  int64_t wb = (int64_t)w * D * 4 + (int64_t)w * w * E;
+  for (int l = 0; l < L; ++l) {
+    wb += (int64_t)(6 * w + qkvd) * w * E + (int64_t)w * qd * E + (int64_t)3 * F * w * E + 6 * w * 4;
+    if (ad_of[l] >= 0) wb += (int64_t)(2 * qd + 2 * kvd) * w * E;
+  }
+  wb += (int64_t)2 * w * w * E + (int64_t)D * w * E;
+  m->weight_bytes = wb;
+  *out = m;
+  return RAVEL_OK;
+}
+
+void ravel_destroy(ravel_model* m) {
+  if (!m) return;
+  if (m->arena) (void)hipFree(m->arena);
+  delete m;
+}
+
+ravel_status ravel_buffer_create(ravel_model* m, int32_t batch, uint64_t seed, ravel_buffer** out) {
+  if (!m || !out) return fail(RAVEL_E_INVALID, "null argument");
+  if (batch < 1) return fail(RAVEL_E_SHAPE, "batch must be >= 1");
+  *out = nullptr;
+  const ravel_config& c = m->cfg;
+  ravel_buffer* b = new ravel_buffer();
+  b->m = m;
+  b->B = batch;
+  b->seed = seed;
+  const int B = batch, H = c.horizon, D = c.action_dim, BH = B * H;
+  const size_t E = m->elt;
+  Arena ar;
+  ar.want((void**)&b->X, (size_t)BH * D * 4);
+  ar.want((void**)&b->t, 8);
+  ar.want((void**)&b->t_obs, (size_t)B * 8);
+  ar.want((void**)&b->slot, (size_t)B * 4);
+  ar.want((void**)&b->ticket, 4);
+  ar.want((void**)&b->v, (size_t)BH * D * 4);
+  ar.want((void**)&b->dbg_flag, 4);
+  size_t part_elems = 0, cnt = 1;
+  if (c.model_kind == RAVEL_TRANSFORMER) {
+    const int w = c.width, qd = c.n_q_heads * c.head_dim, kvd = c.n_kv_heads * c.head_dim;
+    const int qkvd = qd + 2 * kvd, F = c.mlp_dim;
+    b->ctx_elems = (size_t)c.layers * c.prefix_len * kvd;
+    ar.want(&b->ctx_k, 2 * (size_t)B * b->ctx_elems * E);
+    ar.want(&b->ctx_v, 2 * (size_t)B * b->ctx_elems * E);
+    ar.want((void**)&b->x, (size_t)BH * w * 4);
+    ar.want(&b->cond, (size_t)BH * w * E);
+    ar.want(&b->h1, (size_t)B * w * E);
+    ar.want((void**)&b->mod, (size_t)BH * 6 * w * 4);
+    ar.want(&b->y, (size_t)BH * w * E);
+    ar.want(&b->qkv, (size_t)BH * qkvd * E);
+    ar.want(&b->att, (size_t)BH * qd * E);
+    ar.want(&b->qa, (size_t)BH * qd * E);
+    if (m->n_ad > 0) ar.want(&b->kva, (size_t)B * c.n_fop * m->n_ad * 2 * kvd * E);
+    ar.want(&b->u, (size_t)BH * F * E);
+    ar.want((void**)&b->fmod, (size_t)BH * 2 * w * 4);
+    ar.want(&b->fhid, (size_t)B * w * E);
+    ar.want(&b->obs_t, (size_t)B * std::max(c.fop_obs_dim, 1) * E);
+    // GEMM split-K workspace: the largest plan of the step
+    struct Shape { int M, N, K; bool geglu; };
+    std::vector<Shape> shapes = {{B, w, w, false}, {BH, 6 * w, w, false}, {BH, qkvd, w, false},
+                                 {BH, w, qd, false}, {BH, qd, w, false}, {BH, 2 * F, w, true},
+                                 {BH, w, F, false}, {BH, 2 * w, w, false}, {BH, D, w, false},
+                                 {B, w, std::max(c.fop_obs_dim, 8), false}, {B, c.n_fop * w, w, false}};
+    if (m->n_ad > 0) shapes.push_back({B * c.n_fop, m->n_ad * 2 * kvd, w, false});
+    for (auto& s : shapes) {
+      if (s.N <= 0 || s.M <= 0) continue;
+      const GemmPlan p = plan_gemm(s.M, s.N, s.K, s.geglu);
+      if (p.ksplit > 1) part_elems = std::max(part_elems, (size_t)p.ksplit * s.M * s.N);
+      cnt = std::max(cnt, (size_t)p.tiles);
+    }
+    // attention key split: aim for ~256 blocks when B * nq is small, >= 64 keys per split
+    const int nkeys = c.prefix_len + H;
+    const int blocks = B * c.n_q_heads;
+    int ns = 1;
+    if (m->bf16 && blocks < 256) {
+      ns = std::min((nkeys + 63) / 64, (256 + blocks - 1) / blocks);
+      ns = std::max(ns, 1);
+    }
+    int kps = ((nkeys + ns - 1) / ns + 31) / 32 * 32;
+    ns = (nkeys + kps - 1) / kps;
+    b->attn_nsplit = ns;
+    b->attn_kps = kps;
+    if (ns > 1) {
+      const int Hp = (H + 15) / 16 * 16;
+      ar.want((void**)&b->apart_o, (size_t)blocks * ns * Hp * c.head_dim * 4);
+      ar.want((void**)&b->apart_ml, (size_t)blocks * ns * Hp * 2 * 4);
+    }
+    ar.want((void**)&b->acnt, (size_t)blocks * 4);
+  }
+  ar.want((void**)&b->gpart, std::max<size_t>(part_elems, 1) * 4);
+  ar.want((void**)&b->gcnt, cnt * 4);
+  ravel_status st = ar.commit(&b->arena);
+  if (st != RAVEL_OK) {
+    delete b;
+    return st;
+  }
+  auto bail = [&](ravel_status s2) {
+    (void)hipFree(b->arena);
+    delete b;
+    return s2;
+  };
+  if (hipMemset(b->arena, 0, ar.off) != hipSuccess) return bail(fail(RAVEL_E_HIP, "memset"));
+  if (launch_ring_init(b->X, B, H, D, seed, 0) != hipSuccess) return bail(fail(RAVEL_E_HIP, "ring init"));
+  if (hipDeviceSynchronize() != hipSuccess) return bail(fail(RAVEL_E_HIP, "buffer create sync"));
+  b->active.assign(B, 0);
+  b->has_ctx.assign(B, 0);
+  b->tobs_host.assign(B, 0);
+  b->pending.resize(B);
+  b->retire.resize(B);
+  b->retire_valid.assign(B, 0);
+  for (int e = 0; e < B; ++e) {
+    if (hipEventCreateWithFlags(&b->pending[e].ready, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&b->retire[e], hipEventDisableTiming) != hipSuccess)
+      return bail(fail(RAVEL_E_HIP, "event create"));
+  }
+  if (hipStreamCreateWithFlags(&b->cap_stream, hipStreamNonBlocking) != hipSuccess)
+    return bail(fail(RAVEL_E_HIP, "stream create"));
+  if (const char* ev = getenv("RAVEL_SYNC_CONTEXT")) b->sync_ctx = atoi(ev) != 0;
+  if (const char* ev = getenv("RAVEL_NO_GRAPH")) b->use_graph = atoi(ev) == 0;
+  if (const char* ev = getenv("RAVEL_DEBUG")) b->debug = atoi(ev) != 0;
+  *out = b;
+  return RAVEL_OK;
+}
+
+void ravel_buffer_destroy(ravel_buffer* b) {
+  if (!b) return;
+  (void)hipDeviceSynchronize();
+  for (auto& g : b->graphs) {
+    (void)hipGraphExecDestroy(g.exec);
+    (void)hipGraphDestroy(g.graph);
+  }
+  for (int e = 0; e < b->B; ++e) {
+    if (b->pending[e].ready) (void)hipEventDestroy(b->pending[e].ready);
+    if (b->retire[e]) (void)hipEventDestroy(b->retire[e]);
+  }
+  if (b->cap_stream) (void)hipStreamDestroy(b->cap_stream);
+  if (b->arena) (void)hipFree(b->arena);
+  delete b;
+}
+
+ravel_status ravel_buffer_set_option(ravel_buffer* b, int32_t option, int64_t value) {
+  if (!b) return fail(RAVEL_E_INVALID, "null buffer");
+  std::lock_guard<std::mutex> lk(b->mu);
+  switch (option) {
+    case RAVEL_OPT_SYNC_CONTEXT: b->sync_ctx = value != 0; return RAVEL_OK;
+    case RAVEL_OPT_USE_GRAPH: b->use_graph = value != 0; return RAVEL_OK;
+    case RAVEL_OPT_DEBUG: b->debug = value != 0; return RAVEL_OK;
+    default: return fail(RAVEL_E_INVALID, "unknown option");
+  }
+}
+
+ravel_status ravel_context_acquire(ravel_buffer* b, int32_t env, void** k, void** v, void* producer) {
+  if (!b || !k || !v) return fail(RAVEL_E_INVALID, "null argument");
+  if (b->m->cfg.model_kind != RAVEL_TRANSFORMER) return fail(RAVEL_E_STATE, "analytic models have no context");
+  if (env < 0 || env >= b->B) return fail(RAVEL_E_INVALID, "env out of range");
+  std::lock_guard<std::mutex> lk(b->mu);
+  return acquire_locked(b, env, k, v, (hipStream_t)producer);
+}
+
+ravel_status ravel_set_context(ravel_buffer* b, int32_t env, const void* k, const void* v, int64_t t_obs,
+                               void* producer) {
+  if (!b) return fail(RAVEL_E_INVALID, "null buffer");
+  if (b->m->cfg.model_kind != RAVEL_TRANSFORMER) return fail(RAVEL_E_STATE, "analytic models have no context");
+  if (env < 0 || env >= b->B) return fail(RAVEL_E_INVALID, "env out of range");
+  if ((k == nullptr) != (v == nullptr)) return fail(RAVEL_E_INVALID, "k and v must both be given or both NULL");
+  hipStream_t ps = (hipStream_t)producer;
+  std::lock_guard<std::mutex> lk(b->mu);
+  int64_t latest = b->has_ctx[env] ? b->tobs_host[env] : INT64_MIN;
+  if (b->pending[env].valid) latest = std::max(latest, b->pending[env].t_obs);
+  if (t_obs < latest) return fail(RAVEL_E_STATE, "t_obs must not decrease per env");
+  if (k) {
+    void *dk, *dv;
+    RV_TRY(acquire_locked(b, env, &dk, &dv, ps));
+    const size_t bytes = b->ctx_elems * b->m->elt;
+    HIP_TRY(hipMemcpyAsync(dk, k, bytes, hipMemcpyDefault, ps));
+    HIP_TRY(hipMemcpyAsync(dv, v, bytes, hipMemcpyDefault, ps));
+  }
+  HIP_TRY(hipEventRecord(b->pending[env].ready, ps));
+  b->pending[env].valid = true;
+  b->pending[env].t_obs = t_obs;
+  return RAVEL_OK;
+}
+
+ravel_status ravel_step(ravel_buffer* b, const void* fop, float* action, void* stream) {
+  if (!b || !action) return fail(RAVEL_E_INVALID, "null argument");
+  ravel_model* m = b->m;
+  const ravel_config& c = m->cfg;
+  if (c.model_kind == RAVEL_TRANSFORMER && m->n_ad > 0 && !fop)
+    return fail(RAVEL_E_INVALID, "fop_tokens required: the model has FOP adapters");
+  if (fop && ((uintptr_t)fop % 16)) return fail(RAVEL_E_INVALID, "fop_tokens must be 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  std::lock_guard<std::mutex> lk(b->mu);
+  if (c.model_kind == RAVEL_TRANSFORMER) {
+    RV_TRY(apply_publishes(b, s));
+    for (int e = 0; e < b->B; ++e)
+      if (!b->has_ctx[e]) return fail(RAVEL_E_STATE, "env " + std::to_string(e) + " has no context yet");
+  }
+  if (b->use_graph) {
+    GraphEntry* ge = nullptr;
+    for (auto& g : b->graphs)
+      if (g.fop == fop && g.action == action) ge = &g;
+    if (!ge) {
+      GraphEntry g{fop, action, nullptr, nullptr};
+      HIP_TRY(hipStreamBeginCapture(b->cap_stream, hipStreamCaptureModeRelaxed));
+      ravel_status st = enqueue_step(b, fop, action, b->cap_stream, nullptr);
+      hipGraph_t graph = nullptr;
+      hipError_t he = hipStreamEndCapture(b->cap_stream, &graph);
+      if (st != RAVEL_OK) return st;
+      if (he != hipSuccess) return fail(RAVEL_E_HIP, std::string("capture: ") + hipGetErrorString(he));
+      g.graph = graph;
+      HIP_TRY(hipGraphInstantiate(&g.exec, graph, nullptr, nullptr, 0));
+      b->graphs.push_back(g);
+      ge = &b->graphs.back();
+    }
+    HIP_TRY(hipGraphLaunch(ge->exec, s));
+  } else {
+    RV_TRY(enqueue_step(b, fop, action, s, nullptr));
+  }
+  b->t_host += 1;
+  if (b->debug) {
+    HIP_TRY(hipStreamSynchronize(s));
+    HIP_TRY(hipMemset(b->dbg_flag, 0, 4));
+    HIP_TRY(launch_check_finite(b->X, (long long)b->B * c.horizon * c.action_dim, b->dbg_flag, s));
+    HIP_TRY(launch_check_finite(b->v, (long long)b->B * c.horizon * c.action_dim, b->dbg_flag, s));
+    int flag = 0;
+    HIP_TRY(hipMemcpy(&flag, b->dbg_flag, 4, hipMemcpyDeviceToHost));
+    if (flag) return fail(RAVEL_E_STATE, "non-finite values after step " + std::to_string(b->t_host - 1));
+  }
+  return RAVEL_OK;
+}
+
+ravel_status ravel_fop_encode(ravel_buffer* b, const float* obs, void* fop_tokens, void* stream) {
+  if (!b || !obs || !fop_tokens) return fail(RAVEL_E_INVALID, "null argument");
+  ravel_model* m = b->m;
+  const ravel_config& c = m->cfg;
+  if (!m->has_fop_encoder) return fail(RAVEL_E_STATE, "model has no FOP encoder weights");
+  hipStream_t s = (hipStream_t)stream;
+  const int B = b->B, w = c.width, d = c.fop_obs_dim;
+  std::lock_guard<std::mutex> lk(b->mu);
+  GemmArgs e1 = epi_args(EPI_GELU_T);
+  e1.bias = m->f_b1;
+  e1.out_t = b->fhid;
+  e1.ldo_t = w;
+  GemmArgs e2 = epi_args(EPI_T);
+  e2.bias = m->f_b2;
+  e2.out_t = fop_tokens;
+  e2.ldo_t = c.n_fop * w;
+  if (m->bf16) {
+    HIP_TRY(launch_convert<bf16_t>(obs, (bf16_t*)b->obs_t, (long long)B * d, s));
+    RV_TRY(run_gemm<bf16_t>(b, s, nullptr, "fop1", b->obs_t, d, m->f_w1, d, B, w, d, e1));
+    RV_TRY(run_gemm<bf16_t>(b, s, nullptr, "fop2", b->fhid, w, m->f_w2, w, B, c.n_fop * w, w, e2));
+  } else {
+    RV_TRY(run_gemm<float>(b, s, nullptr, "fop1", obs, d, m->f_w1, d, B, w, d, e1));
+    RV_TRY(run_gemm<float>(b, s, nullptr, "fop2", b->fhid, w, m->f_w2, w, B, c.n_fop * w, w, e2));
+  }
+  return RAVEL_OK;
+}
+
+ravel_status ravel_buffer_sync(ravel_buffer* b) {
+  if (!b) return fail(RAVEL_E_INVALID, "null buffer");
+  HIP_TRY(hipDeviceSynchronize());
+  return RAVEL_OK;
+}
+
+ravel_status ravel_debug_state(ravel_buffer* b, float* X_host, int64_t* t, int64_t* t_obs_host) {
+  if (!b) return fail(RAVEL_E_INVALID, "null buffer");
+  const ravel_config& c = b->m->cfg;
+  HIP_TRY(hipDeviceSynchronize());
+  if (X_host) HIP_TRY(hipMemcpy(X_host, b->X, (size_t)b->B * c.horizon * c.action_dim * 4, hipMemcpyDeviceToHost));
+  if (t) HIP_TRY(hipMemcpy(t, b->t, 8, hipMemcpyDeviceToHost));
+  if (t_obs_host) HIP_TRY(hipMemcpy(t_obs_host, b->t_obs, (size_t)b->B * 8, hipMemcpyDeviceToHost));
+  return RAVEL_OK;
+}
+
+ravel_status ravel_publish_log(ravel_buffer* b, int64_t* entries, int32_t* n) {
+  if (!b || !n) return fail(RAVEL_E_INVALID, "null argument");
+  std::lock_guard<std::mutex> lk(b->mu);
+  const int32_t cap = *n;
+  int32_t k = 0;
+  for (auto& r : b->log) {
+    if (k >= cap) break;
+    if (entries) {
+      entries[3 * k + 0] = r[0];
+      entries[3 * k + 1] = r[1];
+      entries[3 * k + 2] = r[2];
+    }
+    ++k;
+  }
+  *n = entries ? k : (int32_t)b->log.size();
+  return RAVEL_OK;
+}
+
+namespace {
+struct BlobHeader {
+  uint64_t magic;
+  int32_t B, H, D, L, P, kvd, dtype, kind;
+  uint64_t seed;
+  int64_t t;
+};
+const uint64_t kMagic = 0x5241564C53544154ull;  // "RAVLSTAT"
+}  // namespace
+
+ravel_status ravel_buffer_save(ravel_buffer* b, void* blob, size_t* n) {
+  if (!b || !n) return fail(RAVEL_E_INVALID, "null argument");
+  const ravel_config& c = b->m->cfg;
+  const size_t xs = (size_t)b->B * c.horizon * c.action_dim * 4;
+  const size_t cs = b->ctx_elems * b->m->elt;
+  const size_t need = sizeof(BlobHeader) + (size_t)b->B * (8 + 4 + 4) + xs + (size_t)b->B * 2 * cs;
+  if (!blob) {
+    *n = need;
+    return RAVEL_OK;
+  }
+  if (*n < need) return fail(RAVEL_E_INVALID, "blob too small");
+  std::lock_guard<std::mutex> lk(b->mu);
+  HIP_TRY(hipDeviceSynchronize());
+  char* p = (char*)blob;
+  BlobHeader h{kMagic, b->B, c.horizon, c.action_dim, c.layers, c.prefix_len,
+               c.n_kv_heads * c.head_dim, c.dtype, c.model_kind, b->seed, 0};
+  HIP_TRY(hipMemcpy(&h.t, b->t, 8, hipMemcpyDeviceToHost));
+  memcpy(p, &h, sizeof h);
+  p += sizeof h;
+  HIP_TRY(hipMemcpy(p, b->t_obs, (size_t)b->B * 8, hipMemcpyDeviceToHost));
+  p += (size_t)b->B * 8;
+  for (int e = 0; e < b->B; ++e) {
+    memcpy(p, &b->active[e], 4);
+    memcpy(p + 4, &b->has_ctx[e], 4);
+    p += 8;
+  }
+  HIP_TRY(hipMemcpy(p, b->X, xs, hipMemcpyDeviceToHost));
+  p += xs;
+  for (int e = 0; e < b->B; ++e) {
+    const size_t off = ((size_t)b->active[e] * b->B + e) * cs;
+    if (cs) {
+      HIP_TRY(hipMemcpy(p, (char*)b->ctx_k + off, cs, hipMemcpyDeviceToHost));
+      HIP_TRY(hipMemcpy(p + cs, (char*)b->ctx_v + off, cs, hipMemcpyDeviceToHost));
+    }
+    p += 2 * cs;
+  }
+  *n = need;
+  return RAVEL_OK;
+}
+
+ravel_status ravel_buffer_load(ravel_buffer* b, const void* blob, size_t n) {
+  if (!b || !blob) return fail(RAVEL_E_INVALID, "null argument");
+  const ravel_config& c = b->m->cfg;
+  const size_t xs = (size_t)b->B * c.horizon * c.action_dim * 4;
+  const size_t cs = b->ctx_elems * b->m->elt;
+  const size_t need = sizeof(BlobHeader) + (size_t)b->B * (8 + 4 + 4) + xs + (size_t)b->B * 2 * cs;
+  if (n < need) return fail(RAVEL_E_INVALID, "blob too small");
+  BlobHeader h;
+  memcpy(&h, blob, sizeof h);
+  if (h.magic != kMagic || h.B != b->B || h.H != c.horizon || h.D != c.action_dim || h.L != c.layers ||
+      h.P != c.prefix_len || h.kvd != c.n_kv_heads * c.head_dim || h.dtype != c.dtype || h.kind != c.model_kind)
+    return fail(RAVEL_E_SHAPE, "checkpoint does not match this model/batch");
+  std::lock_guard<std::mutex> lk(b->mu);
+  HIP_TRY(hipDeviceSynchronize());
+  const char* p = (const char*)blob + sizeof h;
+  b->seed = h.seed;
+  HIP_TRY(hipMemcpy(b->t, &h.t, 8, hipMemcpyHostToDevice));
+  b->t_host = h.t;
+  HIP_TRY(hipMemcpy(b->t_obs, p, (size_t)b->B * 8, hipMemcpyHostToDevice));
+  memcpy(b->tobs_host.data(), p, (size_t)b->B * 8);
+  p += (size_t)b->B * 8;
+  for (int e = 0; e < b->B; ++e) {
+    memcpy(&b->active[e], p, 4);
+    memcpy(&b->has_ctx[e], p + 4, 4);
+    b->pending[e].valid = false;
+    b->retire_valid[e] = 0;
+    p += 8;
+  }
+  HIP_TRY(hipMemcpy(b->slot, b->active.data(), (size_t)b->B * 4, hipMemcpyHostToDevice));
+  HIP_TRY(hipMemcpy(b->X, p, xs, hipMemcpyHostToDevice));
+  p += xs;
+  for (int e = 0; e < b->B; ++e) {
+    const size_t off = ((size_t)b->active[e] * b->B + e) * cs;
+    if (cs) {
+      HIP_TRY(hipMemcpy((char*)b->ctx_k + off, p, cs, hipMemcpyHostToDevice));
+      HIP_TRY(hipMemcpy((char*)b->ctx_v + off, p + cs, cs, hipMemcpyHostToDevice));
+    }
+    p += 2 * cs;
+  }
+  // graphs bake in the seed as a kernel argument: rebuild them
+  for (auto& g : b->graphs) {
+    (void)hipGraphExecDestroy(g.exec);
+    (void)hipGraphDestroy(g.graph);
+  }
+  b->graphs.clear();
+  return RAVEL_OK;
+}
+
+ravel_status ravel_profile_step(ravel_buffer* b, const void* fop, float* action, void* stream,
+                                ravel_kernel_record* records, int32_t* n) {
+  if (!b || !action || !n) return fail(RAVEL_E_INVALID, "null argument");
+  ravel_model* m = b->m;
+  hipStream_t s = (hipStream_t)stream;
+  std::lock_guard<std::mutex> lk(b->mu);
+  if (m->cfg.model_kind == RAVEL_TRANSFORMER) {
+    RV_TRY(apply_publishes(b, s));
+    for (int e = 0; e < b->B; ++e)
+      if (!b->has_ctx[e]) return fail(RAVEL_E_STATE, "env " + std::to_string(e) + " has no context yet");
+  }
+  KernelRecorder rec;
+  rec.stream = s;
+  ravel_status st = enqueue_step(b, fop, action, s, &rec);
+  b->t_host += 1;
+  hipError_t he = hipStreamSynchronize(s);
+  const int32_t cap = *n;
+  int32_t k = 0;
+  for (auto& r : rec.recs) {
+    if (records && k < cap) {
+      ravel_kernel_record& o = records[k];
+      memset(&o, 0, sizeof o);
+      snprintf(o.name, sizeof o.name, "%s", r.name.c_str());
+      o.bytes = r.bytes;
+      o.flops = r.flops;
+      (void)hipEventElapsedTime(&o.ms, r.a, r.b);
+    }
+    ++k;
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  *n = records ? std::min(k, cap) : k;
+  if (st != RAVEL_OK) return st;
+  if (he != hipSuccess) return fail(RAVEL_E_HIP, hipGetErrorString(he));
+  return RAVEL_OK;
+}
+
+}  // extern "C"
