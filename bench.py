@@ -1,0 +1,312 @@
+"""Benchmark of the rolling denoise step on one MI355X.
+
+Default workload: the pi-style action expert at batch 1 (18 layers, width
+1024, 8 query heads / 1 KV head of 256, gated-GeLU MLP 4096, H = 50 slots of
+action dim 32, 816 prefix tokens per layer, 16 FOP tokens), bf16 weights and
+activations with fp32 accumulation, one context published at t = 0.  The
+same model at batch 64 (per-env contexts, staggered refresh every 5 steps)
+is measured too and reported under "batch64".
+
+One step = one ravel_step: the whole expert pass, Euler update, release and
+noise append for every env (one hipGraph replay).  Inputs (weights, contexts,
+FOP tokens) are resident in HBM before timing starts.
+
+Prints ONE JSON line.  Extra measurements:
+  * roofline   -- the dominant kernel class of the step (largest total time in
+                  an eagerly profiled step, HIP events around each launch on
+                  the step stream): algorithmic bytes (or flops) / time;
+  * step_roofline -- the whole step: algorithmic bytes per step / step time;
+  * cpu_baseline -- the numpy oracle (fp32) on a bounded sample of the same
+                  workload on the host cores.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "rolling denoise steps/s (batch-1 latency us, batch-64) + % HBM/MFMA roofline"
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=1000)
+    p.add_argument("--warmup", type=int, default=50)
+    p.add_argument("--workload", default="pi_b1", choices=["pi_b1", "pi_b64", "small_bf16", "large_b16", "tiny_fp32"])
+    p.add_argument("--no-batch64", action="store_true", help="skip the batch-64 secondary measurement")
+    p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--cpu-seconds", type=float, default=15.0)
+    p.add_argument("--profile-steps", type=int, default=3)
+    return p.parse_args()
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(s, batch) -> float:
+    """Bytes one step must move: every weight once plus each env's context and FOP tokens."""
+    import synth
+    elt = 2 if s.dtype == synth.workloads.BF16 else 4
+    n = 0
+    for name, shp in synth.weight_shapes(s, with_fop_encoder=False):
+        if name.startswith("time."):
+            continue  # flow-time conditioning is fixed per slot and precomputed
+        cnt = int(np.prod(shp))
+        if name == "final.mod.w":
+            cnt = cnt * 2 // 3  # the gate chunk of the final modulation is unused
+        if name == "final.mod.b":
+            cnt = cnt * 2 // 3
+        is_vec = len(shp) == 1 or name in ("delta.w1", "in.w")
+        n += cnt * (4 if is_vec else elt)
+    kvd = s.n_kv_heads * s.head_dim
+    n += batch * s.layers * s.prefix_len * kvd * 2 * elt  # prefix K and V
+    n += batch * s.n_fop * s.width * elt  # FOP tokens
+    n += batch * s.horizon * s.action_dim * 4 * 2  # ring read + write
+    return float(n)
+
+
+def algorithmic_flops(s, batch) -> float:
+    w, H, F = s.width, s.horizon, s.mlp_dim
+    qd, kvd = s.n_q_heads * s.head_dim, s.n_kv_heads * s.head_dim
+    M = batch * H
+    f = 2.0 * batch * w * w  # offset MLP
+    f += 2.0 * M * w * s.action_dim * 2  # in / out projections
+    per_layer = 2.0 * M * w * (6 * w + qd + 2 * kvd) + 2.0 * M * qd * w + 2.0 * M * w * 3 * F
+    per_layer += 4.0 * batch * s.n_q_heads * H * (s.prefix_len + H) * s.head_dim
+    f += s.layers * per_layer
+    n_ad = len(s.adapter_layers())
+    f += n_ad * (2.0 * M * w * qd * 2 + 2.0 * batch * s.n_fop * w * 2 * kvd
+                 + 4.0 * batch * s.n_q_heads * H * s.n_fop * s.head_dim)
+    f += 2.0 * M * w * 2 * w  # final modulation
+    return f
+
+
+class Workload:
+    def __init__(self, name, weights=None, seed=0):
+        import torch
+
+        import synth
+        from paper_2609_34170_amd import ravel
+        self.torch = torch
+        self.s = s = synth.get_config(name)
+        self.B = s.batch
+        t0 = time.time()
+        self.W = weights if weights is not None else synth.draw_weights(s, seed=seed)
+        log(f"[{name}] weights drawn in {time.time() - t0:.1f}s")
+        self.model = ravel.Model(s, self.W)
+        self.buf = ravel.Buffer(self.model, self.B, seed)
+        dev = torch.device("cuda:0")
+        tdt = torch.bfloat16 if s.dtype == synth.workloads.BF16 else torch.float32
+        self.stream = torch.cuda.current_stream()
+        # two context generations per env resident in HBM; refreshes alternate between them
+        self.ctx = []
+        for gen in range(2 if s.context_period > 0 else 1):
+            k = torch.empty((self.B, s.layers, s.prefix_len, s.n_kv_heads, s.head_dim), dtype=tdt, device=dev)
+            v = torch.empty_like(k)
+            for e in range(self.B):
+                kk, vv = synth.draw_context(s, seed, e, gen)
+                k[e].copy_(torch.from_numpy(kk))
+                v[e].copy_(torch.from_numpy(vv))
+            self.ctx.append((k, v))
+        self.fop = torch.from_numpy(synth.draw_fop_tokens(s, seed, 0)).to(dev).to(tdt).contiguous()
+        self.action = torch.zeros((self.B, s.action_dim), dtype=torch.float32, device=dev)
+        k, v = self.ctx[0]
+        for e in range(self.B):
+            self.buf.set_context(e, k[e], v[e], 0)
+        self.t = 0
+        self.gen = [0] * self.B
+        log(f"[{name}] ready in {time.time() - t0:.1f}s")
+
+    def refresh(self):
+        """Context refreshes of the workload's policy due before step self.t."""
+        s = self.s
+        if s.context_period <= 0 or self.t == 0:
+            return
+        for e in range(self.B):
+            phase = (self.t + e) if s.stagger else self.t
+            if phase % s.context_period == 0 and self.t >= s.context_period:
+                self.gen[e] ^= 1
+                k, v = self.ctx[self.gen[e]]
+                self.buf.set_context(e, k[e], v[e], self.t - s.context_period)
+
+    def step(self):
+        self.refresh()
+        self.buf.step(self.fop, self.action)
+        self.t += 1
+
+    def timed(self, steps, warmup):
+        torch = self.torch
+        for _ in range(warmup):
+            self.step()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        w0 = time.perf_counter()
+        e0.record(self.stream)
+        for _ in range(steps):
+            self.step()
+        e1.record(self.stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
+        return e0.elapsed_time(e1) / steps, wall
+
+    def latencies(self, n):
+        torch = self.torch
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        for a, b in ev:
+            a.record(self.stream)
+            self.step()
+            b.record(self.stream)
+        torch.cuda.synchronize()
+        return np.array([a.elapsed_time(b) for a, b in ev])
+
+    def profile(self, nsteps):
+        agg = {}
+        total = 0.0
+        for _ in range(nsteps):
+            self.refresh()
+            recs = self.buf.profile_step(self.fop, self.action)
+            self.t += 1
+            for name, by, fl, ms in recs:
+                cls = name.split(":")[0]
+                a = agg.setdefault(cls, [0, 0.0, 0.0, 0.0])
+                a[0] += 1
+                a[1] += by
+                a[2] += fl
+                a[3] += ms
+                total += ms
+        return agg, total / nsteps
+
+
+def roofline_of(agg, bound):
+    dom = max(agg.items(), key=lambda kv: kv[1][3])
+    name, (cnt, by, fl, ms) = dom
+    if bound == "hbm":
+        achieved = by / (ms * 1e-3) / 1e9
+        peak, unit = HBM_PEAK_GBS, "GB/s"
+    else:
+        achieved = fl / (ms * 1e-3) / 1e12
+        peak, unit = BF16_PEAK_TFLOPS, "TFLOP/s"
+    return {"kernel": name, "bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+            "frac": round(achieved / peak, 4), "traffic": None, "launches_per_step_x_steps": cnt,
+            "avg_launch_us": round(ms * 1e3 / cnt, 2)}
+
+
+def cpu_baseline(name, W, seconds):
+    import synth
+    from oracle.rolling import OracleRavel
+    s = synth.get_config(name)
+    envs = [0]
+    o = OracleRavel(s, W, batch=1, seed=0, dtype=np.float32, env_ids=envs)
+    k, v = synth.draw_context(s, 0, 0, 0)
+    o.set_context(0, k, v, 0)
+    z = synth.draw_fop_tokens(s, 0, 0)[:1]
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        o.step(z)
+        n += 1
+        el = time.perf_counter() - t0
+        if el > seconds or n >= 1000:
+            break
+    env_steps_per_s = n / el
+    try:
+        import threadpoolctl
+        info = threadpoolctl.threadpool_info()
+        cores = max([i.get("num_threads", 1) for i in info] + [1])
+    except Exception:
+        cores = os.cpu_count()
+    return {"value": round(env_steps_per_s / s.batch, 4), "unit": "steps/s", "cores": cores, "kind": "oracle",
+            "sample": f"{n} steps of env 0 of {name} with the float32 numpy oracle in {el:.1f}s "
+                      f"(steps/s = env-steps/s / batch {s.batch})"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+
+    import synth
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+
+    wl = Workload(args.workload)
+    s = wl.s
+    bound = "hbm" if wl.B == 1 else "mfma"
+    ms, wall = wl.timed(args.steps, args.warmup)
+    lat = wl.latencies(min(200, args.steps))
+    agg, prof_ms = wl.profile(args.profile_steps)
+    roof = roofline_of(agg, bound)
+    abytes = algorithmic_bytes(s, wl.B)
+    aflops = algorithmic_flops(s, wl.B)
+    step_roof = {
+        "bytes_per_step": abytes, "flops_per_step": aflops,
+        "hbm_GBs": round(abytes / (ms * 1e-3) / 1e9, 1),
+        "hbm_frac": round(abytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "mfma_TFLOPs": round(aflops / (ms * 1e-3) / 1e12, 1),
+        "mfma_frac": round(aflops / (ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+    }
+    out = {
+        "metric": METRIC,
+        "value": round(1000.0 / ms, 2),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "latency_us_p50": round(float(np.percentile(lat, 50)) * 1e3, 1),
+        "latency_us_p95": round(float(np.percentile(lat, 95)) * 1e3, 1),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if s.dtype == synth.workloads.BF16 else "f32",
+        "data": "synthetic (seeded N(0,0.02) weights, N(0,1) prefix KV and FOP tokens)",
+        "config": {"workload": s.name, "batch": wl.B, "layers": s.layers, "width": s.width,
+                   "heads": f"{s.n_q_heads}q/{s.n_kv_heads}kv x {s.head_dim}", "mlp": s.mlp_dim,
+                   "slots": s.horizon, "action_dim": s.action_dim, "prefix_tokens": s.prefix_len,
+                   "fop_tokens": s.n_fop, "parallelism": "single GPU"},
+        "roofline": roof,
+        "step_roofline": step_roof,
+        "profiled_step_ms_eager": round(prof_ms, 4),
+        "wall_s_timed": round(wall, 3),
+    }
+    log(f"[{s.name}] {1000.0 / ms:.1f} steps/s, {ms * 1e3:.1f} us/step")
+    W = wl.W
+    if not args.no_batch64 and args.workload == "pi_b1":
+        del wl
+        torch.cuda.synchronize()
+        w64 = Workload("pi_b64", weights=W)  # the same model at batch 64
+        s64 = w64.s
+        steps64 = max(10, min(200, args.steps // 5))
+        ms64, _ = w64.timed(steps64, 10)
+        agg64, _ = w64.profile(2)
+        out["batch64"] = {
+            "workload": "pi_b64", "steps": steps64, "ms_per_step": round(ms64, 4),
+            "steps_per_s": round(1000.0 / ms64, 2), "env_steps_per_s": round(64 * 1000.0 / ms64, 1),
+            "mfma_TFLOPs": round(algorithmic_flops(s64, 64) / (ms64 * 1e-3) / 1e12, 1),
+            "mfma_frac": round(algorithmic_flops(s64, 64) / (ms64 * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+            "roofline": roofline_of(agg64, "mfma"),
+        }
+        log(f"[pi_b64] {1000.0 / ms64:.1f} steps/s")
+        del w64
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(args.workload, W, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -215,7 +215,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   __threadfence();
   __syncthreads();
   if (tid == 0) {
-    unsigned prev = __hip_atomic_fetch_add(&a.counters[e * a.nq + j], 1u, __ATOMIC_ACQ_REL,
+    unsigned prev = __hip_atomic_fetch_add(&a.counters[(e * a.nq + j) * kCounterStride], 1u, __ATOMIC_ACQ_REL,
                                            __HIP_MEMORY_SCOPE_AGENT);
     s_last = (prev == (unsigned)(a.nsplit - 1));
   }
@@ -236,7 +236,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     }
     out[(size_t)(e * a.Hq + query) * a.ldo + j * HD + d] = f32_to_bf16(num / den);
   }
-  if (tid == 0) a.counters[e * a.nq + j] = 0u;
+  if (tid == 0) a.counters[(e * a.nq + j) * kCounterStride] = 0u;
 }
 
 template <int HD, int MAXQB>

@@ -180,7 +180,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
     __threadfence();
     __syncthreads();
     if (tid == 0) {
-      unsigned prev = __hip_atomic_fetch_add(&a.counters[tile], 1u, __ATOMIC_ACQ_REL,
+      unsigned prev = __hip_atomic_fetch_add(&a.counters[tile * kCounterStride], 1u, __ATOMIC_ACQ_REL,
                                              __HIP_MEMORY_SCOPE_AGENT);
       s_last = (prev == (unsigned)(a.ksplit - 1));
     }
@@ -202,7 +202,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
             acc[i][j][r] = s;
           }
         }
-    if (tid == 0) a.counters[tile] = 0u;
+    if (tid == 0) a.counters[tile * kCounterStride] = 0u;
   }
 
   if constexpr (TN % 2 == 0) {

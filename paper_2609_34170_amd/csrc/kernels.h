@@ -8,6 +8,13 @@
 
 namespace ravel {
 
+// Device-scope tickets (split-K tiles, attention key splits) are spaced one per
+// 256 bytes so that atomics of different tiles never share a cache line.
+#ifndef RAVEL_COUNTER_STRIDE
+#define RAVEL_COUNTER_STRIDE 64
+#endif
+constexpr int kCounterStride = RAVEL_COUNTER_STRIDE;
+
 // ---------------------------------------------------------------------------
 // GEMM  C[M,N] = A[M,K] . B[N,K]^T  (both operands K-contiguous), fp32 accumulate,
 // followed by a fused epilogue.

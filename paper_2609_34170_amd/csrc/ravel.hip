@@ -890,9 +890,9 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
     Arena wa;
     void* warena = nullptr;
     wa.want((void**)&tmp.gpart, part * 4);
-    wa.want((void**)&tmp.gcnt, (size_t)std::max(p1.tiles, 1) * 4);
+    wa.want((void**)&tmp.gcnt, (size_t)std::max(p1.tiles, 1) * 4 * kCounterStride);
     if ((st = wa.commit(&warena)) != RAVEL_OK) return bail(tdone(st));
-    (void)hipMemset(tmp.gcnt, 0, (size_t)std::max(p1.tiles, 1) * 4);
+    (void)hipMemset(tmp.gcnt, 0, (size_t)std::max(p1.tiles, 1) * 4 * kCounterStride);
     hipError_t he = m->bf16 ? launch_time_embedding<bf16_t>(H, w, (bf16_t*)emb, 0)
                             : launch_time_embedding<float>(H, w, (float*)emb, 0);
     if (he != hipSuccess) {
@@ -1010,10 +1010,10 @@ ravel_status ravel_buffer_create(ravel_model* m, int32_t batch, uint64_t seed, r
       ar.want((void**)&b->apart_o, (size_t)blocks * ns * Hp * c.head_dim * 4);
       ar.want((void**)&b->apart_ml, (size_t)blocks * ns * Hp * 2 * 4);
     }
-    ar.want((void**)&b->acnt, (size_t)blocks * 4);
+    ar.want((void**)&b->acnt, (size_t)blocks * 4 * kCounterStride);
   }
   ar.want((void**)&b->gpart, std::max<size_t>(part_elems, 1) * 4);
-  ar.want((void**)&b->gcnt, cnt * 4);
+  ar.want((void**)&b->gcnt, cnt * 4 * kCounterStride);
   ravel_status st = ar.commit(&b->arena);
   if (st != RAVEL_OK) {
     delete b;
