@@ -282,6 +282,8 @@ def main():
         "roofline": roof,
         "step_roofline": step_roof,
         "profiled_step_ms_eager": round(prof_ms, 4),
+        "kernel_classes_ms_per_step": {k: round(v[3] / args.profile_steps, 4) for k, v in
+                                       sorted(agg.items(), key=lambda kv: -kv[1][3])[:8]},
         "wall_s_timed": round(wall, 3),
     }
     log(f"[{s.name}] {1000.0 / ms:.1f} steps/s, {ms * 1e3:.1f} us/step")

@@ -70,30 +70,49 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   }
   const float sl2 = a.scale * kLog2e;
 
-  for (int k0 = kbeg; k0 < kend; k0 += TK) {
-    __syncthreads();
-    // K tile: TK rows x HD, 16-byte chunks
-    for (int c = tid; c < TK * (HD / 8); c += 256) {
+  // K/V tiles: loaded into registers one tile ahead, then written to LDS (V
+  // transposed) so that global latency overlaps the previous tile's MFMAs.
+  constexpr int KCH = (TK * (HD / 8) + 255) / 256;        // K chunks per thread
+  constexpr int VIT = ((TK / 4) * (HD / 8) + 255) / 256;  // V items (4 keys x 8 dims) per thread
+  u32x4_t kreg[KCH];
+  u32x4_t vreg[VIT][4];
+  auto load_tile = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = tid + i * 256;
       const int row = c / (HD / 8), dc = (c % (HD / 8)) * 8;
       const int kidx = k0 + row;
-      u32x4_t val = {0, 0, 0, 0};
-      if (kidx < kend) val = *(const u32x4_t*)(key_base(a, pk, sk, e, kidx, g, HD) + dc);
-      *(u32x4_t*)&Ks[row][dc] = val;
+      kreg[i] = u32x4_t{0, 0, 0, 0};
+      if (c < TK * (HD / 8) && kidx < kend) kreg[i] = *(const u32x4_t*)(key_base(a, pk, sk, e, kidx, g, HD) + dc);
     }
-    // V tile transposed: Vt[d][key]; item = (quad of keys, 8 dims)
-    for (int c = tid; c < (TK / 4) * (HD / 8); c += 256) {
+#pragma unroll
+    for (int it = 0; it < VIT; ++it) {
+      const int c = tid + it * 256;
       const int kq = c / (HD / 8), dc = (c % (HD / 8)) * 8;
-      u32x4_t r4[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int kidx = k0 + kq * 4 + i;
-        r4[i] = u32x4_t{0, 0, 0, 0};
-        if (kidx < kend) r4[i] = *(const u32x4_t*)(key_base(a, pv, sv, e, kidx, g, HD) + dc);
+        vreg[it][i] = u32x4_t{0, 0, 0, 0};
+        if (c < (TK / 4) * (HD / 8) && kidx < kend)
+          vreg[it][i] = *(const u32x4_t*)(key_base(a, pv, sv, e, kidx, g, HD) + dc);
       }
-      const bf16_t* h0 = (const bf16_t*)&r4[0];
-      const bf16_t* h1 = (const bf16_t*)&r4[1];
-      const bf16_t* h2 = (const bf16_t*)&r4[2];
-      const bf16_t* h3 = (const bf16_t*)&r4[3];
+    }
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = tid + i * 256;
+      if (c < TK * (HD / 8)) *(u32x4_t*)&Ks[c / (HD / 8)][(c % (HD / 8)) * 8] = kreg[i];
+    }
+#pragma unroll
+    for (int it = 0; it < VIT; ++it) {
+      const int c = tid + it * 256;
+      if (c >= (TK / 4) * (HD / 8)) continue;
+      const int kq = c / (HD / 8), dc = (c % (HD / 8)) * 8;
+      const bf16_t* h0 = (const bf16_t*)&vreg[it][0];
+      const bf16_t* h1 = (const bf16_t*)&vreg[it][1];
+      const bf16_t* h2 = (const bf16_t*)&vreg[it][2];
+      const bf16_t* h3 = (const bf16_t*)&vreg[it][3];
 #pragma unroll
       for (int dd = 0; dd < 8; ++dd) {
         u32x2_t w;
@@ -102,7 +121,14 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
         *(u32x2_t*)&Vt[dc + dd][kq * 4] = w;
       }
     }
+  };
+
+  if (kbeg < kend) load_tile(kbeg);
+  for (int k0 = kbeg; k0 < kend; k0 += TK) {
     __syncthreads();
+    store_tile();
+    __syncthreads();
+    if (k0 + TK < kend) load_tile(k0 + TK);
 
 #pragma unroll
     for (int qi = 0; qi < MAXQB; ++qi) {
@@ -206,37 +232,48 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     if (qb >= QB) continue;
     float* po = a.part_o + (pidx * Hp + query) * HD;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) *(f32x4_t*)(po + dt * 16 + grp * 4) = o[qi][dt];
+    for (int dt = 0; dt < DT; ++dt) coherent_store4(po + dt * 16 + grp * 4, o[qi][dt]);
     if (grp == 0) {
-      a.part_ml[(pidx * Hp + query) * 2 + 0] = mrow[qi];
-      a.part_ml[(pidx * Hp + query) * 2 + 1] = lrow[qi];
+      coherent_store(&a.part_ml[(pidx * Hp + query) * 2 + 0], mrow[qi]);
+      coherent_store(&a.part_ml[(pidx * Hp + query) * 2 + 1], lrow[qi]);
     }
   }
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    unsigned prev = __hip_atomic_fetch_add(&a.counters[(e * a.nq + j) * kCounterStride], 1u, __ATOMIC_ACQ_REL,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-    s_last = (prev == (unsigned)(a.nsplit - 1));
-  }
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
+  if (!last_block_arrival(&a.counters[(e * a.nq + j) * kCounterStride], (unsigned)a.nsplit, &s_last)) return;
+  // merge the key splits in fixed order: softmax weights of every (split, query)
+  // first (into LDS, reusing the K tile), then each thread owns 4 dims of a query
   const size_t pbase = ((size_t)e * a.nq + j) * a.nsplit;
-  for (int idx = tid; idx < a.Hq * HD; idx += 256) {
-    const int query = idx / HD, d = idx % HD;
+  float* wgt = reinterpret_cast<float*>(&Ks[0][0]);  // [nsplit][Hq] (fits: nsplit*Hq <= TK*(HD+8)/2)
+  for (int query = tid; query < a.Hq; query += 256) {
     float mmax = -INFINITY;
     for (int sp = 0; sp < a.nsplit; ++sp) mmax = fmaxf(mmax, a.part_ml[((pbase + sp) * Hp + query) * 2]);
-    float num = 0.f, den = 0.f;
+    float den = 0.f;
     for (int sp = 0; sp < a.nsplit; ++sp) {
       const float ms = a.part_ml[((pbase + sp) * Hp + query) * 2];
-      const float w = (ms == -INFINITY) ? 0.f : exp2f(ms - mmax);
-      num += w * a.part_o[((pbase + sp) * Hp + query) * HD + d];
-      den += w * a.part_ml[((pbase + sp) * Hp + query) * 2 + 1];
+      const float wv = (ms == -INFINITY) ? 0.f : exp2f(ms - mmax);
+      wgt[sp * a.Hq + query] = wv;
+      den += wv * a.part_ml[((pbase + sp) * Hp + query) * 2 + 1];
     }
-    out[(size_t)(e * a.Hq + query) * a.ldo + j * HD + d] = f32_to_bf16(num / den);
+    const float inv = 1.f / den;
+    for (int sp = 0; sp < a.nsplit; ++sp) wgt[sp * a.Hq + query] *= inv;
   }
-  if (tid == 0) a.counters[(e * a.nq + j) * kCounterStride] = 0u;
+  __syncthreads();
+  for (int idx = tid; idx < a.Hq * (HD / 4); idx += 256) {
+    const int query = idx / (HD / 4), d = (idx % (HD / 4)) * 4;
+    f32x4_t num = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+    for (int sp = 0; sp < a.nsplit; ++sp) {
+      const float wv = wgt[sp * a.Hq + query];
+      const f32x4_t os = *(const f32x4_t*)&a.part_o[((pbase + sp) * Hp + query) * HD + d];
+      num[0] += wv * os[0];
+      num[1] += wv * os[1];
+      num[2] += wv * os[2];
+      num[3] += wv * os[3];
+    }
+    u32x2_t wv;
+    wv[0] = (uint32_t)f32_to_bf16(num[0]) | ((uint32_t)f32_to_bf16(num[1]) << 16);
+    wv[1] = (uint32_t)f32_to_bf16(num[2]) | ((uint32_t)f32_to_bf16(num[3]) << 16);
+    *(u32x2_t*)(out + (size_t)(e * a.Hq + query) * a.ldo + j * HD + d) = wv;
+  }
 }
 
 template <int HD, int MAXQB>
@@ -249,6 +286,8 @@ static hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s) {
   const int QB = (a.Hq + 15) / 16;
   if (QB > 8) return hipErrorInvalidValue;
+  // the split merge keeps nsplit x Hq weights in the K tile's LDS (32 x (hd + 8) bf16)
+  if (a.nsplit > 1 && a.nsplit * a.Hq > 32 * (a.hd + 8) / 2) return hipErrorInvalidValue;
   const bool two = QB > 4;
   switch (a.hd) {
     case 32: return two ? launch_hd<32, 2>(a, s) : launch_hd<32, 1>(a, s);

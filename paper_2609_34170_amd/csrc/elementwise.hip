@@ -186,53 +186,47 @@ RAVEL_DEV float euler_sub(float x, float dt, float v) {
   return x - step;
 }
 
-__global__ __launch_bounds__(64) void euler_release_kernel(float* __restrict__ X, const float* __restrict__ v,
-                                                           int64_t* t, int B, int H, int D, uint64_t seed,
-                                                           float* __restrict__ action, unsigned* ticket) {
-  __shared__ int s_last;
+// One block: every thread first applies the Euler update to independent ring
+// elements (memory-level parallel), then the released slot is copied out and
+// refilled with noise, then t advances.  A single block makes the read of t
+// and its increment ordered by block barriers alone.
+__global__ __launch_bounds__(1024) void euler_release_kernel(float* __restrict__ X, const float* __restrict__ v,
+                                                             int64_t* t, int B, int H, int D, uint64_t seed,
+                                                             float* __restrict__ action) {
   const int64_t tt = *t;
+  const float dt = 1.0f / (float)H;
+  const int h0 = (int)(tt % H);
+  const int total = B * H * D;
+  for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
+    const int d = idx % D, i = (idx / D) % H, e = idx / (D * H);  // logical slot i
+    int ph = h0 + i;
+    if (ph >= H) ph -= H;
+    float* xp = X + ((size_t)e * H + ph) * D + d;
+    *xp = euler_sub(*xp, dt, v[idx]);
+  }
+  __syncthreads();
   const int NG = (D + 3) / 4;
-  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx < B * NG) {
+  for (int idx = threadIdx.x; idx < B * NG; idx += blockDim.x) {
     const int e = idx / NG, c = idx % NG;
-    const float dt = 1.0f / (float)H;
-    const int h0 = (int)(tt % H);
-    float* Xe = X + (size_t)e * H * D;
-    const float* ve = v + (size_t)e * H * D;
-    for (int q = 0; q < 4; ++q) {
-      const int d = c * 4 + q;
-      if (d >= D) break;
-      for (int i = 0; i < H; ++i) {
-        int ph = h0 + i;
-        if (ph >= H) ph -= H;
-        Xe[(size_t)ph * D + d] = euler_sub(Xe[(size_t)ph * D + d], dt, ve[(size_t)i * D + d]);
-      }
-      action[(size_t)e * D + d] = Xe[(size_t)h0 * D + d];
-    }
+    float* xs = X + ((size_t)e * H + h0) * D;
     float z[4];
     ring_noise4(seed, e, tt + H, c, z);
     for (int q = 0; q < 4; ++q) {
       const int d = c * 4 + q;
-      if (d < D) Xe[(size_t)h0 * D + d] = z[q];
+      if (d < D) {
+        action[(size_t)e * D + d] = xs[d];
+        xs[d] = z[q];
+      }
     }
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    const unsigned prev = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    s_last = (prev == gridDim.x - 1);
-  }
-  __syncthreads();
-  if (s_last && threadIdx.x == 0) {
-    *t = tt + 1;
-    *ticket = 0u;
-  }
+  if (threadIdx.x == 0) *t = tt + 1;
 }
 
 hipError_t launch_euler_release(float* X, const float* v, int64_t* t, int B, int H, int D, uint64_t seed,
                                 float* action, unsigned* ticket, hipStream_t s) {
-  const int n = B * ((D + 3) / 4);
-  hipLaunchKernelGGL(euler_release_kernel, dim3((n + 63) / 64), dim3(64), 0, s, X, v, t, B, H, D, seed,
-                     action, ticket);
+  (void)ticket;
+  hipLaunchKernelGGL(euler_release_kernel, dim3(1), dim3(1024), 0, s, X, v, t, B, H, D, seed, action);
   return hipGetLastError();
 }
 

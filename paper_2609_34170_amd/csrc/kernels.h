@@ -37,7 +37,7 @@ struct GemmArgs {
   int M, N, K;
   int ksplit;          // number of K ranges (grid.z); 1 = no split
   int kchunk;          // K elements per range (multiple of 64)
-  float* partial;      // [ksplit][M][N] fp32 workspace (ksplit > 1)
+  float* partial;      // split-K workspace: ksplit x tiles x tile elements, fp32
   unsigned* counters;  // one per output tile, zero; the reducing block re-zeroes it
   int mode;
   const float* bias;
@@ -52,6 +52,9 @@ struct GemmArgs {
 enum GemmTile { TILE_64x64 = 0, TILE_128x128 = 1, TILE_64x128 = 2, TILE_128x64 = 3, TILE_32x64 = 4 };
 
 hipError_t launch_gemm_bf16(const GemmArgs& a, int tile, hipStream_t s);
+// M <= 64 weight-streaming kernel: block columns 64*nfr (nfr 1 or 2, 2 for EPI_GEGLU),
+// K range per block kchunk in {128, 256, 512} (1024 with nfr 1), ksplit ranges (grid.y).
+hipError_t launch_gemm_skinny(const GemmArgs& a, int nfr, hipStream_t s);
 hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------------------

@@ -114,6 +114,8 @@ struct ravel_model {
   float* fmod_b = nullptr;
   void* out_w = nullptr;
   float* out_b = nullptr;
+  void* mod_all_w = nullptr;   // [(6L + 2) w, w]: every layer's modulation rows, then the final norm's
+  float* mod_all_b = nullptr;  // [(6L + 2) w]
   bool has_fop_encoder = false;
   void* f_w1 = nullptr;
   float* f_b1 = nullptr;
@@ -212,34 +214,53 @@ ravel_status upload_all(const ravel_tensor* t, bool to_bf16, void* dst, const St
 
 // GEMM dispatch ---------------------------------------------------------------
 struct GemmPlan {
-  int tile;
+  bool skinny;
+  int nfr;     // skinny: 16-column fragments per wave
+  int tile;    // tiled: GemmTile
   int ksplit;
   int kchunk;
   int tiles;
+  size_t part_elems;  // split-K workspace (floats)
 };
 
 GemmPlan plan_gemm(int M, int N, int K, bool geglu) {
   GemmPlan p;
+  memset(&p, 0, sizeof p);
+  if (M <= 64) {
+    // weight streaming: aim for >= 256 blocks, the largest K range that reaches it,
+    // at most 16 split-K ranges
+    p.skinny = true;
+    p.nfr = geglu ? 2 : 1;
+    p.tiles = (N + 64 * p.nfr - 1) / (64 * p.nfr);
+    if (p.nfr == 1 && K <= 1024 && p.tiles >= 512) {
+      p.kchunk = K <= 128 ? 128 : K <= 256 ? 256 : K <= 512 ? 512 : 1024;
+    } else {
+      for (int kc : {512, 256, 128}) {
+        p.kchunk = kc;
+        if ((long)p.tiles * ((K + kc - 1) / kc) >= 256) break;
+      }
+      while ((K + p.kchunk - 1) / p.kchunk > 16 && p.kchunk < 512) p.kchunk *= 2;
+    }
+    p.ksplit = (K + p.kchunk - 1) / p.kchunk;
+    const size_t tile_elems = (size_t)((M + 15) / 16) * 16 * 64 * p.nfr;
+    p.part_elems = p.ksplit > 1 ? (size_t)p.ksplit * p.tiles * tile_elems : 0;
+    return p;
+  }
   int bm, bn;
-  if (M <= 32 && !geglu) {
-    p.tile = TILE_32x64; bm = 32; bn = 64;
-  } else if (M <= 64) {
-    p.tile = TILE_64x64; bm = 64; bn = 64;
-  } else if (M <= 256) {
+  if (M <= 256) {
     p.tile = TILE_64x128; bm = 64; bn = 128;
   } else {
     p.tile = TILE_128x128; bm = 128; bn = 128;
   }
   p.tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
-  // split K until the grid has about 2 blocks per CU, keeping >= 128 K per range
+  // split K until the grid has about 2 blocks per CU, keeping >= 256 K per range
   int ks = 1;
-  const int target = 512;
-  while (p.tiles * ks * 2 <= target && (K / (ks * 2)) >= 128 && ks < 64) ks *= 2;
+  while (p.tiles * ks * 2 <= 512 && (K / (ks * 2)) >= 256 && ks < 16) ks *= 2;
   int kchunk = (K + ks - 1) / ks;
   kchunk = (kchunk + 63) / 64 * 64;
-  ks = (K + kchunk - 1) / kchunk;
-  p.ksplit = ks;
+  p.ksplit = (K + kchunk - 1) / kchunk;
   p.kchunk = kchunk;
+  p.part_elems = p.ksplit > 1 ? (size_t)p.ksplit * p.tiles * bm * bn : 0;
   return p;
 }
 
@@ -292,11 +313,15 @@ struct ravel_buffer {
   void* obs_t = nullptr;
   float* gpart = nullptr;
   unsigned* gcnt = nullptr;
+  size_t gpart_elems = 0;
+  int gcnt_n = 0;
   float* apart_o = nullptr;
   float* apart_ml = nullptr;
   unsigned* acnt = nullptr;
   int* dbg_flag = nullptr;
   int attn_nsplit = 1, attn_kps = 0;
+  bool mod_all = false;
+  int mod_ld = 0;
   // host
   int64_t t_host = 0;
   std::vector<int> active;
@@ -347,11 +372,21 @@ ravel_status run_gemm(ravel_buffer* b, hipStream_t s, KernelRecorder* rec, const
   epi.kchunk = p.kchunk;
   epi.partial = b->gpart;
   epi.counters = b->gcnt;
+  if (p.part_elems > b->gpart_elems || p.tiles > b->gcnt_n)
+    return fail(RAVEL_E_STATE, std::string(name) + ": GEMM workspace too small");
   if (rec) {
     static const char* tn[] = {"64x64", "128x128", "64x128", "128x64", "32x64"};
     char full[48];
-    snprintf(full, sizeof full, "gemm%s:%s", tn[p.tile], name);
+    if (p.skinny)
+      snprintf(full, sizeof full, "gemm_stream:%s", name);
+    else
+      snprintf(full, sizeof full, "gemm%s:%s", tn[p.tile], name);
     rec->begin(full, bytes, flops);
+  }
+  if (p.skinny) {
+    HIP_TRY(launch_gemm_skinny(epi, p.nfr, s));
+    if (rec) rec->end();
+    return RAVEL_OK;
   }
   HIP_TRY(launch_gemm_bf16(epi, p.tile, s));
   if (rec) rec->end();
@@ -441,18 +476,27 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
     RV_TRY(run_gemm<T>(b, s, rec, "fop_kv", fop, w, m->kva_w, w, B * c.n_fop, m->n_ad * 2 * kvd, w, e));
   }
   const size_t ctx_layer = (size_t)c.prefix_len * kvd;
+  const int ldm = b->mod_ld;
+  if (b->mod_all) {
+    // modulation chunks (s1, b1, g1, s2, b2, g2) of every layer and (s_f, b_f) at once
+    GemmArgs e = epi_args(EPI_F32);
+    e.bias = m->mod_all_b;
+    e.out_f = b->mod;
+    e.ldo_f = ldm;
+    RV_TRY(run_gemm<T>(b, s, rec, "mod_all", b->cond, w, m->mod_all_w, w, BH, ldm, w, e));
+  }
   for (int l = 0; l < c.layers; ++l) {
     const LayerW& L = m->layers[l];
-    // modulation chunks (s1, b1, g1, s2, b2, g2)
-    {
+    const float* mod = b->mod_all ? b->mod + (size_t)l * 6 * w : b->mod;
+    if (!b->mod_all) {
       GemmArgs e = epi_args(EPI_F32);
       e.bias = L.mod_b;
       e.out_f = b->mod;
-      e.ldo_f = 6 * w;
+      e.ldo_f = ldm;
       RV_TRY(run_gemm<T>(b, s, rec, "mod", b->cond, w, L.mod_w, w, BH, 6 * w, w, e));
     }
     REC_BEGIN("adarms", (double)BH * w * (12 + elt), (double)BH * w * 5);
-    HIP_TRY(launch_adarms<T>(b->x, w, BH, w, b->mod, b->mod + w, 6 * w, 0, c.rms_eps, (T*)b->y, w, s));
+    HIP_TRY(launch_adarms<T>(b->x, w, BH, w, mod, mod + w, ldm, 0, c.rms_eps, (T*)b->y, w, s));
     REC_END();
     {
       GemmArgs e = epi_args(EPI_T);
@@ -485,8 +529,8 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
       GemmArgs e = epi_args(EPI_RESID);
       e.out_f = b->x;
       e.ldo_f = w;
-      e.gate = b->mod + 2 * w;
-      e.ldg = 6 * w;
+      e.gate = mod + 2 * w;
+      e.ldg = ldm;
       RV_TRY(run_gemm<T>(b, s, rec, "o", b->att, qd, L.o_w, qd, BH, w, qd, e));
     }
     if (L.adapter >= 0 && fop) {
@@ -530,7 +574,7 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
       }
     }
     REC_BEGIN("adarms", (double)BH * w * (12 + elt), (double)BH * w * 5);
-    HIP_TRY(launch_adarms<T>(b->x, w, BH, w, b->mod + 3 * w, b->mod + 4 * w, 6 * w, 0, c.rms_eps, (T*)b->y, w, s));
+    HIP_TRY(launch_adarms<T>(b->x, w, BH, w, mod + 3 * w, mod + 4 * w, ldm, 0, c.rms_eps, (T*)b->y, w, s));
     REC_END();
     {
       GemmArgs e = epi_args(EPI_GEGLU);
@@ -542,13 +586,15 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
       GemmArgs e = epi_args(EPI_RESID);
       e.out_f = b->x;
       e.ldo_f = w;
-      e.gate = b->mod + 5 * w;
-      e.ldg = 6 * w;
+      e.gate = mod + 5 * w;
+      e.ldg = ldm;
       RV_TRY(run_gemm<T>(b, s, rec, "down", b->u, F, L.down_w, F, BH, w, F, e));
     }
   }
   // final adaptive norm and output head
-  {
+  const float* fmod = b->mod_all ? b->mod + (size_t)c.layers * 6 * w : b->fmod;
+  const int ldf = b->mod_all ? ldm : 2 * w;
+  if (!b->mod_all) {
     GemmArgs e = epi_args(EPI_F32);
     e.bias = m->fmod_b;
     e.out_f = b->fmod;
@@ -556,7 +602,7 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
     RV_TRY(run_gemm<T>(b, s, rec, "final_mod", b->cond, w, m->fmod_w, w, BH, 2 * w, w, e));
   }
   REC_BEGIN("adarms", (double)BH * w * (12 + elt), (double)BH * w * 5);
-  HIP_TRY(launch_adarms<T>(b->x, w, BH, w, b->fmod, b->fmod + w, 2 * w, 0, c.rms_eps, (T*)b->y, w, s));
+  HIP_TRY(launch_adarms<T>(b->x, w, BH, w, fmod, fmod + w, ldf, 0, c.rms_eps, (T*)b->y, w, s));
   REC_END();
   {
     GemmArgs e = epi_args(EPI_F32);
@@ -757,10 +803,10 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
   ar.want((void**)&m->d_b1, (size_t)w * 4);
   ar.want((void**)&m->d_w2, (size_t)w * w * E);
   ar.want((void**)&m->d_b2, (size_t)w * 4);
+  ar.want(&m->mod_all_w, (size_t)(6 * L + 2) * w * w * E);
+  ar.want((void**)&m->mod_all_b, (size_t)(6 * L + 2) * w * 4);
   for (int l = 0; l < L; ++l) {
     LayerW& Lw = m->layers[l];
-    ar.want(&Lw.mod_w, (size_t)6 * w * w * E);
-    ar.want((void**)&Lw.mod_b, (size_t)6 * w * 4);
     ar.want(&Lw.qkv_w, (size_t)qkvd * w * E);
     ar.want(&Lw.o_w, (size_t)w * qd * E);
     ar.want(&Lw.gu_w, (size_t)2 * F * w * E);
@@ -774,8 +820,6 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
     }
   }
   if (n_ad > 0) ar.want(&m->kva_w, (size_t)n_ad * 2 * kvd * w * E);
-  ar.want(&m->fmod_w, (size_t)2 * w * w * E);
-  ar.want((void**)&m->fmod_b, (size_t)2 * w * 4);
   ar.want(&m->out_w, (size_t)D * w * E);
   ar.want((void**)&m->out_b, (size_t)D * 4);
   if (m->has_fop_encoder) {
@@ -786,6 +830,12 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
   }
   m->arena_bytes = ar.off;
   if ((st = ar.commit(&m->arena)) != RAVEL_OK) return bail(st);
+  for (int l = 0; l < L; ++l) {
+    m->layers[l].mod_w = (char*)m->mod_all_w + (size_t)l * 6 * w * w * E;
+    m->layers[l].mod_b = m->mod_all_b + (size_t)l * 6 * w;
+  }
+  m->fmod_w = (char*)m->mod_all_w + (size_t)L * 6 * w * w * E;
+  m->fmod_b = m->mod_all_b + (size_t)L * 6 * w;
 
   // staging (fp32 + converted bf16) for uploads
   Staging stg;
@@ -886,7 +936,9 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
     tmp.m = m;
     tmp.B = 1;
     const GemmPlan p1 = plan_gemm(H, w, w, false);
-    const size_t part = (size_t)p1.ksplit * H * w;
+    const size_t part = std::max<size_t>(p1.part_elems, 1);
+    tmp.gpart_elems = p1.part_elems;
+    tmp.gcnt_n = std::max(p1.tiles, 1);
     Arena wa;
     void* warena = nullptr;
     wa.want((void**)&tmp.gpart, part * 4);
@@ -970,7 +1022,10 @@ ravel_status ravel_buffer_create(ravel_model* m, int32_t batch, uint64_t seed, r
     ar.want((void**)&b->x, (size_t)BH * w * 4);
     ar.want(&b->cond, (size_t)BH * w * E);
     ar.want(&b->h1, (size_t)B * w * E);
-    ar.want((void**)&b->mod, (size_t)BH * 6 * w * 4);
+    // few rows: every layer's modulation comes from one GEMM at the start of the step
+    b->mod_all = BH <= 64;
+    b->mod_ld = b->mod_all ? (6 * c.layers + 2) * w : 6 * w;
+    ar.want((void**)&b->mod, (size_t)BH * b->mod_ld * 4);
     ar.want(&b->y, (size_t)BH * w * E);
     ar.want(&b->qkv, (size_t)BH * qkvd * E);
     ar.want(&b->att, (size_t)BH * qd * E);
@@ -982,7 +1037,8 @@ ravel_status ravel_buffer_create(ravel_model* m, int32_t batch, uint64_t seed, r
     ar.want(&b->obs_t, (size_t)B * std::max(c.fop_obs_dim, 1) * E);
     // GEMM split-K workspace: the largest plan of the step
     struct Shape { int M, N, K; bool geglu; };
-    std::vector<Shape> shapes = {{B, w, w, false}, {BH, 6 * w, w, false}, {BH, qkvd, w, false},
+    std::vector<Shape> shapes = {{B, w, w, false}, {BH, 6 * w, w, false}, {BH, (6 * c.layers + 2) * w, w, false},
+                                 {BH, qkvd, w, false},
                                  {BH, w, qd, false}, {BH, qd, w, false}, {BH, 2 * F, w, true},
                                  {BH, w, F, false}, {BH, 2 * w, w, false}, {BH, D, w, false},
                                  {B, w, std::max(c.fop_obs_dim, 8), false}, {B, c.n_fop * w, w, false}};
@@ -990,16 +1046,19 @@ ravel_status ravel_buffer_create(ravel_model* m, int32_t batch, uint64_t seed, r
     for (auto& s : shapes) {
       if (s.N <= 0 || s.M <= 0) continue;
       const GemmPlan p = plan_gemm(s.M, s.N, s.K, s.geglu);
-      if (p.ksplit > 1) part_elems = std::max(part_elems, (size_t)p.ksplit * s.M * s.N);
+      part_elems = std::max(part_elems, p.part_elems);
       cnt = std::max(cnt, (size_t)p.tiles);
     }
     // attention key split: aim for ~256 blocks when B * nq is small, >= 64 keys per split
     const int nkeys = c.prefix_len + H;
     const int blocks = B * c.n_q_heads;
     int ns = 1;
-    if (m->bf16 && blocks < 256) {
-      ns = std::min((nkeys + 63) / 64, (256 + blocks - 1) / blocks);
-      ns = std::max(ns, 1);
+    if (m->bf16 && blocks < 64) {
+      // a few blocks per CU-group at batch 1: split keys, >= 128 keys per split; the
+      // merge keeps nsplit x H softmax weights in the 32-key tile's LDS
+      ns = std::min((nkeys + 127) / 128, (64 + blocks - 1) / blocks);
+      const int cap = 32 * (c.head_dim + 8) / 2 / H;
+      ns = std::max(1, std::min(ns, cap));
     }
     int kps = ((nkeys + ns - 1) / ns + 31) / 32 * 32;
     ns = (nkeys + kps - 1) / kps;
@@ -1014,6 +1073,8 @@ ravel_status ravel_buffer_create(ravel_model* m, int32_t batch, uint64_t seed, r
   }
   ar.want((void**)&b->gpart, std::max<size_t>(part_elems, 1) * 4);
   ar.want((void**)&b->gcnt, cnt * 4 * kCounterStride);
+  b->gpart_elems = part_elems;
+  b->gcnt_n = (int)cnt;
   ravel_status st = ar.commit(&b->arena);
   if (st != RAVEL_OK) {
     delete b;
