@@ -14,49 +14,147 @@
 
 namespace ravel {
 
-template <typename T>
-RAVEL_DEV void epi_store(const GemmArgs& a, int m, int n, float acc) {
+// Epilogues.  Every MFMA result fragment here holds 4 consecutive output columns
+// n .. n+3 of one row m per lane; epilogues are specialised by mode so that the
+// fully unrolled fragment loops stay small (a large inlined switch there makes
+// the compiler keep the accumulators in scratch memory).
+template <int MODE, typename T>
+RAVEL_DEV void epi1(const GemmArgs& a, int m, int n, float acc) {
   const float b = a.bias ? a.bias[n] : 0.0f;
-  switch (a.mode) {
-    case EPI_F32:
-      a.out_f[(size_t)m * a.ldo_f + n] = acc + b;
-      break;
-    case EPI_T:
-      ((T*)a.out_t)[(size_t)m * a.ldo_t + n] = act<T>::from_f(acc + b);
-      break;
-    case EPI_RESID: {
-      const float g = a.gate ? a.gate[(size_t)m * a.ldg + n] : 1.0f;
-      float* o = a.out_f + (size_t)m * a.ldo_f + n;
-      *o = *o + g * acc;
-      break;
-    }
-    case EPI_RESID_TANH: {
-      const float g = tanhf(*a.gate_scalar);
-      float* o = a.out_f + (size_t)m * a.ldo_f + n;
-      *o = *o + g * acc;
-      break;
-    }
-    case EPI_COND: {
-      const float base = acc + b;
-      for (int i = 0; i < a.H; ++i)
-        ((T*)a.out_t)[((size_t)m * a.H + i) * a.ldo_t + n] =
-            act<T>::from_f(silu_f(a.ctau[(size_t)i * a.N + n] + base));
-      break;
-    }
-    case EPI_GELU_T:
-      ((T*)a.out_t)[(size_t)m * a.ldo_t + n] = act<T>::from_f(gelu_tanh_f(acc + b));
-      break;
-    case EPI_SILU_T:
-      ((T*)a.out_t)[(size_t)m * a.ldo_t + n] = act<T>::from_f(silu_f(acc + b));
-      break;
-    default:
-      break;
+  if constexpr (MODE == EPI_F32) {
+    a.out_f[(size_t)m * a.ldo_f + n] = acc + b;
+  } else if constexpr (MODE == EPI_T) {
+    ((T*)a.out_t)[(size_t)m * a.ldo_t + n] = act<T>::from_f(acc + b);
+  } else if constexpr (MODE == EPI_RESID) {
+    const float g = a.gate ? a.gate[(size_t)m * a.ldg + n] : 1.0f;
+    float* o = a.out_f + (size_t)m * a.ldo_f + n;
+    *o = *o + g * acc;
+  } else if constexpr (MODE == EPI_RESID_TANH) {
+    float* o = a.out_f + (size_t)m * a.ldo_f + n;
+    *o = *o + tanhf(*a.gate_scalar) * acc;
+  } else if constexpr (MODE == EPI_COND) {
+    const float base = acc + b;
+    for (int i = 0; i < a.H; ++i)
+      ((T*)a.out_t)[((size_t)m * a.H + i) * a.ldo_t + n] = act<T>::from_f(silu_f(a.ctau[(size_t)i * a.N + n] + base));
+  } else if constexpr (MODE == EPI_GELU_T) {
+    ((T*)a.out_t)[(size_t)m * a.ldo_t + n] = act<T>::from_f(gelu_tanh_f(acc + b));
+  } else if constexpr (MODE == EPI_SILU_T) {
+    ((T*)a.out_t)[(size_t)m * a.ldo_t + n] = act<T>::from_f(silu_f(acc + b));
   }
 }
 
-template <typename T>
-RAVEL_DEV void epi_geglu(const GemmArgs& a, int m, int f, float g, float u) {
-  ((T*)a.out_t)[(size_t)m * a.ldo_t + f] = act<T>::from_f(gelu_tanh_f(g) * u);
+// Whether the 4-column vector path applies to this launch (row strides aligned).
+RAVEL_DEV bool epi_vec_ok(const GemmArgs& a) {
+  switch (a.mode) {
+    case EPI_F32: return (a.ldo_f % 4) == 0;
+    case EPI_RESID: return (a.ldo_f % 4) == 0 && (!a.gate || (a.ldg % 4) == 0);
+    case EPI_RESID_TANH: return (a.ldo_f % 4) == 0;
+    case EPI_T:
+    case EPI_GELU_T:
+    case EPI_SILU_T: return (a.ldo_t % 4) == 0;
+    case EPI_COND: return (a.ldo_t % 4) == 0 && (a.N % 4) == 0;
+    default: return true;
+  }
+}
+
+RAVEL_DEV void store_bf16x4(bf16_t* p, float v0, float v1, float v2, float v3) {
+  u32x2_t w;
+  w[0] = (uint32_t)f32_to_bf16(v0) | ((uint32_t)f32_to_bf16(v1) << 16);
+  w[1] = (uint32_t)f32_to_bf16(v2) | ((uint32_t)f32_to_bf16(v3) << 16);
+  *(u32x2_t*)p = w;
+}
+
+// bf16 activations; fp32 outputs are written as float4.
+template <int MODE>
+RAVEL_DEV void epi4(const GemmArgs& a, int m, int n, f32x4_t v, bool vec) {
+  if (!(vec && n + 4 <= a.N)) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (n + r < a.N) epi1<MODE, bf16_t>(a, m, n + r, v[r]);
+    return;
+  }
+  f32x4_t b = {0.f, 0.f, 0.f, 0.f};
+  if (a.bias) b = *(const f32x4_t*)(a.bias + n);
+  if constexpr (MODE == EPI_F32) {
+    *(f32x4_t*)(a.out_f + (size_t)m * a.ldo_f + n) = f32x4_t{v[0] + b[0], v[1] + b[1], v[2] + b[2], v[3] + b[3]};
+  } else if constexpr (MODE == EPI_T) {
+    store_bf16x4((bf16_t*)a.out_t + (size_t)m * a.ldo_t + n, v[0] + b[0], v[1] + b[1], v[2] + b[2], v[3] + b[3]);
+  } else if constexpr (MODE == EPI_RESID || MODE == EPI_RESID_TANH) {
+    f32x4_t g = {1.f, 1.f, 1.f, 1.f};
+    if constexpr (MODE == EPI_RESID_TANH) {
+      const float t = tanhf(*a.gate_scalar);
+      g = f32x4_t{t, t, t, t};
+    } else {
+      if (a.gate) g = *(const f32x4_t*)(a.gate + (size_t)m * a.ldg + n);
+    }
+    f32x4_t* o = (f32x4_t*)(a.out_f + (size_t)m * a.ldo_f + n);
+    f32x4_t x = *o;
+    x[0] = x[0] + g[0] * v[0];
+    x[1] = x[1] + g[1] * v[1];
+    x[2] = x[2] + g[2] * v[2];
+    x[3] = x[3] + g[3] * v[3];
+    *o = x;
+  } else if constexpr (MODE == EPI_COND) {
+    for (int i = 0; i < a.H; ++i) {
+      const f32x4_t c = *(const f32x4_t*)(a.ctau + (size_t)i * a.N + n);
+      store_bf16x4((bf16_t*)a.out_t + ((size_t)m * a.H + i) * a.ldo_t + n, silu_f(c[0] + v[0] + b[0]),
+                   silu_f(c[1] + v[1] + b[1]), silu_f(c[2] + v[2] + b[2]), silu_f(c[3] + v[3] + b[3]));
+    }
+  } else if constexpr (MODE == EPI_GELU_T) {
+    store_bf16x4((bf16_t*)a.out_t + (size_t)m * a.ldo_t + n, gelu_tanh_f(v[0] + b[0]), gelu_tanh_f(v[1] + b[1]),
+                 gelu_tanh_f(v[2] + b[2]), gelu_tanh_f(v[3] + b[3]));
+  } else if constexpr (MODE == EPI_SILU_T) {
+    store_bf16x4((bf16_t*)a.out_t + (size_t)m * a.ldo_t + n, silu_f(v[0] + b[0]), silu_f(v[1] + b[1]),
+                 silu_f(v[2] + b[2]), silu_f(v[3] + b[3]));
+  }
+}
+
+// Gated GeLU of a gate fragment g and its up fragment u: columns f .. f+3 of row m.
+RAVEL_DEV void epi_geglu4(const GemmArgs& a, int m, int f, f32x4_t g, f32x4_t u) {
+  store_bf16x4((bf16_t*)a.out_t + (size_t)m * a.ldo_t + f, gelu_tanh_f(g[0]) * u[0], gelu_tanh_f(g[1]) * u[1],
+               gelu_tanh_f(g[2]) * u[2], gelu_tanh_f(g[3]) * u[3]);
+}
+
+// Apply the epilogue to an NI x NJ grid of fragments: fragment (i, j) holds
+// rows m0 + 16 i + l16 and columns n0 + 16 j + 4 grp .. +3.
+template <int MODE, int NI, int NJ>
+RAVEL_DEV void epi_frags(const GemmArgs& a, const f32x4_t (&acc)[NI][NJ], int m0, int n0, int l16, int grp) {
+  const bool vec = epi_vec_ok(a);
+  if constexpr (MODE == EPI_GEGLU) {
+    if constexpr (NJ % 2 == 0) {
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; j += 2) {
+          const int m = m0 + i * 16 + l16;
+          const int ng = n0 + j * 16;  // gate block start (multiple of 32)
+          if (m < a.M && ng < a.N) epi_geglu4(a, m, (ng >> 5) * 16 + grp * 4, acc[i][j], acc[i][j + 1]);
+        }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int m = m0 + i * 16 + l16, n = n0 + j * 16 + grp * 4;
+        if (m < a.M && n < a.N) epi4<MODE>(a, m, n, acc[i][j], vec);
+      }
+  }
+}
+
+template <int NI, int NJ>
+RAVEL_DEV void epilogue(const GemmArgs& a, const f32x4_t (&acc)[NI][NJ], int m0, int n0, int l16, int grp) {
+  switch (a.mode) {
+    case EPI_F32: epi_frags<EPI_F32>(a, acc, m0, n0, l16, grp); break;
+    case EPI_T: epi_frags<EPI_T>(a, acc, m0, n0, l16, grp); break;
+    case EPI_RESID: epi_frags<EPI_RESID>(a, acc, m0, n0, l16, grp); break;
+    case EPI_RESID_TANH: epi_frags<EPI_RESID_TANH>(a, acc, m0, n0, l16, grp); break;
+    case EPI_GEGLU: epi_frags<EPI_GEGLU>(a, acc, m0, n0, l16, grp); break;
+    case EPI_COND: epi_frags<EPI_COND>(a, acc, m0, n0, l16, grp); break;
+    case EPI_GELU_T: epi_frags<EPI_GELU_T>(a, acc, m0, n0, l16, grp); break;
+    case EPI_SILU_T: epi_frags<EPI_SILU_T>(a, acc, m0, n0, l16, grp); break;
+    default: break;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -158,13 +256,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
     }
     if (kt + 1 < nk) sstore(buf ^ 1);
     __syncthreads();
   }
 
-  // acc[i][j][r] = C[m0 + wm*(BM/WM) + i*16 + grp*4 + r][n0 + wn*(BN/WN) + j*16 + l16]
+  // acc[i][j][r] = C[m0 + wm*(BM/WM) + i*16 + l16][n0 + wn*(BN/WN) + j*16 + grp*4 + r]
+  // (the weights are the MFMA's A operand, so each lane owns 4 consecutive columns)
   const int mw = m0 + wm * (BM / WM);
   const int nw = n0 + wn * (BN / WN);
 
@@ -196,36 +295,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
       }
   }
 
-  if constexpr (TN % 2 == 0) {
-    if (a.mode == EPI_GEGLU) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; j += 2)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = mw + i * 16 + grp * 4 + r;
-          const int ng = nw + j * 16;  // gate block start, multiple of 32
-          const int f = (ng >> 5) * 16 + l16;
-          if (m < a.M && ng < a.N)
-            epi_geglu<bf16_t>(a, m, f, acc[i][j][r], acc[i][j + 1][r]);
-        }
-      return;
-    }
-  }
-  {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = mw + i * 16 + grp * 4 + r, n = nw + j * 16 + l16;
-          if (m < a.M && n < a.N) epi_store<bf16_t>(a, m, n, acc[i][j][r]);
-        }
-  }
+  epilogue(a, acc, mw, nw, l16, grp);
 }
-
 
 // ---------------------------------------------------------------------------
 // Weight-streaming kernel for few rows (M <= 64): the regime of one env's H
@@ -242,64 +313,6 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
 // loads before the current tile's epilogue.  Split-K ranges are reduced by the
 // last-arriving block of a tile, in fixed order.
 // ---------------------------------------------------------------------------
-template <typename T>
-RAVEL_DEV void epi_store4(const GemmArgs& a, int m, int n, f32x4_t acc) {
-  // n .. n+3 are valid columns of row m (N is a multiple of 4)
-  f32x4_t b = {0.f, 0.f, 0.f, 0.f};
-  if (a.bias) b = *(const f32x4_t*)(a.bias + n);
-  switch (a.mode) {
-    case EPI_F32: {
-      f32x4_t o = {acc[0] + b[0], acc[1] + b[1], acc[2] + b[2], acc[3] + b[3]};
-      *(f32x4_t*)(a.out_f + (size_t)m * a.ldo_f + n) = o;
-      break;
-    }
-    case EPI_RESID:
-    case EPI_RESID_TANH: {
-      f32x4_t g = {1.f, 1.f, 1.f, 1.f};
-      if (a.mode == EPI_RESID_TANH) {
-        const float t = tanhf(*a.gate_scalar);
-        g = f32x4_t{t, t, t, t};
-      } else if (a.gate) {
-        g = *(const f32x4_t*)(a.gate + (size_t)m * a.ldg + n);
-      }
-      f32x4_t* o = (f32x4_t*)(a.out_f + (size_t)m * a.ldo_f + n);
-      f32x4_t x = *o;
-      x[0] = x[0] + g[0] * acc[0];
-      x[1] = x[1] + g[1] * acc[1];
-      x[2] = x[2] + g[2] * acc[2];
-      x[3] = x[3] + g[3] * acc[3];
-      *o = x;
-      break;
-    }
-    case EPI_T: {
-      if constexpr (sizeof(T) == 2) {
-        u32x2_t w;
-        w[0] = (uint32_t)f32_to_bf16(acc[0] + b[0]) | ((uint32_t)f32_to_bf16(acc[1] + b[1]) << 16);
-        w[1] = (uint32_t)f32_to_bf16(acc[2] + b[2]) | ((uint32_t)f32_to_bf16(acc[3] + b[3]) << 16);
-        *(u32x2_t*)((bf16_t*)a.out_t + (size_t)m * a.ldo_t + n) = w;
-        break;
-      }
-    }
-      [[fallthrough]];
-    default:
-#pragma unroll
-      for (int r = 0; r < 4; ++r) epi_store<T>(a, m, n + r, acc[r]);
-      break;
-  }
-}
-
-// Whether the 4-column vector epilogue applies to this launch (alignment of every
-// row stride it touches).
-RAVEL_DEV bool epi_vec_ok(const GemmArgs& a) {
-  switch (a.mode) {
-    case EPI_F32: return (a.ldo_f % 4) == 0;
-    case EPI_RESID: return (a.ldo_f % 4) == 0 && (!a.gate || (a.ldg % 4) == 0);
-    case EPI_RESID_TANH: return (a.ldo_f % 4) == 0;
-    case EPI_T: return (a.ldo_t % 4) == 0;
-    default: return true;
-  }
-}
-
 template <int MT, int NFR, int KR>
 __global__ __launch_bounds__(256) void gemm_skinny_kernel(GemmArgs a) {
   constexpr int NF = KR / 32;  // weight fragments per lane per 16-column block
@@ -405,45 +418,12 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(GemmArgs a) {
     }
 
     // acc[c][i][r] = C[m = i*16 + l16][n = nw + c*16 + 4*grp + r]
-    bool done = false;
-    if constexpr (NFR % 2 == 0) {
-      if (a.mode == EPI_GEGLU) {
+    f32x4_t t[MT][NFR];
 #pragma unroll
-        for (int c = 0; c < NFR; c += 2)
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
-          for (int i = 0; i < MT; ++i) {
-            const int m = i * 16 + l16;
-            const int ng = nw + c * 16;  // gate block start (multiple of 32)
-            if (m < a.M && ng < a.N) {
-              const int f = (ng >> 5) * 16 + grp * 4;
-              u32x2_t w;
-              w[0] = (uint32_t)f32_to_bf16(gelu_tanh_f(acc[c][i][0]) * acc[c + 1][i][0]) |
-                     ((uint32_t)f32_to_bf16(gelu_tanh_f(acc[c][i][1]) * acc[c + 1][i][1]) << 16);
-              w[1] = (uint32_t)f32_to_bf16(gelu_tanh_f(acc[c][i][2]) * acc[c + 1][i][2]) |
-                     ((uint32_t)f32_to_bf16(gelu_tanh_f(acc[c][i][3]) * acc[c + 1][i][3]) << 16);
-              *(u32x2_t*)((bf16_t*)a.out_t + (size_t)m * a.ldo_t + f) = w;
-            }
-          }
-        done = true;
-      }
-    }
-    if (!done) {
-      const bool vec = epi_vec_ok(a);
-#pragma unroll
-      for (int c = 0; c < NFR; ++c)
-#pragma unroll
-        for (int i = 0; i < MT; ++i) {
-          const int m = i * 16 + l16, n = nw + c * 16 + grp * 4;
-          if (m >= a.M || n >= a.N) continue;
-          if (vec && n + 4 <= a.N) {
-            epi_store4<bf16_t>(a, m, n, acc[c][i]);
-          } else {
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (n + r < a.N) epi_store<bf16_t>(a, m, n + r, acc[c][i][r]);
-          }
-        }
-    }
+      for (int c = 0; c < NFR; ++c) t[i][c] = acc[c][i];
+    epilogue(a, t, 0, nw, l16, grp);
   }
 }
 
@@ -493,6 +473,9 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, int tile, hipStream_t s) {
     case TILE_64x128: return launch_tile<64, 128, 2, 2>(a, s);
     case TILE_128x64: return launch_tile<128, 64, 2, 2>(a, s);
     case TILE_32x64: return launch_tile<32, 64, 1, 4>(a, s);
+    case TILE_256x128: return launch_tile<256, 128, 2, 2>(a, s);
+    case TILE_128x256: return launch_tile<128, 256, 2, 2>(a, s);
+    case TILE_256x256: return launch_tile<256, 256, 2, 2>(a, s);
     case TILE_64x64:
     default: return launch_tile<64, 64, 2, 2>(a, s);
   }
@@ -518,13 +501,22 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
       g += A[k] * bg[k];
       u += A[k] * bu[k];
     }
-    epi_geglu<float>(a, m, n, g, u);
+    ((float*)a.out_t)[(size_t)m * a.ldo_t + n] = gelu_tanh_f(g) * u;
   } else {
     if (n >= a.N) return;
     const float* b = B + (size_t)n * a.ldb;
     float acc = 0.f;
     for (int k = 0; k < a.K; ++k) acc += A[k] * b[k];
-    epi_store<float>(a, m, n, acc);
+    switch (a.mode) {
+      case EPI_F32: epi1<EPI_F32, float>(a, m, n, acc); break;
+      case EPI_T: epi1<EPI_T, float>(a, m, n, acc); break;
+      case EPI_RESID: epi1<EPI_RESID, float>(a, m, n, acc); break;
+      case EPI_RESID_TANH: epi1<EPI_RESID_TANH, float>(a, m, n, acc); break;
+      case EPI_COND: epi1<EPI_COND, float>(a, m, n, acc); break;
+      case EPI_GELU_T: epi1<EPI_GELU_T, float>(a, m, n, acc); break;
+      case EPI_SILU_T: epi1<EPI_SILU_T, float>(a, m, n, acc); break;
+      default: break;
+    }
   }
 }
 

@@ -49,7 +49,10 @@ struct GemmArgs {
 };
 
 // Tile configurations of the bf16 MFMA GEMM.
-enum GemmTile { TILE_64x64 = 0, TILE_128x128 = 1, TILE_64x128 = 2, TILE_128x64 = 3, TILE_32x64 = 4 };
+enum GemmTile {
+  TILE_64x64 = 0, TILE_128x128 = 1, TILE_64x128 = 2, TILE_128x64 = 3, TILE_32x64 = 4,
+  TILE_256x128 = 5, TILE_128x256 = 6, TILE_256x256 = 7
+};
 
 hipError_t launch_gemm_bf16(const GemmArgs& a, int tile, hipStream_t s);
 // M <= 64 weight-streaming kernel: block columns 64*nfr (nfr 1 or 2, 2 for EPI_GEGLU),

@@ -253,9 +253,10 @@ GemmPlan plan_gemm(int M, int N, int K, bool geglu) {
     p.tile = TILE_128x128; bm = 128; bn = 128;
   }
   p.tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
-  // split K until the grid has about 2 blocks per CU, keeping >= 256 K per range
+  // many rows: enough tiles without splitting K (measured: split-K partial traffic
+  // costs more than the wave quantisation it removes); split only tiny grids
   int ks = 1;
-  while (p.tiles * ks * 2 <= 512 && (K / (ks * 2)) >= 256 && ks < 16) ks *= 2;
+  while (p.tiles * ks < 128 && (K / (ks * 2)) >= 512 && ks < 8) ks *= 2;
   int kchunk = (K + ks - 1) / ks;
   kchunk = (kchunk + 63) / 64 * 64;
   p.ksplit = (K + kchunk - 1) / kchunk;
