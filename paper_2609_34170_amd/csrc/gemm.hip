@@ -160,15 +160,25 @@ RAVEL_DEV void epilogue(const GemmArgs& a, const f32x4_t (&acc)[NI][NJ], int m0,
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel
 // ---------------------------------------------------------------------------
+// Blocks are dispatched round-robin over the 8 XCDs (block b runs on XCD b % 8),
+// each with its own L2.  Give every XCD a contiguous range of row-major tiles so
+// that the tiles sharing an activation row panel share one L2.
+RAVEL_DEV int xcd_tile(int b, int T) {
+  const int x = b & 7, local = b >> 3;
+  const int q = T >> 3, r = T & 7;  // XCD x owns q + (x < r) tiles
+  const int start = x * q + (x < r ? x : r);
+  return start + local;
+}
+
 template <int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
+__global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs a) {
+  constexpr int NT = 64 * WM * WN;  // threads per block
   constexpr int BK = 64;
   constexpr int LDK = BK + 8;  // +16 bytes per row: conflict-free 16-byte fragment reads
   constexpr int TM = BM / (16 * WM);
   constexpr int TN = BN / (16 * WN);
-  constexpr int CA = BM * (BK / 8) / 256;  // 16-byte chunks per thread, A tile
-  constexpr int CB = BN * (BK / 8) / 256;
-  static_assert(WM * WN == 4, "4 waves");
+  constexpr int CA = BM * (BK / 8) / NT;  // 16-byte chunks per thread, A tile
+  constexpr int CB = BN * (BK / 8) / NT;
   static_assert(CA >= 1 && CB >= 1, "tile too small");
 
   __shared__ __attribute__((aligned(16))) bf16_t As[2][BM][LDK];
@@ -181,7 +191,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
   const int wm = wave / WN, wn = wave % WN;
 
   const int tiles_n = (a.N + BN - 1) / BN;
-  const int tile = blockIdx.x;
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
   const int m0 = (tile / tiles_n) * BM;
   const int n0 = (tile % tiles_n) * BN;
   const int z = blockIdx.z;
@@ -197,7 +207,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
     const int k0 = kbeg + kt * BK;
 #pragma unroll
     for (int i = 0; i < CA; ++i) {
-      const int c = tid + i * 256;
+      const int c = tid + i * NT;
       const int row = c >> 3, kc = (c & 7) * 8;
       const int m = m0 + row, k = k0 + kc;
       if (m < a.M && k < kend)
@@ -207,7 +217,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < CB; ++i) {
-      const int c = tid + i * 256;
+      const int c = tid + i * NT;
       const int row = c >> 3, kc = (c & 7) * 8;
       const int n = n0 + row, k = k0 + kc;
       if (n < a.N && k < kend)
@@ -219,12 +229,12 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
   auto sstore = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < CA; ++i) {
-      const int c = tid + i * 256;
+      const int c = tid + i * NT;
       *(u32x4_t*)&As[buf][c >> 3][(c & 7) * 8] = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < CB; ++i) {
-      const int c = tid + i * 256;
+      const int c = tid + i * NT;
       *(u32x4_t*)&Bs[buf][c >> 3][(c & 7) * 8] = rb[i];
     }
   };
@@ -459,11 +469,191 @@ hipError_t launch_gemm_skinny(const GemmArgs& a, int nfr, hipStream_t s) {
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// Register-streaming kernel for few rows (M <= 64) and a moderate number of
+// columns.  Block = NW waves = one 64-column tile x all M rows x a K range of
+// 64*NW.  Wave w takes its own 64-wide K slice for all 64 columns: its weight
+// fragments (4 column blocks x 2 k-steps) and activation fragments (MT row
+// blocks x 2 k-steps) are all loaded straight into registers at once, so a
+// block pays one memory latency.  The NW partial tiles are summed through LDS
+// in fixed wave order; K ranges of several blocks (grid.y) are reduced by the
+// last-arriving block in fixed order.
+// ---------------------------------------------------------------------------
+template <int MT, int NW>
+__global__ __launch_bounds__(64 * NW) void gemm_regstream_kernel(GemmArgs a) {
+  constexpr int NC = 4;           // 16-column blocks per tile
+  constexpr int FR = NC * MT;     // accumulator fragments per wave
+  constexpr int KR = 64 * NW;     // K range of the block
+  __shared__ __attribute__((aligned(16))) float red[NW][FR][64][4];
+  __shared__ int s_last;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, grp = lane >> 4;
+  const int tile = blockIdx.x, z = blockIdx.y;
+  const int n0 = tile * 64;
+  const int kw = z * KR + wave * 64;  // this wave's K slice
+  const bf16_t* __restrict__ A = (const bf16_t*)a.A;
+  const bf16_t* __restrict__ B = (const bf16_t*)a.B;
+
+  bf16x8_t wf[NC][2], xf[MT][2];
+#pragma unroll
+  for (int f = 0; f < 2; ++f) {
+    const int k = kw + f * 32 + grp * 8;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int n = n0 + c * 16 + l16;
+      wf[c][f] = (n < a.N && k < a.K) ? *(const bf16x8_t*)(B + (size_t)n * a.ldb + k) : bf16x8_t{};
+    }
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const int m = i * 16 + l16;
+      xf[i][f] = (m < a.M && k < a.K) ? *(const bf16x8_t*)(A + (size_t)m * a.lda + k) : bf16x8_t{};
+    }
+  }
+  f32x4_t acc[NC][MT];
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      acc[c][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int f = 0; f < 2; ++f)
+        acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[c][f], xf[i][f], acc[c][i], 0, 0, 0);
+    }
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int i = 0; i < MT; ++i) *(f32x4_t*)&red[wave][c * MT + i][lane][0] = acc[c][i];
+  __syncthreads();
+
+  // sum the waves' partial tiles in fixed order: item = (fragment, lane)
+  constexpr int ITEMS = FR * 64;
+  constexpr int PER = (ITEMS + 64 * NW - 1) / (64 * NW);
+  f32x4_t sum[PER];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int item = tid + q * 64 * NW;
+    sum[q] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    if (item < ITEMS) {
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        const f32x4_t v = *(const f32x4_t*)&red[w][item >> 6][item & 63][0];
+        sum[q][0] += v[0];
+        sum[q][1] += v[1];
+        sum[q][2] += v[2];
+        sum[q][3] += v[3];
+      }
+    }
+  }
+
+  if (a.ksplit > 1) {
+    const size_t tile_elems = (size_t)ITEMS * 4;
+    float* part = a.partial + ((size_t)z * gridDim.x + tile) * tile_elems;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int item = tid + q * 64 * NW;
+      if (item < ITEMS) coherent_store4(part + (size_t)item * 4, sum[q]);
+    }
+    if (!last_block_arrival(&a.counters[tile * kCounterStride], (unsigned)a.ksplit, &s_last)) return;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int item = tid + q * 64 * NW;
+      if (item >= ITEMS) continue;
+      f32x4_t t = {0.f, 0.f, 0.f, 0.f};
+      for (int zz = 0; zz < a.ksplit; ++zz) {
+        const f32x4_t v = (zz == z) ? sum[q]
+                                    : *(const f32x4_t*)(a.partial + ((size_t)zz * gridDim.x + tile) * tile_elems +
+                                                        (size_t)item * 4);
+        t[0] += v[0];
+        t[1] += v[1];
+        t[2] += v[2];
+        t[3] += v[3];
+      }
+      sum[q] = t;
+    }
+  }
+
+  // item = (c * MT + i) * 64 + lane: rows i*16 + (lane & 15), columns n0 + c*16 + 4*(lane >> 4)
+  if (a.mode == EPI_GEGLU) {
+    // gate block c (even) and up block c + 1 are items (c*MT+i)*64+lane and ((c+1)*MT+i)*64+lane;
+    // route both to the thread owning the gate item through LDS
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int item = tid + q * 64 * NW;
+      if (item < ITEMS) *(f32x4_t*)&red[0][item >> 6][item & 63][0] = sum[q];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int item = tid + q * 64 * NW;
+      if (item >= ITEMS) continue;
+      const int fr = item >> 6, ln = item & 63;
+      const int c = fr / MT, i = fr % MT;
+      if (c & 1) continue;
+      const int m = i * 16 + (ln & 15);
+      const int ng = n0 + c * 16;
+      if (m < a.M && ng < a.N) {
+        const f32x4_t u = *(const f32x4_t*)&red[0][(c + 1) * MT + i][ln][0];
+        epi_geglu4(a, m, (ng >> 5) * 16 + (ln >> 4) * 4, sum[q], u);
+      }
+    }
+    return;
+  }
+  const bool vec = epi_vec_ok(a);
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int item = tid + q * 64 * NW;
+    if (item >= ITEMS) continue;
+    const int fr = item >> 6, ln = item & 63;
+    const int c = fr / MT, i = fr % MT;
+    const int m = i * 16 + (ln & 15), n = n0 + c * 16 + (ln >> 4) * 4;
+    if (m >= a.M || n >= a.N) continue;
+    switch (a.mode) {
+      case EPI_F32: epi4<EPI_F32>(a, m, n, sum[q], vec); break;
+      case EPI_T: epi4<EPI_T>(a, m, n, sum[q], vec); break;
+      case EPI_RESID: epi4<EPI_RESID>(a, m, n, sum[q], vec); break;
+      case EPI_RESID_TANH: epi4<EPI_RESID_TANH>(a, m, n, sum[q], vec); break;
+      case EPI_COND: epi4<EPI_COND>(a, m, n, sum[q], vec); break;
+      case EPI_GELU_T: epi4<EPI_GELU_T>(a, m, n, sum[q], vec); break;
+      case EPI_SILU_T: epi4<EPI_SILU_T>(a, m, n, sum[q], vec); break;
+      default: break;
+    }
+  }
+}
+
+template <int MT, int NW>
+static hipError_t launch_regstream_t(const GemmArgs& a, hipStream_t s) {
+  dim3 grid((a.N + 63) / 64, a.ksplit);
+  hipLaunchKernelGGL((gemm_regstream_kernel<MT, NW>), grid, dim3(64 * NW), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int MT>
+static hipError_t launch_regstream_m(const GemmArgs& a, hipStream_t s) {
+  switch (a.kchunk) {
+    case 256: return launch_regstream_t<MT, 4>(a, s);
+    case 512: return launch_regstream_t<MT, 8>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_gemm_regstream(const GemmArgs& a, hipStream_t s) {
+  if (a.M > 64 || (a.mode == EPI_GEGLU && a.N % 32)) return hipErrorInvalidValue;
+  if (a.ksplit * a.kchunk < a.K) return hipErrorInvalidValue;
+  switch ((a.M + 15) / 16) {
+    case 1: return launch_regstream_m<1>(a, s);
+    case 2: return launch_regstream_m<2>(a, s);
+    case 3: return launch_regstream_m<3>(a, s);
+    default: return launch_regstream_m<4>(a, s);
+  }
+}
+
 template <int BM, int BN, int WM, int WN>
 static hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   dim3 grid(tiles, 1, a.ksplit);
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN>), grid, dim3(256), 0, s, a);
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN>), grid, dim3(64 * WM * WN), 0, s, a);
   return hipGetLastError();
 }
 
@@ -475,7 +665,7 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, int tile, hipStream_t s) {
     case TILE_32x64: return launch_tile<32, 64, 1, 4>(a, s);
     case TILE_256x128: return launch_tile<256, 128, 2, 2>(a, s);
     case TILE_128x256: return launch_tile<128, 256, 2, 2>(a, s);
-    case TILE_256x256: return launch_tile<256, 256, 2, 2>(a, s);
+    case TILE_256x256: return launch_tile<256, 256, 4, 2>(a, s);
     case TILE_64x64:
     default: return launch_tile<64, 64, 2, 2>(a, s);
   }

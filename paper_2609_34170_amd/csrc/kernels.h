@@ -58,6 +58,9 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, int tile, hipStream_t s);
 // M <= 64 weight-streaming kernel: block columns 64*nfr (nfr 1 or 2, 2 for EPI_GEGLU),
 // K range per block kchunk in {128, 256, 512} (1024 with nfr 1), ksplit ranges (grid.y).
 hipError_t launch_gemm_skinny(const GemmArgs& a, int nfr, hipStream_t s);
+// M <= 64, 64-column tiles, waves split the block's K range (kchunk 256 or 512 = 4 or 8
+// waves), ksplit ranges (grid.y).
+hipError_t launch_gemm_regstream(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------------------

@@ -215,6 +215,7 @@ ravel_status upload_all(const ravel_tensor* t, bool to_bf16, void* dst, const St
 // GEMM dispatch ---------------------------------------------------------------
 struct GemmPlan {
   bool skinny;
+  bool regstream;
   int nfr;     // skinny: 16-column fragments per wave
   int tile;    // tiled: GemmTile
   int ksplit;
@@ -227,22 +228,25 @@ GemmPlan plan_gemm(int M, int N, int K, bool geglu) {
   GemmPlan p;
   memset(&p, 0, sizeof p);
   if (M <= 64) {
-    // weight streaming: aim for >= 256 blocks, the largest K range that reaches it,
-    // at most 16 split-K ranges
+    // weight streaming (measured on MI355X at the pi-style batch-1 shapes):
+    //  * many column tiles and K <= 1024: one block per tile, whole K, LDS-staged rows;
+    //  * otherwise: register streaming, waves split a 512 (or 256) wide K range.
     p.skinny = true;
-    p.nfr = geglu ? 2 : 1;
-    p.tiles = (N + 64 * p.nfr - 1) / (64 * p.nfr);
-    if (p.nfr == 1 && K <= 1024 && p.tiles >= 512) {
+    const int tiles64 = (N + 63) / 64;
+    if (!geglu && K <= 1024 && tiles64 >= 512) {
+      p.regstream = false;
+      p.nfr = 1;
+      p.tiles = tiles64;
       p.kchunk = K <= 128 ? 128 : K <= 256 ? 256 : K <= 512 ? 512 : 1024;
-    } else {
-      for (int kc : {512, 256, 128}) {
-        p.kchunk = kc;
-        if ((long)p.tiles * ((K + kc - 1) / kc) >= 256) break;
-      }
-      while ((K + p.kchunk - 1) / p.kchunk > 16 && p.kchunk < 512) p.kchunk *= 2;
+      p.ksplit = 1;
+      p.part_elems = 0;
+      return p;
     }
+    p.regstream = true;
+    p.tiles = tiles64;
+    p.kchunk = K >= 512 ? 512 : 256;
     p.ksplit = (K + p.kchunk - 1) / p.kchunk;
-    const size_t tile_elems = (size_t)((M + 15) / 16) * 16 * 64 * p.nfr;
+    const size_t tile_elems = (size_t)((M + 15) / 16) * 1024;
     p.part_elems = p.ksplit > 1 ? (size_t)p.ksplit * p.tiles * tile_elems : 0;
     return p;
   }
@@ -378,14 +382,19 @@ ravel_status run_gemm(ravel_buffer* b, hipStream_t s, KernelRecorder* rec, const
   if (rec) {
     static const char* tn[] = {"64x64", "128x128", "64x128", "128x64", "32x64"};
     char full[48];
-    if (p.skinny)
-      snprintf(full, sizeof full, "gemm_stream:%s", name);
+    if (p.skinny && p.regstream)
+      snprintf(full, sizeof full, "gemm_regstream<%d>:%s", (M + 15) / 16, name);
+    else if (p.skinny)
+      snprintf(full, sizeof full, "gemm_stream<%d,%d>:%s", (M + 15) / 16, p.kchunk, name);
     else
       snprintf(full, sizeof full, "gemm%s:%s", tn[p.tile], name);
     rec->begin(full, bytes, flops);
   }
   if (p.skinny) {
-    HIP_TRY(launch_gemm_skinny(epi, p.nfr, s));
+    if (p.regstream)
+      HIP_TRY(launch_gemm_regstream(epi, s));
+    else
+      HIP_TRY(launch_gemm_skinny(epi, p.nfr, s));
     if (rec) rec->end();
     return RAVEL_OK;
   }
