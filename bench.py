@@ -172,13 +172,24 @@ class Workload:
         return np.array([a.elapsed_time(b) for a, b in ev])
 
     def profile(self, nsteps):
+        """Per kernel class: [launches, bytes, flops, ms] summed over nsteps eager
+        steps.  Phase records of the persistent kernel ("persistent/<class>")
+        split its time and go to self.phases instead."""
         agg = {}
+        self.phases = {}
         total = 0.0
         for _ in range(nsteps):
             self.refresh()
             recs = self.buf.profile_step(self.fop, self.action)
             self.t += 1
             for name, by, fl, ms in recs:
+                if name.startswith("persistent/"):
+                    a = self.phases.setdefault(name.split("/", 1)[1], [0, 0.0, 0.0, 0.0])
+                    a[0] += 1
+                    a[1] += by
+                    a[2] += fl
+                    a[3] += ms
+                    continue
                 cls = name.split(":")[0]
                 a = agg.setdefault(cls, [0, 0.0, 0.0, 0.0])
                 a[0] += 1
@@ -286,6 +297,12 @@ def main():
                                        sorted(agg.items(), key=lambda kv: -kv[1][3])[:8]},
         "wall_s_timed": round(wall, 3),
     }
+    if wl.phases:
+        # per phase class of the persistent kernel: ms per step and achieved GB/s
+        out["persistent_phases"] = {
+            k: {"ms": round(v[3] / args.profile_steps, 4),
+                "GBs": round(v[1] / (v[3] * 1e-3) / 1e9, 1) if v[3] > 0 else None}
+            for k, v in sorted(wl.phases.items(), key=lambda kv: -kv[1][3])}
     log(f"[{s.name}] {1000.0 / ms:.1f} steps/s, {ms * 1e3:.1f} us/step")
     W = wl.W
     if not args.no_batch64 and args.workload == "pi_b1":

@@ -129,8 +129,12 @@ void ravel_buffer_destroy(ravel_buffer* buf);
  *                           data; 0 (default): applied at the first step whose
  *                           host-side event query finds the data ready.
  *   RAVEL_OPT_USE_GRAPH     1 (default): replay a captured hipGraph per step.
- *   RAVEL_OPT_DEBUG         1: synchronise and check for NaN/Inf after each kernel. */
-enum { RAVEL_OPT_SYNC_CONTEXT = 1, RAVEL_OPT_USE_GRAPH = 2, RAVEL_OPT_DEBUG = 3 };
+ *   RAVEL_OPT_DEBUG         1: synchronise and check for NaN/Inf after each kernel.
+ *   RAVEL_OPT_PERSISTENT    1 (default where available): run the transformer layers
+ *                           of a bf16 model whose B*H rows fit one 64-row tile as a
+ *                           single cooperative persistent kernel; 0: one kernel per
+ *                           operation.  E_STATE if the buffer does not qualify. */
+enum { RAVEL_OPT_SYNC_CONTEXT = 1, RAVEL_OPT_USE_GRAPH = 2, RAVEL_OPT_DEBUG = 3, RAVEL_OPT_PERSISTENT = 4 };
 ravel_status ravel_buffer_set_option(ravel_buffer* buf, int32_t option, int64_t value);
 
 /* Context plane (paper Sec. 3.2: the latest available context is reused
@@ -189,8 +193,12 @@ ravel_status ravel_buffer_load(ravel_buffer* buf, const void* host_blob, size_t 
 
 /* Per-kernel timing of one eagerly launched step (HIP events around every
  * launch on `stream`; synchronises).  Each record: kernel class name,
- * algorithmic bytes and flops of that launch, and its duration.  On input
- * *n is the capacity; on output the number of records. */
+ * algorithmic bytes and flops of that launch, and its duration.  With the
+ * persistent path on, further records "persistent/<phase class>" split the
+ * "persistent_layers" record by phase class (time between the kernel's grid
+ * barriers as seen by its first block, summed over layers); they are not
+ * additional launches.  On input *n is the capacity; on output the number of
+ * records. */
 typedef struct {
   char name[48];
   double bytes;

@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libravel.so")
-SOURCES = ["gemm.hip", "attention.hip", "elementwise.hip", "ravel.hip"]
+SOURCES = ["gemm.hip", "attention.hip", "elementwise.hip", "persistent.hip", "ravel.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

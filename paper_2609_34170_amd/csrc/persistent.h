@@ -1,0 +1,88 @@
+// Phase list of the persistent few-row step (internal to the library).
+#pragma once
+
+#include "kernels.h"
+
+namespace ravel {
+
+enum PhaseType : int { PH_ROWSTATS = 1, PH_GEMM = 2, PH_ATTN = 3 };
+
+// GEMM activation operand
+enum PAMode : int {
+  PA_BF16 = 0,  // A[m][k] in bf16
+  // adaptive RMSNorm applied on load: h[m][k] = r[m] * p[m][k] + shift[m][k] (shift optional), with
+  // p = bf16((1 + scale) * x) written by whoever produced the residual x, and
+  // r[m] = 1 / sqrt(mean_k x[m][k]^2 + eps) from the per-64-column row sums of squares of x
+  PA_NORM = 1,
+};
+enum PEMode : int { PE_BF16 = 0, PE_F32 = 1, PE_GEGLU = 2, PE_RESID = 3 };
+// scale of the next norm, applied to a new residual x to form p: per (row, column)
+// modulation rows, or one vector over columns
+enum NSMode : int { NS_ROW = 0, NS_COL = 1 };
+
+// Grid barrier: kBarrierGroups group counters (one 256-byte line each), a top
+// counter, a generation word and an exit counter; 64 * (3 + groups) words.
+constexpr int kBarrierGroups = 32;
+constexpr int kBarrierWords = 64 * (3 + kBarrierGroups);
+// polls (each a device-coherent load) before a barrier gives up and flags an
+// error: seconds, far above any phase of a step
+constexpr int kBarrierSpinLimit = 1 << 22;
+// split-K ranges per output tile (a GEMM item covers 256 * kw of K, kw in {1, 2};
+// kw = 2 only for plain bf16 activations)
+constexpr int kMaxKSplit = 8;
+// key splits of one attention (env, head)
+constexpr int kMaxAttnSplit = 16;
+// keys of one attention split staged in LDS, by head dimension
+__host__ __device__ constexpr int attn_keys_per_split_max(int hd) { return (32768 / hd) < 256 ? (32768 / hd) : 256; }
+
+// First phase.  Items below N/64: one 64-column tile of x, its rows' sums of
+// squares and p = bf16((1 + scale) * x).  Items above: 8192-element pieces of the
+// bf16 copy of the norm shifts, cvt_out[c][m][n] = bf16(cvt_in[m][c * cvt_stride + n])
+// for chunk c < cvt_chunks, m < M, n < N.
+struct PRowstats {
+  const float* x; int ldx;
+  int M, N;
+  int ns_mode; const float* ns; int ldns;
+  bf16_t* p; int ldp;
+  float* sumsq_out;  // [N/64][64]
+  const float* cvt_in; int cvt_ld, cvt_stride, cvt_chunks;
+  bf16_t* cvt_out;
+};
+
+struct PGemm {
+  int a_mode, e_mode;  // PAMode, PEMode
+  int kw, ksplit;      // K per item = 256 * kw; items = tiles(N, 64) * ksplit
+  int M, N, K;
+  const bf16_t* A; int lda;            // PA_BF16: A; PA_NORM: p
+  const bf16_t* shift; int ld_shift;   // PA_NORM: bf16 shift rows or NULL
+  const float* sumsq_in; float eps;    // PA_NORM: [K/64][64]
+  const bf16_t* W; int ldw;            // weights [N][ldw]
+  const float* bias;                   // PE_F32 (or NULL)
+  bf16_t* out_t; int ldo;              // PE_BF16 / PE_GEGLU
+  float* out_f; int ldof;              // PE_F32 output, or the residual x (PE_RESID)
+  const float* gate; int ldg;          // PE_RESID: gate rows, or NULL and then
+  const float* gate_scalar;            // tanh(*gate_scalar)
+  int ns_mode; const float* ns; int ldns;  // PE_RESID: scale of the next norm
+  bf16_t* p_out; int ldp;              // PE_RESID: p of the next norm
+  float* sumsq_out;                    // PE_RESID: [N/64][64] row sums of squares of the new x
+  float* partial; unsigned* counters;  // split-K partial tiles, per-tile tickets
+};
+
+struct alignas(16) Phase {
+  int type, items, pad0, pad1;
+  union {
+    PGemm g;
+    AttnArgs at;
+    PRowstats rs;
+  };
+};
+
+// env_slot: [nenv] active context slot per env (read once per launch).
+// times: optional [nphase + 1] wall-clock stamps taken by block 0 at the start,
+// after each phase's barrier, and at its end (NULL: none).
+hipError_t launch_persistent(const Phase* phases, int nphase, const int* env_slot, int nenv, int mt, int blocks,
+                             unsigned* bar, int* err, unsigned long long* times, hipStream_t s);
+// Blocks of the persistent kernel that can be co-resident (0 on error).
+int persistent_max_blocks(int mt);
+
+}  // namespace ravel

@@ -1,0 +1,864 @@
+// Persistent few-row step: the transformer layers of a batch whose B*H rows fit
+// one 64-row MFMA tile (B*H <= 64, e.g. one env with 50 slots) run inside ONE
+// cooperative kernel that walks a host-built list of phases separated by
+// hierarchical grid barriers.
+//
+// At these sizes every phase is a chain of memory round trips rather than a
+// bandwidth problem, so the kernel is laid out to keep that chain short:
+//  * the descriptor of phase p + 2 and the weight fragments of this block's
+//    first item of phase p + 1 are fetched while the block waits at barrier
+//    p + 1 (weights and descriptors never change during a launch);
+//  * every load of an item is issued before the first of them is used (no
+//    loops whose trip counts hide loads behind one another);
+//  * one thread per block performs the device-scope acquire after a barrier
+//    or a split ticket, and every wave drains its stores before arriving.
+//
+// Phases:
+//  * ROWSTATS: per 64-column tile of the residual x, the rows' sums of squares
+//    and p = bf16((1 + scale) * x) for the first adaptive norm;
+//  * GEMM: an item is a 64-column tile times a K range of 256 * kw; the four
+//    waves take K quarters and are reduced through LDS; the activation operand
+//    is bf16, or normalised on load as h = r * p + shift with r = 1/rms(x)
+//    from the row sums; split-K ranges are added in fixed order by the last
+//    block to arrive at the tile's ticket, whose epilogue writes bf16 / fp32
+//    outputs, gelu(gate) * up, or a gated residual update of x that also
+//    writes the next norm's p and the new row sums of squares;
+//  * ATTN: an item is one (env, head, key split): its keys and values are
+//    staged in LDS in one batch, the four waves take 16 queries each, and the
+//    splits are merged by the last item of the (env, head) to arrive.
+// Values handed to another block are written with device-coherent stores and
+// read with device-coherent (sc1) buffer loads, which bypass the CU's L1 and are
+// served by the L2, coherent across the XCDs on this part: measured with a
+// stale-read probe (one block rewrites a buffer before each barrier, every block
+// counts stale values after it, with the L1 pre-filled by plain reads) -- zero
+// stale values out of 10^9 -- so no cache-invalidating acquire is needed after a
+// barrier or ticket (an agent-scope acquire invalidates the L2 and costs ~2 us
+// per phase).  Data written before the launch (weights, modulation, context) is
+// read with plain loads.  Producers drain their stores before arriving at a
+// barrier or ticket.  Spins are bounded: a barrier that does not complete sets
+// the error flag and every wave exits.
+#include "kernels.h"
+#include "persistent.h"
+
+namespace ravel {
+namespace {
+
+template <int HD>
+struct AttnCfg {
+  static constexpr int KPS = attn_keys_per_split_max(HD);  // keys staged per split
+  static constexpr int KLD = HD + 8;                       // K row stride in LDS
+  static constexpr int VLD = KPS + 8;                      // V^T row stride in LDS
+  static constexpr int ELEMS = KPS * KLD + HD * VLD;
+};
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+constexpr int kAttnElems =
+    cmax(cmax(AttnCfg<32>::ELEMS, AttnCfg<64>::ELEMS), cmax(AttnCfg<128>::ELEMS, AttnCfg<256>::ELEMS));
+
+struct PSmem {
+  union {
+    float red[4][16][64][4];  // GEMM: per-wave partial tiles
+    bf16_t at[kAttnElems];    // attention: K rows, then V^T
+    struct {
+      float ml[kMaxAttnSplit][64][2];  // attention merge: (max, sum) per split and query
+      float wgt[kMaxAttnSplit][64];    // merge weights
+    } mg;
+  };
+  float rscale[64];
+  float rowsq[64][17];
+  int flag;
+};
+
+RAVEL_DEV int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Loads go through buffer resources on wave-uniform bases with per-lane byte
+// offsets.  A lane with nothing to load passes an offset past the resource's
+// range and reads zeros: no branch around the load, so a batch of predicated
+// loads stays in flight together (a load under a branch that also writes its
+// register on the other path makes the compiler wait for it at once).
+// PLAIN: data written before the launch.  COH: data written during the launch,
+// device-coherent (sc1: bypasses the CU's L1, served by the coherent L2).
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int PLAIN = 0, COH = 16;
+constexpr unsigned kOutOfRange = 0x80000000u;
+RAVEL_DEV rsrc_t rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0x7fffffff, 0x00020000);
+}
+RAVEL_DEV int boff(bool ok, size_t byte_off) { return (int)(ok ? (unsigned)byte_off : kOutOfRange); }
+template <int AUX>
+RAVEL_DEV u32x4_t ld16(rsrc_t r, int off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, AUX);
+}
+template <int AUX>
+RAVEL_DEV f32x4_t ld_f4(rsrc_t r, int off) {
+  const u32x4_t v = ld16<AUX>(r, off);
+  return *reinterpret_cast<const f32x4_t*>(&v);
+}
+template <int AUX>
+RAVEL_DEV bf16x8_t ld_b8(rsrc_t r, int off) {
+  const u32x4_t v = ld16<AUX>(r, off);
+  return *reinterpret_cast<const bf16x8_t*>(&v);
+}
+template <int AUX>
+RAVEL_DEV float ld_f1(rsrc_t r, int off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, AUX));
+}
+template <int AUX>
+RAVEL_DEV float2 ld_f2(rsrc_t r, int off) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, AUX);
+  return float2{__uint_as_float(v[0]), __uint_as_float(v[1])};
+}
+
+// threadIdx.x behind an empty asm: index arithmetic derived from it stays inside
+// the work item that needs it instead of being hoisted out of the phase loop,
+// where the invariants of every item kind would stay live for the whole kernel
+RAVEL_DEV int local_tid() {
+  int t = threadIdx.x;
+  asm volatile("" : "+v"(t));
+  return t;
+}
+
+// A copy of a descriptor held in LDS, with every word made wave-uniform.
+template <class T>
+RAVEL_DEV T make_uniform(const T& s) {
+  static_assert(sizeof(T) % 4 == 0, "descriptor size");
+  T d;
+  const int* si = reinterpret_cast<const int*>(&s);
+  int* di = reinterpret_cast<int*>(&d);
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(T) / 4); ++i) di[i] = __builtin_amdgcn_readfirstlane(si[i]);
+  return d;
+}
+
+RAVEL_DEV void coherent_store_bf16x4(bf16_t* p, float v0, float v1, float v2, float v3) {
+  const uint64_t w = (uint64_t)f32_to_bf16(v0) | ((uint64_t)f32_to_bf16(v1) << 16) |
+                     ((uint64_t)f32_to_bf16(v2) << 32) | ((uint64_t)f32_to_bf16(v3) << 48);
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Ticket of a split tile / split attention head: every wave drains its stores,
+// thread 0 takes the ticket; the last arrival re-arms it.
+RAVEL_DEV bool last_arrival(unsigned* counter, unsigned arrivals, int* s_flag) {
+  wait_memory();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int last = prev == arrivals - 1;
+    if (last) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *s_flag = last;
+  }
+  __syncthreads();
+  return *s_flag != 0;
+}
+
+// Hierarchical grid barrier, split in two so that loads can be issued between
+// arrival and wait.  Group g's counter sits on its own 256-byte line; the last
+// arrival of a group bumps the top counter and the last top arrival publishes
+// the generation word every block polls.
+RAVEL_DEV void barrier_arrive(unsigned* bar, unsigned gen) {
+  const int G = kBarrierGroups;
+  const int g = blockIdx.x % G;
+  const unsigned per = (gridDim.x - g + G - 1) / G;
+  const unsigned prev = __hip_atomic_fetch_add(bar + 64 * (1 + g), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (prev == gen * per - 1) {
+    const unsigned t = __hip_atomic_fetch_add(bar + 64 * (1 + G), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (t == gen * (unsigned)G - 1) __hip_atomic_store(bar, gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+RAVEL_DEV int barrier_wait(unsigned* bar, unsigned gen, int* err) {
+  int spins = 0;
+  while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < gen) {
+    __builtin_amdgcn_s_sleep(1);
+    if (++spins > kBarrierSpinLimit) {
+      __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return 0;
+    }
+  }
+  return 1;
+}
+
+// ---------------------------------------------------------------------------
+// ROWSTATS: one 64-column tile, 4 threads per row, 16 columns each
+// ---------------------------------------------------------------------------
+RAVEL_DEV void convert_item(const PRowstats& r, int piece) {
+  // 8192 elements: 256 threads x 32 consecutive (N is a multiple of 64)
+  const size_t total = (size_t)r.cvt_chunks * r.M * r.N;
+  const size_t e0 = ((size_t)piece * 256 + local_tid()) * 32;
+  if (e0 >= total) return;
+  const int n = (int)(e0 % r.N);
+  const size_t mc = e0 / r.N;
+  const int m = (int)(mc % r.M), c = (int)(mc / r.M);
+  const float* src = r.cvt_in + (size_t)m * r.cvt_ld + (size_t)c * r.cvt_stride + n;
+  f32x4_t v[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = *(const f32x4_t*)(src + 4 * i);
+  bf16_t* dst = r.cvt_out + e0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) coherent_store_bf16x4(dst + 4 * i, v[i][0], v[i][1], v[i][2], v[i][3]);
+}
+
+RAVEL_DEV void rowstats_item(const PRowstats& r, int tile, PSmem& sm) {
+  const int tid = local_tid();
+  const int m = tid >> 2, q = tid & 3;
+  const int n = tile * 64 + q * 16;
+  float s = 0.f;
+  if (m < r.M) {
+    f32x4_t x[4], sc[4];
+    const float* nsp = r.ns_mode == NS_ROW ? r.ns + (size_t)m * r.ldns + n : r.ns + n;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      x[c] = *(const f32x4_t*)(r.x + (size_t)m * r.ldx + n + 4 * c);
+      sc[c] = *(const f32x4_t*)(nsp + 4 * c);
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      s += x[c][0] * x[c][0] + x[c][1] * x[c][1] + x[c][2] * x[c][2] + x[c][3] * x[c][3];
+      coherent_store_bf16x4(r.p + (size_t)m * r.ldp + n + 4 * c, (1.f + sc[c][0]) * x[c][0],
+                            (1.f + sc[c][1]) * x[c][1], (1.f + sc[c][2]) * x[c][2], (1.f + sc[c][3]) * x[c][3]);
+    }
+  }
+  sm.rowsq[m][q] = s;
+  __syncthreads();
+  if (tid < 64 && tid < r.M) {
+    const float t = (sm.rowsq[tid][0] + sm.rowsq[tid][1]) + (sm.rowsq[tid][2] + sm.rowsq[tid][3]);
+    coherent_store(r.sumsq_out + tile * 64 + tid, t);
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// GEMM
+// ---------------------------------------------------------------------------
+// Weight fragments of an item: wave w holds rows n0 + 16c + (lane & 15) and the
+// K range kb + 32f + 8(lane >> 4) .. +7 for its quarter of the item's K range.
+template <int KW>
+RAVEL_DEV void load_w(const PGemm& g, int item, bf16x8_t (&wf)[4][4]) {
+  const int tid = local_tid();
+  const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, grp = lane >> 4;
+  const int tiles = (g.N + 63) >> 6, tile = item % tiles, z = item / tiles;
+  const int n0 = tile * 64, kb = z * 256 * KW + wave * 64 * KW;
+  const rsrc_t rw = rsrc(g.W);
+#pragma unroll
+  for (int f = 0; f < 4; ++f) {
+    const int k = kb + f * 32 + grp * 8;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int n = n0 + c * 16 + l16;
+      wf[c][f] = ld_b8<PLAIN>(rw, boff(f < 2 * KW && n < g.N && k < g.K, ((size_t)n * g.ldw + k) * 2));
+    }
+  }
+}
+
+RAVEL_DEV void load_weights(const PGemm& g, int item, bf16x8_t (&wf)[4][4]) {
+  if (g.kw == 2)
+    load_w<2>(g, item, wf);
+  else
+    load_w<1>(g, item, wf);
+}
+
+template <int MT, int KW>
+RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], PSmem& sm) {
+  constexpr int NF = 2 * KW;
+  const int tid = local_tid(), lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, grp = lane >> 4;
+  const int tiles = (g.N + 63) >> 6, tile = item % tiles, z = item / tiles;
+  const int n0 = tile * 64;
+  const int kb = z * 256 * KW + wave * 64 * KW;
+  const bool norm = g.a_mode == PA_NORM;
+  const bool has_shift = norm && g.shift != nullptr;
+
+  // activations (and, for the norm, shifts and row sums of squares): one batch
+  const rsrc_t rA = rsrc(g.A), rS = rsrc(g.shift);
+  bf16x8_t af[MT][NF], sh[MT][NF];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int f = 0; f < NF; ++f) {
+      const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
+      const bool ok = m < g.M && k < g.K;
+      af[i][f] = ld_b8<COH>(rA, boff(ok, ((size_t)m * g.lda + k) * 2));
+      sh[i][f] = ld_b8<COH>(rS, boff(has_shift && ok, ((size_t)m * g.ld_shift + k) * 2));
+    }
+  if (norm) {
+    // r[m] from the per-tile row sums: thread (part, row) adds tiles part, part + 4, ...
+    const int row = tid & 63, part = tid >> 6, nt = g.K >> 6;
+    const rsrc_t rQ = rsrc(g.sumsq_in);
+    float sq[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int t = part + 4 * j;
+      sq[j] = ld_f1<COH>(rQ, boff(t < nt && row < g.M, (size_t)(t * 64 + row) * 4));
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) s += sq[j];
+    sm.rowsq[row][part] = s;
+    __syncthreads();
+    if (tid < 64) {
+      const float t = (sm.rowsq[tid][0] + sm.rowsq[tid][1]) + (sm.rowsq[tid][2] + sm.rowsq[tid][3]);
+      sm.rscale[tid] = 1.0f / sqrtf(t / (float)g.K + g.eps);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const float r = sm.rscale[i * 16 + l16];
+#pragma unroll
+      for (int f = 0; f < NF; ++f) {
+        const bf16_t* pv = reinterpret_cast<const bf16_t*>(&af[i][f]);
+        const bf16_t* bv = reinterpret_cast<const bf16_t*>(&sh[i][f]);
+        bf16_t hb[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) hb[q] = f32_to_bf16(r * bf16_to_f32(pv[q]) + bf16_to_f32(bv[q]));
+        af[i][f] = *reinterpret_cast<const bf16x8_t*>(hb);
+      }
+    }
+  }
+
+  f32x4_t acc[4][MT];
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      acc[c][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int f = 0; f < NF; ++f)
+        acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[c][f], af[i][f], acc[c][i], 0, 0, 0);
+    }
+  // reduce the four K quarters through LDS.  Item it = tid + 256 q (q < MT) is
+  // fragment fr = it >> 6 (= c * MT + i), lane ln = it & 63: row i*16 + (ln & 15),
+  // columns n0 + 16c + 4(ln >> 4) .. +3.
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int i = 0; i < MT; ++i) *(f32x4_t*)&sm.red[wave][c * MT + i][lane][0] = acc[c][i];
+  __syncthreads();
+  f32x4_t sum[MT];
+#pragma unroll
+  for (int q = 0; q < MT; ++q) {
+    const int it = tid + q * 256;
+    sum[q] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const f32x4_t v = *(const f32x4_t*)&sm.red[w][it >> 6][it & 63][0];
+      sum[q][0] += v[0];
+      sum[q][1] += v[1];
+      sum[q][2] += v[2];
+      sum[q][3] += v[3];
+    }
+  }
+  auto row_of = [&](int q) { return ((tid + q * 256) >> 6) % MT * 16 + ((tid + q * 256) & 15); };
+  auto col_of = [&](int q) { return n0 + ((tid + q * 256) >> 6) / MT * 16 + (((tid + q * 256) & 63) >> 4) * 4; };
+
+  const bool resid = g.e_mode == PE_RESID;
+  // epilogue operands (residual x, gate, next-norm scale, bias), one batch
+  f32x4_t e_x[MT], e_g[MT], e_s[MT], e_b[MT];
+  auto load_epilogue = [&]() {
+    const rsrc_t rX = rsrc(g.out_f), rG = rsrc(g.gate), rN = rsrc(g.ns), rB = rsrc(g.bias);
+#pragma unroll
+    for (int q = 0; q < MT; ++q) {
+      const int m = row_of(q), n = col_of(q);
+      const bool ok = m < g.M && n + 4 <= g.N;
+      e_x[q] = ld_f4<COH>(rX, boff(resid && ok, ((size_t)m * g.ldof + n) * 4));
+      e_g[q] = ld_f4<PLAIN>(rG, boff(resid && ok && g.gate, ((size_t)m * g.ldg + n) * 4));
+      e_s[q] = ld_f4<PLAIN>(rN, boff(resid && ok, (g.ns_mode == NS_ROW ? (size_t)m * g.ldns + n : (size_t)n) * 4));
+      e_b[q] = ld_f4<PLAIN>(rB, boff(!resid && ok && g.bias, (size_t)n * 4));
+    }
+  };
+  if (g.ksplit > 1) {
+    const size_t tile_elems = (size_t)MT * 4 * 64 * 4;
+    float* mine = g.partial + ((size_t)z * tiles + tile) * tile_elems;
+#pragma unroll
+    for (int q = 0; q < MT; ++q)
+      if (row_of(q) < g.M) coherent_store4(mine + (size_t)(tid + q * 256) * 4, sum[q]);
+    if (!last_arrival(&g.counters[tile * kCounterStride], (unsigned)g.ksplit, &sm.flag)) {
+      __syncthreads();
+      return;
+    }
+    // the other K ranges, all in flight at once (with the epilogue operands),
+    // added in fixed order
+    load_epilogue();
+    const rsrc_t rP = rsrc(g.partial);
+    f32x4_t pv[MT][kMaxKSplit];
+#pragma unroll
+    for (int q = 0; q < MT; ++q)
+#pragma unroll
+      for (int zz = 0; zz < kMaxKSplit; ++zz)
+        pv[q][zz] = ld_f4<COH>(rP, boff(zz < g.ksplit && zz != z && row_of(q) < g.M,
+                                        (((size_t)zz * tiles + tile) * tile_elems + (size_t)(tid + q * 256) * 4) * 4));
+#pragma unroll
+    for (int q = 0; q < MT; ++q) {
+      f32x4_t t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int zz = 0; zz < kMaxKSplit; ++zz) {
+        if (zz >= g.ksplit) break;
+        const f32x4_t v = (zz == z) ? sum[q] : pv[q][zz];
+        t[0] += v[0];
+        t[1] += v[1];
+        t[2] += v[2];
+        t[3] += v[3];
+      }
+      sum[q] = t;
+    }
+  }
+
+  if (g.e_mode == PE_GEGLU) {
+    // gate fragments are the even 16-column blocks, up the odd ones
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < MT; ++q) *(f32x4_t*)&sm.red[0][(tid + q * 256) >> 6][(tid + q * 256) & 63][0] = sum[q];
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < MT; ++q) {
+      const int it = tid + q * 256, fr = it >> 6, ln = it & 63;
+      const int c = fr / MT, i = fr % MT;
+      if (c & 1) continue;
+      const int m = i * 16 + (ln & 15), ng = n0 + c * 16;
+      if (m >= g.M || ng >= g.N) continue;
+      const f32x4_t u = *(const f32x4_t*)&sm.red[0][(c + 1) * MT + i][ln][0];
+      const f32x4_t gt = sum[q];
+      coherent_store_bf16x4(g.out_t + (size_t)m * g.ldo + (ng >> 5) * 16 + (ln >> 4) * 4, gelu_tanh_f(gt[0]) * u[0],
+                            gelu_tanh_f(gt[1]) * u[1], gelu_tanh_f(gt[2]) * u[2], gelu_tanh_f(gt[3]) * u[3]);
+    }
+    __syncthreads();
+    return;
+  }
+
+  if (g.ksplit == 1) load_epilogue();
+  float gsc = 1.f;
+  if (resid && !g.gate) gsc = tanhf(*g.gate_scalar);
+
+#pragma unroll
+  for (int q = 0; q < MT; ++q) {
+    const int it = tid + q * 256, fr = it >> 6, ln = it & 63;
+    const int c = fr / MT, i = fr % MT;
+    const int m = row_of(q), n = col_of(q);
+    const f32x4_t v = sum[q];
+    float sq = 0.f;
+    if (m < g.M && n < g.N) {
+      if (g.e_mode == PE_BF16) {
+        coherent_store_bf16x4(g.out_t + (size_t)m * g.ldo + n, v[0], v[1], v[2], v[3]);
+      } else if (g.e_mode == PE_F32) {
+        if (n + 4 <= g.N) {
+          coherent_store4(g.out_f + (size_t)m * g.ldof + n,
+                          f32x4_t{v[0] + e_b[q][0], v[1] + e_b[q][1], v[2] + e_b[q][2], v[3] + e_b[q][3]});
+        } else {
+          for (int r = 0; n + r < g.N; ++r)
+            coherent_store(g.out_f + (size_t)m * g.ldof + n + r, v[r] + (g.bias ? g.bias[n + r] : 0.f));
+        }
+      } else {  // PE_RESID
+        const f32x4_t gt = g.gate ? e_g[q] : f32x4_t{gsc, gsc, gsc, gsc};
+        f32x4_t xn;
+        xn[0] = e_x[q][0] + gt[0] * v[0];
+        xn[1] = e_x[q][1] + gt[1] * v[1];
+        xn[2] = e_x[q][2] + gt[2] * v[2];
+        xn[3] = e_x[q][3] + gt[3] * v[3];
+        coherent_store4(g.out_f + (size_t)m * g.ldof + n, xn);
+        coherent_store_bf16x4(g.p_out + (size_t)m * g.ldp + n, (1.f + e_s[q][0]) * xn[0], (1.f + e_s[q][1]) * xn[1],
+                              (1.f + e_s[q][2]) * xn[2], (1.f + e_s[q][3]) * xn[3]);
+        sq = xn[0] * xn[0] + xn[1] * xn[1] + xn[2] * xn[2] + xn[3] * xn[3];
+      }
+    }
+    if (resid) sm.rowsq[i * 16 + (ln & 15)][c * 4 + (ln >> 4)] = sq;
+  }
+  if (resid) {
+    // row sums of squares of the tile's 64 new columns, fixed order
+    __syncthreads();
+    if (tid < MT * 16 && tid < g.M) {
+      float s = 0.f;
+#pragma unroll
+      for (int h = 0; h < 16; ++h) s += sm.rowsq[tid][h];
+      coherent_store(g.sumsq_out + tile * 64 + tid, s);
+    }
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// attention: one (env, head, key split)
+// ---------------------------------------------------------------------------
+template <int HD>
+RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, PSmem& sm) {
+  using C = AttnCfg<HD>;
+  constexpr int KPS = C::KPS, KLD = C::KLD, VLD = C::VLD;
+  constexpr int KS = HD / 32, DT = HD / 16, CPR = HD / 8;
+  constexpr int KCH = KPS * CPR / 256;        // 16-byte K chunks per thread
+  constexpr int VCH = (KPS / 4) * CPR / 256;  // (4 keys x 8 dims) V groups per thread
+  static_assert(KCH >= 1 && VCH >= 1 && KPS * CPR % 256 == 0 && (KPS / 4) * CPR % 256 == 0, "attention tiling");
+  bf16_t* Ks = sm.at;
+  bf16_t* Vt = sm.at + KPS * KLD;
+  const int tid = local_tid(), lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, grp = lane >> 4;
+  const int split = item % a.nsplit;
+  const int j = (item / a.nsplit) % a.nq;
+  const int e = item / (a.nsplit * a.nq);
+  const int g = (j * a.nkv) / a.nq;
+  const int QB = (a.Hq + 15) / 16;
+  // the first ceil(P / kps) splits cover the prefix, the rest the self keys
+  const int nsp = (a.P + a.keys_per_split - 1) / a.keys_per_split;
+  const bool self_split = split >= nsp;
+  const int kbeg = self_split ? a.P + (split - nsp) * a.keys_per_split : split * a.keys_per_split;
+  const int kend = self_split ? min(a.P + a.S, kbeg + a.keys_per_split) : min(a.P, kbeg + a.keys_per_split);
+  const int slot = a.slot ? slots[e] : 0;
+  const bf16_t* pk = (const bf16_t*)a.pk + slot * a.p_slot_stride + e * a.p_env_stride;
+  const bf16_t* pv = (const bf16_t*)a.pv + slot * a.p_slot_stride + e * a.p_env_stride;
+  const bf16_t* sk = (const bf16_t*)a.sk;
+  const bf16_t* sv = (const bf16_t*)a.sv;
+  // prefix rows were written before the launch (plain loads), self rows by this
+  // launch's QKV phase (coherent loads); a split holds only one kind
+  const rsrc_t rK = self_split ? rsrc(sk + (size_t)e * a.S * a.s_ld) : rsrc(pk);
+  const rsrc_t rV = self_split ? rsrc(sv + (size_t)e * a.S * a.s_ld) : rsrc(pv);
+  const int ld_row = self_split ? a.s_ld : a.p_ld;
+  const int k_row0 = self_split ? a.P : 0;
+  auto row16 = [&](rsrc_t r, int kidx, int dc) -> u32x4_t {
+    const int off = boff(kidx < kend, ((size_t)(kidx - k_row0) * ld_row + g * HD + dc) * 2);
+    return self_split ? ld16<COH>(r, off) : ld16<PLAIN>(r, off);
+  };
+  // keys, values and queries of the split: one batch
+  u32x4_t kr[KCH];
+#pragma unroll
+  for (int r = 0; r < KCH; ++r) {
+    const int c = tid + r * 256, row = c / CPR, dc = (c % CPR) * 8;
+    const int kidx = kbeg + row;
+    kr[r] = row16(rK, kidx, dc);
+  }
+  u32x4_t vr[VCH][4];
+#pragma unroll
+  for (int r = 0; r < VCH; ++r) {
+    const int c = tid + r * 256, kq = c / CPR, dc = (c % CPR) * 8;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int kidx = kbeg + kq * 4 + i;
+      vr[r][i] = row16(rV, kidx, dc);
+    }
+  }
+  const rsrc_t rq = rsrc(a.q);
+  const int query = wave * 16 + l16;
+  const bool active = wave < QB;
+  bf16x8_t qf[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+    qf[ks] = ld_b8<COH>(rq, boff(query < a.Hq, ((size_t)(e * a.Hq + query) * a.ldq + j * HD + ks * 32 + grp * 8) * 2));
+  __syncthreads();  // LDS may still be read by this block's previous item
+#pragma unroll
+  for (int r = 0; r < KCH; ++r) {
+    const int c = tid + r * 256, row = c / CPR, dc = (c % CPR) * 8;
+    *(u32x4_t*)&Ks[row * KLD + dc] = kr[r];
+  }
+#pragma unroll
+  for (int r = 0; r < VCH; ++r) {
+    const int c = tid + r * 256, kq = c / CPR, dc = (c % CPR) * 8;
+    const bf16_t* h0 = (const bf16_t*)&vr[r][0];
+    const bf16_t* h1 = (const bf16_t*)&vr[r][1];
+    const bf16_t* h2 = (const bf16_t*)&vr[r][2];
+    const bf16_t* h3 = (const bf16_t*)&vr[r][3];
+#pragma unroll
+    for (int dd = 0; dd < 8; ++dd) {
+      u32x2_t w;
+      w[0] = (uint32_t)h0[dd] | ((uint32_t)h1[dd] << 16);
+      w[1] = (uint32_t)h2[dd] | ((uint32_t)h3[dd] << 16);
+      *(u32x2_t*)&Vt[(dc + dd) * VLD + kq * 4] = w;
+    }
+  }
+  __syncthreads();
+
+  // S^T = K Q^T per 32-key tile (lane: keys 4grp..+3 and 16+4grp..+3 of query l16),
+  // online softmax, O^T += V^T P^T
+  f32x4_t o[DT];
+  float mrow = -INFINITY, lrow = 0.f;
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const float sl2 = a.scale * 1.4426950408889634f;
+  const int nk = kend - kbeg;
+  if (active) {
+    for (int k0 = 0; k0 < nk; k0 += 32) {
+      f32x4_t s[2];
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+        s[st] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8_t kf = *(const bf16x8_t*)&Ks[(k0 + st * 16 + l16) * KLD + ks * 32 + grp * 8];
+          s[st] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], s[st], 0, 0, 0);
+        }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float x = s[st][r] * sl2;
+          if (k0 + st * 16 + grp * 4 + r >= nk) x = -INFINITY;
+          s[st][r] = x;
+          mx = fmaxf(mx, x);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mnew = fmaxf(mrow, mx);
+      const float corr = (mnew == -INFINITY) ? 1.f : exp2f(mrow - mnew);
+      float psum = 0.f;
+      float p[2][4];
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          p[st][r] = (s[st][r] == -INFINITY) ? 0.f : exp2f(s[st][r] - mnew);
+          psum += p[st][r];
+        }
+      psum += __shfl_xor(psum, 16, 64);
+      psum += __shfl_xor(psum, 32, 64);
+      lrow = lrow * corr + psum;
+      mrow = mnew;
+      bf16_t pb[8];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        pb[r] = f32_to_bf16(p[0][r]);
+        pb[4 + r] = f32_to_bf16(p[1][r]);
+      }
+      const bf16x8_t pf = *(const bf16x8_t*)pb;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        o[dt][0] *= corr;
+        o[dt][1] *= corr;
+        o[dt][2] *= corr;
+        o[dt][3] *= corr;
+        const bf16_t* vrow = &Vt[(dt * 16 + l16) * VLD + k0];
+        const u32x2_t lo = *(const u32x2_t*)(vrow + grp * 4);
+        const u32x2_t hi = *(const u32x2_t*)(vrow + 16 + grp * 4);
+        const u32x4_t vv = {lo[0], lo[1], hi[0], hi[1]};
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8_t*)&vv, pf, o[dt], 0, 0, 0);
+      }
+    }
+  }
+  bf16_t* out = (bf16_t*)a.out;
+  if (a.nsplit == 1) {
+    if (active && query < a.Hq) {
+      const float inv = 1.f / lrow;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+        coherent_store_bf16x4(out + (size_t)(e * a.Hq + query) * a.ldo + j * HD + dt * 16 + grp * 4, o[dt][0] * inv,
+                              o[dt][1] * inv, o[dt][2] * inv, o[dt][3] * inv);
+    }
+    __syncthreads();
+    return;
+  }
+  const int Hp = QB * 16;
+  const size_t pbase = ((size_t)e * a.nq + j) * a.nsplit;
+  if (active && query < a.Hq) {
+    float* po = a.part_o + ((pbase + split) * Hp + query) * HD;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) coherent_store4(po + dt * 16 + grp * 4, o[dt]);
+    if (grp == 0) {
+      coherent_store(&a.part_ml[((pbase + split) * Hp + query) * 2 + 0], mrow);
+      coherent_store(&a.part_ml[((pbase + split) * Hp + query) * 2 + 1], lrow);
+    }
+  }
+  if (!last_arrival(&a.counters[(e * a.nq + j) * kCounterStride], (unsigned)a.nsplit, &sm.flag)) {
+    __syncthreads();
+    return;
+  }
+  // merge: (max, sum) of every split and query, then weights, then outputs
+  {
+    float2 mlv[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int t = tid + r * 256, sp = t >> 6, qq = t & 63;
+      mlv[r] = ld_f2<COH>(rsrc(a.part_ml), boff(sp < a.nsplit && qq < a.Hq, ((pbase + sp) * Hp + qq) * 2 * 4));
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int t = tid + r * 256, sp = t >> 6, qq = t & 63;
+      sm.mg.ml[sp][qq][0] = (sp < a.nsplit && qq < a.Hq) ? mlv[r].x : -INFINITY;
+      sm.mg.ml[sp][qq][1] = mlv[r].y;
+    }
+  }
+  __syncthreads();
+  if (tid < a.Hq) {
+    float mmax = -INFINITY;
+    for (int sp = 0; sp < a.nsplit; ++sp) mmax = fmaxf(mmax, sm.mg.ml[sp][tid][0]);
+    float den = 0.f;
+    for (int sp = 0; sp < a.nsplit; ++sp) {
+      const float ms = sm.mg.ml[sp][tid][0];
+      const float wv = (ms == -INFINITY) ? 0.f : exp2f(ms - mmax);
+      sm.mg.wgt[sp][tid] = wv;
+      den += wv * sm.mg.ml[sp][tid][1];
+    }
+    const float inv = 1.f / den;
+    for (int sp = 0; sp < a.nsplit; ++sp) sm.mg.wgt[sp][tid] *= inv;
+  }
+  __syncthreads();
+  const int total = a.Hq * (HD / 4);
+  for (int base = 0; base < total; base += 4 * 256) {
+    f32x4_t num[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) num[r] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int sp0 = 0; sp0 < a.nsplit; sp0 += 8) {
+      f32x4_t pvl[4][8];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int el = base + r * 256 + tid;
+        const int qq = el / (HD / 4), d = (el % (HD / 4)) * 4;
+#pragma unroll
+        for (int s8 = 0; s8 < 8; ++s8)
+          pvl[r][s8] = ld_f4<COH>(rsrc(a.part_o),
+                                  boff(el < total && sp0 + s8 < a.nsplit, (((pbase + sp0 + s8) * Hp + qq) * HD + d) * 4));
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int el = base + r * 256 + tid;
+        const int qq = el < total ? el / (HD / 4) : 0;
+#pragma unroll
+        for (int s8 = 0; s8 < 8; ++s8) {
+          if (sp0 + s8 >= a.nsplit) break;
+          const float wv = sm.mg.wgt[sp0 + s8][qq];
+          num[r][0] += wv * pvl[r][s8][0];
+          num[r][1] += wv * pvl[r][s8][1];
+          num[r][2] += wv * pvl[r][s8][2];
+          num[r][3] += wv * pvl[r][s8][3];
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int el = base + r * 256 + tid;
+      if (el >= total) continue;
+      const int qq = el / (HD / 4), d = (el % (HD / 4)) * 4;
+      coherent_store_bf16x4(out + (size_t)(e * a.Hq + qq) * a.ldo + j * HD + d, num[r][0], num[r][1], num[r][2],
+                            num[r][3]);
+    }
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// the persistent kernel
+// ---------------------------------------------------------------------------
+constexpr int kDescChunks = (int)(sizeof(Phase) / 16);
+static_assert(sizeof(Phase) % 16 == 0 && kDescChunks <= 256, "phase descriptor size");
+
+template <int MT>
+__global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __restrict__ phases, int nphase,
+                                                              const int* __restrict__ env_slot, int nenv,
+                                                              unsigned* bar, int* err, unsigned long long* times) {
+  __shared__ PSmem sm;
+  __shared__ Phase desc[3];
+  __shared__ int slots[64];
+  __shared__ int ok;
+  const int tid = threadIdx.x;
+  const bool stamp = times != nullptr && blockIdx.x == 0 && tid == 0;
+  if (stamp) times[0] = wall_clock64();
+  for (int d = 0; d < 2 && d < nphase; ++d)
+    if (tid < kDescChunks)
+      reinterpret_cast<u32x4_t*>(&desc[d])[tid] = reinterpret_cast<const u32x4_t*>(&phases[d])[tid];
+  if (env_slot && tid < nenv && tid < 64) slots[tid] = env_slot[tid];
+  __syncthreads();
+
+  // weights of this block's first item of the coming GEMM phase (zero otherwise)
+  bf16x8_t wreg[4][4];
+  auto prefetch = [&](const Phase& nx) {
+    if (uni(nx.type) == PH_GEMM && (int)blockIdx.x < uni(nx.items)) {
+      load_weights(make_uniform(nx.g), blockIdx.x, wreg);
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int f = 0; f < 4; ++f) wreg[c][f] = bf16x8_t{};
+    }
+  };
+  prefetch(desc[0]);
+
+  for (int p = 0; p < nphase; ++p) {
+    const Phase& ph = desc[p % 3];
+    const int type = uni(ph.type), items = uni(ph.items);
+    if (type == PH_GEMM) {
+      const PGemm g = make_uniform(ph.g);
+      for (int item = blockIdx.x; item < items; item += gridDim.x) {
+        if (item != (int)blockIdx.x) load_weights(g, item, wreg);
+        if (g.kw == 2)
+          gemm_item<MT, 2>(g, item, wreg, sm);
+        else
+          gemm_item<MT, 1>(g, item, wreg, sm);
+      }
+    } else if (type == PH_ATTN) {
+      const AttnArgs a = make_uniform(ph.at);
+      for (int item = blockIdx.x; item < items; item += gridDim.x) {
+        switch (a.hd) {
+          case 32: attn_item<32>(a, item, slots, sm); break;
+          case 64: attn_item<64>(a, item, slots, sm); break;
+          case 128: attn_item<128>(a, item, slots, sm); break;
+          default: attn_item<256>(a, item, slots, sm); break;
+        }
+      }
+    } else if (type == PH_ROWSTATS) {
+      const PRowstats r = make_uniform(ph.rs);
+      const int ntile = r.N >> 6;
+      for (int item = blockIdx.x; item < items; item += gridDim.x) {
+        if (item < ntile)
+          rowstats_item(r, item, sm);
+        else
+          convert_item(r, item - ntile);
+      }
+    }
+    if (p + 1 == nphase) break;
+    // barrier between phases p and p + 1; while waiting, fetch descriptor p + 2
+    // and this block's weights of phase p + 1
+    wait_memory();
+    __syncthreads();
+    const unsigned gen = (unsigned)(p + 1);
+    if (tid == 0) barrier_arrive(bar, gen);
+    u32x4_t dreg = {0, 0, 0, 0};
+    if (p + 2 < nphase && tid < kDescChunks) dreg = reinterpret_cast<const u32x4_t*>(&phases[p + 2])[tid];
+    prefetch(desc[(p + 1) % 3]);
+    if (tid == 0) ok = barrier_wait(bar, gen, err);
+    __syncthreads();
+    if (!ok) return;
+    if (p + 2 < nphase && tid < kDescChunks) reinterpret_cast<u32x4_t*>(&desc[(p + 2) % 3])[tid] = dreg;
+    if (stamp) times[p + 1] = wall_clock64();
+  }
+  if (stamp) times[nphase] = wall_clock64();
+  // re-arm the barrier: the last block to get here has seen every block pass
+  // every barrier, and zeroes the counters for the next launch
+  wait_memory();
+  __syncthreads();
+  if (tid == 0) {
+    unsigned* ex = bar + 64 * (2 + kBarrierGroups);
+    const unsigned prev = __hip_atomic_fetch_add(ex, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (prev == gridDim.x - 1) {
+      for (int i = 0; i < 2 + kBarrierGroups; ++i)
+        __hip_atomic_store(bar + 64 * i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(ex, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+const void* kernel_for(int mt) {
+  switch (mt) {
+    case 1: return (const void*)persistent_step_kernel<1>;
+    case 2: return (const void*)persistent_step_kernel<2>;
+    case 4: return (const void*)persistent_step_kernel<4>;
+    default: return nullptr;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_persistent(const Phase* phases, int nphase, const int* env_slot, int nenv, int mt, int blocks,
+                             unsigned* bar, int* err, unsigned long long* times, hipStream_t s) {
+  const void* fn = kernel_for(mt);
+  if (!fn || nenv > 64 || nphase < 1) return hipErrorInvalidValue;
+  void* args[] = {(void*)&phases, (void*)&nphase, (void*)&env_slot, (void*)&nenv,
+                  (void*)&bar,    (void*)&err,    (void*)&times};
+  return hipLaunchCooperativeKernel(fn, dim3(blocks), dim3(256), args, 0, s);
+}
+
+int persistent_max_blocks(int mt) {
+  const void* fn = kernel_for(mt);
+  if (!fn) return 0;
+  int per_cu = 0, dev = 0, cus = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 256, 0) != hipSuccess) return 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  return per_cu * cus;
+}
+
+}  // namespace ravel

@@ -14,6 +14,7 @@
 #include <vector>
 
 #include "kernels.h"
+#include "persistent.h"
 #include "ravel.h"
 
 using namespace ravel;
@@ -327,6 +328,21 @@ struct ravel_buffer {
   int attn_nsplit = 1, attn_kps = 0;
   bool mod_all = false;
   int mod_ld = 0;
+  // persistent few-row path
+  bool persistent = false;
+  std::vector<Phase> phases;
+  Phase* d_phases = nullptr;
+  unsigned* pbar = nullptr;
+  int* perr = nullptr;
+  float* sumsq[2] = {nullptr, nullptr};
+  bf16_t* pnorm = nullptr;             // p = bf16((1 + scale) * x) of the next norm, [B*H][w]
+  std::vector<void*> pallocs;          // device memory of the persistent path
+  int pblocks = 0, pmt = 4;
+  double p_bytes = 0, p_flops = 0;
+  // per phase: class name and algorithmic bytes / flops; device time stamps
+  std::vector<std::string> pnames;
+  std::vector<double> ph_bytes, ph_flops;
+  unsigned long long* ptimes = nullptr;
   // host
   int64_t t_host = 0;
   std::vector<int> active;
@@ -687,6 +703,347 @@ ravel_status acquire_locked(ravel_buffer* b, int env, void** k, void** v, hipStr
   const size_t off = ((size_t)inactive * b->B + env) * b->ctx_elems * m->elt;
   *k = (char*)b->ctx_k + off;
   *v = (char*)b->ctx_v + off;
+  return RAVEL_OK;
+}
+
+
+// ---------------------------------------------------------------------------
+// Persistent few-row path: phase list of the transformer layers
+// ---------------------------------------------------------------------------
+bool persistent_eligible(const ravel_buffer* b) {
+  const ravel_model* m = b->m;
+  const ravel_config& c = m->cfg;
+  if (!m->bf16 || c.model_kind != RAVEL_TRANSFORMER || !b->mod_all) return false;
+  const int BH = b->B * c.horizon, hd = c.head_dim;
+  const int qd = c.n_q_heads * hd, kvd = c.n_kv_heads * hd;
+  if (BH > 64 || b->B > 64) return false;
+  if (hd != 32 && hd != 64 && hd != 128 && hd != 256) return false;
+  // 64-column output tiles everywhere but the output head; K ranges of 256 or
+  // 512 with at most kMaxKSplit of them
+  if (c.width % 64 || qd % 64 || (qd + 2 * kvd) % 64 || c.mlp_dim % 32) return false;
+  for (int K : {c.width, qd, c.mlp_dim})
+    if (K % 8 || (K + 511) / 512 > kMaxKSplit) return false;
+  if (c.width > 4096) return false;  // row sums of squares: at most 64 tiles
+  if (c.n_fop > attn_keys_per_split_max(hd)) return false;
+  const int kmax = attn_keys_per_split_max(hd);
+  if ((c.prefix_len + kmax - 1) / kmax + (c.horizon + kmax - 1) / kmax > kMaxAttnSplit) return false;
+  return true;
+}
+
+template <class T>
+ravel_status palloc(ravel_buffer* b, T** p, size_t bytes, bool zero) {
+  void* q = nullptr;
+  HIP_TRY(hipMalloc(&q, std::max<size_t>(bytes, 256)));
+  b->pallocs.push_back(q);
+  if (zero) HIP_TRY(hipMemset(q, 0, std::max<size_t>(bytes, 256)));
+  *p = (T*)q;
+  return RAVEL_OK;
+}
+
+// Phase list of the persistent kernel (see persistent.hip), with its workspaces.
+ravel_status build_persistent(ravel_buffer* b) {
+  ravel_model* m = b->m;
+  const ravel_config& c = m->cfg;
+  const int B = b->B, H = c.horizon, w = c.width, D = c.action_dim, BH = B * H, F = c.mlp_dim, hd = c.head_dim;
+  const int qd = c.n_q_heads * hd, kvd = c.n_kv_heads * hd, qkvd = qd + 2 * kvd;
+  const int ldm = b->mod_ld;
+  int mt = (BH + 15) / 16;
+  if (mt == 3) mt = 4;
+  b->pmt = mt;
+  b->pblocks = std::min(persistent_max_blocks(mt), 256);
+  if (b->pblocks < 64) return fail(RAVEL_E_STATE, "persistent kernel does not fit");
+  auto tiles = [](int n) { return (n + 63) / 64; };
+  RV_TRY(palloc(b, &b->pbar, kBarrierWords * 4, true));
+  RV_TRY(palloc(b, &b->perr, 64, true));
+  RV_TRY(palloc(b, &b->sumsq[0], (size_t)(w / 64) * 64 * 4, true));
+  RV_TRY(palloc(b, &b->sumsq[1], (size_t)(w / 64) * 64 * 4, true));
+  RV_TRY(palloc(b, &b->pnorm, (size_t)BH * w * 2, true));
+  // bf16 copies of the norm shifts: chunk 2l (attention) and 2l + 1 (MLP) of
+  // layer l, 2L the final norm; in the modulation rows they sit 3w apart
+  // starting at column w
+  const int nshift = 2 * c.layers + 1;
+  bf16_t* pshift = nullptr;
+  RV_TRY(palloc(b, &pshift, (size_t)nshift * BH * w * 2, true));
+  auto shift_of = [&](int chunk) -> const bf16_t* { return pshift + (size_t)chunk * BH * w; };
+  size_t part = 0;
+  int max_tiles = 1;
+  int cur = 0;
+  std::vector<Phase>& P = b->phases;
+  P.clear();
+  b->pnames.clear();
+  auto push = [&](const Phase& ph, const char* name) {
+    P.push_back(ph);
+    b->pnames.push_back(name);
+  };
+  auto gemm = [&](const void* A, int lda, const bf16_t* shift, bool norm, const void* W, int N, int K, int e_mode) {
+    Phase ph;
+    memset(&ph, 0, sizeof ph);
+    ph.type = PH_GEMM;
+    PGemm& g = ph.g;
+    g.a_mode = norm ? PA_NORM : PA_BF16;
+    g.A = (const bf16_t*)A;
+    g.lda = lda;
+    g.shift = shift;
+    g.ld_shift = w;
+    g.sumsq_in = b->sumsq[cur];
+    g.eps = c.rms_eps;
+    g.W = (const bf16_t*)W;
+    g.ldw = K;
+    g.M = BH;
+    g.N = N;
+    g.K = K;
+    const int ks1 = (K + 255) / 256;
+    g.kw = (norm || (ks1 <= kMaxKSplit && tiles(N) * ks1 <= b->pblocks)) ? 1 : 2;
+    if ((K + 256 * g.kw - 1) / (256 * g.kw) > kMaxKSplit) g.kw = 0;  // rejected below
+    g.ksplit = (K + 256 * g.kw - 1) / (256 * g.kw);
+    g.e_mode = e_mode;
+    g.counters = nullptr;  // patched below
+    ph.items = tiles(N) * g.ksplit;
+    part = std::max(part, (size_t)g.ksplit * tiles(N) * mt * 4 * 64 * 4);
+    max_tiles = std::max(max_tiles, tiles(N));
+    return ph;
+  };
+  auto resid = [&](Phase& ph, const float* gate, const float* gate_scalar, int ns_mode, const float* ns) {
+    PGemm& g = ph.g;
+    g.out_f = b->x;
+    g.ldof = w;
+    g.gate = gate;
+    g.ldg = ldm;
+    g.gate_scalar = gate_scalar;
+    g.ns_mode = ns_mode;
+    g.ns = ns;
+    g.ldns = ldm;
+    g.p_out = (bf16_t*)b->pnorm;
+    g.ldp = w;
+    g.sumsq_out = b->sumsq[cur ^ 1];
+    cur ^= 1;
+  };
+  const float* mod0 = b->mod;  // layer 0 chunks: scale, shift, gate, scale, shift, gate
+  // row sums of squares of the input projection and p of the first norm
+  {
+    Phase ph;
+    memset(&ph, 0, sizeof ph);
+    ph.type = PH_ROWSTATS;
+    ph.rs.x = b->x;
+    ph.rs.ldx = w;
+    ph.rs.M = BH;
+    ph.rs.N = w;
+    ph.rs.ns_mode = NS_ROW;
+    ph.rs.ns = mod0;
+    ph.rs.ldns = ldm;
+    ph.rs.p = (bf16_t*)b->pnorm;
+    ph.rs.ldp = w;
+    ph.rs.sumsq_out = b->sumsq[cur];
+    ph.rs.cvt_in = b->mod + w;
+    ph.rs.cvt_ld = ldm;
+    ph.rs.cvt_stride = 3 * w;
+    ph.rs.cvt_chunks = nshift;
+    ph.rs.cvt_out = pshift;
+    ph.items = w / 64 + (int)(((size_t)nshift * BH * w + 8191) / 8192);
+    push(ph, "rowstats");
+  }
+  int max_attn_parts = 1, max_attn_heads = 1;
+  auto attn_phase = [&](AttnArgs a) {
+    Phase ph;
+    memset(&ph, 0, sizeof ph);
+    ph.type = PH_ATTN;
+    a.B = B;
+    a.nq = c.n_q_heads;
+    a.nkv = c.n_kv_heads;
+    a.hd = hd;
+    a.scale = 1.0f / sqrtf((float)hd);
+    // splits of at most kmax keys (a multiple of 32) over the prefix, then over
+    // the self keys: no split holds both kinds
+    const int kmax = attn_keys_per_split_max(hd);
+    const int np = std::max((a.P + kmax - 1) / kmax, 1);
+    a.keys_per_split = std::min(kmax, (((a.P + np - 1) / np + 31) / 32) * 32);
+    a.keys_per_split = std::max(a.keys_per_split, std::min(kmax, ((a.S + 31) / 32) * 32));
+    a.nsplit = (a.P + a.keys_per_split - 1) / a.keys_per_split + (a.S + a.keys_per_split - 1) / a.keys_per_split;
+    ph.at = a;
+    ph.items = B * c.n_q_heads * a.nsplit;
+    max_attn_parts = std::max(max_attn_parts, B * c.n_q_heads * a.nsplit);
+    max_attn_heads = std::max(max_attn_heads, B * c.n_q_heads);
+    return ph;
+  };
+  const size_t ctx_layer = (size_t)c.prefix_len * kvd;
+  for (int l = 0; l < c.layers; ++l) {
+    const LayerW& L = m->layers[l];
+    const float* mod = b->mod + (size_t)l * 6 * w;
+    const float* next_scale = b->mod + (size_t)(l + 1) * 6 * w;  // next layer's (or the final) chunk 0
+    {
+      Phase ph = gemm(b->pnorm, w, shift_of(2 * l), true, L.qkv_w, qkvd, w, PE_BF16);
+      ph.g.out_t = (bf16_t*)b->qkv;
+      ph.g.ldo = qkvd;
+      push(ph, "qkv");
+    }
+    {
+      AttnArgs a;
+      memset(&a, 0, sizeof a);
+      a.q = b->qkv;
+      a.ldq = qkvd;
+      a.Hq = H;
+      a.pk = (const char*)b->ctx_k + l * ctx_layer * m->elt;
+      a.pv = (const char*)b->ctx_v + l * ctx_layer * m->elt;
+      a.p_env_stride = (long long)b->ctx_elems;
+      a.p_slot_stride = (long long)b->ctx_elems * B;
+      a.slot = b->slot;
+      a.P = c.prefix_len;
+      a.p_ld = kvd;
+      a.sk = (const char*)b->qkv + (size_t)qd * m->elt;
+      a.sv = (const char*)b->qkv + (size_t)(qd + kvd) * m->elt;
+      a.S = H;
+      a.s_ld = qkvd;
+      a.out = b->att;
+      a.ldo = qd;
+      push(attn_phase(a), "self_attn");
+    }
+    {
+      Phase ph = gemm(b->att, qd, nullptr, false, L.o_w, w, qd, PE_RESID);
+      if (L.adapter >= 0)
+        resid(ph, mod + 2 * w, nullptr, NS_COL, L.gamma);
+      else
+        resid(ph, mod + 2 * w, nullptr, NS_ROW, mod + 3 * w);
+      push(ph, "o_proj");
+    }
+    if (L.adapter >= 0) {
+      {
+        Phase ph = gemm(b->pnorm, w, nullptr, true, L.qa_w, qd, w, PE_BF16);
+        ph.g.out_t = (bf16_t*)b->qa;
+        ph.g.ldo = qd;
+        push(ph, "q_adapter");
+      }
+      {
+        AttnArgs a;
+        memset(&a, 0, sizeof a);
+        const int ld = m->n_ad * 2 * kvd;
+        a.q = b->qa;
+        a.ldq = qd;
+        a.Hq = H;
+        a.pk = (const char*)b->kva + (size_t)L.adapter * 2 * kvd * m->elt;
+        a.pv = (const char*)b->kva + (size_t)(L.adapter * 2 * kvd + kvd) * m->elt;
+        a.p_env_stride = (long long)c.n_fop * ld;
+        a.P = c.n_fop;
+        a.p_ld = ld;
+        a.S = 0;
+        a.out = b->att;
+        a.ldo = qd;
+        push(attn_phase(a), "cross_attn");
+      }
+      {
+        Phase ph = gemm(b->att, qd, nullptr, false, L.oa_w, w, qd, PE_RESID);
+        resid(ph, nullptr, L.alpha, NS_ROW, mod + 3 * w);
+        push(ph, "o_adapter");
+      }
+    }
+    {
+      Phase ph = gemm(b->pnorm, w, shift_of(2 * l + 1), true, L.gu_w, 2 * F, w, PE_GEGLU);
+      ph.g.out_t = (bf16_t*)b->u;
+      ph.g.ldo = F;
+      push(ph, "gate_up");
+    }
+    {
+      Phase ph = gemm(b->u, F, nullptr, false, L.down_w, w, F, PE_RESID);
+      resid(ph, mod + 5 * w, nullptr, NS_ROW, next_scale);
+      push(ph, "down");
+    }
+  }
+  // final adaptive norm (chunks scale, shift) and output head
+  {
+    Phase ph = gemm(b->pnorm, w, shift_of(2 * c.layers), true, m->out_w, D, w, PE_F32);
+    ph.g.out_f = b->v;
+    ph.g.ldof = D;
+    ph.g.bias = m->out_b;
+    push(ph, "out_head");
+  }
+  for (auto& ph : P)
+    if (ph.type == PH_GEMM && ph.g.kw == 0) return fail(RAVEL_E_STATE, "persistent: K range too long");
+  // workspaces, patched into the list
+  float *gpart, *ao, *aml;
+  unsigned *gcnt, *acnt;
+  const int Hp = ((H + 15) / 16) * 16;
+  RV_TRY(palloc(b, &gpart, part * 4, false));
+  RV_TRY(palloc(b, &gcnt, (size_t)max_tiles * 4 * kCounterStride, true));
+  RV_TRY(palloc(b, &ao, (size_t)max_attn_parts * Hp * hd * 4, false));
+  RV_TRY(palloc(b, &aml, (size_t)max_attn_parts * Hp * 2 * 4, false));
+  RV_TRY(palloc(b, &acnt, (size_t)max_attn_heads * 4 * kCounterStride, true));
+  for (auto& ph : P) {
+    if (ph.type == PH_GEMM) {
+      ph.g.partial = gpart;
+      ph.g.counters = gcnt;
+    } else if (ph.type == PH_ATTN) {
+      ph.at.part_o = ao;
+      ph.at.part_ml = aml;
+      ph.at.counters = acnt;
+    }
+  }
+  RV_TRY(palloc(b, &b->d_phases, P.size() * sizeof(Phase), false));
+  HIP_TRY(hipMemcpy(b->d_phases, P.data(), P.size() * sizeof(Phase), hipMemcpyHostToDevice));
+  // algorithmic work of the persistent kernel and of each phase (for profiling):
+  // weights (bf16) for GEMMs, keys and values (bf16) for attention
+  double by = 0, fl = 0;
+  b->ph_bytes.assign(P.size(), 0.0);
+  b->ph_flops.assign(P.size(), 0.0);
+  for (size_t i = 0; i < P.size(); ++i) {
+    const Phase& ph = P[i];
+    if (ph.type == PH_GEMM) {
+      b->ph_bytes[i] = (double)ph.g.N * ph.g.K * 2;
+      b->ph_flops[i] = 2.0 * ph.g.M * ph.g.N * ph.g.K;
+    } else if (ph.type == PH_ATTN) {
+      const int nk = ph.at.P + ph.at.S;
+      b->ph_bytes[i] = (double)B * nk * kvd * 4;
+      b->ph_flops[i] = 4.0 * B * c.n_q_heads * H * nk * hd;
+    }
+    by += b->ph_bytes[i];
+    fl += b->ph_flops[i];
+  }
+  b->p_bytes = by;
+  b->p_flops = fl;
+  RV_TRY(palloc(b, &b->ptimes, (P.size() + 1) * sizeof(unsigned long long), true));
+  return RAVEL_OK;
+}
+
+ravel_status enqueue_persistent_step(ravel_buffer* b, const void* fop, float* action, hipStream_t s,
+                                     KernelRecorder* rec) {
+  ravel_model* m = b->m;
+  const ravel_config& c = m->cfg;
+  const int B = b->B, H = c.horizon, w = c.width, D = c.action_dim, BH = B * H;
+  const int kvd = c.n_kv_heads * c.head_dim;
+  const double elt = (double)m->elt;
+  REC_BEGIN("delta_hidden", (double)B * w * (8 + elt), (double)B * w * 4);
+  HIP_TRY(launch_delta_hidden<bf16_t>(b->t, b->t_obs, B, H, c.delta_bias, m->d_w1, m->d_b1, w, (bf16_t*)b->h1, s));
+  REC_END();
+  {
+    GemmArgs e = epi_args(EPI_COND);
+    e.bias = m->d_b2;
+    e.out_t = b->cond;
+    e.ldo_t = w;
+    e.ctau = m->ctau;
+    e.H = H;
+    RV_TRY(run_gemm<bf16_t>(b, s, rec, "cond", b->h1, w, m->d_w2, w, B, w, w, e));
+  }
+  REC_BEGIN("in_proj", (double)BH * (D + w) * 4, 2.0 * BH * w * D);
+  HIP_TRY(launch_in_proj(b->X, b->t, B, H, D, m->in_w, m->in_b, w, b->x, s));
+  REC_END();
+  {
+    GemmArgs e = epi_args(EPI_F32);
+    e.bias = m->mod_all_b;
+    e.out_f = b->mod;
+    e.ldo_f = b->mod_ld;
+    RV_TRY(run_gemm<bf16_t>(b, s, rec, "mod_all", b->cond, w, m->mod_all_w, w, BH, b->mod_ld, w, e));
+  }
+  if (m->n_ad > 0) {
+    GemmArgs e = epi_args(EPI_T);
+    e.out_t = b->kva;
+    e.ldo_t = m->n_ad * 2 * kvd;
+    RV_TRY(run_gemm<bf16_t>(b, s, rec, "fop_kv", fop, w, m->kva_w, w, B * c.n_fop, m->n_ad * 2 * kvd, w, e));
+  }
+  REC_BEGIN("persistent_layers", b->p_bytes, b->p_flops);
+  HIP_TRY(launch_persistent(b->d_phases, (int)b->phases.size(), b->slot, B, b->pmt, b->pblocks, b->pbar, b->perr,
+                            rec ? b->ptimes : nullptr, s));
+  REC_END();
+  REC_BEGIN("euler_release", (double)B * H * D * 12 + (double)B * D * 4, (double)B * H * D * 2);
+  HIP_TRY(launch_euler_release(b->X, b->v, b->t, B, H, D, b->seed, action, b->ticket, s));
+  REC_END();
   return RAVEL_OK;
 }
 
@@ -1111,6 +1468,19 @@ ravel_status ravel_buffer_create(ravel_model* m, int32_t batch, uint64_t seed, r
   }
   if (hipStreamCreateWithFlags(&b->cap_stream, hipStreamNonBlocking) != hipSuccess)
     return bail(fail(RAVEL_E_HIP, "stream create"));
+  if (persistent_eligible(b)) {
+    if (build_persistent(b) == RAVEL_OK) {
+      b->persistent = true;
+    } else {
+      for (void* p : b->pallocs) (void)hipFree(p);
+      b->pallocs.clear();
+      b->d_phases = nullptr;
+      b->pbar = nullptr;
+      b->perr = nullptr;
+      b->persistent = false;
+    }
+    if (const char* ev = getenv("RAVEL_NO_PERSISTENT")) b->persistent = b->persistent && atoi(ev) == 0;
+  }
   if (const char* ev = getenv("RAVEL_SYNC_CONTEXT")) b->sync_ctx = atoi(ev) != 0;
   if (const char* ev = getenv("RAVEL_NO_GRAPH")) b->use_graph = atoi(ev) == 0;
   if (const char* ev = getenv("RAVEL_DEBUG")) b->debug = atoi(ev) != 0;
@@ -1130,6 +1500,7 @@ void ravel_buffer_destroy(ravel_buffer* b) {
     if (b->retire[e]) (void)hipEventDestroy(b->retire[e]);
   }
   if (b->cap_stream) (void)hipStreamDestroy(b->cap_stream);
+  for (void* p : b->pallocs) (void)hipFree(p);
   if (b->arena) (void)hipFree(b->arena);
   delete b;
 }
@@ -1141,6 +1512,10 @@ ravel_status ravel_buffer_set_option(ravel_buffer* b, int32_t option, int64_t va
     case RAVEL_OPT_SYNC_CONTEXT: b->sync_ctx = value != 0; return RAVEL_OK;
     case RAVEL_OPT_USE_GRAPH: b->use_graph = value != 0; return RAVEL_OK;
     case RAVEL_OPT_DEBUG: b->debug = value != 0; return RAVEL_OK;
+    case RAVEL_OPT_PERSISTENT:
+      if (value != 0 && !b->d_phases) return fail(RAVEL_E_STATE, "persistent path not available for this model/batch");
+      b->persistent = value != 0;
+      return RAVEL_OK;
     default: return fail(RAVEL_E_INVALID, "unknown option");
   }
 }
@@ -1191,7 +1566,9 @@ ravel_status ravel_step(ravel_buffer* b, const void* fop, float* action, void* s
     for (int e = 0; e < b->B; ++e)
       if (!b->has_ctx[e]) return fail(RAVEL_E_STATE, "env " + std::to_string(e) + " has no context yet");
   }
-  if (b->use_graph) {
+  if (b->persistent) {
+    RV_TRY(enqueue_persistent_step(b, fop, action, s, nullptr));
+  } else if (b->use_graph) {
     GraphEntry* ge = nullptr;
     for (auto& g : b->graphs)
       if (g.fop == fop && g.action == action) ge = &g;
@@ -1252,16 +1629,32 @@ ravel_status ravel_fop_encode(ravel_buffer* b, const float* obs, void* fop_token
   return RAVEL_OK;
 }
 
+namespace {
+ravel_status check_persistent_error(ravel_buffer* b) {
+  if (!b->perr) return RAVEL_OK;
+  int e = 0;
+  HIP_TRY(hipMemcpy(&e, b->perr, 4, hipMemcpyDeviceToHost));
+  if (e) {
+    // the blocks that gave up left the barrier counters behind: re-arm them
+    HIP_TRY(hipMemset(b->pbar, 0, kBarrierWords * 4));
+    HIP_TRY(hipMemset(b->perr, 0, 64));
+    return fail(RAVEL_E_HIP, "persistent kernel: a grid barrier timed out");
+  }
+  return RAVEL_OK;
+}
+}  // namespace
+
 ravel_status ravel_buffer_sync(ravel_buffer* b) {
   if (!b) return fail(RAVEL_E_INVALID, "null buffer");
   HIP_TRY(hipDeviceSynchronize());
-  return RAVEL_OK;
+  return check_persistent_error(b);
 }
 
 ravel_status ravel_debug_state(ravel_buffer* b, float* X_host, int64_t* t, int64_t* t_obs_host) {
   if (!b) return fail(RAVEL_E_INVALID, "null buffer");
   const ravel_config& c = b->m->cfg;
   HIP_TRY(hipDeviceSynchronize());
+  RV_TRY(check_persistent_error(b));
   if (X_host) HIP_TRY(hipMemcpy(X_host, b->X, (size_t)b->B * c.horizon * c.action_dim * 4, hipMemcpyDeviceToHost));
   if (t) HIP_TRY(hipMemcpy(t, b->t, 8, hipMemcpyDeviceToHost));
   if (t_obs_host) HIP_TRY(hipMemcpy(t_obs_host, b->t_obs, (size_t)b->B * 8, hipMemcpyDeviceToHost));
@@ -1397,7 +1790,8 @@ ravel_status ravel_profile_step(ravel_buffer* b, const void* fop, float* action,
   }
   KernelRecorder rec;
   rec.stream = s;
-  ravel_status st = enqueue_step(b, fop, action, s, &rec);
+  ravel_status st = b->persistent ? enqueue_persistent_step(b, fop, action, s, &rec)
+                                  : enqueue_step(b, fop, action, s, &rec);
   b->t_host += 1;
   hipError_t he = hipStreamSynchronize(s);
   const int32_t cap = *n;
@@ -1414,6 +1808,42 @@ ravel_status ravel_profile_step(ravel_buffer* b, const void* fop, float* action,
     ++k;
     (void)hipEventDestroy(r.a);
     (void)hipEventDestroy(r.b);
+  }
+  // persistent kernel: one more record per phase class ("persistent/<class>"),
+  // timed by block 0's stamps after each phase barrier; these split the
+  // "persistent_layers" record and do not add to it
+  if (st == RAVEL_OK && he == hipSuccess && b->persistent) {
+    const size_t np = b->phases.size();
+    std::vector<unsigned long long> ts(np + 1);
+    int dev = 0, khz = 0;
+    he = hipMemcpy(ts.data(), b->ptimes, ts.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost);
+    if (he == hipSuccess) he = hipGetDevice(&dev);
+    if (he == hipSuccess) he = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev);
+    if (he == hipSuccess && khz > 0) {
+      std::vector<std::string> order;
+      std::map<std::string, std::array<double, 3>> agg;
+      for (size_t i = 0; i < np; ++i) {
+        const std::string nm = "persistent/" + b->pnames[i];
+        if (!agg.count(nm)) {
+          order.push_back(nm);
+          agg[nm] = {0.0, 0.0, 0.0};
+        }
+        agg[nm][0] += (double)(ts[i + 1] - ts[i]) / (double)khz;
+        agg[nm][1] += b->ph_bytes[i];
+        agg[nm][2] += b->ph_flops[i];
+      }
+      for (auto& nm : order) {
+        if (records && k < cap) {
+          ravel_kernel_record& o = records[k];
+          memset(&o, 0, sizeof o);
+          snprintf(o.name, sizeof o.name, "%s", nm.c_str());
+          o.ms = (float)agg[nm][0];
+          o.bytes = agg[nm][1];
+          o.flops = agg[nm][2];
+        }
+        ++k;
+      }
+    }
   }
   *n = records ? std::min(k, cap) : k;
   if (st != RAVEL_OK) return st;

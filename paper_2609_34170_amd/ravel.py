@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libravel.so
 
 F32, BF16 = 0, 1
 TRANSFORMER, ANALYTIC_OT, ANALYTIC_LINEAR = 0, 1, 2
-OPT_SYNC_CONTEXT, OPT_USE_GRAPH, OPT_DEBUG = 1, 2, 3
+OPT_SYNC_CONTEXT, OPT_USE_GRAPH, OPT_DEBUG, OPT_PERSISTENT = 1, 2, 3, 4
 
 _STATUS = {0: "OK", -1: "E_INVALID", -2: "E_NOMEM", -3: "E_HIP", -4: "E_SHAPE", -5: "E_STATE"}
 
