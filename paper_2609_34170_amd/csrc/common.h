@@ -15,12 +15,14 @@ typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2_t;
 
 RAVEL_DEV float bf16_to_f32(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
-// float -> bfloat16, round to nearest even (inputs here are finite).
-RAVEL_DEV bf16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
+// float -> bfloat16, round to nearest even (v_cvt_pk_bf16_f32).
+typedef __attribute__((__vector_size__(2 * sizeof(float)))) float f32x2_t;
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2_t;
+RAVEL_DEV uint32_t pack_bf16x2(float lo, float hi) {
+  const bf16x2_t r = __builtin_convertvector((f32x2_t{lo, hi}), bf16x2_t);
+  return __builtin_bit_cast(uint32_t, r);
 }
+RAVEL_DEV bf16_t f32_to_bf16(float f) { return (bf16_t)(pack_bf16x2(f, 0.f) & 0xFFFFu); }
 
 // Activation element type traits: float (fp32 models) or bf16_t.
 template <typename T> struct act;

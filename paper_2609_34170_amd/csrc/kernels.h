@@ -84,6 +84,7 @@ struct AttnArgs {
   float* part_o;                   // [B*nq*nsplit][Hq_pad][hd]
   float* part_ml;                  // [B*nq*nsplit][Hq_pad][2]
   unsigned* counters;              // [B*nq]
+  int coop;                        // persistent kernel: the splits of a head merge together
 };
 
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s);

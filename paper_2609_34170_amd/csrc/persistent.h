@@ -66,6 +66,9 @@ struct PGemm {
   bf16_t* p_out; int ldp;              // PE_RESID: p of the next norm
   float* sumsq_out;                    // PE_RESID: [N/64][64] row sums of squares of the new x
   float* partial; unsigned* counters;  // split-K partial tiles, per-tile tickets
+  // 1: the ksplit blocks of a tile meet and each finishes a slice of its rows
+  // (needs one item per block); 0: the last block to arrive finishes the tile
+  int coop;
 };
 
 struct alignas(16) Phase {

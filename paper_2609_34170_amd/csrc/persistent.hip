@@ -130,8 +130,7 @@ RAVEL_DEV T make_uniform(const T& s) {
 }
 
 RAVEL_DEV void coherent_store_bf16x4(bf16_t* p, float v0, float v1, float v2, float v3) {
-  const uint64_t w = (uint64_t)f32_to_bf16(v0) | ((uint64_t)f32_to_bf16(v1) << 16) |
-                     ((uint64_t)f32_to_bf16(v2) << 32) | ((uint64_t)f32_to_bf16(v3) << 48);
+  const uint64_t w = (uint64_t)pack_bf16x2(v0, v1) | ((uint64_t)pack_bf16x2(v2, v3) << 32);
   __hip_atomic_store(reinterpret_cast<uint64_t*>(p), w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -148,6 +147,43 @@ RAVEL_DEV bool last_arrival(unsigned* counter, unsigned arrivals, int* s_flag) {
   }
   __syncthreads();
   return *s_flag != 0;
+}
+
+// Meeting point of the blocks of one split tile / split head (each holds one
+// item of the phase, so all of them are running): every wave drains its stores,
+// thread 0 arrives and polls until all have arrived (bounded; on timeout the
+// error flag is set and false returned).
+RAVEL_DEV bool group_meet(unsigned* counter, unsigned arrivals, int* err, int* s_flag) {
+  wait_memory();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int ok = 1;
+    __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int spins = 0;
+    while (__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < arrivals) {
+      __builtin_amdgcn_s_sleep(1);
+      if (++spins > kBarrierSpinLimit) {
+        __hip_atomic_fetch_or(err, 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ok = 0;
+        break;
+      }
+    }
+    *s_flag = ok;
+  }
+  __syncthreads();
+  return *s_flag != 0;
+}
+
+// After the group's work: the last block to leave re-arms the meeting word (every
+// block has passed its poll by then) and the leaving word, at counter + 32.
+RAVEL_DEV void group_leave(unsigned* counter, unsigned arrivals) {
+  if (threadIdx.x == 0) {
+    const unsigned prev = __hip_atomic_fetch_add(counter + 32, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (prev == arrivals - 1) {
+      __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(counter + 32, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
 }
 
 // Hierarchical grid barrier, split in two so that loads can be issued between
@@ -256,8 +292,11 @@ RAVEL_DEV void load_weights(const PGemm& g, int item, bf16x8_t (&wf)[4][4]) {
     load_w<1>(g, item, wf);
 }
 
+template <int MT>
+RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& sm);
+
 template <int MT, int KW>
-RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], PSmem& sm) {
+RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], int* err, PSmem& sm) {
   constexpr int NF = 2 * KW;
   const int tid = local_tid(), lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, grp = lane >> 4;
@@ -306,10 +345,12 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], P
       for (int f = 0; f < NF; ++f) {
         const bf16_t* pv = reinterpret_cast<const bf16_t*>(&af[i][f]);
         const bf16_t* bv = reinterpret_cast<const bf16_t*>(&sh[i][f]);
-        bf16_t hb[8];
+        u32x4_t hb;
 #pragma unroll
-        for (int q = 0; q < 8; ++q) hb[q] = f32_to_bf16(r * bf16_to_f32(pv[q]) + bf16_to_f32(bv[q]));
-        af[i][f] = *reinterpret_cast<const bf16x8_t*>(hb);
+        for (int q = 0; q < 4; ++q)
+          hb[q] = pack_bf16x2(r * bf16_to_f32(pv[2 * q]) + bf16_to_f32(bv[2 * q]),
+                              r * bf16_to_f32(pv[2 * q + 1]) + bf16_to_f32(bv[2 * q + 1]));
+        af[i][f] = *reinterpret_cast<const bf16x8_t*>(&hb);
       }
     }
   }
@@ -371,6 +412,13 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], P
 #pragma unroll
     for (int q = 0; q < MT; ++q)
       if (row_of(q) < g.M) coherent_store4(mine + (size_t)(tid + q * 256) * 4, sum[q]);
+    if (g.coop) {
+      unsigned* ctr = &g.counters[tile * kCounterStride];
+      if (group_meet(ctr, (unsigned)g.ksplit, err, &sm.flag)) coop_epilogue<MT>(g, tile, z, tiles, sm);
+      group_leave(ctr, (unsigned)g.ksplit);
+      __syncthreads();
+      return;
+    }
     if (!last_arrival(&g.counters[tile * kCounterStride], (unsigned)g.ksplit, &sm.flag)) {
       __syncthreads();
       return;
@@ -474,11 +522,105 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], P
   __syncthreads();
 }
 
+// A split-K tile finished by its ksplit blocks together: block z takes rows
+// [z*rp, min(M, (z+1)*rp)), rp = ceil(M / ksplit), adds the partials of each of its
+// (row, 4-column) slots in split order and applies the epilogue; the new rows' sums
+// of squares of a residual update are added in fixed column order.
+template <int MT>
+RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& sm) {
+  const int tid = local_tid();
+  const int n0 = tile * 64;
+  const int rp = (g.M + g.ksplit - 1) / g.ksplit;
+  const int r0 = z * rp, r1 = min(g.M, r0 + rp);
+  const size_t tile_elems = (size_t)MT * 4 * 64 * 4;
+  const bool geglu = g.e_mode == PE_GEGLU, resid = g.e_mode == PE_RESID;
+  const int per_row = geglu ? 8 : 16;
+  const int nslots = max(r1 - r0, 0) * per_row;
+  const rsrc_t rP = rsrc(g.partial), rX = rsrc(g.out_f), rG = rsrc(g.gate), rN = rsrc(g.ns), rB = rsrc(g.bias);
+  float gsc = 1.f;
+  if (resid && !g.gate) gsc = tanhf(*g.gate_scalar);
+  for (int s0 = 0; s0 < nslots; s0 += 256) {
+    const int slot = s0 + tid;
+    const bool valid = slot < nslots;
+    const int row = r0 + (valid ? slot / per_row : 0), rem = slot % per_row;
+    const int grp = rem & 3, cb = rem >> 2;  // 4-column group, 16-column block (GEGLU: block pair)
+    const int c = geglu ? 2 * cb : cb;
+    const int n = n0 + c * 16 + grp * 4;
+    const int it = (c * MT + (row >> 4)) * 64 + grp * 16 + (row & 15);
+    const int it_up = ((c + 1) * MT + (row >> 4)) * 64 + grp * 16 + (row & 15);
+    const bool ok = valid && n + 4 <= g.N;
+    // epilogue operands and partials: one batch
+    const f32x4_t ex = ld_f4<COH>(rX, boff(resid && ok, ((size_t)row * g.ldof + n) * 4));
+    const f32x4_t eg = ld_f4<PLAIN>(rG, boff(resid && ok && g.gate, ((size_t)row * g.ldg + n) * 4));
+    const f32x4_t es =
+        ld_f4<PLAIN>(rN, boff(resid && ok, (g.ns_mode == NS_ROW ? (size_t)row * g.ldns + n : (size_t)n) * 4));
+    const f32x4_t eb = ld_f4<PLAIN>(rB, boff(!resid && !geglu && ok && g.bias, (size_t)n * 4));
+    f32x4_t pv[kMaxKSplit], pu[kMaxKSplit];
+#pragma unroll
+    for (int zz = 0; zz < kMaxKSplit; ++zz) {
+      const size_t base = ((size_t)zz * tiles + tile) * tile_elems;
+      pv[zz] = ld_f4<COH>(rP, boff(valid && zz < g.ksplit, (base + (size_t)it * 4) * 4));
+      pu[zz] = ld_f4<COH>(rP, boff(geglu && valid && zz < g.ksplit, (base + (size_t)it_up * 4) * 4));
+    }
+    f32x4_t v = {0.f, 0.f, 0.f, 0.f}, u = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int zz = 0; zz < kMaxKSplit; ++zz) {
+      if (zz >= g.ksplit) break;
+      v[0] += pv[zz][0];
+      v[1] += pv[zz][1];
+      v[2] += pv[zz][2];
+      v[3] += pv[zz][3];
+      u[0] += pu[zz][0];
+      u[1] += pu[zz][1];
+      u[2] += pu[zz][2];
+      u[3] += pu[zz][3];
+    }
+    float sq = 0.f;
+    if (valid && n < g.N) {
+      if (geglu) {
+        coherent_store_bf16x4(g.out_t + (size_t)row * g.ldo + (n0 >> 1) + cb * 16 + grp * 4, gelu_tanh_f(v[0]) * u[0],
+                              gelu_tanh_f(v[1]) * u[1], gelu_tanh_f(v[2]) * u[2], gelu_tanh_f(v[3]) * u[3]);
+      } else if (g.e_mode == PE_BF16) {
+        coherent_store_bf16x4(g.out_t + (size_t)row * g.ldo + n, v[0], v[1], v[2], v[3]);
+      } else if (g.e_mode == PE_F32) {
+        if (n + 4 <= g.N) {
+          coherent_store4(g.out_f + (size_t)row * g.ldof + n,
+                          f32x4_t{v[0] + eb[0], v[1] + eb[1], v[2] + eb[2], v[3] + eb[3]});
+        } else {
+          for (int r = 0; n + r < g.N; ++r)
+            coherent_store(g.out_f + (size_t)row * g.ldof + n + r, v[r] + (g.bias ? g.bias[n + r] : 0.f));
+        }
+      } else {  // PE_RESID
+        const f32x4_t gt = g.gate ? eg : f32x4_t{gsc, gsc, gsc, gsc};
+        f32x4_t xn;
+        xn[0] = ex[0] + gt[0] * v[0];
+        xn[1] = ex[1] + gt[1] * v[1];
+        xn[2] = ex[2] + gt[2] * v[2];
+        xn[3] = ex[3] + gt[3] * v[3];
+        coherent_store4(g.out_f + (size_t)row * g.ldof + n, xn);
+        coherent_store_bf16x4(g.p_out + (size_t)row * g.ldp + n, (1.f + es[0]) * xn[0], (1.f + es[1]) * xn[1],
+                              (1.f + es[2]) * xn[2], (1.f + es[3]) * xn[3]);
+        sq = xn[0] * xn[0] + xn[1] * xn[1] + xn[2] * xn[2] + xn[3] * xn[3];
+      }
+    }
+    if (resid && valid) sm.rowsq[row - r0][c * 4 + grp] = sq;
+  }
+  if (resid) {
+    __syncthreads();
+    if (tid < r1 - r0) {
+      float s = 0.f;
+#pragma unroll
+      for (int h = 0; h < 16; ++h) s += sm.rowsq[tid][h];
+      coherent_store(g.sumsq_out + tile * 64 + r0 + tid, s);
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // attention: one (env, head, key split)
 // ---------------------------------------------------------------------------
 template <int HD>
-RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, PSmem& sm) {
+RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err, PSmem& sm) {
   using C = AttnCfg<HD>;
   constexpr int KPS = C::KPS, KLD = C::KLD, VLD = C::VLD;
   constexpr int KS = HD / 32, DT = HD / 16, CPR = HD / 8;
@@ -609,13 +751,9 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, PSmem& s
       psum += __shfl_xor(psum, 32, 64);
       lrow = lrow * corr + psum;
       mrow = mnew;
-      bf16_t pb[8];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        pb[r] = f32_to_bf16(p[0][r]);
-        pb[4 + r] = f32_to_bf16(p[1][r]);
-      }
-      const bf16x8_t pf = *(const bf16x8_t*)pb;
+      const u32x4_t pb = {pack_bf16x2(p[0][0], p[0][1]), pack_bf16x2(p[0][2], p[0][3]), pack_bf16x2(p[1][0], p[1][1]),
+                          pack_bf16x2(p[1][2], p[1][3])};
+      const bf16x8_t pf = *reinterpret_cast<const bf16x8_t*>(&pb);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         o[dt][0] *= corr;
@@ -652,6 +790,76 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, PSmem& s
       coherent_store(&a.part_ml[((pbase + split) * Hp + query) * 2 + 0], mrow);
       coherent_store(&a.part_ml[((pbase + split) * Hp + query) * 2 + 1], lrow);
     }
+  }
+  if (a.coop) {
+    // the splits of this (env, head) meet; each merges a share of the output
+    unsigned* ctr = &a.counters[(e * a.nq + j) * kCounterStride];
+    if (group_meet(ctr, (unsigned)a.nsplit, err, &sm.flag)) {
+      const int total = a.Hq * (HD / 4);
+      const int share = (total + a.nsplit - 1) / a.nsplit;
+      const int el0 = split * share, el1 = min(total, el0 + share);
+      const rsrc_t rML = rsrc(a.part_ml), rO = rsrc(a.part_o);
+      float2 mlv[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = tid + r * 256, sp = t >> 6, qq = t & 63;
+        mlv[r] = ld_f2<COH>(rML, boff(sp < a.nsplit && qq < a.Hq, ((pbase + sp) * Hp + qq) * 2 * 4));
+      }
+      for (int b0 = el0; b0 < el1; b0 += 512) {
+        f32x4_t pvl[2][8];
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+          const int el = b0 + r * 256 + tid;
+          const int qq = el / (HD / 4), d = (el % (HD / 4)) * 4;
+#pragma unroll
+          for (int s8 = 0; s8 < 8; ++s8)
+            pvl[r][s8] = ld_f4<COH>(rO, boff(el < el1 && s8 < a.nsplit, (((pbase + s8) * Hp + qq) * HD + d) * 4));
+        }
+        if (b0 == el0) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int t = tid + r * 256, sp = t >> 6, qq = t & 63;
+            sm.mg.ml[sp][qq][0] = (sp < a.nsplit && qq < a.Hq) ? mlv[r].x : -INFINITY;
+            sm.mg.ml[sp][qq][1] = mlv[r].y;
+          }
+          __syncthreads();
+          if (tid < a.Hq) {
+            float mmax = -INFINITY;
+            for (int sp = 0; sp < a.nsplit; ++sp) mmax = fmaxf(mmax, sm.mg.ml[sp][tid][0]);
+            float den = 0.f;
+            for (int sp = 0; sp < a.nsplit; ++sp) {
+              const float ms = sm.mg.ml[sp][tid][0];
+              const float wv = (ms == -INFINITY) ? 0.f : exp2f(ms - mmax);
+              sm.mg.wgt[sp][tid] = wv;
+              den += wv * sm.mg.ml[sp][tid][1];
+            }
+            const float inv = 1.f / den;
+            for (int sp = 0; sp < a.nsplit; ++sp) sm.mg.wgt[sp][tid] *= inv;
+          }
+          __syncthreads();
+        }
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+          const int el = b0 + r * 256 + tid;
+          if (el >= el1) continue;
+          const int qq = el / (HD / 4), d = (el % (HD / 4)) * 4;
+          f32x4_t num = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s8 = 0; s8 < 8; ++s8) {
+            if (s8 >= a.nsplit) break;
+            const float wv = sm.mg.wgt[s8][qq];
+            num[0] += wv * pvl[r][s8][0];
+            num[1] += wv * pvl[r][s8][1];
+            num[2] += wv * pvl[r][s8][2];
+            num[3] += wv * pvl[r][s8][3];
+          }
+          coherent_store_bf16x4(out + (size_t)(e * a.Hq + qq) * a.ldo + j * HD + d, num[0], num[1], num[2], num[3]);
+        }
+      }
+    }
+    group_leave(ctr, (unsigned)a.nsplit);
+    __syncthreads();
+    return;
   }
   if (!last_arrival(&a.counters[(e * a.nq + j) * kCounterStride], (unsigned)a.nsplit, &sm.flag)) {
     __syncthreads();
@@ -775,18 +983,18 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
       for (int item = blockIdx.x; item < items; item += gridDim.x) {
         if (item != (int)blockIdx.x) load_weights(g, item, wreg);
         if (g.kw == 2)
-          gemm_item<MT, 2>(g, item, wreg, sm);
+          gemm_item<MT, 2>(g, item, wreg, err, sm);
         else
-          gemm_item<MT, 1>(g, item, wreg, sm);
+          gemm_item<MT, 1>(g, item, wreg, err, sm);
       }
     } else if (type == PH_ATTN) {
       const AttnArgs a = make_uniform(ph.at);
       for (int item = blockIdx.x; item < items; item += gridDim.x) {
         switch (a.hd) {
-          case 32: attn_item<32>(a, item, slots, sm); break;
-          case 64: attn_item<64>(a, item, slots, sm); break;
-          case 128: attn_item<128>(a, item, slots, sm); break;
-          default: attn_item<256>(a, item, slots, sm); break;
+          case 32: attn_item<32>(a, item, slots, err, sm); break;
+          case 64: attn_item<64>(a, item, slots, err, sm); break;
+          case 128: attn_item<128>(a, item, slots, err, sm); break;
+          default: attn_item<256>(a, item, slots, err, sm); break;
         }
       }
     } else if (type == PH_ROWSTATS) {

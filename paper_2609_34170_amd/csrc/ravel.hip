@@ -793,12 +793,13 @@ ravel_status build_persistent(ravel_buffer* b) {
     g.N = N;
     g.K = K;
     const int ks1 = (K + 255) / 256;
-    g.kw = (norm || (ks1 <= kMaxKSplit && tiles(N) * ks1 <= b->pblocks)) ? 1 : 2;
+    g.kw = (ks1 <= kMaxKSplit && tiles(N) * ks1 <= b->pblocks) ? 1 : 2;
     if ((K + 256 * g.kw - 1) / (256 * g.kw) > kMaxKSplit) g.kw = 0;  // rejected below
     g.ksplit = (K + 256 * g.kw - 1) / (256 * g.kw);
     g.e_mode = e_mode;
     g.counters = nullptr;  // patched below
     ph.items = tiles(N) * g.ksplit;
+    g.coop = g.ksplit > 1 && ph.items <= b->pblocks;
     part = std::max(part, (size_t)g.ksplit * tiles(N) * mt * 4 * 64 * 4);
     max_tiles = std::max(max_tiles, tiles(N));
     return ph;
@@ -859,8 +860,9 @@ ravel_status build_persistent(ravel_buffer* b) {
     a.keys_per_split = std::min(kmax, (((a.P + np - 1) / np + 31) / 32) * 32);
     a.keys_per_split = std::max(a.keys_per_split, std::min(kmax, ((a.S + 31) / 32) * 32));
     a.nsplit = (a.P + a.keys_per_split - 1) / a.keys_per_split + (a.S + a.keys_per_split - 1) / a.keys_per_split;
-    ph.at = a;
     ph.items = B * c.n_q_heads * a.nsplit;
+    a.coop = a.nsplit > 1 && a.nsplit <= 8 && ph.items <= b->pblocks;
+    ph.at = a;
     max_attn_parts = std::max(max_attn_parts, B * c.n_q_heads * a.nsplit);
     max_attn_heads = std::max(max_attn_heads, B * c.n_q_heads);
     return ph;
