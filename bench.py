@@ -17,12 +17,18 @@ Prints ONE JSON line.  Extra measurements:
                   the step stream): algorithmic bytes (or flops) / time;
   * step_roofline -- the whole step: algorithmic bytes per step / step time;
   * cpu_baseline -- the numpy oracle (fp32) on a bounded sample of the same
-                  workload on the host cores.
+                  workload on the host cores;
+  * roofline.traffic -- HBM bytes per launch of the dominant kernel from
+                  rocprofv3 FETCH_SIZE / WRITE_SIZE runs scaled by the same
+                  counters on a plain copy of known size (profiles/traffic.json,
+                  written from those runs); null unless the kernel's source
+                  files still hash to the values recorded there.
 """
 
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -48,7 +54,57 @@ def parse():
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
     p.add_argument("--profile-steps", type=int, default=3)
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                   help="first run 5 plain device copies of MIB MiB (counter calibration under rocprofv3)")
     return p.parse_args()
+
+
+# source files that define each kernel class (for the traffic record's hash)
+KERNEL_SOURCES = {
+    "persistent_layers": ["persistent.hip", "persistent.h", "common.h", "kernels.h"],
+    "gemm": ["gemm.hip", "common.h", "kernels.h"],
+    "attn": ["attention.hip", "common.h", "kernels.h"],
+}
+
+
+def sources_sha256(kernel: str):
+    key = "persistent_layers" if kernel.startswith("persistent") else kernel.split("<")[0].rstrip("0123456789x")
+    key = "gemm" if key.startswith("gemm") else key
+    files = KERNEL_SOURCES.get(key)
+    if not files:
+        return None
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2609_34170_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def traffic_of(kernel: str, workload: str):
+    """HBM bytes per launch recorded for this kernel and workload, if its sources are unchanged."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    digest = sources_sha256(kernel)
+    for e in rec.get("entries", []):
+        if e.get("kernel") == kernel and e.get("workload") == workload and e.get("sources_sha256") == digest:
+            return e.get("bytes_per_launch")
+    return None
+
+
+def copy_calibration(mib: int):
+    import torch
+    n = mib << 20
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"[copy calibration] 5 copies of {n} bytes (read {n}, write {n} per copy)")
+    del src, dst
 
 
 def log(msg):
@@ -200,7 +256,7 @@ class Workload:
         return agg, total / nsteps
 
 
-def roofline_of(agg, bound):
+def roofline_of(agg, bound, workload=None):
     dom = max(agg.items(), key=lambda kv: kv[1][3])
     name, (cnt, by, fl, ms) = dom
     if bound == "hbm":
@@ -210,7 +266,8 @@ def roofline_of(agg, bound):
         achieved = fl / (ms * 1e-3) / 1e12
         peak, unit = BF16_PEAK_TFLOPS, "TFLOP/s"
     return {"kernel": name, "bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-            "frac": round(achieved / peak, 4), "traffic": None, "launches_per_step_x_steps": cnt,
+            "frac": round(achieved / peak, 4), "traffic": traffic_of(name, workload) if workload else None,
+            "algorithmic_bytes_per_launch": round(by / cnt), "launches_per_step_x_steps": cnt,
             "avg_launch_us": round(ms * 1e3 / cnt, 2)}
 
 
@@ -254,6 +311,8 @@ def main():
     import synth
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.copy_calibration > 0:
+        copy_calibration(args.copy_calibration)
 
     wl = Workload(args.workload)
     s = wl.s
@@ -261,7 +320,7 @@ def main():
     ms, wall = wl.timed(args.steps, args.warmup)
     lat = wl.latencies(min(200, args.steps))
     agg, prof_ms = wl.profile(args.profile_steps)
-    roof = roofline_of(agg, bound)
+    roof = roofline_of(agg, bound, s.name)
     abytes = algorithmic_bytes(s, wl.B)
     aflops = algorithmic_flops(s, wl.B)
     step_roof = {
@@ -318,7 +377,7 @@ def main():
             "steps_per_s": round(1000.0 / ms64, 2), "env_steps_per_s": round(64 * 1000.0 / ms64, 1),
             "mfma_TFLOPs": round(algorithmic_flops(s64, 64) / (ms64 * 1e-3) / 1e12, 1),
             "mfma_frac": round(algorithmic_flops(s64, 64) / (ms64 * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
-            "roofline": roofline_of(agg64, "mfma"),
+            "roofline": roofline_of(agg64, "mfma", "pi_b64"),
         }
         log(f"[pi_b64] {1000.0 / ms64:.1f} steps/s")
         del w64

@@ -189,7 +189,8 @@ RAVEL_DEV void group_leave(unsigned* counter, unsigned arrivals) {
 // Hierarchical grid barrier, split in two so that loads can be issued between
 // arrival and wait.  Group g's counter sits on its own 256-byte line; the last
 // arrival of a group bumps the top counter and the last top arrival publishes
-// the generation word every block polls.
+// the generation word every block polls (polling the top counter itself instead
+// is slower: the polls delay the group arrivals on that line).
 RAVEL_DEV void barrier_arrive(unsigned* bar, unsigned gen) {
   const int G = kBarrierGroups;
   const int g = blockIdx.x % G;
