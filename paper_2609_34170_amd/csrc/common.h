@@ -68,22 +68,30 @@ RAVEL_DEV float wave_max(float v) {
 // before the block takes its ticket, and only the block that takes the last
 // ticket reads the other blocks' data.  Nothing ever spins.
 // ---------------------------------------------------------------------------
+// Pointers in the global address space: atomics on generic pointers become
+// flat instructions, which also count against the LDS counter (every later LDS
+// wait then waits for them) and cannot be widened.
+#define RAVEL_GLOBAL __attribute__((address_space(1)))
+template <class T>
+RAVEL_DEV RAVEL_GLOBAL T* gptr(T* p) {
+  return (RAVEL_GLOBAL T*)p;
+}
 RAVEL_DEV void coherent_store(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(gptr(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 RAVEL_DEV float coherent_load(const float* p) {
-  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return __hip_atomic_load(gptr(const_cast<float*>(p)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 RAVEL_DEV void coherent_store4(float* p, f32x4_t v) {
   uint64_t* q = reinterpret_cast<uint64_t*>(p);
   const u32x4_t u = __builtin_bit_cast(u32x4_t, v);
-  __hip_atomic_store(q, (uint64_t)u[0] | ((uint64_t)u[1] << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  __hip_atomic_store(q + 1, (uint64_t)u[2] | ((uint64_t)u[3] << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(gptr(q), (uint64_t)u[0] | ((uint64_t)u[1] << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(gptr(q + 1), (uint64_t)u[2] | ((uint64_t)u[3] << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 RAVEL_DEV f32x4_t coherent_load4(const float* p) {
   uint64_t* q = reinterpret_cast<uint64_t*>(const_cast<float*>(p));
-  const uint64_t lo = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  const uint64_t hi = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const uint64_t lo = __hip_atomic_load(gptr(q), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const uint64_t hi = __hip_atomic_load(gptr(q + 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const u32x4_t u = {(uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32)};
   return __builtin_bit_cast(f32x4_t, u);
 }
@@ -104,10 +112,10 @@ RAVEL_DEV bool last_block_arrival(unsigned* counter, unsigned arrivals, int* s_f
   wait_memory();
   __syncthreads();
   if (threadIdx.x == 0) {
-    const unsigned prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned prev = __hip_atomic_fetch_add(gptr(counter), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     *s_flag = (prev == arrivals - 1);
     if (prev == arrivals - 1)
-      __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(gptr(counter), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   __syncthreads();
   const bool last = *s_flag != 0;

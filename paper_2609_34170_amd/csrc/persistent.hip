@@ -107,6 +107,18 @@ RAVEL_DEV float2 ld_f2(rsrc_t r, int off) {
   const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, AUX);
   return float2{__uint_as_float(v[0]), __uint_as_float(v[1])};
 }
+// device-coherent stores (sc1 buffer stores: what a relaxed agent-scope atomic
+// store lowers to, but widened to 16 bytes and issued as global accesses)
+RAVEL_DEV void st_f4(rsrc_t r, size_t byte_off, f32x4_t v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), r, (int)byte_off, 0, COH);
+}
+RAVEL_DEV void st_f1(rsrc_t r, size_t byte_off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)byte_off, 0, COH);
+}
+RAVEL_DEV void st_bf16x4(rsrc_t r, size_t byte_off, float v0, float v1, float v2, float v3) {
+  const u32x2_t w = {pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+  __builtin_amdgcn_raw_buffer_store_b64(w, r, (int)byte_off, 0, COH);
+}
 
 // threadIdx.x behind an empty asm: index arithmetic derived from it stays inside
 // the work item that needs it instead of being hoisted out of the phase loop,
@@ -129,10 +141,6 @@ RAVEL_DEV T make_uniform(const T& s) {
   return d;
 }
 
-RAVEL_DEV void coherent_store_bf16x4(bf16_t* p, float v0, float v1, float v2, float v3) {
-  const uint64_t w = (uint64_t)pack_bf16x2(v0, v1) | ((uint64_t)pack_bf16x2(v2, v3) << 32);
-  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 // Ticket of a split tile / split attention head: every wave drains its stores,
 // thread 0 takes the ticket; the last arrival re-arms it.
@@ -140,9 +148,9 @@ RAVEL_DEV bool last_arrival(unsigned* counter, unsigned arrivals, int* s_flag) {
   wait_memory();
   __syncthreads();
   if (threadIdx.x == 0) {
-    const unsigned prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned prev = __hip_atomic_fetch_add(gptr(counter), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int last = prev == arrivals - 1;
-    if (last) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (last) __hip_atomic_store(gptr(counter), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     *s_flag = last;
   }
   __syncthreads();
@@ -158,12 +166,12 @@ RAVEL_DEV bool group_meet(unsigned* counter, unsigned arrivals, int* err, int* s
   __syncthreads();
   if (threadIdx.x == 0) {
     int ok = 1;
-    __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_fetch_add(gptr(counter), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     int spins = 0;
-    while (__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < arrivals) {
+    while (__hip_atomic_load(gptr(counter), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < arrivals) {
       __builtin_amdgcn_s_sleep(1);
       if (++spins > kBarrierSpinLimit) {
-        __hip_atomic_fetch_or(err, 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_or(gptr(err), 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         ok = 0;
         break;
       }
@@ -178,10 +186,10 @@ RAVEL_DEV bool group_meet(unsigned* counter, unsigned arrivals, int* err, int* s
 // block has passed its poll by then) and the leaving word, at counter + 32.
 RAVEL_DEV void group_leave(unsigned* counter, unsigned arrivals) {
   if (threadIdx.x == 0) {
-    const unsigned prev = __hip_atomic_fetch_add(counter + 32, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned prev = __hip_atomic_fetch_add(gptr(counter + 32), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (prev == arrivals - 1) {
-      __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(counter + 32, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(gptr(counter), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(gptr(counter + 32), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
@@ -195,19 +203,19 @@ RAVEL_DEV void barrier_arrive(unsigned* bar, unsigned gen) {
   const int G = kBarrierGroups;
   const int g = blockIdx.x % G;
   const unsigned per = (gridDim.x - g + G - 1) / G;
-  const unsigned prev = __hip_atomic_fetch_add(bar + 64 * (1 + g), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const unsigned prev = __hip_atomic_fetch_add(gptr(bar + 64 * (1 + g)), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (prev == gen * per - 1) {
-    const unsigned t = __hip_atomic_fetch_add(bar + 64 * (1 + G), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (t == gen * (unsigned)G - 1) __hip_atomic_store(bar, gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned t = __hip_atomic_fetch_add(gptr(bar + 64 * (1 + G)), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (t == gen * (unsigned)G - 1) __hip_atomic_store(gptr(bar), gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
 RAVEL_DEV int barrier_wait(unsigned* bar, unsigned gen, int* err) {
   int spins = 0;
-  while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < gen) {
+  while (__hip_atomic_load(gptr(bar), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < gen) {
     __builtin_amdgcn_s_sleep(1);
     if (++spins > kBarrierSpinLimit) {
-      __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_fetch_or(gptr(err), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       return 0;
     }
   }
@@ -228,10 +236,13 @@ RAVEL_DEV void convert_item(const PRowstats& r, int piece) {
   const float* src = r.cvt_in + (size_t)m * r.cvt_ld + (size_t)c * r.cvt_stride + n;
   f32x4_t v[8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) v[i] = *(const f32x4_t*)(src + 4 * i);
-  bf16_t* dst = r.cvt_out + e0;
+  for (int i = 0; i < 8; ++i) v[i] = *gptr((const f32x4_t*)(src + 4 * i));
+  const rsrc_t rd = rsrc(r.cvt_out);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) coherent_store_bf16x4(dst + 4 * i, v[i][0], v[i][1], v[i][2], v[i][3]);
+  for (int i = 0; i < 8; i += 2)
+    st_f4(rd, (e0 + 4 * i) * 2,
+          __builtin_bit_cast(f32x4_t, u32x4_t{pack_bf16x2(v[i][0], v[i][1]), pack_bf16x2(v[i][2], v[i][3]),
+                                              pack_bf16x2(v[i + 1][0], v[i + 1][1]), pack_bf16x2(v[i + 1][2], v[i + 1][3])}));
 }
 
 RAVEL_DEV void rowstats_item(const PRowstats& r, int tile, PSmem& sm) {
@@ -244,21 +255,21 @@ RAVEL_DEV void rowstats_item(const PRowstats& r, int tile, PSmem& sm) {
     const float* nsp = r.ns_mode == NS_ROW ? r.ns + (size_t)m * r.ldns + n : r.ns + n;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      x[c] = *(const f32x4_t*)(r.x + (size_t)m * r.ldx + n + 4 * c);
-      sc[c] = *(const f32x4_t*)(nsp + 4 * c);
+      x[c] = *gptr((const f32x4_t*)(r.x + (size_t)m * r.ldx + n + 4 * c));
+      sc[c] = *gptr((const f32x4_t*)(nsp + 4 * c));
     }
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       s += x[c][0] * x[c][0] + x[c][1] * x[c][1] + x[c][2] * x[c][2] + x[c][3] * x[c][3];
-      coherent_store_bf16x4(r.p + (size_t)m * r.ldp + n + 4 * c, (1.f + sc[c][0]) * x[c][0],
-                            (1.f + sc[c][1]) * x[c][1], (1.f + sc[c][2]) * x[c][2], (1.f + sc[c][3]) * x[c][3]);
+      st_bf16x4(rsrc(r.p), ((size_t)m * r.ldp + n + 4 * c) * 2, (1.f + sc[c][0]) * x[c][0], (1.f + sc[c][1]) * x[c][1],
+                (1.f + sc[c][2]) * x[c][2], (1.f + sc[c][3]) * x[c][3]);
     }
   }
   sm.rowsq[m][q] = s;
   __syncthreads();
   if (tid < 64 && tid < r.M) {
     const float t = (sm.rowsq[tid][0] + sm.rowsq[tid][1]) + (sm.rowsq[tid][2] + sm.rowsq[tid][3]);
-    coherent_store(r.sumsq_out + tile * 64 + tid, t);
+    st_f1(rsrc(r.sumsq_out), (size_t)(tile * 64 + tid) * 4, t);
   }
   __syncthreads();
 }
@@ -409,10 +420,11 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], i
   };
   if (g.ksplit > 1) {
     const size_t tile_elems = (size_t)MT * 4 * 64 * 4;
-    float* mine = g.partial + ((size_t)z * tiles + tile) * tile_elems;
+    const rsrc_t rPw = rsrc(g.partial);
 #pragma unroll
     for (int q = 0; q < MT; ++q)
-      if (row_of(q) < g.M) coherent_store4(mine + (size_t)(tid + q * 256) * 4, sum[q]);
+      if (row_of(q) < g.M)
+        st_f4(rPw, (((size_t)z * tiles + tile) * tile_elems + (size_t)(tid + q * 256) * 4) * 4, sum[q]);
     if (g.coop) {
       unsigned* ctr = &g.counters[tile * kCounterStride];
       if (group_meet(ctr, (unsigned)g.ksplit, err, &sm.flag)) coop_epilogue<MT>(g, tile, z, tiles, sm);
@@ -466,8 +478,8 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], i
       if (m >= g.M || ng >= g.N) continue;
       const f32x4_t u = *(const f32x4_t*)&sm.red[0][(c + 1) * MT + i][ln][0];
       const f32x4_t gt = sum[q];
-      coherent_store_bf16x4(g.out_t + (size_t)m * g.ldo + (ng >> 5) * 16 + (ln >> 4) * 4, gelu_tanh_f(gt[0]) * u[0],
-                            gelu_tanh_f(gt[1]) * u[1], gelu_tanh_f(gt[2]) * u[2], gelu_tanh_f(gt[3]) * u[3]);
+      st_bf16x4(rsrc(g.out_t), ((size_t)m * g.ldo + (ng >> 5) * 16 + (ln >> 4) * 4) * 2, gelu_tanh_f(gt[0]) * u[0],
+                gelu_tanh_f(gt[1]) * u[1], gelu_tanh_f(gt[2]) * u[2], gelu_tanh_f(gt[3]) * u[3]);
     }
     __syncthreads();
     return;
@@ -475,7 +487,7 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], i
 
   if (g.ksplit == 1) load_epilogue();
   float gsc = 1.f;
-  if (resid && !g.gate) gsc = tanhf(*g.gate_scalar);
+  if (resid && !g.gate) gsc = tanhf(*gptr(g.gate_scalar));
 
 #pragma unroll
   for (int q = 0; q < MT; ++q) {
@@ -486,14 +498,14 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], i
     float sq = 0.f;
     if (m < g.M && n < g.N) {
       if (g.e_mode == PE_BF16) {
-        coherent_store_bf16x4(g.out_t + (size_t)m * g.ldo + n, v[0], v[1], v[2], v[3]);
+        st_bf16x4(rsrc(g.out_t), ((size_t)m * g.ldo + n) * 2, v[0], v[1], v[2], v[3]);
       } else if (g.e_mode == PE_F32) {
         if (n + 4 <= g.N) {
-          coherent_store4(g.out_f + (size_t)m * g.ldof + n,
-                          f32x4_t{v[0] + e_b[q][0], v[1] + e_b[q][1], v[2] + e_b[q][2], v[3] + e_b[q][3]});
+          st_f4(rsrc(g.out_f), ((size_t)m * g.ldof + n) * 4,
+                f32x4_t{v[0] + e_b[q][0], v[1] + e_b[q][1], v[2] + e_b[q][2], v[3] + e_b[q][3]});
         } else {
           for (int r = 0; n + r < g.N; ++r)
-            coherent_store(g.out_f + (size_t)m * g.ldof + n + r, v[r] + (g.bias ? g.bias[n + r] : 0.f));
+            st_f1(rsrc(g.out_f), ((size_t)m * g.ldof + n + r) * 4, v[r] + (g.bias ? *gptr(g.bias + n + r) : 0.f));
         }
       } else {  // PE_RESID
         const f32x4_t gt = g.gate ? e_g[q] : f32x4_t{gsc, gsc, gsc, gsc};
@@ -502,9 +514,9 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], i
         xn[1] = e_x[q][1] + gt[1] * v[1];
         xn[2] = e_x[q][2] + gt[2] * v[2];
         xn[3] = e_x[q][3] + gt[3] * v[3];
-        coherent_store4(g.out_f + (size_t)m * g.ldof + n, xn);
-        coherent_store_bf16x4(g.p_out + (size_t)m * g.ldp + n, (1.f + e_s[q][0]) * xn[0], (1.f + e_s[q][1]) * xn[1],
-                              (1.f + e_s[q][2]) * xn[2], (1.f + e_s[q][3]) * xn[3]);
+        st_f4(rsrc(g.out_f), ((size_t)m * g.ldof + n) * 4, xn);
+        st_bf16x4(rsrc(g.p_out), ((size_t)m * g.ldp + n) * 2, (1.f + e_s[q][0]) * xn[0], (1.f + e_s[q][1]) * xn[1],
+                  (1.f + e_s[q][2]) * xn[2], (1.f + e_s[q][3]) * xn[3]);
         sq = xn[0] * xn[0] + xn[1] * xn[1] + xn[2] * xn[2] + xn[3] * xn[3];
       }
     }
@@ -517,7 +529,7 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], i
       float s = 0.f;
 #pragma unroll
       for (int h = 0; h < 16; ++h) s += sm.rowsq[tid][h];
-      coherent_store(g.sumsq_out + tile * 64 + tid, s);
+      st_f1(rsrc(g.sumsq_out), (size_t)(tile * 64 + tid) * 4, s);
     }
   }
   __syncthreads();
@@ -539,7 +551,7 @@ RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& 
   const int nslots = max(r1 - r0, 0) * per_row;
   const rsrc_t rP = rsrc(g.partial), rX = rsrc(g.out_f), rG = rsrc(g.gate), rN = rsrc(g.ns), rB = rsrc(g.bias);
   float gsc = 1.f;
-  if (resid && !g.gate) gsc = tanhf(*g.gate_scalar);
+  if (resid && !g.gate) gsc = tanhf(*gptr(g.gate_scalar));
   for (int s0 = 0; s0 < nslots; s0 += 256) {
     const int slot = s0 + tid;
     const bool valid = slot < nslots;
@@ -579,17 +591,16 @@ RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& 
     float sq = 0.f;
     if (valid && n < g.N) {
       if (geglu) {
-        coherent_store_bf16x4(g.out_t + (size_t)row * g.ldo + (n0 >> 1) + cb * 16 + grp * 4, gelu_tanh_f(v[0]) * u[0],
-                              gelu_tanh_f(v[1]) * u[1], gelu_tanh_f(v[2]) * u[2], gelu_tanh_f(v[3]) * u[3]);
+        st_bf16x4(rsrc(g.out_t), ((size_t)row * g.ldo + (n0 >> 1) + cb * 16 + grp * 4) * 2, gelu_tanh_f(v[0]) * u[0],
+                  gelu_tanh_f(v[1]) * u[1], gelu_tanh_f(v[2]) * u[2], gelu_tanh_f(v[3]) * u[3]);
       } else if (g.e_mode == PE_BF16) {
-        coherent_store_bf16x4(g.out_t + (size_t)row * g.ldo + n, v[0], v[1], v[2], v[3]);
+        st_bf16x4(rsrc(g.out_t), ((size_t)row * g.ldo + n) * 2, v[0], v[1], v[2], v[3]);
       } else if (g.e_mode == PE_F32) {
         if (n + 4 <= g.N) {
-          coherent_store4(g.out_f + (size_t)row * g.ldof + n,
-                          f32x4_t{v[0] + eb[0], v[1] + eb[1], v[2] + eb[2], v[3] + eb[3]});
+          st_f4(rsrc(g.out_f), ((size_t)row * g.ldof + n) * 4, f32x4_t{v[0] + eb[0], v[1] + eb[1], v[2] + eb[2], v[3] + eb[3]});
         } else {
           for (int r = 0; n + r < g.N; ++r)
-            coherent_store(g.out_f + (size_t)row * g.ldof + n + r, v[r] + (g.bias ? g.bias[n + r] : 0.f));
+            st_f1(rsrc(g.out_f), ((size_t)row * g.ldof + n + r) * 4, v[r] + (g.bias ? *gptr(g.bias + n + r) : 0.f));
         }
       } else {  // PE_RESID
         const f32x4_t gt = g.gate ? eg : f32x4_t{gsc, gsc, gsc, gsc};
@@ -598,9 +609,9 @@ RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& 
         xn[1] = ex[1] + gt[1] * v[1];
         xn[2] = ex[2] + gt[2] * v[2];
         xn[3] = ex[3] + gt[3] * v[3];
-        coherent_store4(g.out_f + (size_t)row * g.ldof + n, xn);
-        coherent_store_bf16x4(g.p_out + (size_t)row * g.ldp + n, (1.f + es[0]) * xn[0], (1.f + es[1]) * xn[1],
-                              (1.f + es[2]) * xn[2], (1.f + es[3]) * xn[3]);
+        st_f4(rsrc(g.out_f), ((size_t)row * g.ldof + n) * 4, xn);
+        st_bf16x4(rsrc(g.p_out), ((size_t)row * g.ldp + n) * 2, (1.f + es[0]) * xn[0], (1.f + es[1]) * xn[1],
+                  (1.f + es[2]) * xn[2], (1.f + es[3]) * xn[3]);
         sq = xn[0] * xn[0] + xn[1] * xn[1] + xn[2] * xn[2] + xn[3] * xn[3];
       }
     }
@@ -612,7 +623,7 @@ RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& 
       float s = 0.f;
 #pragma unroll
       for (int h = 0; h < 16; ++h) s += sm.rowsq[tid][h];
-      coherent_store(g.sumsq_out + tile * 64 + r0 + tid, s);
+      st_f1(rsrc(g.sumsq_out), (size_t)(tile * 64 + r0 + tid) * 4, s);
     }
   }
 }
@@ -775,8 +786,8 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
       const float inv = 1.f / lrow;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
-        coherent_store_bf16x4(out + (size_t)(e * a.Hq + query) * a.ldo + j * HD + dt * 16 + grp * 4, o[dt][0] * inv,
-                              o[dt][1] * inv, o[dt][2] * inv, o[dt][3] * inv);
+        st_bf16x4(rsrc(out), ((size_t)(e * a.Hq + query) * a.ldo + j * HD + dt * 16 + grp * 4) * 2, o[dt][0] * inv,
+                  o[dt][1] * inv, o[dt][2] * inv, o[dt][3] * inv);
     }
     __syncthreads();
     return;
@@ -784,12 +795,13 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
   const int Hp = QB * 16;
   const size_t pbase = ((size_t)e * a.nq + j) * a.nsplit;
   if (active && query < a.Hq) {
-    float* po = a.part_o + ((pbase + split) * Hp + query) * HD;
+    const rsrc_t rPo = rsrc(a.part_o), rPml = rsrc(a.part_ml);
+    const size_t po = ((pbase + split) * Hp + query) * HD;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) coherent_store4(po + dt * 16 + grp * 4, o[dt]);
+    for (int dt = 0; dt < DT; ++dt) st_f4(rPo, (po + dt * 16 + grp * 4) * 4, o[dt]);
     if (grp == 0) {
-      coherent_store(&a.part_ml[((pbase + split) * Hp + query) * 2 + 0], mrow);
-      coherent_store(&a.part_ml[((pbase + split) * Hp + query) * 2 + 1], lrow);
+      st_f1(rPml, (((pbase + split) * Hp + query) * 2 + 0) * 4, mrow);
+      st_f1(rPml, (((pbase + split) * Hp + query) * 2 + 1) * 4, lrow);
     }
   }
   if (a.coop) {
@@ -854,7 +866,7 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
             num[2] += wv * pvl[r][s8][2];
             num[3] += wv * pvl[r][s8][3];
           }
-          coherent_store_bf16x4(out + (size_t)(e * a.Hq + qq) * a.ldo + j * HD + d, num[0], num[1], num[2], num[3]);
+          st_bf16x4(rsrc(out), ((size_t)(e * a.Hq + qq) * a.ldo + j * HD + d) * 2, num[0], num[1], num[2], num[3]);
         }
       }
     }
@@ -932,8 +944,8 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
       const int el = base + r * 256 + tid;
       if (el >= total) continue;
       const int qq = el / (HD / 4), d = (el % (HD / 4)) * 4;
-      coherent_store_bf16x4(out + (size_t)(e * a.Hq + qq) * a.ldo + j * HD + d, num[r][0], num[r][1], num[r][2],
-                            num[r][3]);
+      st_bf16x4(rsrc(out), ((size_t)(e * a.Hq + qq) * a.ldo + j * HD + d) * 2, num[r][0], num[r][1], num[r][2],
+                num[r][3]);
     }
   }
   __syncthreads();
@@ -955,11 +967,11 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
   __shared__ int ok;
   const int tid = threadIdx.x;
   const bool stamp = times != nullptr && blockIdx.x == 0 && tid == 0;
-  if (stamp) times[0] = wall_clock64();
+  if (stamp) *gptr(times) = wall_clock64();
   for (int d = 0; d < 2 && d < nphase; ++d)
     if (tid < kDescChunks)
-      reinterpret_cast<u32x4_t*>(&desc[d])[tid] = reinterpret_cast<const u32x4_t*>(&phases[d])[tid];
-  if (env_slot && tid < nenv && tid < 64) slots[tid] = env_slot[tid];
+      reinterpret_cast<u32x4_t*>(&desc[d])[tid] = *gptr(reinterpret_cast<const u32x4_t*>(&phases[d]) + tid);
+  if (env_slot && tid < nenv && tid < 64) slots[tid] = *gptr(env_slot + tid);
   __syncthreads();
 
   // weights of this block's first item of the coming GEMM phase (zero otherwise)
@@ -1016,26 +1028,26 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
     const unsigned gen = (unsigned)(p + 1);
     if (tid == 0) barrier_arrive(bar, gen);
     u32x4_t dreg = {0, 0, 0, 0};
-    if (p + 2 < nphase && tid < kDescChunks) dreg = reinterpret_cast<const u32x4_t*>(&phases[p + 2])[tid];
+    if (p + 2 < nphase && tid < kDescChunks) dreg = *gptr(reinterpret_cast<const u32x4_t*>(&phases[p + 2]) + tid);
     prefetch(desc[(p + 1) % 3]);
     if (tid == 0) ok = barrier_wait(bar, gen, err);
     __syncthreads();
     if (!ok) return;
     if (p + 2 < nphase && tid < kDescChunks) reinterpret_cast<u32x4_t*>(&desc[(p + 2) % 3])[tid] = dreg;
-    if (stamp) times[p + 1] = wall_clock64();
+    if (stamp) *gptr(times + p + 1) = wall_clock64();
   }
-  if (stamp) times[nphase] = wall_clock64();
+  if (stamp) *gptr(times + nphase) = wall_clock64();
   // re-arm the barrier: the last block to get here has seen every block pass
   // every barrier, and zeroes the counters for the next launch
   wait_memory();
   __syncthreads();
   if (tid == 0) {
     unsigned* ex = bar + 64 * (2 + kBarrierGroups);
-    const unsigned prev = __hip_atomic_fetch_add(ex, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned prev = __hip_atomic_fetch_add(gptr(ex), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (prev == gridDim.x - 1) {
       for (int i = 0; i < 2 + kBarrierGroups; ++i)
-        __hip_atomic_store(bar + 64 * i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(ex, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(gptr(bar + 64 * i), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(gptr(ex), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
