@@ -251,9 +251,16 @@ GemmPlan plan_gemm(int M, int N, int K, bool geglu) {
     p.part_elems = p.ksplit > 1 ? (size_t)p.ksplit * p.tiles * tile_elems : 0;
     return p;
   }
+  // tile by shape (measured on MI355X at M = 3200, the pi-style batch-64 rows:
+  // 128x128 597 TF/s at N = 2560, K = 1024; 128x64 428 vs 382 TF/s at N = 1024,
+  // K = 2048 and 464 vs 423 at K = 4096; 256x256 651 vs 593 TF/s at N = 8192)
   int bm, bn;
   if (M <= 256) {
     p.tile = TILE_64x128; bm = 64; bn = 128;
+  } else if (N <= 1024) {
+    p.tile = TILE_128x64; bm = 128; bn = 64;
+  } else if (N >= 8192 && M >= 2048) {
+    p.tile = TILE_256x256; bm = 256; bn = 256;
   } else {
     p.tile = TILE_128x128; bm = 128; bn = 128;
   }
@@ -396,7 +403,7 @@ ravel_status run_gemm(ravel_buffer* b, hipStream_t s, KernelRecorder* rec, const
   if (p.part_elems > b->gpart_elems || p.tiles > b->gcnt_n)
     return fail(RAVEL_E_STATE, std::string(name) + ": GEMM workspace too small");
   if (rec) {
-    static const char* tn[] = {"64x64", "128x128", "64x128", "128x64", "32x64"};
+    static const char* tn[] = {"64x64", "128x128", "64x128", "128x64", "32x64", "256x128", "128x256", "256x256"};
     char full[48];
     if (p.skinny && p.regstream)
       snprintf(full, sizeof full, "gemm_regstream<%d>:%s", (M + 15) / 16, name);
