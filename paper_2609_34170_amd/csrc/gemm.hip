@@ -308,6 +308,155 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs a) {
   epilogue(a, acc, mw, nw, l16, grp);
 }
 
+
+// ---------------------------------------------------------------------------
+// Tiled GEMM, many rows, K tiles loaded straight into LDS (global_load_lds,
+// 16 bytes per lane): no register staging and no LDS store instructions.
+// STAGES LDS buffers; tile kt + STAGES - 1 is in flight while tile kt is
+// multiplied.  Rows are 64 bf16 (128 bytes, unpadded); the 16-byte chunk c of
+// row r sits at chunk position c ^ ((r >> 1) & 7), so the 16 rows read by one
+// fragment load hit 16 distinct bank groups.  Loads clamp rows to the matrix
+// (rows / columns past M / N only feed outputs that are never written); K and
+// the K range must be multiples of 64.  The fragment reads are inline asm with
+// an explicit LDS wait: as plain loads the compiler would wait for every
+// global->LDS load in flight (including later stages) before each of them, and
+// __syncthreads() would wait for them too, so the K loop uses s_barrier after
+// an explicit wait for this wave's loads of the current tile.
+// ---------------------------------------------------------------------------
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef const __attribute__((address_space(1))) void gmem_void_t;
+
+// gfx9 s_waitcnt immediate: vmcnt <= n, expcnt and lgkmcnt not waited for
+constexpr unsigned waitcnt_vm(int n) { return (unsigned)((n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8)); }
+
+template <int BM, int BN, int WM, int WN, int STAGES>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_lds_kernel(GemmArgs a) {
+  constexpr int NW = WM * WN;
+  constexpr int BK = 64;
+  constexpr int TM = BM / (16 * WM), TN = BN / (16 * WN);
+  constexpr int LA = BM / 8 / NW, LB = BN / 8 / NW;  // 1 KB (8-row) segments per wave per tile
+  static_assert(LA >= 1 && LB >= 1 && (BM / 8) % NW == 0 && (BN / 8) % NW == 0, "segments per wave");
+  constexpr int AHEAD = STAGES - 1;
+  static_assert(AHEAD >= 1 && AHEAD <= 3, "stages");
+  __shared__ __attribute__((aligned(1024))) bf16_t As[STAGES][BM * BK];
+  __shared__ __attribute__((aligned(1024))) bf16_t Bs[STAGES][BN * BK];
+  __shared__ int s_last;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, grp = lane >> 4;
+  const int wm = wave / WN, wn = wave % WN;
+  const int tiles_n = (a.N + BN - 1) / BN;
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
+  const int z = blockIdx.z;
+  const int kbeg = z * a.kchunk;
+  const int kend = min(a.K, kbeg + a.kchunk);
+  const int nk = (kend - kbeg) / BK;
+  const bf16_t* __restrict__ A = (const bf16_t*)a.A;
+  const bf16_t* __restrict__ B = (const bf16_t*)a.B;
+
+  const int srow = lane >> 3, spos = lane & 7;  // lane -> (row in segment, chunk position)
+  auto issue = [&](int kt, int st) {
+    const int k0 = kbeg + kt * BK;
+#pragma unroll
+    for (int i = 0; i < LA; ++i) {
+      const int seg = wave * LA + i, row = seg * 8 + srow;
+      const int m = min(m0 + row, a.M - 1);
+      const int c = spos ^ ((row >> 1) & 7);
+      __builtin_amdgcn_global_load_lds((gmem_void_t*)(A + (size_t)m * a.lda + k0 + c * 8), (lds_void_t*)&As[st][seg * 512],
+                                       16, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < LB; ++i) {
+      const int seg = wave * LB + i, row = seg * 8 + srow;
+      const int n = min(n0 + row, a.N - 1);
+      const int c = spos ^ ((row >> 1) & 7);
+      __builtin_amdgcn_global_load_lds((gmem_void_t*)(B + (size_t)n * a.ldb + k0 + c * 8), (lds_void_t*)&Bs[st][seg * 512],
+                                       16, 0, 0);
+    }
+  };
+  auto frag = [&](const bf16_t* base, int row, int c) -> bf16x8_t {
+    const unsigned addr =
+        (unsigned)(size_t)(const __attribute__((address_space(3))) bf16_t*)(&base[row * BK + ((c ^ ((row >> 1) & 7)) * 8)]);
+    bf16x8_t v;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
+    return v;
+  };
+
+  f32x4_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int t = 0; t < AHEAD; ++t)
+    if (t < nk) issue(t, t);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int st = kt % STAGES;
+    // this wave's loads of tile kt are complete once at most the later tiles'
+    // loads are outstanding (vector memory operations complete in order)
+    const int later = min(AHEAD - 1, nk - 1 - kt);
+    if (later >= 2)
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * (LA + LB)));
+    else if (later == 1)
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(LA + LB));
+    else
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    __builtin_amdgcn_s_barrier();  // every wave's part of tile kt is in LDS; tile kt-1's buffer is free
+    if (kt + AHEAD < nk) issue(kt + AHEAD, (kt + AHEAD) % STAGES);
+    const bf16_t* as = As[st];
+    const bf16_t* bs = Bs[st];
+#pragma unroll
+    for (int ks = 0; ks < BK / 32; ++ks) {
+      bf16x8_t af[TM], bfr[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[i] = frag(as, wm * (BM / WM) + i * 16 + l16, ks * 4 + grp);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bfr[j] = frag(bs, wn * (BN / WN) + j * 16 + l16, ks * 4 + grp);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+      for (int i = 0; i < TM; ++i) asm volatile("" : "+v"(af[i]));
+#pragma unroll
+      for (int j = 0; j < TN; ++j) asm volatile("" : "+v"(bfr[j]));
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+    }
+  }
+
+  const int mw = m0 + wm * (BM / WM);
+  const int nw = n0 + wn * (BN / WN);
+  if (a.ksplit > 1) {
+    const size_t tile_elems = (size_t)BM * BN;
+    float* part = a.partial + ((size_t)z * gridDim.x + tile) * tile_elems;
+    const int wbase = (wave * TM * TN) * 256;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) coherent_store4(part + wbase + ((i * TN + j) * 64 + lane) * 4, acc[i][j]);
+    if (!last_block_arrival(&a.counters[tile * kCounterStride], (unsigned)a.ksplit, &s_last)) return;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        f32x4_t sum = {0.f, 0.f, 0.f, 0.f};
+        for (int zz = 0; zz < a.ksplit; ++zz) {
+          const f32x4_t v = (zz == z) ? acc[i][j]
+                                      : *(const f32x4_t*)(a.partial + ((size_t)zz * gridDim.x + tile) * tile_elems + wbase +
+                                                          ((i * TN + j) * 64 + lane) * 4);
+          sum[0] += v[0];
+          sum[1] += v[1];
+          sum[2] += v[2];
+          sum[3] += v[3];
+        }
+        acc[i][j] = sum;
+      }
+  }
+  epilogue(a, acc, mw, nw, l16, grp);
+}
+
 // ---------------------------------------------------------------------------
 // Weight-streaming kernel for few rows (M <= 64): the regime of one env's H
 // slots, where every weight byte is used by at most 64 rows and the GEMM is
@@ -657,7 +806,22 @@ static hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int BM, int BN, int WM, int WN, int STAGES>
+static hipError_t launch_lds_tile(const GemmArgs& a, hipStream_t s) {
+  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  dim3 grid(tiles, 1, a.ksplit);
+  hipLaunchKernelGGL((gemm_lds_kernel<BM, BN, WM, WN, STAGES>), grid, dim3(64 * WM * WN), 0, s, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm_bf16(const GemmArgs& a, int tile, hipStream_t s) {
+  // direct-to-LDS variants (measured on MI355X at M = 3200: 128x128 with two
+  // stages 744-804 TF/s at K = 1024; 128x64 with three stages 514-581 TF/s at
+  // N = 1024, K = 2048-4096) where K tiles are whole and rows 16-byte aligned
+  const bool lds_ok = a.K % 64 == 0 && a.kchunk % 64 == 0 && a.lda % 8 == 0 && a.ldb % 8 == 0 &&
+                      ((uintptr_t)a.A % 16) == 0 && ((uintptr_t)a.B % 16) == 0 && a.M > 0 && a.N > 0;
+  if (lds_ok && tile == TILE_128x128) return launch_lds_tile<128, 128, 2, 2, 2>(a, s);
+  if (lds_ok && tile == TILE_128x64) return launch_lds_tile<128, 64, 2, 2, 3>(a, s);
   switch (tile) {
     case TILE_128x128: return launch_tile<128, 128, 2, 2>(a, s);
     case TILE_64x128: return launch_tile<64, 128, 2, 2>(a, s);

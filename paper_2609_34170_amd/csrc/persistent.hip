@@ -716,67 +716,77 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
   }
   __syncthreads();
 
-  // S^T = K Q^T per 32-key tile (lane: keys 4grp..+3 and 16+4grp..+3 of query l16),
-  // online softmax, O^T += V^T P^T
+  // A split holds at most KPS keys, so its scores are computed at once: S^T = K Q^T
+  // for every 32-key tile t (lane: query l16, keys 32t + 4grp..+3 and 32t + 16 +
+  // 4grp..+3) as 2 x NT independent MFMA chains, then one softmax over the split
+  // and O^T = V^T P^T with no running rescale.
+  constexpr int NT = KPS / 32;
+  const int nk = kend - kbeg;
+  const int ntile = (nk + 31) / 32;
   f32x4_t o[DT];
   float mrow = -INFINITY, lrow = 0.f;
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   const float sl2 = a.scale * 1.4426950408889634f;
-  const int nk = kend - kbeg;
   if (active) {
-    for (int k0 = 0; k0 < nk; k0 += 32) {
-      f32x4_t s[2];
+    f32x4_t sc[NT][2];
 #pragma unroll
-      for (int st = 0; st < 2; ++st) {
-        s[st] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < NT; ++t) sc[t][0] = sc[t][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8_t kf = *(const bf16x8_t*)&Ks[(k0 + st * 16 + l16) * KLD + ks * 32 + grp * 8];
-          s[st] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], s[st], 0, 0, 0);
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        if (t >= ntile) continue;  // wave-uniform
+#pragma unroll
+        for (int st = 0; st < 2; ++st) {
+          const bf16x8_t kf = *(const bf16x8_t*)&Ks[(t * 32 + st * 16 + l16) * KLD + ks * 32 + grp * 8];
+          sc[t][st] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], sc[t][st], 0, 0, 0);
         }
       }
-      float mx = -INFINITY;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
 #pragma unroll
       for (int st = 0; st < 2; ++st)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          float x = s[st][r] * sl2;
-          if (k0 + st * 16 + grp * 4 + r >= nk) x = -INFINITY;
-          s[st][r] = x;
+          float x = sc[t][st][r] * sl2;
+          if (t * 32 + st * 16 + grp * 4 + r >= nk) x = -INFINITY;
+          sc[t][st][r] = x;
           mx = fmaxf(mx, x);
         }
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mnew = fmaxf(mrow, mx);
-      const float corr = (mnew == -INFINITY) ? 1.f : exp2f(mrow - mnew);
-      float psum = 0.f;
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    float psum = 0.f;
+    bf16x8_t pf[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
       float p[2][4];
 #pragma unroll
       for (int st = 0; st < 2; ++st)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          p[st][r] = (s[st][r] == -INFINITY) ? 0.f : exp2f(s[st][r] - mnew);
+          p[st][r] = (sc[t][st][r] == -INFINITY) ? 0.f : exp2f(sc[t][st][r] - mx);
           psum += p[st][r];
         }
-      psum += __shfl_xor(psum, 16, 64);
-      psum += __shfl_xor(psum, 32, 64);
-      lrow = lrow * corr + psum;
-      mrow = mnew;
       const u32x4_t pb = {pack_bf16x2(p[0][0], p[0][1]), pack_bf16x2(p[0][2], p[0][3]), pack_bf16x2(p[1][0], p[1][1]),
                           pack_bf16x2(p[1][2], p[1][3])};
-      const bf16x8_t pf = *reinterpret_cast<const bf16x8_t*>(&pb);
+      pf[t] = *reinterpret_cast<const bf16x8_t*>(&pb);
+    }
+    psum += __shfl_xor(psum, 16, 64);
+    psum += __shfl_xor(psum, 32, 64);
+    mrow = mx;
+    lrow = psum;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      if (t >= ntile) continue;  // wave-uniform
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        o[dt][0] *= corr;
-        o[dt][1] *= corr;
-        o[dt][2] *= corr;
-        o[dt][3] *= corr;
-        const bf16_t* vrow = &Vt[(dt * 16 + l16) * VLD + k0];
+        const bf16_t* vrow = &Vt[(dt * 16 + l16) * VLD + t * 32];
         const u32x2_t lo = *(const u32x2_t*)(vrow + grp * 4);
         const u32x2_t hi = *(const u32x2_t*)(vrow + 16 + grp * 4);
         const u32x4_t vv = {lo[0], lo[1], hi[0], hi[1]};
-        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8_t*)&vv, pf, o[dt], 0, 0, 0);
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8_t*)&vv, pf[t], o[dt], 0, 0, 0);
       }
     }
   }

@@ -251,16 +251,14 @@ GemmPlan plan_gemm(int M, int N, int K, bool geglu) {
     p.part_elems = p.ksplit > 1 ? (size_t)p.ksplit * p.tiles * tile_elems : 0;
     return p;
   }
-  // tile by shape (measured on MI355X at M = 3200, the pi-style batch-64 rows:
-  // 128x128 597 TF/s at N = 2560, K = 1024; 128x64 428 vs 382 TF/s at N = 1024,
-  // K = 2048 and 464 vs 423 at K = 4096; 256x256 651 vs 593 TF/s at N = 8192)
+  // tile by shape (direct-to-LDS kernels, measured on MI355X at M = 3200, the
+  // pi-style batch-64 rows: 128x128 744-804 TF/s at K = 1024; 128x64 514 and 581
+  // TF/s at N = 1024, K = 2048 and 4096, where 128x128 gives 200 tiles)
   int bm, bn;
   if (M <= 256) {
     p.tile = TILE_64x128; bm = 64; bn = 128;
   } else if (N <= 1024) {
     p.tile = TILE_128x64; bm = 128; bn = 64;
-  } else if (N >= 8192 && M >= 2048) {
-    p.tile = TILE_256x256; bm = 256; bn = 256;
   } else {
     p.tile = TILE_128x128; bm = 128; bn = 128;
   }
