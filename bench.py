@@ -378,6 +378,9 @@ def main():
             "mfma_TFLOPs": round(algorithmic_flops(s64, 64) / (ms64 * 1e-3) / 1e12, 1),
             "mfma_frac": round(algorithmic_flops(s64, 64) / (ms64 * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
             "roofline": roofline_of(agg64, "mfma", "pi_b64"),
+            # eager profile steps: ms per step and achieved TFLOP/s per kernel class
+            "kernel_classes": {k: {"ms": round(v[3] / 2, 4), "TFs": round(v[2] / (v[3] * 1e-3) / 1e12, 1)}
+                               for k, v in sorted(agg64.items(), key=lambda kv: -kv[1][3])[:8]},
         }
         log(f"[pi_b64] {1000.0 / ms64:.1f} steps/s")
         del w64

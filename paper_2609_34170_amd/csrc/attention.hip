@@ -276,6 +276,225 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Grouped-query form for whole-range (unsplit) attention.  The G = nq/nkv query
+// heads that share one K/V head are flattened with the queries into one row
+// space of G*Hq rows (row = h*Hq + query), cut into 16-row MFMA blocks; a
+// block of NW waves owns NW consecutive row blocks (one per wave) of one
+// (env, KV head) and streams all keys once, so each K/V tile is staged in LDS
+// once for every query head of the group.  With 8 waves two share each SIMD:
+// one wave's MFMAs run while the other does its softmax or waits on LDS.  K/V
+// tiles are double-buffered in LDS (one barrier per tile) and the next tile's
+// global loads are in flight during the current tile's MFMAs.  V is written
+// transposed with 8 keys x 4-lane groups per row so that the stores (row stride
+// 18 dwords) and the MFMA operand reads are free of bank conflicts.
+//
+// Softmax rescaling is lazy: the running maximum m of a row only moves when a
+// tile raises it by more than kLazy (log2 units), so between moves exp2(s - m)
+// <= 2^kLazy and the O rescale (a VALU pass over all accumulators) is skipped
+// for the wave unless one of its rows moved.  The result is the same softmax;
+// only the reference point of the bf16-rounded probabilities differs.
+// ---------------------------------------------------------------------------
+static constexpr float kLazy = 8.f;
+
+template <int HD, int NW>
+__global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunks) {
+  constexpr int NT = NW * 64;
+  constexpr int TK = 32;
+  constexpr int KS = HD / 32;
+  constexpr int DT = HD / 16;
+  constexpr int KLD = HD + 8;
+  constexpr int VLD = TK + 4;
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][TK][KLD];
+  __shared__ __attribute__((aligned(16))) bf16_t Vt[2][HD][VLD];
+
+  // blocks that share an (env, KV head) sit on one XCD (dispatch is round-robin
+  // over the 8 XCDs), so the group's K/V is fetched into one L2 only
+  const int total = gridDim.x;
+  const int L = blockIdx.x;
+  const int w = (total % 8 == 0) ? (L % 8) * (total / 8) + L / 8 : L;
+  const int chunk = w % chunks;
+  const int g = (w / chunks) % a.nkv;
+  const int e = w / (chunks * a.nkv);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, grp = lane >> 4;
+  const int G = a.nq / a.nkv;
+  const int R = G * a.Hq;
+  const int nkeys = a.P + a.S;
+  const int row = (chunk * NW + wave) * 16 + l16;  // this lane's row
+
+  const bf16_t* q = (const bf16_t*)a.q;
+  const int slot = a.slot ? a.slot[e] : 0;
+  const bf16_t* pk = (const bf16_t*)a.pk + slot * a.p_slot_stride + e * a.p_env_stride;
+  const bf16_t* pv = (const bf16_t*)a.pv + slot * a.p_slot_stride + e * a.p_env_stride;
+  const bf16_t* sk = (const bf16_t*)a.sk;
+  const bf16_t* sv = (const bf16_t*)a.sv;
+
+  // rows past the group are clamped to a real row, computed and never stored
+  bf16x8_t qf[KS];
+  {
+    const int r = min(row, R - 1);
+    const int h = r / a.Hq, query = r % a.Hq;
+    const bf16_t* qr = q + (size_t)(e * a.Hq + query) * a.ldq + (g * G + h) * HD + grp * 8;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = *(const bf16x8_t*)(qr + ks * 32);
+  }
+  f32x4_t o[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float mrow = -INFINITY, lrow = 0.f;
+  const float sl2 = a.scale * kLog2e;
+
+  // K: 16-byte chunks, row-major.  V: items of 4 keys x 8 dims, kq fastest so
+  // that 8 lanes fill one 64-byte row segment of V^T.  Keys past the range are
+  // clamped to the last key: finite values whose probabilities are exactly 0.
+  constexpr int KCHUNKS = TK * (HD / 8), VITEMS = (TK / 4) * (HD / 8);
+  constexpr int KCH = (KCHUNKS + NT - 1) / NT;
+  constexpr int VIT = (VITEMS + NT - 1) / NT;
+  u32x4_t kreg[KCH];
+  u32x4_t vreg[VIT][4];
+  auto load_tile = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = tid + i * NT;
+      if (KCHUNKS % NT == 0 || c < KCHUNKS) {
+        const int kidx = min(k0 + c / (HD / 8), nkeys - 1);
+        kreg[i] = *(const u32x4_t*)(key_base(a, pk, sk, e, kidx, g, HD) + (c % (HD / 8)) * 8);
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < VIT; ++it) {
+      const int c = tid + it * NT;
+      if (VITEMS % NT == 0 || c < VITEMS) {
+        const int kq = c % (TK / 4), dc = (c / (TK / 4)) * 8;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int kidx = min(k0 + kq * 4 + i, nkeys - 1);
+          vreg[it][i] = *(const u32x4_t*)(key_base(a, pv, sv, e, kidx, g, HD) + dc);
+        }
+      }
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = tid + i * NT;
+      if (KCHUNKS % NT == 0 || c < KCHUNKS) *(u32x4_t*)&Ks[buf][c / (HD / 8)][(c % (HD / 8)) * 8] = kreg[i];
+    }
+#pragma unroll
+    for (int it = 0; it < VIT; ++it) {
+      const int c = tid + it * NT;
+      if (VITEMS % NT == 0 || c < VITEMS) {
+        const int kq = c % (TK / 4), dc = (c / (TK / 4)) * 8;
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          const uint32_t a0 = vreg[it][0][m], a1 = vreg[it][1][m];
+          const uint32_t a2 = vreg[it][2][m], a3 = vreg[it][3][m];
+          u32x2_t lo, hi;  // dims dc+2m (low halves) and dc+2m+1 (high halves)
+          lo[0] = (a0 & 0xFFFFu) | (a1 << 16);
+          lo[1] = (a2 & 0xFFFFu) | (a3 << 16);
+          hi[0] = (a0 >> 16) | (a1 & 0xFFFF0000u);
+          hi[1] = (a2 >> 16) | (a3 & 0xFFFF0000u);
+          *(u32x2_t*)&Vt[buf][dc + 2 * m][kq * 4] = lo;
+          *(u32x2_t*)&Vt[buf][dc + 2 * m + 1][kq * 4] = hi;
+        }
+      }
+    }
+  };
+
+  const int ntile = (nkeys + TK - 1) / TK;
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+  for (int t = 0; t < ntile; ++t) {
+    const int k0 = t * TK, buf = t & 1;
+    if (t + 1 < ntile) load_tile(k0 + TK);
+    // S^T[key][row] for two 16-key sub-tiles
+    f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8_t k0f = *(const bf16x8_t*)&Ks[buf][l16][ks * 32 + grp * 8];
+      const bf16x8_t k1f = *(const bf16x8_t*)&Ks[buf][16 + l16][ks * 32 + grp * 8];
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0f, qf[ks], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1f, qf[ks], s1, 0, 0, 0);
+    }
+    float x[8];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      x[r] = s0[r] * sl2;
+      x[4 + r] = s1[r] * sl2;
+    }
+    if (k0 + TK > nkeys) {  // uniform: the ragged last tile
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        if (k0 + grp * 4 + r >= nkeys) x[r] = -INFINITY;
+        if (k0 + 16 + grp * 4 + r >= nkeys) x[4 + r] = -INFINITY;
+      }
+    }
+    float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    // every tile holds a valid key, so mx is finite; the first tile always moves
+    const bool mv = mx > mrow + kLazy;
+    if (__any(mv)) {
+      const float mnew = mv ? mx : mrow;
+      const float corr = exp2f(mrow - mnew);
+      mrow = mnew;
+      lrow *= corr;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        o[dt][0] *= corr;
+        o[dt][1] *= corr;
+        o[dt][2] *= corr;
+        o[dt][3] *= corr;
+      }
+    }
+    float p[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) p[r] = exp2f(x[r] - mrow);
+    // the row sum stays split over the 4 lane groups until the end
+    lrow += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+    // P^T as the B operand: slot jj of group grp is key (jj<4 ? 4grp+jj : 16+4grp+jj-4)
+    const u32x4_t pw = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
+                        pack_bf16x2(p[6], p[7])};
+    const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pw);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const bf16_t* vrow = &Vt[buf][dt * 16 + l16][0];
+      const u32x2_t lo = *(const u32x2_t*)(vrow + grp * 4);
+      const u32x2_t hi = *(const u32x2_t*)(vrow + 16 + grp * 4);
+      const u32x4_t vv = {lo[0], lo[1], hi[0], hi[1]};
+      o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vv), pf, o[dt], 0, 0, 0);
+    }
+    if (t + 1 < ntile) store_tile(buf ^ 1);
+    __syncthreads();
+  }
+
+  // o[dt][r] = O^T[d = dt*16 + 4grp + r][row]
+  lrow += __shfl_xor(lrow, 16, 64);
+  lrow += __shfl_xor(lrow, 32, 64);
+  if (row >= R) return;
+  const int h = row / a.Hq, query = row % a.Hq;
+  const float inv = 1.f / lrow;
+  bf16_t* orow = (bf16_t*)a.out + (size_t)(e * a.Hq + query) * a.ldo + (g * G + h) * HD + grp * 4;
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) {
+    u32x2_t wv;
+    wv[0] = pack_bf16x2(o[dt][0] * inv, o[dt][1] * inv);
+    wv[1] = pack_bf16x2(o[dt][2] * inv, o[dt][3] * inv);
+    *(u32x2_t*)(orow + dt * 16) = wv;
+  }
+}
+
+template <int HD, int NW>
+static hipError_t launch_gqa(const AttnArgs& a, hipStream_t s) {
+  const int rb = (a.nq / a.nkv * a.Hq + 15) / 16;
+  const int chunks = (rb + NW - 1) / NW;
+  hipLaunchKernelGGL((attn_gqa_kernel<HD, NW>), dim3(chunks * a.nkv * a.B), dim3(NW * 64), 0, s, a, chunks);
+  return hipGetLastError();
+}
+
 template <int HD, int MAXQB>
 static hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
   dim3 grid(a.nsplit, a.nq, a.B);
@@ -288,6 +507,18 @@ hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s) {
   if (QB > 8) return hipErrorInvalidValue;
   // the split merge keeps nsplit x Hq weights in the K tile's LDS (32 x (hd + 8) bf16)
   if (a.nsplit > 1 && a.nsplit * a.Hq > 32 * (a.hd + 8) / 2) return hipErrorInvalidValue;
+  if (a.nsplit == 1 && a.nkv > 0 && a.nq % a.nkv == 0 && a.P + a.S > 0) {
+    // whole key range: grouped-query kernel, 8 waves once the group has at
+    // least 8 row blocks
+    const bool eight = (a.nq / a.nkv * a.Hq + 15) / 16 >= 8;
+    switch (a.hd) {
+      case 32: return eight ? launch_gqa<32, 8>(a, s) : launch_gqa<32, 4>(a, s);
+      case 64: return eight ? launch_gqa<64, 8>(a, s) : launch_gqa<64, 4>(a, s);
+      case 128: return eight ? launch_gqa<128, 8>(a, s) : launch_gqa<128, 4>(a, s);
+      case 256: return eight ? launch_gqa<256, 8>(a, s) : launch_gqa<256, 4>(a, s);
+      default: return hipErrorInvalidValue;
+    }
+  }
   const bool two = QB > 4;
   switch (a.hd) {
     case 32: return two ? launch_hd<32, 2>(a, s) : launch_hd<32, 1>(a, s);
