@@ -133,19 +133,32 @@ def algorithmic_bytes(s, batch) -> float:
     return float(n)
 
 
+def modulation_rows(s, batch) -> int:
+    """Buffer rows whose modulation the step computes.  With more than 64 rows the
+    modulation GEMMs run once per distinct offset conditioning (envs with equal
+    context age share delta): at steady state the refresh policy leaves
+    min(batch, period) distinct ages when staggered, one otherwise."""
+    H = s.horizon
+    if batch * H <= 64 or batch == 1:
+        return batch * H
+    groups = min(batch, s.context_period) if (s.stagger and s.context_period > 0) else 1
+    return groups * H
+
+
 def algorithmic_flops(s, batch) -> float:
     w, H, F = s.width, s.horizon, s.mlp_dim
     qd, kvd = s.n_q_heads * s.head_dim, s.n_kv_heads * s.head_dim
     M = batch * H
+    Mm = modulation_rows(s, batch)
     f = 2.0 * batch * w * w  # offset MLP
     f += 2.0 * M * w * s.action_dim * 2  # in / out projections
-    per_layer = 2.0 * M * w * (6 * w + qd + 2 * kvd) + 2.0 * M * qd * w + 2.0 * M * w * 3 * F
+    per_layer = 2.0 * Mm * w * 6 * w + 2.0 * M * w * (qd + 2 * kvd) + 2.0 * M * qd * w + 2.0 * M * w * 3 * F
     per_layer += 4.0 * batch * s.n_q_heads * H * (s.prefix_len + H) * s.head_dim
     f += s.layers * per_layer
     n_ad = len(s.adapter_layers())
     f += n_ad * (2.0 * M * w * qd * 2 + 2.0 * batch * s.n_fop * w * 2 * kvd
                  + 4.0 * batch * s.n_q_heads * H * s.n_fop * s.head_dim)
-    f += 2.0 * M * w * 2 * w  # final modulation
+    f += 2.0 * Mm * w * 2 * w  # final modulation
     return f
 
 
@@ -379,7 +392,8 @@ def main():
             "mfma_frac": round(algorithmic_flops(s64, 64) / (ms64 * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
             "roofline": roofline_of(agg64, "mfma", "pi_b64"),
             # eager profile steps: ms per step and achieved TFLOP/s per kernel class
-            "kernel_classes": {k: {"ms": round(v[3] / 2, 4), "TFs": round(v[2] / (v[3] * 1e-3) / 1e12, 1)}
+            "kernel_classes": {k: {"ms": round(v[3] / 2, 4),
+                                   "TFs": round(v[2] / (v[3] * 1e-3) / 1e12, 1) if v[2] > 0 else None}
                                for k, v in sorted(agg64.items(), key=lambda kv: -kv[1][3])[:8]},
         }
         log(f"[pi_b64] {1000.0 / ms64:.1f} steps/s")

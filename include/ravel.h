@@ -197,8 +197,10 @@ ravel_status ravel_buffer_load(ravel_buffer* buf, const void* host_blob, size_t 
  * persistent path on, further records "persistent/<phase class>" split the
  * "persistent_layers" record by phase class (time between the kernel's grid
  * barriers as seen by its first block, summed over layers); they are not
- * additional launches.  On input *n is the capacity; on output the number of
- * records. */
+ * additional launches.  Launches whose row count is decided on the device
+ * (the modulation GEMMs run on the rows of distinct offset conditionings,
+ * class "gemm_rows") carry bytes = flops = 0.  On input *n is the
+ * capacity; on output the number of records. */
 typedef struct {
   char name[48];
   double bytes;

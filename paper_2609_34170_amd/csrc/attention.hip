@@ -410,20 +410,36 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
   for (int t = 0; t < ntile; ++t) {
     const int k0 = t * TK, buf = t & 1;
     if (t + 1 < ntile) load_tile(k0 + TK);
-    // S^T[key][row] for two 16-key sub-tiles
-    f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+    // S^T[key][row] for two 16-key sub-tiles, each summed in two independent
+    // MFMA chains (even / odd k-steps)
+    f32x4_t sa0 = {0.f, 0.f, 0.f, 0.f}, sa1 = sa0, sb0 = sa0, sb1 = sa0;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
+    for (int ks = 0; ks < KS; ks += 2) {
       const bf16x8_t k0f = *(const bf16x8_t*)&Ks[buf][l16][ks * 32 + grp * 8];
       const bf16x8_t k1f = *(const bf16x8_t*)&Ks[buf][16 + l16][ks * 32 + grp * 8];
-      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0f, qf[ks], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1f, qf[ks], s1, 0, 0, 0);
+      sa0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0f, qf[ks], sa0, 0, 0, 0);
+      sa1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1f, qf[ks], sa1, 0, 0, 0);
+      if (ks + 1 < KS) {
+        const bf16x8_t k2f = *(const bf16x8_t*)&Ks[buf][l16][(ks + 1) * 32 + grp * 8];
+        const bf16x8_t k3f = *(const bf16x8_t*)&Ks[buf][16 + l16][(ks + 1) * 32 + grp * 8];
+        sb0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k2f, qf[ks + 1], sb0, 0, 0, 0);
+        sb1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k3f, qf[ks + 1], sb1, 0, 0, 0);
+      }
+    }
+    // the V^T operands of the whole tile, read ahead of the softmax
+    u32x4_t vv[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const bf16_t* vrow = &Vt[buf][dt * 16 + l16][0];
+      const u32x2_t lo = *(const u32x2_t*)(vrow + grp * 4);
+      const u32x2_t hi = *(const u32x2_t*)(vrow + 16 + grp * 4);
+      vv[dt] = u32x4_t{lo[0], lo[1], hi[0], hi[1]};
     }
     float x[8];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      x[r] = s0[r] * sl2;
-      x[4 + r] = s1[r] * sl2;
+      x[r] = (sa0[r] + sb0[r]) * sl2;
+      x[4 + r] = (sa1[r] + sb1[r]) * sl2;
     }
     if (k0 + TK > nkeys) {  // uniform: the ragged last tile
 #pragma unroll
@@ -432,13 +448,15 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
         if (k0 + 16 + grp * 4 + r >= nkeys) x[4 + r] = -INFINITY;
       }
     }
-    float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    // every tile holds a valid key, so mx is finite; the first tile always moves
-    const bool mv = mx > mrow + kLazy;
-    if (__any(mv)) {
-      const float mnew = mv ? mx : mrow;
+    // The row maximum needs the 4 lane groups only when some lane of the wave
+    // sees a score above mrow + kLazy; otherwise mrow (equal on the row's lanes)
+    // stays the reference.  Every tile holds a valid key, so the maximum is
+    // finite, and the first tile always moves.
+    const float lmx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+    if (__any(lmx > mrow + kLazy)) {
+      float mx = fmaxf(lmx, __shfl_xor(lmx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mnew = mx > mrow + kLazy ? mx : mrow;
       const float corr = exp2f(mrow - mnew);
       mrow = mnew;
       lrow *= corr;
@@ -460,13 +478,8 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
                         pack_bf16x2(p[6], p[7])};
     const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pw);
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const bf16_t* vrow = &Vt[buf][dt * 16 + l16][0];
-      const u32x2_t lo = *(const u32x2_t*)(vrow + grp * 4);
-      const u32x2_t hi = *(const u32x2_t*)(vrow + 16 + grp * 4);
-      const u32x4_t vv = {lo[0], lo[1], hi[0], hi[1]};
-      o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vv), pf, o[dt], 0, 0, 0);
-    }
+    for (int dt = 0; dt < DT; ++dt)
+      o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vv[dt]), pf, o[dt], 0, 0, 0);
     if (t + 1 < ntile) store_tile(buf ^ 1);
     __syncthreads();
   }

@@ -52,10 +52,23 @@ RAVEL_DEV void ring_noise4(uint64_t seed, int e, int64_t r, int c, float z[4]) {
 // Adaptive RMSNorm
 // ---------------------------------------------------------------------------
 template <typename T>
+RAVEL_DEV void store4(T* p, float v0, float v1, float v2, float v3);
+template <>
+RAVEL_DEV void store4<float>(float* p, float v0, float v1, float v2, float v3) {
+  *(f32x4_t*)p = f32x4_t{v0, v1, v2, v3};
+}
+template <>
+RAVEL_DEV void store4<bf16_t>(bf16_t* p, float v0, float v1, float v2, float v3) {
+  *(u32x2_t*)p = u32x2_t{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+}
+
+// One wavefront per row, 4 consecutive features per lane and access.
+template <typename T>
 __global__ __launch_bounds__(256) void adarms_kernel(const float* __restrict__ x, int ldx, int M, int w,
                                                      const float* __restrict__ scale,
                                                      const float* __restrict__ shift, int ldm, int mode,
-                                                     float eps, T* __restrict__ y, int ldy) {
+                                                     const int* __restrict__ rowmap, float eps,
+                                                     T* __restrict__ y, int ldy) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= M) return;
@@ -67,33 +80,89 @@ __global__ __launch_bounds__(256) void adarms_kernel(const float* __restrict__ x
   }
   ss = wave_sum(ss);
   const float r = 1.0f / sqrtf(ss / (float)w + eps);
+  const size_t mrow = rowmap ? (size_t)rowmap[row] : (size_t)row;
   T* yr = y + (size_t)row * ldy;
   for (int n = lane * 4; n < w; n += 256) {
     const f32x4_t v = *(const f32x4_t*)(xr + n);
+    float o[4];
+    if (mode == 0) {
+      const f32x4_t sc = *(const f32x4_t*)(scale + mrow * ldm + n);
+      const f32x4_t sh = *(const f32x4_t*)(shift + mrow * ldm + n);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float o;
-      if (mode == 0)
-        o = v[i] * r * (1.0f + scale[(size_t)row * ldm + n + i]) + shift[(size_t)row * ldm + n + i];
-      else
-        o = v[i] * r * (1.0f + scale[n + i]);
-      yr[n + i] = act<T>::from_f(o);
+      for (int i = 0; i < 4; ++i) o[i] = v[i] * r * (1.0f + sc[i]) + sh[i];
+    } else {
+      const f32x4_t sc = *(const f32x4_t*)(scale + n);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[i] = v[i] * r * (1.0f + sc[i]);
     }
+    store4<T>(yr + n, o[0], o[1], o[2], o[3]);
   }
 }
 
 template <typename T>
 hipError_t launch_adarms(const float* x, int ldx, int M, int w, const float* scale, const float* shift,
-                         int ldm, int mode, float eps, T* y, int ldy, hipStream_t s) {
-  if (w % 4) return hipErrorInvalidValue;
+                         int ldm, int mode, const int* rowmap, float eps, T* y, int ldy, hipStream_t s) {
+  // 16-byte accesses: w, the row strides and the base pointers must be multiples of 4 floats
+  if (w % 4 || ldx % 4 || ldy % 4 || (mode == 0 && ldm % 4) || ((uintptr_t)x | (uintptr_t)scale) % 16 ||
+      (mode == 0 && (uintptr_t)shift % 16) || (uintptr_t)y % (4 * sizeof(T)))
+    return hipErrorInvalidValue;
   hipLaunchKernelGGL(adarms_kernel<T>, dim3((M + 3) / 4), dim3(256), 0, s, x, ldx, M, w, scale, shift,
-                     ldm, mode, eps, y, ldy);
+                     ldm, mode, rowmap, eps, y, ldy);
   return hipGetLastError();
 }
 template hipError_t launch_adarms<float>(const float*, int, int, int, const float*, const float*, int, int,
-                                         float, float*, int, hipStream_t);
+                                         const int*, float, float*, int, hipStream_t);
 template hipError_t launch_adarms<bf16_t>(const float*, int, int, int, const float*, const float*, int,
-                                          int, float, bf16_t*, int, hipStream_t);
+                                          int, const int*, float, bf16_t*, int, hipStream_t);
+
+// ---------------------------------------------------------------------------
+// Conditioning groups: envs with equal t_obs share delta, hence cond and every
+// modulation row, within a step.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void cond_groups_kernel(const int64_t* __restrict__ t_obs, int B, int H,
+                                                          int* __restrict__ grp, int* __restrict__ rowmap,
+                                                          int* __restrict__ rows) {
+  __shared__ int64_t to[kCondGroupsMaxB];
+  __shared__ int first[kCondGroupsMaxB];  // first env with the same t_obs
+  __shared__ int rank[kCondGroupsMaxB];   // group index of a first env
+  const int tid = threadIdx.x;
+  for (int e = tid; e < B; e += 256) to[e] = t_obs[e];
+  __syncthreads();
+  for (int e = tid; e < B; e += 256) {
+    int f = e;
+    for (int j = 0; j < e; ++j)
+      if (to[j] == to[e]) {
+        f = j;
+        break;
+      }
+    first[e] = f;
+  }
+  __syncthreads();
+  for (int e = tid; e < B; e += 256) {
+    if (first[e] != e) continue;
+    int c = 0;
+    for (int j = 0; j < e; ++j) c += first[j] == j;
+    rank[e] = c;
+  }
+  __syncthreads();
+  for (int e = tid; e < B; e += 256) {
+    const int g = rank[first[e]];
+    grp[e] = first[e] == e ? g : -1 - g;
+  }
+  for (int m = tid; m < B * H; m += 256) rowmap[m] = rank[first[m / H]] * H + m % H;
+  if (tid == 0) {
+    int n = 0;
+    for (int e = 0; e < B; ++e) n += first[e] == e;
+    rows[0] = n * H;
+  }
+}
+
+hipError_t launch_cond_groups(const int64_t* t_obs, int B, int H, int* grp, int* rowmap, int* rows,
+                              hipStream_t s) {
+  if (B < 1 || B > kCondGroupsMaxB || H < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(cond_groups_kernel, dim3(1), dim3(256), 0, s, t_obs, B, H, grp, rowmap, rows);
+  return hipGetLastError();
+}
 
 // ---------------------------------------------------------------------------
 // Offset conditioning hidden layer

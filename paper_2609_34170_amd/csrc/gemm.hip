@@ -26,16 +26,19 @@ RAVEL_DEV void epi1(const GemmArgs& a, int m, int n, float acc) {
   } else if constexpr (MODE == EPI_T) {
     ((T*)a.out_t)[(size_t)m * a.ldo_t + n] = act<T>::from_f(acc + b);
   } else if constexpr (MODE == EPI_RESID) {
-    const float g = a.gate ? a.gate[(size_t)m * a.ldg + n] : 1.0f;
+    const size_t gm = a.gate_rows ? (size_t)a.gate_rows[m] : (size_t)m;
+    const float g = a.gate ? a.gate[gm * a.ldg + n] : 1.0f;
     float* o = a.out_f + (size_t)m * a.ldo_f + n;
     *o = *o + g * acc;
   } else if constexpr (MODE == EPI_RESID_TANH) {
     float* o = a.out_f + (size_t)m * a.ldo_f + n;
     *o = *o + tanhf(*a.gate_scalar) * acc;
   } else if constexpr (MODE == EPI_COND) {
+    const int blk = a.cond_grp ? a.cond_grp[m] : m;
+    if (blk < 0) return;
     const float base = acc + b;
     for (int i = 0; i < a.H; ++i)
-      ((T*)a.out_t)[((size_t)m * a.H + i) * a.ldo_t + n] = act<T>::from_f(silu_f(a.ctau[(size_t)i * a.N + n] + base));
+      ((T*)a.out_t)[((size_t)blk * a.H + i) * a.ldo_t + n] = act<T>::from_f(silu_f(a.ctau[(size_t)i * a.N + n] + base));
   } else if constexpr (MODE == EPI_GELU_T) {
     ((T*)a.out_t)[(size_t)m * a.ldo_t + n] = act<T>::from_f(gelu_tanh_f(acc + b));
   } else if constexpr (MODE == EPI_SILU_T) {
@@ -85,7 +88,7 @@ RAVEL_DEV void epi4(const GemmArgs& a, int m, int n, f32x4_t v, bool vec) {
       const float t = tanhf(*a.gate_scalar);
       g = f32x4_t{t, t, t, t};
     } else {
-      if (a.gate) g = *(const f32x4_t*)(a.gate + (size_t)m * a.ldg + n);
+      if (a.gate) g = *(const f32x4_t*)(a.gate + (a.gate_rows ? (size_t)a.gate_rows[m] : (size_t)m) * a.ldg + n);
     }
     f32x4_t* o = (f32x4_t*)(a.out_f + (size_t)m * a.ldo_f + n);
     f32x4_t x = *o;
@@ -95,9 +98,11 @@ RAVEL_DEV void epi4(const GemmArgs& a, int m, int n, f32x4_t v, bool vec) {
     x[3] = x[3] + g[3] * v[3];
     *o = x;
   } else if constexpr (MODE == EPI_COND) {
+    const int blk = a.cond_grp ? a.cond_grp[m] : m;
+    if (blk < 0) return;
     for (int i = 0; i < a.H; ++i) {
       const f32x4_t c = *(const f32x4_t*)(a.ctau + (size_t)i * a.N + n);
-      store_bf16x4((bf16_t*)a.out_t + ((size_t)m * a.H + i) * a.ldo_t + n, silu_f(c[0] + v[0] + b[0]),
+      store_bf16x4((bf16_t*)a.out_t + ((size_t)blk * a.H + i) * a.ldo_t + n, silu_f(c[0] + v[0] + b[0]),
                    silu_f(c[1] + v[1] + b[1]), silu_f(c[2] + v[2] + b[2]), silu_f(c[3] + v[3] + b[3]));
     }
   } else if constexpr (MODE == EPI_GELU_T) {
@@ -194,6 +199,8 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs a) {
   const int tile = xcd_tile(blockIdx.x, gridDim.x);
   const int m0 = (tile / tiles_n) * BM;
   const int n0 = (tile % tiles_n) * BN;
+  if (a.m_rows) a.M = min(a.M, *a.m_rows);
+  if (m0 >= a.M) return;  // whole tile past a device-side row count (every K range alike)
   const int z = blockIdx.z;
   const int kbeg = z * a.kchunk;
   const int kend = min(a.K, kbeg + a.kchunk);
@@ -329,7 +336,10 @@ typedef const __attribute__((address_space(1))) void gmem_void_t;
 // gfx9 s_waitcnt immediate: vmcnt <= n, expcnt and lgkmcnt not waited for
 constexpr unsigned waitcnt_vm(int n) { return (unsigned)((n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8)); }
 
-template <int BM, int BN, int WM, int WN, int STAGES>
+// ROWLOOP: the row count is known on the device only (a.m_rows); block b owns
+// column tile b and runs every live row tile of it in turn (no K split, fp32
+// output: EPI_F32 only).
+template <int BM, int BN, int WM, int WN, int STAGES, bool ROWLOOP = false>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_lds_kernel(GemmArgs a) {
   constexpr int NW = WM * WN;
   constexpr int BK = 64;
@@ -346,8 +356,19 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_lds_kernel(GemmArgs a) {
   const int l16 = lane & 15, grp = lane >> 4;
   const int wm = wave / WN, wn = wave % WN;
   const int tiles_n = (a.N + BN - 1) / BN;
-  const int tile = xcd_tile(blockIdx.x, gridDim.x);
-  const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
+  int tile, m0, n0;
+  if constexpr (ROWLOOP) {
+    tile = blockIdx.x;
+    m0 = 0;
+    n0 = tile * BN;
+    a.M = min(a.M, *a.m_rows);
+  } else {
+    tile = xcd_tile(blockIdx.x, gridDim.x);
+    m0 = (tile / tiles_n) * BM;
+    n0 = (tile % tiles_n) * BN;
+    if (a.m_rows) a.M = min(a.M, *a.m_rows);
+  }
+  if (m0 >= a.M) return;  // whole tile past a device-side row count (every K range alike)
   const int z = blockIdx.z;
   const int kbeg = z * a.kchunk;
   const int kend = min(a.K, kbeg + a.kchunk);
@@ -383,6 +404,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_lds_kernel(GemmArgs a) {
     return v;
   };
 
+  for (;;) {  // once, or (ROWLOOP) once per live row tile
   f32x4_t acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
@@ -454,7 +476,17 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_lds_kernel(GemmArgs a) {
         acc[i][j] = sum;
       }
   }
-  epilogue(a, acc, mw, nw, l16, grp);
+  if constexpr (ROWLOOP)
+    epi_frags<EPI_F32>(a, acc, mw, nw, l16, grp);  // the only mode of row-loop launches
+  else
+    epilogue(a, acc, mw, nw, l16, grp);
+  if constexpr (!ROWLOOP) break;
+  m0 += BM;
+  if (m0 >= a.M) break;
+  // every wave's LDS reads of this tile completed before its MFMAs; the next
+  // tile's loads may overwrite the stages once all waves are here
+  __syncthreads();
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -814,12 +846,23 @@ static hipError_t launch_lds_tile(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int BM, int BN, int WM, int WN, int STAGES>
+static hipError_t launch_lds_rows(const GemmArgs& a, hipStream_t s) {
+  if (a.ksplit != 1 || !a.m_rows || a.mode != EPI_F32) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((gemm_lds_kernel<BM, BN, WM, WN, STAGES, true>), dim3((a.N + BN - 1) / BN), dim3(64 * WM * WN),
+                     0, s, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm_bf16(const GemmArgs& a, int tile, hipStream_t s) {
   // direct-to-LDS variants (measured on MI355X at M = 3200: 128x128 with two
   // stages 744-804 TF/s at K = 1024; 128x64 with three stages 514-581 TF/s at
   // N = 1024, K = 2048-4096) where K tiles are whole and rows 16-byte aligned
   const bool lds_ok = a.K % 64 == 0 && a.kchunk % 64 == 0 && a.lda % 8 == 0 && a.ldb % 8 == 0 &&
                       ((uintptr_t)a.A % 16) == 0 && ((uintptr_t)a.B % 16) == 0 && a.M > 0 && a.N > 0;
+  // device-side row count (few distinct rows, many columns): 256-row tiles, one
+  // block per column tile, so every weight byte is streamed once
+  if (lds_ok && a.m_rows && a.ksplit == 1 && a.mode == EPI_F32) return launch_lds_rows<256, 128, 4, 2, 2>(a, s);
   if (lds_ok && tile == TILE_128x128) return launch_lds_tile<128, 128, 2, 2, 2>(a, s);
   if (lds_ok && tile == TILE_128x64) return launch_lds_tile<128, 64, 2, 2, 3>(a, s);
   switch (tile) {
@@ -841,6 +884,7 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, int tile, hipStream_t s) {
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   const int n = blockIdx.x * 64 + (threadIdx.x & 63);
   const int m = blockIdx.y * 4 + (threadIdx.x >> 6);
+  if (a.m_rows) a.M = min(a.M, *a.m_rows);
   if (m >= a.M) return;
   const float* __restrict__ A = (const float*)a.A + (size_t)m * a.lda;
   const float* __restrict__ B = (const float*)a.B;

@@ -46,6 +46,10 @@ struct GemmArgs {
   const float* gate; int ldg;
   const float* gate_scalar;
   const float* ctau; int H;
+  // Rows that share their modulation (see launch_cond_groups); all optional:
+  const int* m_rows;     // device row count: rows >= min(M, *m_rows) are neither computed nor stored
+  const int* gate_rows;  // [M]: EPI_RESID reads gate row gate_rows[m] instead of row m
+  const int* cond_grp;   // [M], EPI_COND: output block cond_grp[m] (>= 0), or nothing (< 0)
 };
 
 // Tile configurations of the bf16 MFMA GEMM.
@@ -95,10 +99,19 @@ hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t s);
 // ---------------------------------------------------------------------------
 // y[m,:] = T( x/rms(x) * (1 + scale) + shift ), per-row modulation rows of stride ldm
 // (mode 0) or a per-feature scale without shift (mode 1: scale[n], shift ignored).
+// With rowmap (mode 0), row m takes its scale/shift from row rowmap[m].
 template <typename T>
 hipError_t launch_adarms(const float* x, int ldx, int M, int w, const float* scale,
-                         const float* shift, int ldm, int mode, float eps, T* y, int ldy,
+                         const float* shift, int ldm, int mode, const int* rowmap, float eps, T* y, int ldy,
                          hipStream_t s);
+// Groups of envs whose offset conditioning is identical within a step (equal
+// observation time t_obs, hence equal context age and delta): group g is the
+// g-th distinct t_obs in env order.  grp[e] = g for the first env of its group
+// and -1 - g for the others; rowmap[e*H + i] = g*H + i; *rows = (#groups)*H.
+// One block; B <= kCondGroupsMaxB.
+constexpr int kCondGroupsMaxB = 1024;
+hipError_t launch_cond_groups(const int64_t* t_obs, int B, int H, int* grp, int* rowmap, int* rows,
+                              hipStream_t s);
 
 // Offset conditioning hidden layer: h1[e,n] = T(silu(wd1[n]*delta_e + bd1[n])),
 // delta_e = (t - t_obs[e]) / H + delta_bias.

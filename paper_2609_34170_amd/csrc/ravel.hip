@@ -333,6 +333,11 @@ struct ravel_buffer {
   int attn_nsplit = 1, attn_kps = 0;
   bool mod_all = false;
   int mod_ld = 0;
+  // per-layer modulation on the rows of distinct offset conditionings only
+  bool cgroups = false;
+  int* cgrp = nullptr;     // [B] conditioning group of each env (negative: not the group's first env)
+  int* crowmap = nullptr;  // [B*H] modulation row of each buffer row
+  int* crows = nullptr;    // (#groups) * H
   // persistent few-row path
   bool persistent = false;
   std::vector<Phase> phases;
@@ -387,29 +392,32 @@ ravel_status run_gemm(ravel_buffer* b, hipStream_t s, KernelRecorder* rec, const
   if (!m->bf16) {
     epi.ksplit = 1;
     epi.kchunk = K;
-    if (rec) rec->begin(name, bytes, flops);
+    if (rec) rec->begin(name, epi.m_rows ? 0.0 : bytes, epi.m_rows ? 0.0 : flops);
     HIP_TRY(launch_gemm_f32(epi, s));
     if (rec) rec->end();
     return RAVEL_OK;
   }
   if ((K % 8) || (lda % 8) || (ldb % 8)) return fail(RAVEL_E_SHAPE, std::string(name) + ": K and strides must be multiples of 8");
   const GemmPlan p = plan_gemm(M, N, K, epi.mode == EPI_GEGLU);
-  epi.ksplit = p.ksplit;
-  epi.kchunk = p.kchunk;
+  epi.ksplit = epi.m_rows ? 1 : p.ksplit;  // device row count: whole K per block
+  epi.kchunk = epi.m_rows ? K : p.kchunk;
   epi.partial = b->gpart;
   epi.counters = b->gcnt;
   if (p.part_elems > b->gpart_elems || p.tiles > b->gcnt_n)
     return fail(RAVEL_E_STATE, std::string(name) + ": GEMM workspace too small");
+  if (epi.m_rows && p.skinny) return fail(RAVEL_E_STATE, std::string(name) + ": device row count needs a tiled GEMM");
   if (rec) {
     static const char* tn[] = {"64x64", "128x128", "64x128", "128x64", "32x64", "256x128", "128x256", "256x256"};
     char full[48];
-    if (p.skinny && p.regstream)
+    if (epi.m_rows)  // rows known on the device only: no byte / flop figures
+      snprintf(full, sizeof full, "gemm_rows:%s", name);
+    else if (p.skinny && p.regstream)
       snprintf(full, sizeof full, "gemm_regstream<%d>:%s", (M + 15) / 16, name);
     else if (p.skinny)
       snprintf(full, sizeof full, "gemm_stream<%d,%d>:%s", (M + 15) / 16, p.kchunk, name);
     else
       snprintf(full, sizeof full, "gemm%s:%s", tn[p.tile], name);
-    rec->begin(full, bytes, flops);
+    rec->begin(full, epi.m_rows ? 0.0 : bytes, epi.m_rows ? 0.0 : flops);
   }
   if (p.skinny) {
     if (p.regstream)
@@ -486,6 +494,15 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
   REC_BEGIN("delta_hidden", (double)B * w * (8 + elt), (double)B * w * 4);
   HIP_TRY(launch_delta_hidden<T>(b->t, b->t_obs, B, H, c.delta_bias, m->d_w1, m->d_b1, w, (T*)b->h1, s));
   REC_END();
+  // Envs with equal t_obs have equal delta, so equal cond rows and modulation
+  // rows: cond is written once per group (compacted) and the modulation GEMM
+  // runs on the groups' rows only.
+  const int* rowmap = b->cgroups ? b->crowmap : nullptr;
+  if (b->cgroups) {
+    REC_BEGIN("cond_groups", (double)B * 8 + (double)BH * 4, 0.0);
+    HIP_TRY(launch_cond_groups(b->t_obs, B, H, b->cgrp, b->crowmap, b->crows, s));
+    REC_END();
+  }
   {
     GemmArgs e = epi_args(EPI_COND);
     e.bias = m->d_b2;
@@ -493,6 +510,7 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
     e.ldo_t = w;
     e.ctau = m->ctau;
     e.H = H;
+    e.cond_grp = b->cgroups ? b->cgrp : nullptr;
     RV_TRY(run_gemm<T>(b, s, rec, "cond", b->h1, w, m->d_w2, w, B, w, w, e));
   }
   // 2. input projection of the buffer in logical order
@@ -514,6 +532,7 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
     e.bias = m->mod_all_b;
     e.out_f = b->mod;
     e.ldo_f = ldm;
+    e.m_rows = b->cgroups ? b->crows : nullptr;
     RV_TRY(run_gemm<T>(b, s, rec, "mod_all", b->cond, w, m->mod_all_w, w, BH, ldm, w, e));
   }
   for (int l = 0; l < c.layers; ++l) {
@@ -527,7 +546,7 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
       RV_TRY(run_gemm<T>(b, s, rec, "mod", b->cond, w, L.mod_w, w, BH, 6 * w, w, e));
     }
     REC_BEGIN("adarms", (double)BH * w * (12 + elt), (double)BH * w * 5);
-    HIP_TRY(launch_adarms<T>(b->x, w, BH, w, mod, mod + w, ldm, 0, c.rms_eps, (T*)b->y, w, s));
+    HIP_TRY(launch_adarms<T>(b->x, w, BH, w, mod, mod + w, ldm, 0, rowmap, c.rms_eps, (T*)b->y, w, s));
     REC_END();
     {
       GemmArgs e = epi_args(EPI_T);
@@ -562,11 +581,12 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
       e.ldo_f = w;
       e.gate = mod + 2 * w;
       e.ldg = ldm;
+      e.gate_rows = rowmap;
       RV_TRY(run_gemm<T>(b, s, rec, "o", b->att, qd, L.o_w, qd, BH, w, qd, e));
     }
     if (L.adapter >= 0 && fop) {
       REC_BEGIN("adarms", (double)BH * w * (8 + elt), (double)BH * w * 4);
-      HIP_TRY(launch_adarms<T>(b->x, w, BH, w, L.gamma, nullptr, 0, 1, c.rms_eps, (T*)b->y, w, s));
+      HIP_TRY(launch_adarms<T>(b->x, w, BH, w, L.gamma, nullptr, 0, 1, nullptr, c.rms_eps, (T*)b->y, w, s));
       REC_END();
       {
         GemmArgs e = epi_args(EPI_T);
@@ -605,7 +625,7 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
       }
     }
     REC_BEGIN("adarms", (double)BH * w * (12 + elt), (double)BH * w * 5);
-    HIP_TRY(launch_adarms<T>(b->x, w, BH, w, mod + 3 * w, mod + 4 * w, ldm, 0, c.rms_eps, (T*)b->y, w, s));
+    HIP_TRY(launch_adarms<T>(b->x, w, BH, w, mod + 3 * w, mod + 4 * w, ldm, 0, rowmap, c.rms_eps, (T*)b->y, w, s));
     REC_END();
     {
       GemmArgs e = epi_args(EPI_GEGLU);
@@ -619,6 +639,7 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
       e.ldo_f = w;
       e.gate = mod + 5 * w;
       e.ldg = ldm;
+      e.gate_rows = rowmap;
       RV_TRY(run_gemm<T>(b, s, rec, "down", b->u, F, L.down_w, F, BH, w, F, e));
     }
   }
@@ -633,7 +654,7 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
     RV_TRY(run_gemm<T>(b, s, rec, "final_mod", b->cond, w, m->fmod_w, w, BH, 2 * w, w, e));
   }
   REC_BEGIN("adarms", (double)BH * w * (12 + elt), (double)BH * w * 5);
-  HIP_TRY(launch_adarms<T>(b->x, w, BH, w, fmod, fmod + w, ldf, 0, c.rms_eps, (T*)b->y, w, s));
+  HIP_TRY(launch_adarms<T>(b->x, w, BH, w, fmod, fmod + w, ldf, 0, rowmap, c.rms_eps, (T*)b->y, w, s));
   REC_END();
   {
     GemmArgs e = epi_args(EPI_F32);
@@ -1397,8 +1418,16 @@ ravel_status ravel_buffer_create(ravel_model* m, int32_t batch, uint64_t seed, r
     ar.want(&b->cond, (size_t)BH * w * E);
     ar.want(&b->h1, (size_t)B * w * E);
     // few rows: every layer's modulation comes from one GEMM at the start of the step
-    b->mod_all = BH <= 64;
+    // Few rows, or rows grouped by offset conditioning: every layer's modulation
+    // comes from one GEMM at the start of the step (on the groups' rows only).
+    b->cgroups = BH > 64 && B > 1 && B <= kCondGroupsMaxB;
+    b->mod_all = BH <= 64 || b->cgroups;
     b->mod_ld = b->mod_all ? (6 * c.layers + 2) * w : 6 * w;
+    if (b->cgroups) {
+      ar.want((void**)&b->cgrp, (size_t)B * 4);
+      ar.want((void**)&b->crowmap, (size_t)BH * 4);
+      ar.want((void**)&b->crows, 16);
+    }
     ar.want((void**)&b->mod, (size_t)BH * b->mod_ld * 4);
     ar.want(&b->y, (size_t)BH * w * E);
     ar.want(&b->qkv, (size_t)BH * qkvd * E);

@@ -128,6 +128,20 @@ def test_edge_shapes_bf16(shape_kw, batch):
     print(f"edge {shape_kw['horizon']}x{shape_kw['head_dim']} B={batch}: {ea:.2e} {ex:.2e}")
 
 
+@pytest.mark.parametrize("dtype,batch", [(W.BF16, 7), (W.F32, 10)])
+def test_conditioning_groups_staggered_refresh(dtype, batch):
+    # staggered refreshes with period 3: three distinct context ages among the envs,
+    # so several envs share each group and the groups' first envs are 0, 1, 2; more
+    # than 64 buffer rows, so the per-layer modulation runs on the groups' rows
+    s = synth.RavelShape(layers=2, width=128, n_q_heads=4, n_kv_heads=2, head_dim=32, mlp_dim=256,
+                         horizon=12, action_dim=6, prefix_len=40, n_fop=4, fop_obs_dim=16,
+                         context_period=3, stagger=True, dtype=dtype, batch=batch, name="groups")
+    assert batch * s.horizon > 64
+    wts = synth.draw_weights(s, seed=5, stress=True)
+    ea, ex, n = run_parity(s, wts, batch=batch, seed=2, steps=9, oracle_dtype=np.float64, check_every=3)
+    print(f"groups {dtype} B={batch}: {ea:.2e} {ex:.2e}")
+
+
 def test_pi_b1_full_size_steps():
     s = synth.get_config("pi_b1")
     wts = synth.draw_weights(s, seed=0)
