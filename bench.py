@@ -252,6 +252,8 @@ class Workload:
             recs = self.buf.profile_step(self.fop, self.action)
             self.t += 1
             for name, by, fl, ms in recs:
+                if name.startswith("phase/"):
+                    continue  # single phases of the persistent kernel (already in its classes)
                 if name.startswith("persistent/"):
                     a = self.phases.setdefault(name.split("/", 1)[1], [0, 0.0, 0.0, 0.0])
                     a[0] += 1

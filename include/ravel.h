@@ -196,8 +196,9 @@ ravel_status ravel_buffer_load(ravel_buffer* buf, const void* host_blob, size_t 
  * algorithmic bytes and flops of that launch, and its duration.  With the
  * persistent path on, further records "persistent/<phase class>" split the
  * "persistent_layers" record by phase class (time between the kernel's grid
- * barriers as seen by its first block, summed over layers); they are not
- * additional launches.  Launches whose row count is decided on the device
+ * barriers as seen by its first block, summed over layers), followed by one
+ * record "phase/<index>/<phase class>" per phase in launch order; neither kind
+ * is an additional launch.  Launches whose row count is decided on the device
  * (the modulation GEMMs run on the rows of distinct offset conditionings,
  * class "gemm_rows") carry bytes = flops = 0.  On input *n is the
  * capacity; on output the number of records. */

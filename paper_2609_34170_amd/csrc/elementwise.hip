@@ -191,27 +191,110 @@ template hipError_t launch_delta_hidden<bf16_t>(const int64_t*, const int64_t*, 
                                                 const float*, int, bf16_t*, hipStream_t);
 
 // ---------------------------------------------------------------------------
-// Input projection (logical slot order)
+// Offset conditioning rows: cond[blk*H + i, n] = T(silu(ctau[i, n] + d[e, n]))
 // ---------------------------------------------------------------------------
-__global__ void in_proj_kernel(const float* __restrict__ X, const int64_t* t, int B, int H, int D,
-                               const float* __restrict__ w_in, const float* __restrict__ b_in, int w,
-                               float* __restrict__ x) {
-  const int row = blockIdx.y;  // e*H + i
-  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+template <typename T>
+__global__ void cond_expand_kernel(const float* __restrict__ d, int B, int H, int w, const float* __restrict__ ctau,
+                                   const int* __restrict__ grp, T* __restrict__ cond) {
+  // thread: 4 consecutive columns of one (env, slot) row
+  const int i = blockIdx.y, e = blockIdx.z;
+  const int blk = grp ? grp[e] : e;
+  if (blk < 0) return;
+  const int n = (blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (n >= w) return;
-  const int e = row / H, i = row % H;
-  const int ph = (int)((*t + i) % H);
-  const float* a = X + ((size_t)e * H + ph) * D;
-  const float* wr = w_in + (size_t)n * D;
-  float acc = 0.f;
-  for (int d = 0; d < D; ++d) acc += wr[d] * a[d];
-  x[(size_t)row * w + n] = acc + b_in[n];
+  T* o = cond + ((size_t)blk * H + i) * w;
+  if (n + 4 <= w && (w % 4) == 0) {
+    const f32x4_t dv = *(const f32x4_t*)(d + (size_t)e * w + n);
+    const f32x4_t c = *(const f32x4_t*)(ctau + (size_t)i * w + n);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) o[n + r] = act<T>::from_f(silu_f(c[r] + dv[r]));
+    return;
+  }
+  for (int r = 0; r < 4 && n + r < w; ++r)
+    o[n + r] = act<T>::from_f(silu_f(ctau[(size_t)i * w + n + r] + d[(size_t)e * w + n + r]));
 }
 
-hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D, const float* w_in,
-                          const float* b_in, int w, float* x, hipStream_t s) {
-  hipLaunchKernelGGL(in_proj_kernel, dim3((w + 255) / 256, B * H), dim3(256), 0, s, X, t, B, H, D, w_in,
-                     b_in, w, x);
+template <typename T>
+hipError_t launch_cond_expand(const float* d, int B, int H, int w, const float* ctau, const int* grp, T* cond,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(cond_expand_kernel<T>, dim3((w + 255) / 256, H, B), dim3(64), 0, s, d, B, H, w, ctau, grp, cond);
+  return hipGetLastError();
+}
+template hipError_t launch_cond_expand<float>(const float*, int, int, int, const float*, const int*, float*, hipStream_t);
+template hipError_t launch_cond_expand<bf16_t>(const float*, int, int, int, const float*, const int*, bf16_t*,
+                                               hipStream_t);
+
+// ---------------------------------------------------------------------------
+// Input projection (logical slot order)
+// ---------------------------------------------------------------------------
+__global__ void transpose_f32_kernel(const float* __restrict__ src, int R, int C, float* __restrict__ dst) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= R * C) return;
+  const int r = idx / C, c = idx % C;
+  dst[(size_t)c * R + r] = src[idx];
+}
+
+hipError_t launch_transpose_f32(const float* src, int R, int C, float* dst, hipStream_t s) {
+  hipLaunchKernelGGL(transpose_f32_kernel, dim3((R * C + 255) / 256), dim3(256), 0, s, src, R, C, dst);
+  return hipGetLastError();
+}
+
+// Block = 4 waves over 256 consecutive columns (one 64-column tile per wave) and
+// kInProjRows rows.  The weights are read transposed (w_inT[d, n]: consecutive
+// lanes, consecutive addresses); the ring row of each slot is wave-uniform.
+constexpr int kInProjRows = 1;
+__global__ __launch_bounds__(256) void in_proj_kernel(const float* __restrict__ X, const int64_t* t, int B, int H, int D,
+                                                      const float* __restrict__ w_inT, const float* __restrict__ b_in,
+                                                      int w, float* __restrict__ x, InProjNorm nrm) {
+  const int n = blockIdx.x * 256 + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int BH = B * H;
+  const int64_t tt = *t;
+  const float bias = n < w ? b_in[n] : 0.f;
+  for (int rr = 0; rr < kInProjRows; ++rr) {
+    const int row = blockIdx.y * kInProjRows + rr;
+    if (row >= BH) break;
+    const int e = row / H, i = row % H;
+    const int ph = (int)((tt + i) % H);
+    const float* a = X + ((size_t)e * H + ph) * D;
+    float acc = bias;
+    if (n < w)
+      for (int d = 0; d < D; ++d) acc += w_inT[(size_t)d * w + n] * a[d];
+    if (n < w) x[(size_t)row * w + n] = acc;
+    if (!nrm.p) continue;
+    // first adaptive norm of the persistent step: p = bf16((1 + scale) x), the
+    // 64-column tile's sum of squares of the row, and the bf16 shift copies
+    float v = n < w ? acc : 0.f;
+    if (n < w) nrm.p[(size_t)row * w + n] = f32_to_bf16((1.f + nrm.scale[(size_t)row * nrm.ldm + n]) * acc);
+    const float sq = wave_sum(v * v);
+    if (lane == 0 && n < w) nrm.sumsq[(size_t)(n >> 6) * 64 + row] = sq;
+  }
+}
+
+// bf16 copies of the norm shifts: thread = 8 consecutive columns of one (chunk, row)
+__global__ __launch_bounds__(256) void shift_copy_kernel(int M, int w, InProjNorm nrm) {
+  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const int per_row = w / 8;
+  const size_t total = (size_t)nrm.cvt_chunks * M * per_row;
+  if (idx >= total) return;
+  const int n = (int)(idx % per_row) * 8;
+  const int row = (int)((idx / per_row) % M);
+  const int c = (int)(idx / ((size_t)per_row * M));
+  const float* src = nrm.cvt_in + (size_t)row * nrm.cvt_ld + (size_t)c * nrm.cvt_stride + n;
+  const f32x4_t a = *(const f32x4_t*)src, b = *(const f32x4_t*)(src + 4);
+  const u32x4_t o = {pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3])};
+  *(u32x4_t*)(nrm.cvt_out + ((size_t)c * M + row) * w + n) = o;
+}
+
+hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D, const float* w_inT,
+                          const float* b_in, int w, float* x, const InProjNorm& nrm, hipStream_t s) {
+  if (nrm.p && (B * H > 64 || (w % 64) != 0)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(in_proj_kernel, dim3((w + 255) / 256, (B * H + kInProjRows - 1) / kInProjRows), dim3(256), 0, s,
+                     X, t, B, H, D, w_inT, b_in, w, x, nrm);
+  if (nrm.p && nrm.cvt_chunks > 0) {
+    const size_t total = (size_t)nrm.cvt_chunks * B * H * (w / 8);
+    hipLaunchKernelGGL(shift_copy_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, B * H, w, nrm);
+  }
   return hipGetLastError();
 }
 

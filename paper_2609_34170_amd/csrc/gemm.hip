@@ -100,10 +100,19 @@ RAVEL_DEV void epi4(const GemmArgs& a, int m, int n, f32x4_t v, bool vec) {
   } else if constexpr (MODE == EPI_COND) {
     const int blk = a.cond_grp ? a.cond_grp[m] : m;
     if (blk < 0) return;
-    for (int i = 0; i < a.H; ++i) {
-      const f32x4_t c = *(const f32x4_t*)(a.ctau + (size_t)i * a.N + n);
-      store_bf16x4((bf16_t*)a.out_t + ((size_t)blk * a.H + i) * a.ldo_t + n, silu_f(c[0] + v[0] + b[0]),
-                   silu_f(c[1] + v[1] + b[1]), silu_f(c[2] + v[2] + b[2]), silu_f(c[3] + v[3] + b[3]));
+    // the time embeddings of 8 slots are loaded before any of their outputs is
+    // stored: one memory latency per 8 slots (the stores could alias the loads,
+    // so the compiler would otherwise wait for each load in turn)
+    for (int i0 = 0; i0 < a.H; i0 += 8) {
+      f32x4_t c[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        c[j] = (i0 + j < a.H) ? *(const f32x4_t*)(a.ctau + (size_t)(i0 + j) * a.N + n) : f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (i0 + j < a.H)
+          store_bf16x4((bf16_t*)a.out_t + ((size_t)blk * a.H + i0 + j) * a.ldo_t + n, silu_f(c[j][0] + v[0] + b[0]),
+                       silu_f(c[j][1] + v[1] + b[1]), silu_f(c[j][2] + v[2] + b[2]), silu_f(c[j][3] + v[3] + b[3]));
     }
   } else if constexpr (MODE == EPI_GELU_T) {
     store_bf16x4((bf16_t*)a.out_t + (size_t)m * a.ldo_t + n, gelu_tanh_f(v[0] + b[0]), gelu_tanh_f(v[1] + b[1]),
@@ -519,20 +528,16 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(GemmArgs a) {
   const bf16_t* __restrict__ B = (const bf16_t*)a.B;
 
   bf16x8_t wfr[NFR][NF];
+  auto load_frag = [&](int tile, int c, int f) -> bf16x8_t {
+    const int n = tile * (64 * NFR) + wave * (16 * NFR) + c * 16 + l16;
+    const int k = kbeg + f * 32 + grp * 8;
+    return (n < a.N && k < a.K) ? *(const bf16x8_t*)(B + (size_t)n * a.ldb + k) : bf16x8_t{};
+  };
   auto load_w = [&](int tile) {
-    const int nw = tile * (64 * NFR) + wave * (16 * NFR);
 #pragma unroll
-    for (int c = 0; c < NFR; ++c) {
-      const int n = nw + c * 16 + l16;
+    for (int c = 0; c < NFR; ++c)
 #pragma unroll
-      for (int f = 0; f < NF; ++f) {
-        const int k = kbeg + f * 32 + grp * 8;
-        if (n < a.N && k < a.K)
-          wfr[c][f] = *(const bf16x8_t*)(B + (size_t)n * a.ldb + k);
-        else
-          wfr[c][f] = bf16x8_t{};
-      }
-    }
+      for (int f = 0; f < NF; ++f) wfr[c][f] = load_frag(tile, c, f);
   };
   int tile = blockIdx.x;
   if (tile >= tiles) return;
@@ -567,6 +572,11 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(GemmArgs a) {
     for (int c = 0; c < NFR; ++c)
 #pragma unroll
       for (int i = 0; i < MT; ++i) acc[c][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // each weight fragment is reloaded with the next tile's as soon as its last
+    // MFMA has read it: the next tile streams in during this tile's MFMAs and
+    // epilogue, with no second register buffer
+    const int next = tile + (int)gridDim.x;
+    const bool more = next < tiles;
 #pragma unroll
     for (int f = 0; f < NF; ++f) {
 #pragma unroll
@@ -576,9 +586,11 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(GemmArgs a) {
         for (int c = 0; c < NFR; ++c)
           acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wfr[c][f], xf, acc[c][i], 0, 0, 0);
       }
+      if (more) {
+#pragma unroll
+        for (int c = 0; c < NFR; ++c) wfr[c][f] = load_frag(next, c, f);
+      }
     }
-    // overlap: the next tile's weights stream in during this tile's epilogue
-    if (tile + (int)gridDim.x < tiles) load_w(tile + gridDim.x);
 
     if (a.ksplit > 1) {
       constexpr int FR = MT * NFR;  // fragments per wave
@@ -621,8 +633,18 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(GemmArgs a) {
 template <int MT, int NFR, int KR>
 static hipError_t launch_skinny_t(const GemmArgs& a, hipStream_t s) {
   const int tiles = (a.N + 64 * NFR - 1) / (64 * NFR);
-  // at most ~2 resident waves of blocks; extra tiles are looped over inside a block
-  const int cap = (a.ksplit > 1) ? tiles : std::max(1, std::min(tiles, 512));
+  // one resident round of blocks (the row tile in LDS decides how many fit on a
+  // CU); extra tiles are looped over inside a block, with their weights pipelined
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+      cus = 256;
+  }
+  constexpr int lds_bytes = MT * 16 * (KR + 8) * 2;
+  constexpr int per_cu = lds_bytes > 80 * 1024 ? 1 : 2;
+  const int cap = (a.ksplit > 1) ? tiles : std::max(1, std::min(tiles, per_cu * cus));
   dim3 grid(cap, a.ksplit);
   hipLaunchKernelGGL((gemm_skinny_kernel<MT, NFR, KR>), grid, dim3(256), 0, s, a);
   return hipGetLastError();

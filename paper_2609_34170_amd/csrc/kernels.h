@@ -119,9 +119,32 @@ template <typename T>
 hipError_t launch_delta_hidden(const int64_t* t, const int64_t* t_obs, int B, int H, float delta_bias,
                                const float* wd1, const float* bd1, int w, T* h1, hipStream_t s);
 
-// Input projection in logical slot order: x[e*H+i, n] = W_in[n,:] . X[e, (t+i) mod H, :] + b_in[n].
-hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D, const float* w_in,
-                          const float* b_in, int w, float* x, hipStream_t s);
+// Offset conditioning rows: cond[blk*H + i, n] = T(silu(ctau[i, n] + d[e, n])) for every env e
+// with blk = grp[e] (>= 0; envs with grp[e] < 0 write nothing) or blk = e without grp.
+template <typename T>
+hipError_t launch_cond_expand(const float* d, int B, int H, int w, const float* ctau, const int* grp, T* cond,
+                              hipStream_t s);
+
+// dst[c, r] = src[r, c] for an R x C fp32 matrix.
+hipError_t launch_transpose_f32(const float* src, int R, int C, float* dst, hipStream_t s);
+
+// Optional outputs of the input projection for a persistent step (B*H <= 64 rows,
+// w a multiple of 64): the first adaptive norm's p[row, n] = bf16((1 + scale[row*ldm + n]) x),
+// the rows' sums of squares per 64-column tile sumsq[(n/64)*64 + row], and bf16 copies
+// cvt_out[c][row][n] = bf16(cvt_in[row*cvt_ld + c*cvt_stride + n]) for c < cvt_chunks.
+// p = NULL: none of these.
+struct InProjNorm {
+  const float* scale; int ldm;
+  bf16_t* p;
+  float* sumsq;
+  const float* cvt_in; int cvt_ld, cvt_stride, cvt_chunks;
+  bf16_t* cvt_out;
+};
+
+// Input projection in logical slot order: x[e*H+i, n] = W_in[n,:] . X[e, (t+i) mod H, :] + b_in[n],
+// with the weights given transposed (w_inT[d, n] = W_in[n, d]).
+hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D, const float* w_inT,
+                          const float* b_in, int w, float* x, const InProjNorm& nrm, hipStream_t s);
 
 // Analytic velocity fields (logical order): OT v = (x - a*)/tau_i, LINEAR v = lambda x.
 hipError_t launch_analytic_velocity(int kind, const float* X, const int64_t* t, int B, int H, int D,

@@ -5,7 +5,7 @@
 
 namespace ravel {
 
-enum PhaseType : int { PH_ROWSTATS = 1, PH_GEMM = 2, PH_ATTN = 3 };
+enum PhaseType : int { PH_GEMM = 2, PH_ATTN = 3 };
 
 // GEMM activation operand
 enum PAMode : int {
@@ -31,23 +31,11 @@ constexpr int kBarrierSpinLimit = 1 << 22;
 // kw = 2 only for plain bf16 activations)
 constexpr int kMaxKSplit = 8;
 // key splits of one attention (env, head)
-constexpr int kMaxAttnSplit = 16;
-// keys of one attention split staged in LDS, by head dimension
-__host__ __device__ constexpr int attn_keys_per_split_max(int hd) { return (32768 / hd) < 256 ? (32768 / hd) : 256; }
-
-// First phase.  Items below N/64: one 64-column tile of x, its rows' sums of
-// squares and p = bf16((1 + scale) * x).  Items above: 8192-element pieces of the
-// bf16 copy of the norm shifts, cvt_out[c][m][n] = bf16(cvt_in[m][c * cvt_stride + n])
-// for chunk c < cvt_chunks, m < M, n < N.
-struct PRowstats {
-  const float* x; int ldx;
-  int M, N;
-  int ns_mode; const float* ns; int ldns;
-  bf16_t* p; int ldp;
-  float* sumsq_out;  // [N/64][64]
-  const float* cvt_in; int cvt_ld, cvt_stride, cvt_chunks;
-  bf16_t* cvt_out;
-};
+constexpr int kMaxAttnSplit = 32;
+// keys of one attention split: 32 KB of keys and values (a split's share is
+// fetched into registers, 128 bytes per thread, while the block waits at the
+// barrier that opens the phase)
+__host__ __device__ constexpr int attn_keys_per_split_max(int hd) { return (8192 / hd) < 256 ? (8192 / hd) : 256; }
 
 struct PGemm {
   int a_mode, e_mode;  // PAMode, PEMode
@@ -76,16 +64,16 @@ struct alignas(16) Phase {
   union {
     PGemm g;
     AttnArgs at;
-    PRowstats rs;
   };
 };
 
 // env_slot: [nenv] active context slot per env (read once per launch).
 // times: optional [nphase + 1] wall-clock stamps taken by block 0 at the start,
 // after each phase's barrier, and at its end (NULL: none).
-hipError_t launch_persistent(const Phase* phases, int nphase, const int* env_slot, int nenv, int mt, int blocks,
+hipError_t launch_persistent(const Phase* phases, int nphase, const int* env_slot, int nenv, int mt, int hd, int blocks,
                              unsigned* bar, int* err, unsigned long long* times, hipStream_t s);
-// Blocks of the persistent kernel that can be co-resident (0 on error).
-int persistent_max_blocks(int mt);
+// Blocks of the persistent kernel (row tiles mt, head dimension hd) that can be
+// co-resident (0 on error).
+int persistent_max_blocks(int mt, int hd);
 
 }  // namespace ravel

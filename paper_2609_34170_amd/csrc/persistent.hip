@@ -13,9 +13,8 @@
 //  * one thread per block performs the device-scope acquire after a barrier
 //    or a split ticket, and every wave drains its stores before arriving.
 //
-// Phases:
-//  * ROWSTATS: per 64-column tile of the residual x, the rows' sums of squares
-//    and p = bf16((1 + scale) * x) for the first adaptive norm;
+// Phases (the input projection, launched before, writes the first norm's
+// operands):
 //  * GEMM: an item is a 64-column tile times a K range of 256 * kw; the four
 //    waves take K quarters and are reduced through LDS; the activation operand
 //    is bf16, or normalised on load as h = r * p + shift with r = 1/rms(x)
@@ -223,64 +222,12 @@ RAVEL_DEV int barrier_wait(unsigned* bar, unsigned gen, int* err) {
 }
 
 // ---------------------------------------------------------------------------
-// ROWSTATS: one 64-column tile, 4 threads per row, 16 columns each
-// ---------------------------------------------------------------------------
-RAVEL_DEV void convert_item(const PRowstats& r, int piece) {
-  // 8192 elements: 256 threads x 32 consecutive (N is a multiple of 64)
-  const size_t total = (size_t)r.cvt_chunks * r.M * r.N;
-  const size_t e0 = ((size_t)piece * 256 + local_tid()) * 32;
-  if (e0 >= total) return;
-  const int n = (int)(e0 % r.N);
-  const size_t mc = e0 / r.N;
-  const int m = (int)(mc % r.M), c = (int)(mc / r.M);
-  const float* src = r.cvt_in + (size_t)m * r.cvt_ld + (size_t)c * r.cvt_stride + n;
-  f32x4_t v[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) v[i] = *gptr((const f32x4_t*)(src + 4 * i));
-  const rsrc_t rd = rsrc(r.cvt_out);
-#pragma unroll
-  for (int i = 0; i < 8; i += 2)
-    st_f4(rd, (e0 + 4 * i) * 2,
-          __builtin_bit_cast(f32x4_t, u32x4_t{pack_bf16x2(v[i][0], v[i][1]), pack_bf16x2(v[i][2], v[i][3]),
-                                              pack_bf16x2(v[i + 1][0], v[i + 1][1]), pack_bf16x2(v[i + 1][2], v[i + 1][3])}));
-}
-
-RAVEL_DEV void rowstats_item(const PRowstats& r, int tile, PSmem& sm) {
-  const int tid = local_tid();
-  const int m = tid >> 2, q = tid & 3;
-  const int n = tile * 64 + q * 16;
-  float s = 0.f;
-  if (m < r.M) {
-    f32x4_t x[4], sc[4];
-    const float* nsp = r.ns_mode == NS_ROW ? r.ns + (size_t)m * r.ldns + n : r.ns + n;
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      x[c] = *gptr((const f32x4_t*)(r.x + (size_t)m * r.ldx + n + 4 * c));
-      sc[c] = *gptr((const f32x4_t*)(nsp + 4 * c));
-    }
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      s += x[c][0] * x[c][0] + x[c][1] * x[c][1] + x[c][2] * x[c][2] + x[c][3] * x[c][3];
-      st_bf16x4(rsrc(r.p), ((size_t)m * r.ldp + n + 4 * c) * 2, (1.f + sc[c][0]) * x[c][0], (1.f + sc[c][1]) * x[c][1],
-                (1.f + sc[c][2]) * x[c][2], (1.f + sc[c][3]) * x[c][3]);
-    }
-  }
-  sm.rowsq[m][q] = s;
-  __syncthreads();
-  if (tid < 64 && tid < r.M) {
-    const float t = (sm.rowsq[tid][0] + sm.rowsq[tid][1]) + (sm.rowsq[tid][2] + sm.rowsq[tid][3]);
-    st_f1(rsrc(r.sumsq_out), (size_t)(tile * 64 + tid) * 4, t);
-  }
-  __syncthreads();
-}
-
-// ---------------------------------------------------------------------------
 // GEMM
 // ---------------------------------------------------------------------------
 // Weight fragments of an item: wave w holds rows n0 + 16c + (lane & 15) and the
 // K range kb + 32f + 8(lane >> 4) .. +7 for its quarter of the item's K range.
 template <int KW>
-RAVEL_DEV void load_w(const PGemm& g, int item, bf16x8_t (&wf)[4][4]) {
+RAVEL_DEV void load_w(const PGemm& g, int item, u32x4_t (&wf)[16]) {
   const int tid = local_tid();
   const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, grp = lane >> 4;
   const int tiles = (g.N + 63) >> 6, tile = item % tiles, z = item / tiles;
@@ -292,23 +239,37 @@ RAVEL_DEV void load_w(const PGemm& g, int item, bf16x8_t (&wf)[4][4]) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const int n = n0 + c * 16 + l16;
-      wf[c][f] = ld_b8<PLAIN>(rw, boff(f < 2 * KW && n < g.N && k < g.K, ((size_t)n * g.ldw + k) * 2));
+      wf[c * 4 + f] = ld16<PLAIN>(rw, boff(f < 2 * KW && n < g.N && k < g.K, ((size_t)n * g.ldw + k) * 2));
     }
   }
 }
 
-RAVEL_DEV void load_weights(const PGemm& g, int item, bf16x8_t (&wf)[4][4]) {
+RAVEL_DEV void load_weights(const PGemm& g, int item, u32x4_t (&wf)[16]) {
   if (g.kw == 2)
     load_w<2>(g, item, wf);
   else
     load_w<1>(g, item, wf);
 }
 
+// Epilogue operands of one slot of a cooperative split-K tile: residual x,
+// gate, next norm scale, bias (loaded at the start of the item, long before the
+// split meets).
+struct CoopOps {
+  f32x4_t ex, eg, es, eb;
+};
 template <int MT>
-RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& sm);
+RAVEL_DEV CoopOps coop_operands(const PGemm& g, int tile, int z, int s0, bool use);
+template <int MT>
+RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& sm, const CoopOps& first);
 
-template <int MT, int KW>
-RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], int* err, PSmem& sm) {
+template <int MT, int KW, class AfterLoads>
+RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int* err, PSmem& sm,
+                         AfterLoads&& after_loads) {
+  bf16x8_t wf[4][4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int f = 0; f < 4; ++f) wf[c][f] = __builtin_bit_cast(bf16x8_t, w16[c * 4 + f]);
   constexpr int NF = 2 * KW;
   const int tid = local_tid(), lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, grp = lane >> 4;
@@ -318,7 +279,9 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], i
   const bool norm = g.a_mode == PA_NORM;
   const bool has_shift = norm && g.shift != nullptr;
 
-  // activations (and, for the norm, shifts and row sums of squares): one batch
+  // one batch of loads: the norm's shift rows (written before the launch: plain
+  // loads) first, then the activations and the row sums of squares written by the
+  // previous phase (coherent loads)
   const rsrc_t rA = rsrc(g.A), rS = rsrc(g.shift);
   bf16x8_t af[MT][NF], sh[MT][NF];
 #pragma unroll
@@ -326,57 +289,87 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], i
 #pragma unroll
     for (int f = 0; f < NF; ++f) {
       const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
-      const bool ok = m < g.M && k < g.K;
-      af[i][f] = ld_b8<COH>(rA, boff(ok, ((size_t)m * g.lda + k) * 2));
-      sh[i][f] = ld_b8<COH>(rS, boff(has_shift && ok, ((size_t)m * g.ld_shift + k) * 2));
+      sh[i][f] = ld_b8<PLAIN>(rS, boff(has_shift && m < g.M && k < g.K, ((size_t)m * g.ld_shift + k) * 2));
     }
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int f = 0; f < NF; ++f) {
+      const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
+      af[i][f] = ld_b8<COH>(rA, boff(m < g.M && k < g.K, ((size_t)m * g.lda + k) * 2));
+    }
+  float sq[16];
+  const int row = tid & 63, part = tid >> 6, nt = g.K >> 6;
   if (norm) {
-    // r[m] from the per-tile row sums: thread (part, row) adds tiles part, part + 4, ...
-    const int row = tid & 63, part = tid >> 6, nt = g.K >> 6;
     const rsrc_t rQ = rsrc(g.sumsq_in);
-    float sq[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const int t = part + 4 * j;
       sq[j] = ld_f1<COH>(rQ, boff(t < nt && row < g.M, (size_t)(t * 64 + row) * 4));
     }
-    float s = 0.f;
-#pragma unroll
-    for (int j = 0; j < 16; ++j) s += sq[j];
-    sm.rowsq[row][part] = s;
-    __syncthreads();
-    if (tid < 64) {
-      const float t = (sm.rowsq[tid][0] + sm.rowsq[tid][1]) + (sm.rowsq[tid][2] + sm.rowsq[tid][3]);
-      sm.rscale[tid] = 1.0f / sqrtf(t / (float)g.K + g.eps);
-    }
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      const float r = sm.rscale[i * 16 + l16];
-#pragma unroll
-      for (int f = 0; f < NF; ++f) {
-        const bf16_t* pv = reinterpret_cast<const bf16_t*>(&af[i][f]);
-        const bf16_t* bv = reinterpret_cast<const bf16_t*>(&sh[i][f]);
-        u32x4_t hb;
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          hb[q] = pack_bf16x2(r * bf16_to_f32(pv[2 * q]) + bf16_to_f32(bv[2 * q]),
-                              r * bf16_to_f32(pv[2 * q + 1]) + bf16_to_f32(bv[2 * q + 1]));
-        af[i][f] = *reinterpret_cast<const bf16x8_t*>(&hb);
-      }
-    }
   }
+  // a cooperative split tile's epilogue operands of this block's first slots
+  const CoopOps ops = coop_operands<MT>(g, tile, z, 0, g.ksplit > 1 && g.coop);
+  after_loads();
 
+  // The norm's operand is h = r p + shift (r = 1 / rms(x) per row), so
+  // W h = r (W p + W shift / r): the shift product runs while p is in flight,
+  // and no bf16 h is formed.  Lane (l16, grp) of fragment (c, i) holds row
+  // i*16 + l16, columns n0 + 16c + 4grp .. +3.
   f32x4_t acc[4][MT];
 #pragma unroll
   for (int c = 0; c < 4; ++c)
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
       acc[c][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      if (has_shift) {
+#pragma unroll
+        for (int f = 0; f < NF; ++f)
+          acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[c][f], sh[i][f], acc[c][i], 0, 0, 0);
+      }
+    }
+  if (norm) {
+    // r[m] from the per-tile row sums: thread (part, row) adds tiles part, part + 4, ...
+    float ssum = 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) ssum += sq[j];
+    sm.rowsq[row][part] = ssum;
+    __syncthreads();
+    if (tid < 64) {
+      const float t = (sm.rowsq[tid][0] + sm.rowsq[tid][1]) + (sm.rowsq[tid][2] + sm.rowsq[tid][3]);
+      const float ms = t / (float)g.K + g.eps;
+      sm.rscale[tid] = 1.0f / sqrtf(ms);
+      sm.rowsq[tid][16] = sqrtf(ms);
+    }
+    __syncthreads();
+    if (has_shift) {
+#pragma unroll
+      for (int i = 0; i < MT; ++i) {
+        const float rms = sm.rowsq[i * 16 + l16][16];
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) acc[c][i][q] *= rms;
+      }
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
       for (int f = 0; f < NF; ++f)
         acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[c][f], af[i][f], acc[c][i], 0, 0, 0);
+  if (norm) {
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const float r = sm.rscale[i * 16 + l16];
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[c][i][q] *= r;
     }
+  }
   // reduce the four K quarters through LDS.  Item it = tid + 256 q (q < MT) is
   // fragment fr = it >> 6 (= c * MT + i), lane ln = it & 63: row i*16 + (ln & 15),
   // columns n0 + 16c + 4(ln >> 4) .. +3.
@@ -427,7 +420,7 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], i
         st_f4(rPw, (((size_t)z * tiles + tile) * tile_elems + (size_t)(tid + q * 256) * 4) * 4, sum[q]);
     if (g.coop) {
       unsigned* ctr = &g.counters[tile * kCounterStride];
-      if (group_meet(ctr, (unsigned)g.ksplit, err, &sm.flag)) coop_epilogue<MT>(g, tile, z, tiles, sm);
+      if (group_meet(ctr, (unsigned)g.ksplit, err, &sm.flag)) coop_epilogue<MT>(g, tile, z, tiles, sm, ops);
       group_leave(ctr, (unsigned)g.ksplit);
       __syncthreads();
       return;
@@ -539,8 +532,53 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const bf16x8_t (&wf)[4][4], i
 // [z*rp, min(M, (z+1)*rp)), rp = ceil(M / ksplit), adds the partials of each of its
 // (row, 4-column) slots in split order and applies the epilogue; the new rows' sums
 // of squares of a residual update are added in fixed column order.
+// Slot s of the block's share: row r0 + s / per_row, 4-column group and 16-column
+// block (GEGLU: block pair) from s % per_row.
+struct CoopSlot {
+  int row, grp, cb, c, n, it, it_up;
+  bool valid, ok;
+};
 template <int MT>
-RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& sm) {
+RAVEL_DEV CoopSlot coop_slot(const PGemm& g, int tile, int z, int slot) {
+  const int rp = (g.M + g.ksplit - 1) / g.ksplit;
+  const int r0 = z * rp, r1 = min(g.M, r0 + rp);
+  const bool geglu = g.e_mode == PE_GEGLU;
+  const int per_row = geglu ? 8 : 16;
+  const int nslots = max(r1 - r0, 0) * per_row;
+  CoopSlot q;
+  q.valid = slot < nslots;
+  q.row = r0 + (q.valid ? slot / per_row : 0);
+  const int rem = slot % per_row;
+  q.grp = rem & 3;
+  q.cb = rem >> 2;
+  q.c = geglu ? 2 * q.cb : q.cb;
+  q.n = tile * 64 + q.c * 16 + q.grp * 4;
+  q.it = (q.c * MT + (q.row >> 4)) * 64 + q.grp * 16 + (q.row & 15);
+  q.it_up = ((q.c + 1) * MT + (q.row >> 4)) * 64 + q.grp * 16 + (q.row & 15);
+  q.ok = q.valid && q.n + 4 <= g.N;
+  return q;
+}
+
+template <int MT>
+RAVEL_DEV CoopOps coop_operands(const PGemm& g, int tile, int z, int s0, bool use) {
+  CoopSlot q = coop_slot<MT>(g, tile, z, s0 + local_tid());
+  q.ok = q.ok && use;
+  const bool geglu = g.e_mode == PE_GEGLU, resid = g.e_mode == PE_RESID;
+  const rsrc_t rX = rsrc(g.out_f), rG = rsrc(g.gate), rN = rsrc(g.ns), rB = rsrc(g.bias);
+  CoopOps o;
+  o.ex = ld_f4<COH>(rX, boff(resid && q.ok, ((size_t)q.row * g.ldof + q.n) * 4));
+  o.eg = ld_f4<PLAIN>(rG, boff(resid && q.ok && g.gate, ((size_t)q.row * g.ldg + q.n) * 4));
+  o.es = ld_f4<PLAIN>(rN, boff(resid && q.ok, (g.ns_mode == NS_ROW ? (size_t)q.row * g.ldns + q.n : (size_t)q.n) * 4));
+  o.eb = ld_f4<PLAIN>(rB, boff(!resid && !geglu && q.ok && g.bias, (size_t)q.n * 4));
+  return o;
+}
+
+// A split-K tile finished by its ksplit blocks together: block z takes rows
+// [z*rp, min(M, (z+1)*rp)), rp = ceil(M / ksplit), adds the partials of each of its
+// (row, 4-column) slots in split order and applies the epilogue; the new rows' sums
+// of squares of a residual update are added in fixed column order.
+template <int MT>
+RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& sm, const CoopOps& first) {
   const int tid = local_tid();
   const int n0 = tile * 64;
   const int rp = (g.M + g.ksplit - 1) / g.ksplit;
@@ -549,25 +587,15 @@ RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& 
   const bool geglu = g.e_mode == PE_GEGLU, resid = g.e_mode == PE_RESID;
   const int per_row = geglu ? 8 : 16;
   const int nslots = max(r1 - r0, 0) * per_row;
-  const rsrc_t rP = rsrc(g.partial), rX = rsrc(g.out_f), rG = rsrc(g.gate), rN = rsrc(g.ns), rB = rsrc(g.bias);
+  const rsrc_t rP = rsrc(g.partial);
   float gsc = 1.f;
   if (resid && !g.gate) gsc = tanhf(*gptr(g.gate_scalar));
   for (int s0 = 0; s0 < nslots; s0 += 256) {
-    const int slot = s0 + tid;
-    const bool valid = slot < nslots;
-    const int row = r0 + (valid ? slot / per_row : 0), rem = slot % per_row;
-    const int grp = rem & 3, cb = rem >> 2;  // 4-column group, 16-column block (GEGLU: block pair)
-    const int c = geglu ? 2 * cb : cb;
-    const int n = n0 + c * 16 + grp * 4;
-    const int it = (c * MT + (row >> 4)) * 64 + grp * 16 + (row & 15);
-    const int it_up = ((c + 1) * MT + (row >> 4)) * 64 + grp * 16 + (row & 15);
-    const bool ok = valid && n + 4 <= g.N;
-    // epilogue operands and partials: one batch
-    const f32x4_t ex = ld_f4<COH>(rX, boff(resid && ok, ((size_t)row * g.ldof + n) * 4));
-    const f32x4_t eg = ld_f4<PLAIN>(rG, boff(resid && ok && g.gate, ((size_t)row * g.ldg + n) * 4));
-    const f32x4_t es =
-        ld_f4<PLAIN>(rN, boff(resid && ok, (g.ns_mode == NS_ROW ? (size_t)row * g.ldns + n : (size_t)n) * 4));
-    const f32x4_t eb = ld_f4<PLAIN>(rB, boff(!resid && !geglu && ok && g.bias, (size_t)n * 4));
+    const CoopSlot q = coop_slot<MT>(g, tile, z, s0 + tid);
+    const bool valid = q.valid;
+    const int row = q.row, grp = q.grp, cb = q.cb, c = q.c, n = q.n, it = q.it, it_up = q.it_up;
+    const CoopOps o = s0 == 0 ? first : coop_operands<MT>(g, tile, z, s0, true);
+    const f32x4_t ex = o.ex, eg = o.eg, es = o.es, eb = o.eb;
     f32x4_t pv[kMaxKSplit], pu[kMaxKSplit];
 #pragma unroll
     for (int zz = 0; zz < kMaxKSplit; ++zz) {
@@ -631,61 +659,144 @@ RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& 
 // ---------------------------------------------------------------------------
 // attention: one (env, head, key split)
 // ---------------------------------------------------------------------------
+// Where the keys of item's split start and end, and whether they are prefix keys.
+struct SplitKeys {
+  int e, j, g, split, kbeg, kend;
+  bool self;
+};
+RAVEL_DEV SplitKeys split_keys(const AttnArgs& a, int item) {
+  SplitKeys k;
+  k.split = item % a.nsplit;
+  k.j = (item / a.nsplit) % a.nq;
+  k.e = item / (a.nsplit * a.nq);
+  k.g = (k.j * a.nkv) / a.nq;
+  // the first ceil(P / kps) splits cover the prefix, the rest the self keys
+  const int nsp = (a.P + a.keys_per_split - 1) / a.keys_per_split;
+  k.self = k.split >= nsp;
+  k.kbeg = k.self ? a.P + (k.split - nsp) * a.keys_per_split : k.split * a.keys_per_split;
+  k.kend = k.self ? min(a.P + a.S, k.kbeg + a.keys_per_split) : min(a.P, k.kbeg + a.keys_per_split);
+  return k;
+}
+
+// The split's keys and values into registers: kv[0..3] are 16-byte K chunks
+// (chunk c = tid + 256 r: key c / (HD/8), dims (c % (HD/8)) * 8), kv[4..7] the V
+// chunks of keys 4 (tid / (HD/8)) + i, i < 4, at dims (tid % (HD/8)) * 8.  Prefix
+// rows were written before the launch (plain loads, and may be fetched before the
+// barrier that opens the phase); self rows by this launch (coherent loads).
 template <int HD>
-RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err, PSmem& sm) {
+RAVEL_DEV void attn_load_kv(const AttnArgs& a, const SplitKeys& k, const int* slots, u32x4_t (&kv)[8]) {
+  constexpr int CPR = HD / 8;
+  const int tid = local_tid();
+  const int slot = a.slot ? slots[k.e] : 0;
+  const bf16_t* pk = (const bf16_t*)a.pk + slot * a.p_slot_stride + k.e * a.p_env_stride;
+  const bf16_t* pv = (const bf16_t*)a.pv + slot * a.p_slot_stride + k.e * a.p_env_stride;
+  const rsrc_t rK = k.self ? rsrc((const bf16_t*)a.sk + (size_t)k.e * a.S * a.s_ld) : rsrc(pk);
+  const rsrc_t rV = k.self ? rsrc((const bf16_t*)a.sv + (size_t)k.e * a.S * a.s_ld) : rsrc(pv);
+  const int ld_row = k.self ? a.s_ld : a.p_ld;
+  const int k_row0 = k.self ? a.P : 0;
+  auto off = [&](int kidx, int dc) {
+    return boff(kidx < k.kend, ((size_t)(kidx - k_row0) * ld_row + k.g * HD + dc) * 2);
+  };
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int c = tid + r * 256;
+    const int o = off(k.kbeg + c / CPR, (c % CPR) * 8);
+    kv[r] = k.self ? ld16<COH>(rK, o) : ld16<PLAIN>(rK, o);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int o = off(k.kbeg + (tid / CPR) * 4 + i, (tid % CPR) * 8);
+    kv[4 + i] = k.self ? ld16<COH>(rV, o) : ld16<PLAIN>(rV, o);
+  }
+}
+
+// Weighted sum of the splits' partial outputs for output elements [el0, el1) of
+// one (env, head) (element = 4 dims of one query), bf16 to a.out.  The weight of
+// split s for query q is exp2(m_s - m) / sum_s' exp2(m_s' - m) l_s' (fixed order).
+template <int HD>
+RAVEL_DEV void attn_merge(const AttnArgs& a, int e, int j, int el0, int el1, PSmem& sm) {
+  const int tid = local_tid();
+  const int Hp = ((a.Hq + 15) / 16) * 16;
+  const size_t pbase = ((size_t)e * a.nq + j) * a.nsplit;
+  const rsrc_t rML = rsrc(a.part_ml), rO = rsrc(a.part_o);
+  // (max, sum) of every split and query: kMaxAttnSplit x 64 pairs, 8 per thread
+  float2 mlv[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    const int t = tid + r * 256, sp = t >> 6, qq = t & 63;
+    mlv[r] = ld_f2<COH>(rML, boff(sp < a.nsplit && qq < a.Hq, ((pbase + sp) * Hp + qq) * 2 * 4));
+  }
+  // each thread sums one element over the splits, 16 splits per batch of loads
+  constexpr int SB = 16;
+  f32x4_t pvl[SB];
+  auto load_parts = [&](int el, int sp0) {
+    const int qq = el / (HD / 4), d = (el % (HD / 4)) * 4;
+#pragma unroll
+    for (int i = 0; i < SB; ++i)
+      pvl[i] = ld_f4<COH>(rO, boff(el < el1 && sp0 + i < a.nsplit, (((pbase + sp0 + i) * Hp + qq) * HD + d) * 4));
+  };
+  load_parts(el0 + tid, 0);  // in flight with the (max, sum) loads
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    const int t = tid + r * 256, sp = t >> 6, qq = t & 63;
+    sm.mg.ml[sp][qq][0] = (sp < a.nsplit && qq < a.Hq) ? mlv[r].x : -INFINITY;
+    sm.mg.ml[sp][qq][1] = mlv[r].y;
+  }
+  __syncthreads();
+  if (tid < a.Hq) {
+    float mmax = -INFINITY;
+    for (int sp = 0; sp < a.nsplit; ++sp) mmax = fmaxf(mmax, sm.mg.ml[sp][tid][0]);
+    float den = 0.f;
+    for (int sp = 0; sp < a.nsplit; ++sp) {
+      const float ms = sm.mg.ml[sp][tid][0];
+      const float wv = (ms == -INFINITY) ? 0.f : exp2f(ms - mmax);
+      sm.mg.wgt[sp][tid] = wv;
+      den += wv * sm.mg.ml[sp][tid][1];
+    }
+    const float inv = 1.f / den;
+    for (int sp = 0; sp < a.nsplit; ++sp) sm.mg.wgt[sp][tid] *= inv;
+  }
+  __syncthreads();
+  for (int b0 = el0; b0 < el1; b0 += 256) {
+    const int el = b0 + tid;
+    const int qq = el < el1 ? el / (HD / 4) : 0, d = (el % (HD / 4)) * 4;
+    f32x4_t num = {0.f, 0.f, 0.f, 0.f};
+    for (int sp0 = 0; sp0 < a.nsplit; sp0 += SB) {
+      if (b0 != el0 || sp0 != 0) load_parts(el, sp0);
+#pragma unroll
+      for (int i = 0; i < SB; ++i) {
+        if (sp0 + i >= a.nsplit) break;
+        const float wv = sm.mg.wgt[sp0 + i][qq];
+        num[0] += wv * pvl[i][0];
+        num[1] += wv * pvl[i][1];
+        num[2] += wv * pvl[i][2];
+        num[3] += wv * pvl[i][3];
+      }
+    }
+    if (el < el1)
+      st_bf16x4(rsrc(a.out), ((size_t)(e * a.Hq + qq) * a.ldo + j * HD + d) * 2, num[0], num[1], num[2], num[3]);
+  }
+}
+
+// One split: its keys and values (kv, fetched ahead when `have_kv`) are staged in
+// LDS, the four waves take 16 queries each, S^T = K Q^T with the split's softmax,
+// O^T = V^T P^T; a single split writes the output, otherwise the splits' partial
+// outputs and (max, sum) are merged by the head's splits together (coop) or by the
+// last split to arrive.
+template <int HD, class AfterLoads>
+RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err, PSmem& sm, u32x4_t (&kv)[8],
+                         bool have_kv, AfterLoads&& after_loads) {
   using C = AttnCfg<HD>;
   constexpr int KPS = C::KPS, KLD = C::KLD, VLD = C::VLD;
   constexpr int KS = HD / 32, DT = HD / 16, CPR = HD / 8;
-  constexpr int KCH = KPS * CPR / 256;        // 16-byte K chunks per thread
-  constexpr int VCH = (KPS / 4) * CPR / 256;  // (4 keys x 8 dims) V groups per thread
-  static_assert(KCH >= 1 && VCH >= 1 && KPS * CPR % 256 == 0 && (KPS / 4) * CPR % 256 == 0, "attention tiling");
   bf16_t* Ks = sm.at;
   bf16_t* Vt = sm.at + KPS * KLD;
   const int tid = local_tid(), lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, grp = lane >> 4;
-  const int split = item % a.nsplit;
-  const int j = (item / a.nsplit) % a.nq;
-  const int e = item / (a.nsplit * a.nq);
-  const int g = (j * a.nkv) / a.nq;
+  const SplitKeys k = split_keys(a, item);
+  const int e = k.e, j = k.j, split = k.split;
   const int QB = (a.Hq + 15) / 16;
-  // the first ceil(P / kps) splits cover the prefix, the rest the self keys
-  const int nsp = (a.P + a.keys_per_split - 1) / a.keys_per_split;
-  const bool self_split = split >= nsp;
-  const int kbeg = self_split ? a.P + (split - nsp) * a.keys_per_split : split * a.keys_per_split;
-  const int kend = self_split ? min(a.P + a.S, kbeg + a.keys_per_split) : min(a.P, kbeg + a.keys_per_split);
-  const int slot = a.slot ? slots[e] : 0;
-  const bf16_t* pk = (const bf16_t*)a.pk + slot * a.p_slot_stride + e * a.p_env_stride;
-  const bf16_t* pv = (const bf16_t*)a.pv + slot * a.p_slot_stride + e * a.p_env_stride;
-  const bf16_t* sk = (const bf16_t*)a.sk;
-  const bf16_t* sv = (const bf16_t*)a.sv;
-  // prefix rows were written before the launch (plain loads), self rows by this
-  // launch's QKV phase (coherent loads); a split holds only one kind
-  const rsrc_t rK = self_split ? rsrc(sk + (size_t)e * a.S * a.s_ld) : rsrc(pk);
-  const rsrc_t rV = self_split ? rsrc(sv + (size_t)e * a.S * a.s_ld) : rsrc(pv);
-  const int ld_row = self_split ? a.s_ld : a.p_ld;
-  const int k_row0 = self_split ? a.P : 0;
-  auto row16 = [&](rsrc_t r, int kidx, int dc) -> u32x4_t {
-    const int off = boff(kidx < kend, ((size_t)(kidx - k_row0) * ld_row + g * HD + dc) * 2);
-    return self_split ? ld16<COH>(r, off) : ld16<PLAIN>(r, off);
-  };
-  // keys, values and queries of the split: one batch
-  u32x4_t kr[KCH];
-#pragma unroll
-  for (int r = 0; r < KCH; ++r) {
-    const int c = tid + r * 256, row = c / CPR, dc = (c % CPR) * 8;
-    const int kidx = kbeg + row;
-    kr[r] = row16(rK, kidx, dc);
-  }
-  u32x4_t vr[VCH][4];
-#pragma unroll
-  for (int r = 0; r < VCH; ++r) {
-    const int c = tid + r * 256, kq = c / CPR, dc = (c % CPR) * 8;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int kidx = kbeg + kq * 4 + i;
-      vr[r][i] = row16(rV, kidx, dc);
-    }
-  }
+  if (!have_kv) attn_load_kv<HD>(a, k, slots, kv);
   const rsrc_t rq = rsrc(a.q);
   const int query = wave * 16 + l16;
   const bool active = wave < QB;
@@ -693,19 +804,19 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks)
     qf[ks] = ld_b8<COH>(rq, boff(query < a.Hq, ((size_t)(e * a.Hq + query) * a.ldq + j * HD + ks * 32 + grp * 8) * 2));
+  after_loads();
   __syncthreads();  // LDS may still be read by this block's previous item
 #pragma unroll
-  for (int r = 0; r < KCH; ++r) {
-    const int c = tid + r * 256, row = c / CPR, dc = (c % CPR) * 8;
-    *(u32x4_t*)&Ks[row * KLD + dc] = kr[r];
+  for (int r = 0; r < 4; ++r) {
+    const int c = tid + r * 256;
+    *(u32x4_t*)&Ks[(c / CPR) * KLD + (c % CPR) * 8] = kv[r];
   }
-#pragma unroll
-  for (int r = 0; r < VCH; ++r) {
-    const int c = tid + r * 256, kq = c / CPR, dc = (c % CPR) * 8;
-    const bf16_t* h0 = (const bf16_t*)&vr[r][0];
-    const bf16_t* h1 = (const bf16_t*)&vr[r][1];
-    const bf16_t* h2 = (const bf16_t*)&vr[r][2];
-    const bf16_t* h3 = (const bf16_t*)&vr[r][3];
+  {
+    const int kq = tid / CPR, dc = (tid % CPR) * 8;
+    const bf16_t* h0 = (const bf16_t*)&kv[4];
+    const bf16_t* h1 = (const bf16_t*)&kv[5];
+    const bf16_t* h2 = (const bf16_t*)&kv[6];
+    const bf16_t* h3 = (const bf16_t*)&kv[7];
 #pragma unroll
     for (int dd = 0; dd < 8; ++dd) {
       u32x2_t w;
@@ -721,7 +832,7 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
   // 4grp..+3) as 2 x NT independent MFMA chains, then one softmax over the split
   // and O^T = V^T P^T with no running rescale.
   constexpr int NT = KPS / 32;
-  const int nk = kend - kbeg;
+  const int nk = k.kend - k.kbeg;
   const int ntile = (nk + 31) / 32;
   f32x4_t o[DT];
   float mrow = -INFINITY, lrow = 0.f;
@@ -814,150 +925,20 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
       st_f1(rPml, (((pbase + split) * Hp + query) * 2 + 1) * 4, lrow);
     }
   }
+  const int total = a.Hq * (HD / 4);
+  unsigned* ctr = &a.counters[(e * a.nq + j) * kCounterStride];
   if (a.coop) {
     // the splits of this (env, head) meet; each merges a share of the output
-    unsigned* ctr = &a.counters[(e * a.nq + j) * kCounterStride];
     if (group_meet(ctr, (unsigned)a.nsplit, err, &sm.flag)) {
-      const int total = a.Hq * (HD / 4);
       const int share = (total + a.nsplit - 1) / a.nsplit;
       const int el0 = split * share, el1 = min(total, el0 + share);
-      const rsrc_t rML = rsrc(a.part_ml), rO = rsrc(a.part_o);
-      float2 mlv[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int t = tid + r * 256, sp = t >> 6, qq = t & 63;
-        mlv[r] = ld_f2<COH>(rML, boff(sp < a.nsplit && qq < a.Hq, ((pbase + sp) * Hp + qq) * 2 * 4));
-      }
-      for (int b0 = el0; b0 < el1; b0 += 512) {
-        f32x4_t pvl[2][8];
-#pragma unroll
-        for (int r = 0; r < 2; ++r) {
-          const int el = b0 + r * 256 + tid;
-          const int qq = el / (HD / 4), d = (el % (HD / 4)) * 4;
-#pragma unroll
-          for (int s8 = 0; s8 < 8; ++s8)
-            pvl[r][s8] = ld_f4<COH>(rO, boff(el < el1 && s8 < a.nsplit, (((pbase + s8) * Hp + qq) * HD + d) * 4));
-        }
-        if (b0 == el0) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int t = tid + r * 256, sp = t >> 6, qq = t & 63;
-            sm.mg.ml[sp][qq][0] = (sp < a.nsplit && qq < a.Hq) ? mlv[r].x : -INFINITY;
-            sm.mg.ml[sp][qq][1] = mlv[r].y;
-          }
-          __syncthreads();
-          if (tid < a.Hq) {
-            float mmax = -INFINITY;
-            for (int sp = 0; sp < a.nsplit; ++sp) mmax = fmaxf(mmax, sm.mg.ml[sp][tid][0]);
-            float den = 0.f;
-            for (int sp = 0; sp < a.nsplit; ++sp) {
-              const float ms = sm.mg.ml[sp][tid][0];
-              const float wv = (ms == -INFINITY) ? 0.f : exp2f(ms - mmax);
-              sm.mg.wgt[sp][tid] = wv;
-              den += wv * sm.mg.ml[sp][tid][1];
-            }
-            const float inv = 1.f / den;
-            for (int sp = 0; sp < a.nsplit; ++sp) sm.mg.wgt[sp][tid] *= inv;
-          }
-          __syncthreads();
-        }
-#pragma unroll
-        for (int r = 0; r < 2; ++r) {
-          const int el = b0 + r * 256 + tid;
-          if (el >= el1) continue;
-          const int qq = el / (HD / 4), d = (el % (HD / 4)) * 4;
-          f32x4_t num = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int s8 = 0; s8 < 8; ++s8) {
-            if (s8 >= a.nsplit) break;
-            const float wv = sm.mg.wgt[s8][qq];
-            num[0] += wv * pvl[r][s8][0];
-            num[1] += wv * pvl[r][s8][1];
-            num[2] += wv * pvl[r][s8][2];
-            num[3] += wv * pvl[r][s8][3];
-          }
-          st_bf16x4(rsrc(out), ((size_t)(e * a.Hq + qq) * a.ldo + j * HD + d) * 2, num[0], num[1], num[2], num[3]);
-        }
-      }
+      attn_merge<HD>(a, e, j, el0, el1, sm);
     }
     group_leave(ctr, (unsigned)a.nsplit);
     __syncthreads();
     return;
   }
-  if (!last_arrival(&a.counters[(e * a.nq + j) * kCounterStride], (unsigned)a.nsplit, &sm.flag)) {
-    __syncthreads();
-    return;
-  }
-  // merge: (max, sum) of every split and query, then weights, then outputs
-  {
-    float2 mlv[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int t = tid + r * 256, sp = t >> 6, qq = t & 63;
-      mlv[r] = ld_f2<COH>(rsrc(a.part_ml), boff(sp < a.nsplit && qq < a.Hq, ((pbase + sp) * Hp + qq) * 2 * 4));
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int t = tid + r * 256, sp = t >> 6, qq = t & 63;
-      sm.mg.ml[sp][qq][0] = (sp < a.nsplit && qq < a.Hq) ? mlv[r].x : -INFINITY;
-      sm.mg.ml[sp][qq][1] = mlv[r].y;
-    }
-  }
-  __syncthreads();
-  if (tid < a.Hq) {
-    float mmax = -INFINITY;
-    for (int sp = 0; sp < a.nsplit; ++sp) mmax = fmaxf(mmax, sm.mg.ml[sp][tid][0]);
-    float den = 0.f;
-    for (int sp = 0; sp < a.nsplit; ++sp) {
-      const float ms = sm.mg.ml[sp][tid][0];
-      const float wv = (ms == -INFINITY) ? 0.f : exp2f(ms - mmax);
-      sm.mg.wgt[sp][tid] = wv;
-      den += wv * sm.mg.ml[sp][tid][1];
-    }
-    const float inv = 1.f / den;
-    for (int sp = 0; sp < a.nsplit; ++sp) sm.mg.wgt[sp][tid] *= inv;
-  }
-  __syncthreads();
-  const int total = a.Hq * (HD / 4);
-  for (int base = 0; base < total; base += 4 * 256) {
-    f32x4_t num[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) num[r] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int sp0 = 0; sp0 < a.nsplit; sp0 += 8) {
-      f32x4_t pvl[4][8];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int el = base + r * 256 + tid;
-        const int qq = el / (HD / 4), d = (el % (HD / 4)) * 4;
-#pragma unroll
-        for (int s8 = 0; s8 < 8; ++s8)
-          pvl[r][s8] = ld_f4<COH>(rsrc(a.part_o),
-                                  boff(el < total && sp0 + s8 < a.nsplit, (((pbase + sp0 + s8) * Hp + qq) * HD + d) * 4));
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int el = base + r * 256 + tid;
-        const int qq = el < total ? el / (HD / 4) : 0;
-#pragma unroll
-        for (int s8 = 0; s8 < 8; ++s8) {
-          if (sp0 + s8 >= a.nsplit) break;
-          const float wv = sm.mg.wgt[sp0 + s8][qq];
-          num[r][0] += wv * pvl[r][s8][0];
-          num[r][1] += wv * pvl[r][s8][1];
-          num[r][2] += wv * pvl[r][s8][2];
-          num[r][3] += wv * pvl[r][s8][3];
-        }
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int el = base + r * 256 + tid;
-      if (el >= total) continue;
-      const int qq = el / (HD / 4), d = (el % (HD / 4)) * 4;
-      st_bf16x4(rsrc(out), ((size_t)(e * a.Hq + qq) * a.ldo + j * HD + d) * 2, num[r][0], num[r][1], num[r][2],
-                num[r][3]);
-    }
-  }
+  if (last_arrival(ctr, (unsigned)a.nsplit, &sm.flag)) attn_merge<HD>(a, e, j, 0, total, sm);
   __syncthreads();
 }
 
@@ -967,7 +948,7 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
 constexpr int kDescChunks = (int)(sizeof(Phase) / 16);
 static_assert(sizeof(Phase) % 16 == 0 && kDescChunks <= 256, "phase descriptor size");
 
-template <int MT>
+template <int MT, int HD>
 __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __restrict__ phases, int nphase,
                                                               const int* __restrict__ env_slot, int nenv,
                                                               unsigned* bar, int* err, unsigned long long* times) {
@@ -984,19 +965,33 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
   if (env_slot && tid < nenv && tid < 64) slots[tid] = *gptr(env_slot + tid);
   __syncthreads();
 
-  // weights of this block's first item of the coming GEMM phase (zero otherwise)
-  bf16x8_t wreg[4][4];
+  // What this block's first item of the coming phase reads from memory written
+  // before the launch -- GEMM weight fragments (16), or the keys and values (8) of
+  // a prefix attention split (kv_ready) -- is fetched while the block waits at the
+  // barrier that opens the phase.  (Issued any earlier, these loads would sit in
+  // front of the current phase's own loads and stores in the wave's in-order
+  // memory counter, and every wait of the phase would wait for them too.)
+  u32x4_t pre[16];
+  bool kv_ready = false;
   auto prefetch = [&](const Phase& nx) {
-    if (uni(nx.type) == PH_GEMM && (int)blockIdx.x < uni(nx.items)) {
-      load_weights(make_uniform(nx.g), blockIdx.x, wreg);
-    } else {
+    kv_ready = false;
+    const int type = uni(nx.type);
+    if (type == PH_GEMM && (int)blockIdx.x < uni(nx.items)) {
+      load_weights(make_uniform(nx.g), blockIdx.x, pre);
+    } else if (type == PH_ATTN && (int)blockIdx.x < uni(nx.items)) {
+      const AttnArgs a = make_uniform(nx.at);
+      const SplitKeys k = split_keys(a, blockIdx.x);
+      if (!k.self) {
+        u32x4_t kv[8];
+        attn_load_kv<HD>(a, k, slots, kv);
 #pragma unroll
-      for (int c = 0; c < 4; ++c)
-#pragma unroll
-        for (int f = 0; f < 4; ++f) wreg[c][f] = bf16x8_t{};
+        for (int i = 0; i < 8; ++i) pre[i] = kv[i];
+        kv_ready = true;
+      }
     }
   };
   prefetch(desc[0]);
+  auto none = [] {};
 
   for (int p = 0; p < nphase; ++p) {
     const Phase& ph = desc[p % 3];
@@ -1004,35 +999,24 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
     if (type == PH_GEMM) {
       const PGemm g = make_uniform(ph.g);
       for (int item = blockIdx.x; item < items; item += gridDim.x) {
-        if (item != (int)blockIdx.x) load_weights(g, item, wreg);
+        if (item != (int)blockIdx.x) load_weights(g, item, pre);
         if (g.kw == 2)
-          gemm_item<MT, 2>(g, item, wreg, err, sm);
+          gemm_item<MT, 2>(g, item, pre, err, sm, none);
         else
-          gemm_item<MT, 1>(g, item, wreg, err, sm);
+          gemm_item<MT, 1>(g, item, pre, err, sm, none);
       }
     } else if (type == PH_ATTN) {
       const AttnArgs a = make_uniform(ph.at);
       for (int item = blockIdx.x; item < items; item += gridDim.x) {
-        switch (a.hd) {
-          case 32: attn_item<32>(a, item, slots, err, sm); break;
-          case 64: attn_item<64>(a, item, slots, err, sm); break;
-          case 128: attn_item<128>(a, item, slots, err, sm); break;
-          default: attn_item<256>(a, item, slots, err, sm); break;
-        }
-      }
-    } else if (type == PH_ROWSTATS) {
-      const PRowstats r = make_uniform(ph.rs);
-      const int ntile = r.N >> 6;
-      for (int item = blockIdx.x; item < items; item += gridDim.x) {
-        if (item < ntile)
-          rowstats_item(r, item, sm);
-        else
-          convert_item(r, item - ntile);
+        u32x4_t kv[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) kv[i] = pre[i];
+        attn_item<HD>(a, item, slots, err, sm, kv, item == (int)blockIdx.x && kv_ready, none);
       }
     }
     if (p + 1 == nphase) break;
     // barrier between phases p and p + 1; while waiting, fetch descriptor p + 2
-    // and this block's weights of phase p + 1
+    // and what this block's item of phase p + 1 reads from before the launch
     wait_memory();
     __syncthreads();
     const unsigned gen = (unsigned)(p + 1);
@@ -1062,28 +1046,39 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
   }
 }
 
-const void* kernel_for(int mt) {
+template <int MT>
+const void* kernel_for_hd(int hd) {
+  switch (hd) {
+    case 32: return (const void*)persistent_step_kernel<MT, 32>;
+    case 64: return (const void*)persistent_step_kernel<MT, 64>;
+    case 128: return (const void*)persistent_step_kernel<MT, 128>;
+    case 256: return (const void*)persistent_step_kernel<MT, 256>;
+    default: return nullptr;
+  }
+}
+
+const void* kernel_for(int mt, int hd) {
   switch (mt) {
-    case 1: return (const void*)persistent_step_kernel<1>;
-    case 2: return (const void*)persistent_step_kernel<2>;
-    case 4: return (const void*)persistent_step_kernel<4>;
+    case 1: return kernel_for_hd<1>(hd);
+    case 2: return kernel_for_hd<2>(hd);
+    case 4: return kernel_for_hd<4>(hd);
     default: return nullptr;
   }
 }
 
 }  // namespace
 
-hipError_t launch_persistent(const Phase* phases, int nphase, const int* env_slot, int nenv, int mt, int blocks,
+hipError_t launch_persistent(const Phase* phases, int nphase, const int* env_slot, int nenv, int mt, int hd, int blocks,
                              unsigned* bar, int* err, unsigned long long* times, hipStream_t s) {
-  const void* fn = kernel_for(mt);
+  const void* fn = kernel_for(mt, hd);
   if (!fn || nenv > 64 || nphase < 1) return hipErrorInvalidValue;
   void* args[] = {(void*)&phases, (void*)&nphase, (void*)&env_slot, (void*)&nenv,
                   (void*)&bar,    (void*)&err,    (void*)&times};
   return hipLaunchCooperativeKernel(fn, dim3(blocks), dim3(256), args, 0, s);
 }
 
-int persistent_max_blocks(int mt) {
-  const void* fn = kernel_for(mt);
+int persistent_max_blocks(int mt, int hd) {
+  const void* fn = kernel_for(mt, hd);
   if (!fn) return 0;
   int per_cu = 0, dev = 0, cus = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 256, 0) != hipSuccess) return 0;

@@ -105,6 +105,7 @@ struct ravel_model {
   size_t arena_bytes = 0;
   int64_t weight_bytes = 0;
   float *in_w = nullptr, *in_b = nullptr;
+  float* in_wT = nullptr;  // [D, w]: in_w transposed (input projection reads it)
   float* ctau = nullptr;  // [H, w]
   float *d_w1 = nullptr, *d_b1 = nullptr, *d_b2 = nullptr;
   void* d_w2 = nullptr;
@@ -311,6 +312,8 @@ struct ravel_buffer {
   float* x = nullptr;
   void* cond = nullptr;
   void* h1 = nullptr;
+  float* dvec = nullptr;  // [B, w] offset embedding d = W_d2 h1 + b_d2
+  bf16_t* pshift = nullptr;  // persistent step: bf16 copies of the norm shifts
   float* mod = nullptr;
   void* y = nullptr;
   void* qkv = nullptr;
@@ -504,18 +507,18 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
     REC_END();
   }
   {
-    GemmArgs e = epi_args(EPI_COND);
+    GemmArgs e = epi_args(EPI_F32);
     e.bias = m->d_b2;
-    e.out_t = b->cond;
-    e.ldo_t = w;
-    e.ctau = m->ctau;
-    e.H = H;
-    e.cond_grp = b->cgroups ? b->cgrp : nullptr;
+    e.out_f = b->dvec;
+    e.ldo_f = w;
     RV_TRY(run_gemm<T>(b, s, rec, "cond", b->h1, w, m->d_w2, w, B, w, w, e));
   }
+  REC_BEGIN("cond_expand", (double)B * w * 4 + (double)H * w * 4 + (double)BH * w * elt, (double)BH * w * 4);
+  HIP_TRY(launch_cond_expand<T>(b->dvec, B, H, w, m->ctau, b->cgroups ? b->cgrp : nullptr, (T*)b->cond, s));
+  REC_END();
   // 2. input projection of the buffer in logical order
   REC_BEGIN("in_proj", (double)BH * (D + w) * 4, 2.0 * BH * w * D);
-  HIP_TRY(launch_in_proj(b->X, b->t, B, H, D, m->in_w, m->in_b, w, b->x, s));
+  HIP_TRY(launch_in_proj(b->X, b->t, B, H, D, m->in_wT, m->in_b, w, b->x, InProjNorm{}, s));
   REC_END();
   // FOP adapter keys/values of every adapter layer at once
   if (m->n_ad > 0) {
@@ -776,7 +779,7 @@ ravel_status build_persistent(ravel_buffer* b) {
   int mt = (BH + 15) / 16;
   if (mt == 3) mt = 4;
   b->pmt = mt;
-  b->pblocks = std::min(persistent_max_blocks(mt), 256);
+  b->pblocks = std::min(persistent_max_blocks(mt, hd), 256);
   if (b->pblocks < 64) return fail(RAVEL_E_STATE, "persistent kernel does not fit");
   auto tiles = [](int n) { return (n + 63) / 64; };
   RV_TRY(palloc(b, &b->pbar, kBarrierWords * 4, true));
@@ -788,8 +791,8 @@ ravel_status build_persistent(ravel_buffer* b) {
   // layer l, 2L the final norm; in the modulation rows they sit 3w apart
   // starting at column w
   const int nshift = 2 * c.layers + 1;
-  bf16_t* pshift = nullptr;
-  RV_TRY(palloc(b, &pshift, (size_t)nshift * BH * w * 2, true));
+  RV_TRY(palloc(b, &b->pshift, (size_t)nshift * BH * w * 2, true));
+  const bf16_t* pshift = b->pshift;
   auto shift_of = [&](int chunk) -> const bf16_t* { return pshift + (size_t)chunk * BH * w; };
   size_t part = 0;
   int max_tiles = 1;
@@ -845,30 +848,8 @@ ravel_status build_persistent(ravel_buffer* b) {
     g.sumsq_out = b->sumsq[cur ^ 1];
     cur ^= 1;
   };
-  const float* mod0 = b->mod;  // layer 0 chunks: scale, shift, gate, scale, shift, gate
-  // row sums of squares of the input projection and p of the first norm
-  {
-    Phase ph;
-    memset(&ph, 0, sizeof ph);
-    ph.type = PH_ROWSTATS;
-    ph.rs.x = b->x;
-    ph.rs.ldx = w;
-    ph.rs.M = BH;
-    ph.rs.N = w;
-    ph.rs.ns_mode = NS_ROW;
-    ph.rs.ns = mod0;
-    ph.rs.ldns = ldm;
-    ph.rs.p = (bf16_t*)b->pnorm;
-    ph.rs.ldp = w;
-    ph.rs.sumsq_out = b->sumsq[cur];
-    ph.rs.cvt_in = b->mod + w;
-    ph.rs.cvt_ld = ldm;
-    ph.rs.cvt_stride = 3 * w;
-    ph.rs.cvt_chunks = nshift;
-    ph.rs.cvt_out = pshift;
-    ph.items = w / 64 + (int)(((size_t)nshift * BH * w + 8191) / 8192);
-    push(ph, "rowstats");
-  }
+  // the input projection writes the first norm's p and row sums of squares
+  // (b->sumsq[0]) and the bf16 shifts before the launch
   int max_attn_parts = 1, max_attn_heads = 1;
   auto attn_phase = [&](AttnArgs a) {
     Phase ph;
@@ -887,7 +868,7 @@ ravel_status build_persistent(ravel_buffer* b) {
     a.keys_per_split = std::max(a.keys_per_split, std::min(kmax, ((a.S + 31) / 32) * 32));
     a.nsplit = (a.P + a.keys_per_split - 1) / a.keys_per_split + (a.S + a.keys_per_split - 1) / a.keys_per_split;
     ph.items = B * c.n_q_heads * a.nsplit;
-    a.coop = a.nsplit > 1 && a.nsplit <= 8 && ph.items <= b->pblocks;
+    a.coop = a.nsplit > 1 && ph.items <= b->pblocks;
     ph.at = a;
     max_attn_parts = std::max(max_attn_parts, B * c.n_q_heads * a.nsplit);
     max_attn_heads = std::max(max_attn_heads, B * c.n_q_heads);
@@ -1041,16 +1022,14 @@ ravel_status enqueue_persistent_step(ravel_buffer* b, const void* fop, float* ac
   HIP_TRY(launch_delta_hidden<bf16_t>(b->t, b->t_obs, B, H, c.delta_bias, m->d_w1, m->d_b1, w, (bf16_t*)b->h1, s));
   REC_END();
   {
-    GemmArgs e = epi_args(EPI_COND);
+    GemmArgs e = epi_args(EPI_F32);
     e.bias = m->d_b2;
-    e.out_t = b->cond;
-    e.ldo_t = w;
-    e.ctau = m->ctau;
-    e.H = H;
+    e.out_f = b->dvec;
+    e.ldo_f = w;
     RV_TRY(run_gemm<bf16_t>(b, s, rec, "cond", b->h1, w, m->d_w2, w, B, w, w, e));
   }
-  REC_BEGIN("in_proj", (double)BH * (D + w) * 4, 2.0 * BH * w * D);
-  HIP_TRY(launch_in_proj(b->X, b->t, B, H, D, m->in_w, m->in_b, w, b->x, s));
+  REC_BEGIN("cond_expand", (double)B * w * 4 + (double)H * w * 4 + (double)BH * w * elt, (double)BH * w * 4);
+  HIP_TRY(launch_cond_expand<bf16_t>(b->dvec, B, H, w, m->ctau, nullptr, (bf16_t*)b->cond, s));
   REC_END();
   {
     GemmArgs e = epi_args(EPI_F32);
@@ -1059,6 +1038,25 @@ ravel_status enqueue_persistent_step(ravel_buffer* b, const void* fop, float* ac
     e.ldo_f = b->mod_ld;
     RV_TRY(run_gemm<bf16_t>(b, s, rec, "mod_all", b->cond, w, m->mod_all_w, w, BH, b->mod_ld, w, e));
   }
+  {
+    // input projection with the first layer's norm operands: p of the first norm,
+    // the rows' sums of squares, and the bf16 shifts of every norm (chunk 2l and
+    // 2l + 1 of layer l, 2L the final norm: 3w apart in the modulation rows,
+    // starting at column w)
+    InProjNorm nrm;
+    nrm.scale = b->mod;
+    nrm.ldm = b->mod_ld;
+    nrm.p = b->pnorm;
+    nrm.sumsq = b->sumsq[0];
+    nrm.cvt_in = b->mod + w;
+    nrm.cvt_ld = b->mod_ld;
+    nrm.cvt_stride = 3 * w;
+    nrm.cvt_chunks = 2 * c.layers + 1;
+    nrm.cvt_out = b->pshift;
+    REC_BEGIN("in_proj", (double)BH * (D + w) * 4 + (double)BH * w * (6 + nrm.cvt_chunks * 6), 2.0 * BH * w * D);
+    HIP_TRY(launch_in_proj(b->X, b->t, B, H, D, m->in_wT, m->in_b, w, b->x, nrm, s));
+    REC_END();
+  }
   if (m->n_ad > 0) {
     GemmArgs e = epi_args(EPI_T);
     e.out_t = b->kva;
@@ -1066,7 +1064,7 @@ ravel_status enqueue_persistent_step(ravel_buffer* b, const void* fop, float* ac
     RV_TRY(run_gemm<bf16_t>(b, s, rec, "fop_kv", fop, w, m->kva_w, w, B * c.n_fop, m->n_ad * 2 * kvd, w, e));
   }
   REC_BEGIN("persistent_layers", b->p_bytes, b->p_flops);
-  HIP_TRY(launch_persistent(b->d_phases, (int)b->phases.size(), b->slot, B, b->pmt, b->pblocks, b->pbar, b->perr,
+  HIP_TRY(launch_persistent(b->d_phases, (int)b->phases.size(), b->slot, B, b->pmt, c.head_dim, b->pblocks, b->pbar, b->perr,
                             rec ? b->ptimes : nullptr, s));
   REC_END();
   REC_BEGIN("euler_release", (double)B * H * D * 12 + (double)B * D * 4, (double)B * H * D * 2);
@@ -1192,6 +1190,7 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
   const size_t E = m->elt;
   Arena ar;
   ar.want((void**)&m->in_w, (size_t)w * D * 4);
+  ar.want((void**)&m->in_wT, (size_t)w * D * 4);
   ar.want((void**)&m->in_b, (size_t)w * 4);
   ar.want((void**)&m->ctau, (size_t)H * w * 4);
   ar.want((void**)&m->d_w1, (size_t)w * 4);
@@ -1253,6 +1252,7 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
     if ((st = up(name, dst, md)) != RAVEL_OK) return bail(done(st)); \
   } while (0)
   UP("in.w", m->in_w, false);
+  if (launch_transpose_f32(m->in_w, w, D, m->in_wT, 0) != hipSuccess) return bail(done(fail(RAVEL_E_HIP, "in.w transpose")));
   UP("in.b", m->in_b, false);
   UP("delta.w1", m->d_w1, false);
   UP("delta.b1", m->d_b1, false);
@@ -1417,6 +1417,7 @@ ravel_status ravel_buffer_create(ravel_model* m, int32_t batch, uint64_t seed, r
     ar.want((void**)&b->x, (size_t)BH * w * 4);
     ar.want(&b->cond, (size_t)BH * w * E);
     ar.want(&b->h1, (size_t)B * w * E);
+    ar.want((void**)&b->dvec, (size_t)B * w * 4);
     // few rows: every layer's modulation comes from one GEMM at the start of the step
     // Few rows, or rows grouped by offset conditioning: every layer's modulation
     // comes from one GEMM at the start of the step (on the groups' rows only).
@@ -1876,6 +1877,18 @@ ravel_status ravel_profile_step(ravel_buffer* b, const void* fop, float* action,
           o.ms = (float)agg[nm][0];
           o.bytes = agg[nm][1];
           o.flops = agg[nm][2];
+        }
+        ++k;
+      }
+      // then every phase on its own, in launch order: "phase/<index>/<class>"
+      for (size_t i = 0; i < np; ++i) {
+        if (records && k < cap) {
+          ravel_kernel_record& o = records[k];
+          memset(&o, 0, sizeof o);
+          snprintf(o.name, sizeof o.name, "phase/%zu/%s", i, b->pnames[i].c_str());
+          o.ms = (float)((double)(ts[i + 1] - ts[i]) / (double)khz);
+          o.bytes = b->ph_bytes[i];
+          o.flops = b->ph_flops[i];
         }
         ++k;
       }
