@@ -28,7 +28,6 @@ Prints ONE JSON line.  Extra measurements:
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -59,27 +58,6 @@ def parse():
     return p.parse_args()
 
 
-# source files that define each kernel class (for the traffic record's hash)
-KERNEL_SOURCES = {
-    "persistent_layers": ["persistent.hip", "persistent.h", "common.h", "kernels.h"],
-    "gemm": ["gemm.hip", "common.h", "kernels.h"],
-    "attn": ["attention.hip", "common.h", "kernels.h"],
-}
-
-
-def sources_sha256(kernel: str):
-    key = "persistent_layers" if kernel.startswith("persistent") else kernel.split("<")[0].rstrip("0123456789x")
-    key = "gemm" if key.startswith("gemm") else key
-    files = KERNEL_SOURCES.get(key)
-    if not files:
-        return None
-    h = hashlib.sha256()
-    for f in files:
-        with open(os.path.join(ROOT, "paper_2609_34170_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()
-
-
 def traffic_of(kernel: str, workload: str):
     """HBM bytes per launch recorded for this kernel and workload, if its sources are unchanged."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
@@ -87,6 +65,7 @@ def traffic_of(kernel: str, workload: str):
         return None
     with open(path) as fh:
         rec = json.load(fh)
+    from paper_2609_34170_amd.profiling import sources_sha256
     digest = sources_sha256(kernel)
     for e in rec.get("entries", []):
         if e.get("kernel") == kernel and e.get("workload") == workload and e.get("sources_sha256") == digest:

@@ -348,7 +348,9 @@ constexpr unsigned waitcnt_vm(int n) { return (unsigned)((n & 0xF) | ((n >> 4) <
 // ROWLOOP: the row count is known on the device only (a.m_rows); block b owns
 // column tile b and runs every live row tile of it in turn (no K split, fp32
 // output: EPI_F32 only).
-template <int BM, int BN, int WM, int WN, int STAGES, bool ROWLOOP = false>
+// MODE: the epilogue, fixed at compile time (a run-time switch over the modes
+// makes the compiler keep the accumulators in scratch memory).
+template <int BM, int BN, int WM, int WN, int STAGES, int MODE, bool ROWLOOP = false>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_lds_kernel(GemmArgs a) {
   constexpr int NW = WM * WN;
   constexpr int BK = 64;
@@ -485,10 +487,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_lds_kernel(GemmArgs a) {
         acc[i][j] = sum;
       }
   }
-  if constexpr (ROWLOOP)
-    epi_frags<EPI_F32>(a, acc, mw, nw, l16, grp);  // the only mode of row-loop launches
-  else
-    epilogue(a, acc, mw, nw, l16, grp);
+  epi_frags<MODE>(a, acc, mw, nw, l16, grp);
   if constexpr (!ROWLOOP) break;
   m0 += BM;
   if (m0 >= a.M) break;
@@ -860,19 +859,34 @@ static hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES>
-static hipError_t launch_lds_tile(const GemmArgs& a, hipStream_t s) {
+template <int BM, int BN, int WM, int WN, int STAGES, int MODE>
+static hipError_t launch_lds_tile_m(const GemmArgs& a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   dim3 grid(tiles, 1, a.ksplit);
-  hipLaunchKernelGGL((gemm_lds_kernel<BM, BN, WM, WN, STAGES>), grid, dim3(64 * WM * WN), 0, s, a);
+  hipLaunchKernelGGL((gemm_lds_kernel<BM, BN, WM, WN, STAGES, MODE>), grid, dim3(64 * WM * WN), 0, s, a);
   return hipGetLastError();
 }
 
 template <int BM, int BN, int WM, int WN, int STAGES>
+static hipError_t launch_lds_tile(const GemmArgs& a, hipStream_t s) {
+  switch (a.mode) {
+    case EPI_F32: return launch_lds_tile_m<BM, BN, WM, WN, STAGES, EPI_F32>(a, s);
+    case EPI_T: return launch_lds_tile_m<BM, BN, WM, WN, STAGES, EPI_T>(a, s);
+    case EPI_RESID: return launch_lds_tile_m<BM, BN, WM, WN, STAGES, EPI_RESID>(a, s);
+    case EPI_RESID_TANH: return launch_lds_tile_m<BM, BN, WM, WN, STAGES, EPI_RESID_TANH>(a, s);
+    case EPI_GEGLU: return launch_lds_tile_m<BM, BN, WM, WN, STAGES, EPI_GEGLU>(a, s);
+    case EPI_COND: return launch_lds_tile_m<BM, BN, WM, WN, STAGES, EPI_COND>(a, s);
+    case EPI_GELU_T: return launch_lds_tile_m<BM, BN, WM, WN, STAGES, EPI_GELU_T>(a, s);
+    case EPI_SILU_T: return launch_lds_tile_m<BM, BN, WM, WN, STAGES, EPI_SILU_T>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// row-loop launches (device-side row count) have the fp32 epilogue only
+template <int BM, int BN, int WM, int WN, int STAGES>
 static hipError_t launch_lds_rows(const GemmArgs& a, hipStream_t s) {
-  if (a.ksplit != 1 || !a.m_rows || a.mode != EPI_F32) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((gemm_lds_kernel<BM, BN, WM, WN, STAGES, true>), dim3((a.N + BN - 1) / BN), dim3(64 * WM * WN),
-                     0, s, a);
+  hipLaunchKernelGGL((gemm_lds_kernel<BM, BN, WM, WN, STAGES, EPI_F32, true>), dim3((a.N + BN - 1) / BN),
+                     dim3(64 * WM * WN), 0, s, a);
   return hipGetLastError();
 }
 
@@ -887,6 +901,10 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, int tile, hipStream_t s) {
   if (lds_ok && a.m_rows && a.ksplit == 1 && a.mode == EPI_F32) return launch_lds_rows<256, 128, 4, 2, 2>(a, s);
   if (lds_ok && tile == TILE_128x128) return launch_lds_tile<128, 128, 2, 2, 2>(a, s);
   if (lds_ok && tile == TILE_128x64) return launch_lds_tile<128, 64, 2, 2, 3>(a, s);
+  // larger wave tiles (64x128 .. 128x128) read less LDS per MFMA flop
+  if (lds_ok && tile == TILE_128x256) return launch_lds_tile<128, 256, 2, 2, 2>(a, s);
+  if (lds_ok && tile == TILE_256x128) return launch_lds_tile<256, 128, 2, 2, 2>(a, s);
+  if (lds_ok && tile == TILE_256x256) return launch_lds_tile<256, 256, 2, 2, 2>(a, s);
   switch (tile) {
     case TILE_128x128: return launch_tile<128, 128, 2, 2>(a, s);
     case TILE_64x128: return launch_tile<64, 128, 2, 2>(a, s);
