@@ -14,6 +14,8 @@ Modules:
               gated-GeLU MLP, output head) and the FOP stand-in encoder.
   rolling  -- the rolling buffer: Euler update, release, noise append,
               context publication and temporal offset.
+  full     -- the full-horizon synchronous baseline (all slots share one flow
+              time, S Euler steps per chunk).
 
 Parity status: model output beyond the pins in tests/test_oracle_*.py is
 "parity unpinned" -- no trained weights or worked numeric example exist, so
@@ -23,3 +25,4 @@ the oracle is the definition (see the pins for what is fixed independently).
 from .expert import Expert, fop_encode  # noqa: F401
 from .philox import philox4x32_10, ring_noise  # noqa: F401
 from .rolling import OracleRavel  # noqa: F401
+from .full import expert_velocity, full_denoise  # noqa: F401

@@ -113,13 +113,20 @@ class Expert:
         self._ctau = None
 
     # -- conditioning -----------------------------------------------------
-    def tau_conditioning(self) -> np.ndarray:
-        """c_tau(i) for every logical slot: [H, w]. Fixed because tau_i is fixed."""
-        if self._ctau is None:
-            W = self.W
-            emb = time_embedding(flow_times(self.s.horizon), self.s.width).astype(self.dt)
+    def tau_conditioning(self, taus=None) -> np.ndarray:
+        """c_tau for every slot: [H, w].  Default: the rolling buffer's fixed
+        profile tau_i = (i+1)/H; otherwise the given flow time of each slot."""
+        W = self.W
+
+        def ctau(t):
+            emb = time_embedding(t, self.s.width).astype(self.dt)
             h = silu(linear(emb, W["time.w1"], W["time.b1"]))
-            self._ctau = linear(h, W["time.w2"], W["time.b2"])
+            return linear(h, W["time.w2"], W["time.b2"])
+
+        if taus is not None:
+            return ctau(np.asarray(taus, dtype=np.float64))
+        if self._ctau is None:
+            self._ctau = ctau(flow_times(self.s.horizon))
         return self._ctau
 
     def delta_conditioning(self, delta: float) -> np.ndarray:
@@ -129,14 +136,15 @@ class Expert:
         h = silu(W["delta.w1"][:, 0] * dl[0] + W["delta.b1"])
         return W["delta.w2"] @ h + W["delta.b2"]
 
-    def conditioning(self, delta: float) -> np.ndarray:
-        return silu(self.tau_conditioning() + self.delta_conditioning(delta)[None, :])
+    def conditioning(self, delta: float, taus=None) -> np.ndarray:
+        return silu(self.tau_conditioning(taus) + self.delta_conditioning(delta)[None, :])
 
     # -- one pass ---------------------------------------------------------
-    def velocity(self, a_slots, ctx_k, ctx_v, delta: float, z=None, hooks=None) -> np.ndarray:
+    def velocity(self, a_slots, ctx_k, ctx_v, delta: float, z=None, hooks=None, taus=None) -> np.ndarray:
         """Velocity of every slot.
 
-        a_slots: [H, D_a] noisy actions in logical order (slot i has tau_i).
+        a_slots: [H, D_a] noisy actions in logical order (slot i has tau_i, the
+        rolling profile, unless taus gives each slot's flow time).
         ctx_k, ctx_v: [L, P, n_kv, hd] prefix caches of the active context.
         z: [n_fop, w] FOP tokens (ignored when the expert has no adapters).
         hooks: optional set of sub-block names to switch off ("attn",
@@ -148,7 +156,7 @@ class Expert:
         qd, kvd = nq * hd, nkv * hd
         eps = s.rms_eps
         a = np.asarray(a_slots, dtype=dt)
-        cond = self.conditioning(0.0 if "delta" in hooks else delta)
+        cond = self.conditioning(0.0 if "delta" in hooks else delta, taus)
         h = linear(a, W["in.w"], W["in.b"])
         adapters = set(s.adapter_layers())
         for l in range(s.layers):
