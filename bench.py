@@ -18,6 +18,9 @@ Prints ONE JSON line.  Extra measurements:
   * step_roofline -- the whole step: algorithmic bytes per step / step time;
   * cpu_baseline -- the numpy oracle (fp32) on a bounded sample of the same
                   workload on the host cores;
+  * full_denoise -- the full-horizon synchronous baseline on the same kernels
+                  (batch-1 workloads): ms per chunk of 10 and of H Euler steps
+                  and its first-action time relative to one rolling step;
   * roofline.traffic -- HBM bytes per launch of the dominant kernel from
                   rocprofv3 FETCH_SIZE / WRITE_SIZE runs scaled by the same
                   counters on a plain copy of known size (profiles/traffic.json,
@@ -51,6 +54,7 @@ def parse():
     p.add_argument("--workload", default="pi_b1", choices=["pi_b1", "pi_b64", "small_bf16", "large_b16", "tiny_fp32"])
     p.add_argument("--no-batch64", action="store_true", help="skip the batch-64 secondary measurement")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--no-full", action="store_true", help="skip the full-horizon denoising baseline")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
     p.add_argument("--profile-steps", type=int, default=3)
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -209,6 +213,28 @@ class Workload:
         wall = time.perf_counter() - w0
         return e0.elapsed_time(e1) / steps, wall
 
+    def full_denoise_timing(self, steps_list, reps=5):
+        """Full-horizon synchronous baseline: ms per chunk (steps expert passes) for each
+        step count, timed with HIP events after one untimed call (which also builds the
+        step count's flow-time table)."""
+        torch = self.torch
+        s = self.s
+        noise = torch.randn((self.B, s.horizon, s.action_dim), dtype=torch.float32, device="cuda",
+                            generator=torch.Generator(device="cuda").manual_seed(0))
+        chunk = torch.empty_like(noise)
+        res = []
+        for S in steps_list:
+            self.buf.full_denoise(S, self.fop, noise, chunk)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(self.stream)
+            for _ in range(reps):
+                self.buf.full_denoise(S, self.fop, noise, chunk)
+            e1.record(self.stream)
+            torch.cuda.synchronize()
+            res.append((S, e0.elapsed_time(e1) / reps))
+        return res
+
     def latencies(self, n):
         torch = self.torch
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
@@ -357,6 +383,15 @@ def main():
                 "GBs": round(v[1] / (v[3] * 1e-3) / 1e9, 1) if v[3] > 0 else None}
             for k, v in sorted(wl.phases.items(), key=lambda kv: -kv[1][3])}
     log(f"[{s.name}] {1000.0 / ms:.1f} steps/s, {ms * 1e3:.1f} us/step")
+    if not args.no_full and wl.B == 1:
+        # the synchronous baseline on the same kernels: a chunk needs `steps` expert
+        # passes before its first action, a rolling step one (Sec. 4.1 latency table)
+        out["full_denoise"] = [
+            {"steps": S, "ms_per_chunk": round(fm, 4), "ms_per_pass": round(fm / S, 4),
+             "first_action_vs_rolling_step": round(fm / ms, 2)}
+            for S, fm in wl.full_denoise_timing(sorted({10, s.horizon}))]
+        log(f"[{s.name}] full denoise: " + ", ".join(f"{d['steps']} steps {d['ms_per_chunk']} ms"
+                                                       for d in out["full_denoise"]))
     W = wl.W
     if not args.no_batch64 and args.workload == "pi_b1":
         del wl

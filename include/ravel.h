@@ -191,6 +191,29 @@ ravel_status ravel_publish_log(ravel_buffer* buf, int64_t* entries, int32_t* n);
 ravel_status ravel_buffer_save(ravel_buffer* buf, void* host_blob, size_t* n);
 ravel_status ravel_buffer_load(ravel_buffer* buf, const void* host_blob, size_t n);
 
+/* Full-horizon synchronous denoising: the baseline rolling inference is compared with
+ * (Sec. 4.1 synchronous evaluation and App. B.1: the same budget of expert passes spent on
+ * full-horizon denoising steps, and the first-action latency table of Sec. 4.1).  A fresh
+ * chunk of H slots per env starts as the given noise at flow time 1; every slot shares one
+ * flow time, and `steps` Euler steps of size 1/steps -- step k evaluates the expert with
+ * every slot at tau = (steps - k)/steps and applies chunk -= v / steps -- bring it to 0.
+ * Each step is one expert pass over the chunk with the buffer's contexts at age 0 (offset
+ * delta = delta_bias) and the given FOP tokens (as in ravel_step; NULL only for a model
+ * without adapters).  Context publications are applied first exactly as ravel_step applies
+ * them (and logged at the current step index).  Analytic models use their velocity field
+ * at the shared tau.
+ *   noise: [B, H, D_a] fp32, device; chunk_out: [B, H, D_a] fp32, device (may be noise
+ *   itself); chunk_out holds the denoised chunk when the stream reaches the end of the call.
+ *   steps: 1 .. 1024.
+ * Does not touch the rolling ring or the step counter t; it shares the buffer's
+ * activations with ravel_step, so it must not overlap a step (or
+ * another call of this) on the same buffer.  The first call with a given step count builds
+ * that count's flow-time conditioning table on the device and synchronises; later calls
+ * enqueue on `stream` and return.  Errors: RAVEL_E_INVALID (null pointers, missing FOP
+ * tokens), RAVEL_E_SHAPE (steps), RAVEL_E_STATE (an env without a context). */
+ravel_status ravel_full_denoise(ravel_buffer* buf, int32_t steps, const void* fop_tokens, const float* noise,
+                                float* chunk_out, void* stream);
+
 /* Per-kernel timing of one eagerly launched step (HIP events around every
  * launch on `stream`; synchronises).  Each record: kernel class name,
  * algorithmic bytes and flops of that launch, and its duration.  With the

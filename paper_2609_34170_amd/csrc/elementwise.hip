@@ -173,7 +173,7 @@ __global__ void delta_hidden_kernel(const int64_t* t, const int64_t* t_obs, int 
   const int e = blockIdx.y;
   const int n = blockIdx.x * blockDim.x + threadIdx.x;
   if (n >= w || e >= B) return;
-  const float p = (float)(*t - t_obs[e]);
+  const float p = t ? (float)(*t - t_obs[e]) : 0.f;  // no step counter: context age 0
   const float delta = p / (float)H + delta_bias;
   h1[(size_t)e * w + n] = act<T>::from_f(silu_f(wd1[n] * delta + bd1[n]));
 }
@@ -195,9 +195,10 @@ template hipError_t launch_delta_hidden<bf16_t>(const int64_t*, const int64_t*, 
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ void cond_expand_kernel(const float* __restrict__ d, int B, int H, int w, const float* __restrict__ ctau,
-                                   const int* __restrict__ grp, T* __restrict__ cond) {
+                                   int tau_row, const int* __restrict__ grp, T* __restrict__ cond) {
   // thread: 4 consecutive columns of one (env, slot) row
   const int i = blockIdx.y, e = blockIdx.z;
+  const int ti = tau_row >= 0 ? tau_row : i;  // conditioning table row of this slot
   const int blk = grp ? grp[e] : e;
   if (blk < 0) return;
   const int n = (blockIdx.x * blockDim.x + threadIdx.x) * 4;
@@ -205,23 +206,25 @@ __global__ void cond_expand_kernel(const float* __restrict__ d, int B, int H, in
   T* o = cond + ((size_t)blk * H + i) * w;
   if (n + 4 <= w && (w % 4) == 0) {
     const f32x4_t dv = *(const f32x4_t*)(d + (size_t)e * w + n);
-    const f32x4_t c = *(const f32x4_t*)(ctau + (size_t)i * w + n);
+    const f32x4_t c = *(const f32x4_t*)(ctau + (size_t)ti * w + n);
 #pragma unroll
     for (int r = 0; r < 4; ++r) o[n + r] = act<T>::from_f(silu_f(c[r] + dv[r]));
     return;
   }
   for (int r = 0; r < 4 && n + r < w; ++r)
-    o[n + r] = act<T>::from_f(silu_f(ctau[(size_t)i * w + n + r] + d[(size_t)e * w + n + r]));
+    o[n + r] = act<T>::from_f(silu_f(ctau[(size_t)ti * w + n + r] + d[(size_t)e * w + n + r]));
 }
 
 template <typename T>
-hipError_t launch_cond_expand(const float* d, int B, int H, int w, const float* ctau, const int* grp, T* cond,
-                              hipStream_t s) {
-  hipLaunchKernelGGL(cond_expand_kernel<T>, dim3((w + 255) / 256, H, B), dim3(64), 0, s, d, B, H, w, ctau, grp, cond);
+hipError_t launch_cond_expand(const float* d, int B, int H, int w, const float* ctau, int tau_row, const int* grp,
+                              T* cond, hipStream_t s) {
+  hipLaunchKernelGGL(cond_expand_kernel<T>, dim3((w + 255) / 256, H, B), dim3(64), 0, s, d, B, H, w, ctau, tau_row,
+                     grp, cond);
   return hipGetLastError();
 }
-template hipError_t launch_cond_expand<float>(const float*, int, int, int, const float*, const int*, float*, hipStream_t);
-template hipError_t launch_cond_expand<bf16_t>(const float*, int, int, int, const float*, const int*, bf16_t*,
+template hipError_t launch_cond_expand<float>(const float*, int, int, int, const float*, int, const int*, float*,
+                                              hipStream_t);
+template hipError_t launch_cond_expand<bf16_t>(const float*, int, int, int, const float*, int, const int*, bf16_t*,
                                                hipStream_t);
 
 // ---------------------------------------------------------------------------
@@ -249,13 +252,13 @@ __global__ __launch_bounds__(256) void in_proj_kernel(const float* __restrict__ 
   const int n = blockIdx.x * 256 + threadIdx.x;
   const int lane = threadIdx.x & 63;
   const int BH = B * H;
-  const int64_t tt = *t;
+  const int64_t tt = t ? *t : 0;  // no step counter: X is a chunk in logical order
   const float bias = n < w ? b_in[n] : 0.f;
   for (int rr = 0; rr < kInProjRows; ++rr) {
     const int row = blockIdx.y * kInProjRows + rr;
     if (row >= BH) break;
     const int e = row / H, i = row % H;
-    const int ph = (int)((tt + i) % H);
+    const int ph = t ? (int)((tt + i) % H) : i;
     const float* a = X + ((size_t)e * H + ph) * D;
     float acc = bias;
     if (n < w)
@@ -302,16 +305,16 @@ hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D,
 // Analytic velocity fields
 // ---------------------------------------------------------------------------
 __global__ void analytic_velocity_kernel(int kind, const float* __restrict__ X, const int64_t* t, int B,
-                                         int H, int D, const float* __restrict__ param,
+                                         int H, int D, const float* __restrict__ param, float tau_all,
                                          float* __restrict__ v) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= B * H * D) return;
   const int d = idx % D, i = (idx / D) % H, e = idx / (D * H);
-  const int ph = (int)((*t + i) % H);
+  const int ph = t ? (int)((*t + i) % H) : i;
   const float x = X[((size_t)e * H + ph) * D + d];
   float out;
-  if (kind == 1) {  // OT: (x - a*) / tau_i, tau_i = (i+1)/H
-    const float tau = (float)(i + 1) / (float)H;
+  if (kind == 1) {  // OT: (x - a*) / tau, tau_i = (i+1)/H on the ring, tau_all for a chunk
+    const float tau = tau_all > 0.f ? tau_all : (float)(i + 1) / (float)H;
     out = (x - param[d]) / tau;
   } else {  // LINEAR: lambda * x
     out = param[0] * x;
@@ -320,12 +323,13 @@ __global__ void analytic_velocity_kernel(int kind, const float* __restrict__ X, 
 }
 
 hipError_t launch_analytic_velocity(int kind, const float* X, const int64_t* t, int B, int H, int D,
-                                    const float* param, float* v, hipStream_t s) {
+                                    const float* param, float tau_all, float* v, hipStream_t s) {
   const int n = B * H * D;
   hipLaunchKernelGGL(analytic_velocity_kernel, dim3((n + 255) / 256), dim3(256), 0, s, kind, X, t, B, H, D,
-                     param, v);
+                     param, tau_all, v);
   return hipGetLastError();
 }
+
 
 // ---------------------------------------------------------------------------
 // Euler update + release + noise append + step counter
@@ -336,6 +340,18 @@ RAVEL_DEV float euler_sub(float x, float dt, float v) {
 #pragma clang fp contract(off)
   const float step = dt * v;
   return x - step;
+}
+
+// Euler step of a full-horizon chunk: X[e, i, :] -= dt * v[e*H + i, :] for every slot.
+__global__ void euler_chunk_kernel(float* __restrict__ X, const float* __restrict__ v, int n, float dt) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx < n) X[idx] = euler_sub(X[idx], dt, v[idx]);
+}
+
+hipError_t launch_euler_chunk(float* X, const float* v, int B, int H, int D, float dt, hipStream_t s) {
+  const int n = B * H * D;
+  hipLaunchKernelGGL(euler_chunk_kernel, dim3((n + 255) / 256), dim3(256), 0, s, X, v, n, dt);
+  return hipGetLastError();
 }
 
 // One block: every thread first applies the Euler update to independent ring

@@ -119,11 +119,12 @@ template <typename T>
 hipError_t launch_delta_hidden(const int64_t* t, const int64_t* t_obs, int B, int H, float delta_bias,
                                const float* wd1, const float* bd1, int w, T* h1, hipStream_t s);
 
-// Offset conditioning rows: cond[blk*H + i, n] = T(silu(ctau[i, n] + d[e, n])) for every env e
-// with blk = grp[e] (>= 0; envs with grp[e] < 0 write nothing) or blk = e without grp.
+// Offset conditioning rows: cond[blk*H + i, n] = T(silu(ctau[r, n] + d[e, n])) for every env e
+// with blk = grp[e] (>= 0; envs with grp[e] < 0 write nothing) or blk = e without grp, and
+// table row r = i (tau_row < 0: each slot its own flow time) or r = tau_row (every slot).
 template <typename T>
-hipError_t launch_cond_expand(const float* d, int B, int H, int w, const float* ctau, const int* grp, T* cond,
-                              hipStream_t s);
+hipError_t launch_cond_expand(const float* d, int B, int H, int w, const float* ctau, int tau_row, const int* grp,
+                              T* cond, hipStream_t s);
 
 // dst[c, r] = src[r, c] for an R x C fp32 matrix.
 hipError_t launch_transpose_f32(const float* src, int R, int C, float* dst, hipStream_t s);
@@ -142,13 +143,20 @@ struct InProjNorm {
 };
 
 // Input projection in logical slot order: x[e*H+i, n] = W_in[n,:] . X[e, (t+i) mod H, :] + b_in[n],
-// with the weights given transposed (w_inT[d, n] = W_in[n, d]).
+// with the weights given transposed (w_inT[d, n] = W_in[n, d]); t = NULL: X is a chunk
+// already in logical order (row i of env e).  The offset MLP's hidden layer likewise takes
+// t = NULL for context age 0.
 hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D, const float* w_inT,
                           const float* b_in, int w, float* x, const InProjNorm& nrm, hipStream_t s);
 
-// Analytic velocity fields (logical order): OT v = (x - a*)/tau_i, LINEAR v = lambda x.
+// Analytic velocity fields (logical order): OT v = (x - a*)/tau, LINEAR v = lambda x, with
+// tau = tau_i = (i+1)/H of the ring (rotated by t), or tau_all for every slot of a chunk
+// (t = NULL: X in logical order).
 hipError_t launch_analytic_velocity(int kind, const float* X, const int64_t* t, int B, int H, int D,
-                                    const float* param, float* v, hipStream_t s);
+                                    const float* param, float tau_all, float* v, hipStream_t s);
+
+// Euler step of a full-horizon chunk: X[e, i, :] -= dt * v[e*H + i, :].
+hipError_t launch_euler_chunk(float* X, const float* v, int B, int H, int D, float dt, hipStream_t s);
 
 // Euler update of every slot, release of logical slot 0 into action[e,:], Philox
 // noise for action index r = t + H into the released physical slot, t += 1.

@@ -107,6 +107,8 @@ struct ravel_model {
   float *in_w = nullptr, *in_b = nullptr;
   float* in_wT = nullptr;  // [D, w]: in_w transposed (input projection reads it)
   float* ctau = nullptr;  // [H, w]
+  void *t_w1 = nullptr, *t_w2 = nullptr;  // flow-time MLP (model dtype), kept for other step counts
+  float *t_b1 = nullptr, *t_b2 = nullptr;
   float *d_w1 = nullptr, *d_b1 = nullptr, *d_b2 = nullptr;
   void* d_w2 = nullptr;
   std::vector<LayerW> layers;
@@ -369,6 +371,7 @@ struct ravel_buffer {
   bool sync_ctx = false, use_graph = true, debug = false;
   hipStream_t cap_stream = nullptr;
   std::vector<GraphEntry> graphs;
+  std::map<int, float*> full_tables;  // flow-time conditioning per full-horizon step count
 };
 
 namespace {
@@ -481,8 +484,20 @@ ravel_status run_attn(ravel_buffer* b, hipStream_t s, KernelRecorder* rec, const
 #define REC_END() \
   if (rec) rec->end()
 
+constexpr int kMaxFullSteps = 1024;  // Euler steps of one full-horizon chunk
+
+// What one expert pass reads: the rolling ring (its slots at the buffer's flow-time
+// profile, context age t - t_obs), or a full-horizon chunk whose slots share one
+// flow time (row tau_row of the table ctau) at context age 0.
+struct PassIn {
+  const float* X = nullptr;     // [B, H, D] chunk in logical order; NULL: the ring
+  const float* ctau = nullptr;  // conditioning table; NULL: the model's rolling table
+  int tau_row = -1;             // every slot uses this table row; -1: slot i uses row i
+};
+
 template <typename T>
-ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s, KernelRecorder* rec) {
+ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s, KernelRecorder* rec,
+                                 const PassIn& pin) {
   ravel_model* m = b->m;
   const ravel_config& c = m->cfg;
   const int B = b->B, H = c.horizon, w = c.width, D = c.action_dim;
@@ -495,7 +510,8 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
   // 1. offset conditioning: delta_e = p/H + delta_0, d = W_d2 silu(W_d1 delta + b_d1) + b_d2,
   //    cond[e,i] = silu(c_tau(i) + d)
   REC_BEGIN("delta_hidden", (double)B * w * (8 + elt), (double)B * w * 4);
-  HIP_TRY(launch_delta_hidden<T>(b->t, b->t_obs, B, H, c.delta_bias, m->d_w1, m->d_b1, w, (T*)b->h1, s));
+  HIP_TRY(launch_delta_hidden<T>(pin.X ? nullptr : b->t, b->t_obs, B, H, c.delta_bias, m->d_w1, m->d_b1, w,
+                                 (T*)b->h1, s));
   REC_END();
   // Envs with equal t_obs have equal delta, so equal cond rows and modulation
   // rows: cond is written once per group (compacted) and the modulation GEMM
@@ -514,11 +530,13 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
     RV_TRY(run_gemm<T>(b, s, rec, "cond", b->h1, w, m->d_w2, w, B, w, w, e));
   }
   REC_BEGIN("cond_expand", (double)B * w * 4 + (double)H * w * 4 + (double)BH * w * elt, (double)BH * w * 4);
-  HIP_TRY(launch_cond_expand<T>(b->dvec, B, H, w, m->ctau, b->cgroups ? b->cgrp : nullptr, (T*)b->cond, s));
+  HIP_TRY(launch_cond_expand<T>(b->dvec, B, H, w, pin.ctau ? pin.ctau : m->ctau, pin.tau_row,
+                                b->cgroups ? b->cgrp : nullptr, (T*)b->cond, s));
   REC_END();
   // 2. input projection of the buffer in logical order
   REC_BEGIN("in_proj", (double)BH * (D + w) * 4, 2.0 * BH * w * D);
-  HIP_TRY(launch_in_proj(b->X, b->t, B, H, D, m->in_wT, m->in_b, w, b->x, InProjNorm{}, s));
+  HIP_TRY(launch_in_proj(pin.X ? pin.X : b->X, pin.X ? nullptr : b->t, B, H, D, m->in_wT, m->in_b, w, b->x,
+                         InProjNorm{}, s));
   REC_END();
   // FOP adapter keys/values of every adapter layer at once
   if (m->n_ad > 0) {
@@ -675,12 +693,12 @@ ravel_status enqueue_step(ravel_buffer* b, const void* fop, float* action, hipSt
   const int B = b->B, H = c.horizon, D = c.action_dim;
   if (c.model_kind == RAVEL_TRANSFORMER) {
     if (m->bf16)
-      RV_TRY(enqueue_transformer<bf16_t>(b, fop, s, rec));
+      RV_TRY(enqueue_transformer<bf16_t>(b, fop, s, rec, PassIn{}));
     else
-      RV_TRY(enqueue_transformer<float>(b, fop, s, rec));
+      RV_TRY(enqueue_transformer<float>(b, fop, s, rec, PassIn{}));
   } else {
     REC_BEGIN("analytic_velocity", (double)B * H * D * 8, (double)B * H * D * 2);
-    HIP_TRY(launch_analytic_velocity(c.model_kind, b->X, b->t, B, H, D, m->analytic, b->v, s));
+    HIP_TRY(launch_analytic_velocity(c.model_kind, b->X, b->t, B, H, D, m->analytic, 0.f, b->v, s));
     REC_END();
   }
   REC_BEGIN("euler_release", (double)B * H * D * 12 + (double)B * D * 4, (double)B * H * D * 2);
@@ -1011,15 +1029,16 @@ ravel_status build_persistent(ravel_buffer* b) {
   return RAVEL_OK;
 }
 
-ravel_status enqueue_persistent_step(ravel_buffer* b, const void* fop, float* action, hipStream_t s,
-                                     KernelRecorder* rec) {
+ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream_t s, KernelRecorder* rec,
+                                     const PassIn& pin) {
   ravel_model* m = b->m;
   const ravel_config& c = m->cfg;
   const int B = b->B, H = c.horizon, w = c.width, D = c.action_dim, BH = B * H;
   const int kvd = c.n_kv_heads * c.head_dim;
   const double elt = (double)m->elt;
   REC_BEGIN("delta_hidden", (double)B * w * (8 + elt), (double)B * w * 4);
-  HIP_TRY(launch_delta_hidden<bf16_t>(b->t, b->t_obs, B, H, c.delta_bias, m->d_w1, m->d_b1, w, (bf16_t*)b->h1, s));
+  HIP_TRY(launch_delta_hidden<bf16_t>(pin.X ? nullptr : b->t, b->t_obs, B, H, c.delta_bias, m->d_w1, m->d_b1, w,
+                                      (bf16_t*)b->h1, s));
   REC_END();
   {
     GemmArgs e = epi_args(EPI_F32);
@@ -1029,7 +1048,8 @@ ravel_status enqueue_persistent_step(ravel_buffer* b, const void* fop, float* ac
     RV_TRY(run_gemm<bf16_t>(b, s, rec, "cond", b->h1, w, m->d_w2, w, B, w, w, e));
   }
   REC_BEGIN("cond_expand", (double)B * w * 4 + (double)H * w * 4 + (double)BH * w * elt, (double)BH * w * 4);
-  HIP_TRY(launch_cond_expand<bf16_t>(b->dvec, B, H, w, m->ctau, nullptr, (bf16_t*)b->cond, s));
+  HIP_TRY(launch_cond_expand<bf16_t>(b->dvec, B, H, w, pin.ctau ? pin.ctau : m->ctau, pin.tau_row, nullptr,
+                                     (bf16_t*)b->cond, s));
   REC_END();
   {
     GemmArgs e = epi_args(EPI_F32);
@@ -1054,7 +1074,8 @@ ravel_status enqueue_persistent_step(ravel_buffer* b, const void* fop, float* ac
     nrm.cvt_chunks = 2 * c.layers + 1;
     nrm.cvt_out = b->pshift;
     REC_BEGIN("in_proj", (double)BH * (D + w) * 4 + (double)BH * w * (6 + nrm.cvt_chunks * 6), 2.0 * BH * w * D);
-    HIP_TRY(launch_in_proj(b->X, b->t, B, H, D, m->in_wT, m->in_b, w, b->x, nrm, s));
+    HIP_TRY(launch_in_proj(pin.X ? pin.X : b->X, pin.X ? nullptr : b->t, B, H, D, m->in_wT, m->in_b, w, b->x, nrm,
+                           s));
     REC_END();
   }
   if (m->n_ad > 0) {
@@ -1067,6 +1088,14 @@ ravel_status enqueue_persistent_step(ravel_buffer* b, const void* fop, float* ac
   HIP_TRY(launch_persistent(b->d_phases, (int)b->phases.size(), b->slot, B, b->pmt, c.head_dim, b->pblocks, b->pbar, b->perr,
                             rec ? b->ptimes : nullptr, s));
   REC_END();
+  return RAVEL_OK;
+}
+
+ravel_status enqueue_persistent_step(ravel_buffer* b, const void* fop, float* action, hipStream_t s,
+                                     KernelRecorder* rec) {
+  RV_TRY(enqueue_persistent_pass(b, fop, s, rec, PassIn{}));
+  const ravel_config& c = b->m->cfg;
+  const int B = b->B, H = c.horizon, D = c.action_dim;
   REC_BEGIN("euler_release", (double)B * H * D * 12 + (double)B * D * 4, (double)B * H * D * 2);
   HIP_TRY(launch_euler_release(b->X, b->v, b->t, B, H, D, b->seed, action, b->ticket, s));
   REC_END();
@@ -1074,6 +1103,58 @@ ravel_status enqueue_persistent_step(ravel_buffer* b, const void* fop, float* ac
 }
 
 }  // namespace
+
+// c_tau(tau_i) = W_t2 silu(W_t1 emb(tau_i) + b_t1) + b_t2 for tau_i = (i+1)/S, i < S:
+// out [S, w] fp32 (synchronous; temporary device memory is freed before it returns).
+// With S = H this is the rolling buffer's table; with S Euler steps of a full-horizon
+// chunk, step s has tau = (S - s)/S, row S - 1 - s.
+static ravel_status flow_time_table(ravel_model* m, int S, float* out) {
+  const int w = m->cfg.width;
+  const size_t E = m->elt;
+  void *emb = nullptr, *hid = nullptr;
+  ravel_buffer tmp;  // GEMM workspace only
+  tmp.m = m;
+  tmp.B = 1;
+  const GemmPlan p1 = plan_gemm(S, w, w, false);
+  tmp.gpart_elems = p1.part_elems;
+  tmp.gcnt_n = std::max(p1.tiles, 1);
+  Arena ta;
+  void* tarena = nullptr;
+  ta.want(&emb, (size_t)S * w * E);
+  ta.want(&hid, (size_t)S * w * E);
+  ta.want((void**)&tmp.gpart, std::max<size_t>(p1.part_elems, 1) * 4);
+  ta.want((void**)&tmp.gcnt, (size_t)tmp.gcnt_n * 4 * kCounterStride);
+  ravel_status st = ta.commit(&tarena);
+  if (st != RAVEL_OK) return st;
+  auto done = [&](ravel_status s2) {
+    (void)hipFree(tarena);
+    return s2;
+  };
+  if (hipMemset(tmp.gcnt, 0, (size_t)tmp.gcnt_n * 4 * kCounterStride) != hipSuccess)
+    return done(fail(RAVEL_E_HIP, "flow-time table workspace"));
+  hipError_t he = m->bf16 ? launch_time_embedding<bf16_t>(S, w, (bf16_t*)emb, 0)
+                          : launch_time_embedding<float>(S, w, (float*)emb, 0);
+  if (he != hipSuccess) return done(fail(RAVEL_E_HIP, hipGetErrorString(he)));
+  GemmArgs e1 = epi_args(EPI_SILU_T);
+  e1.bias = m->t_b1;
+  e1.out_t = hid;
+  e1.ldo_t = w;
+  GemmArgs e2 = epi_args(EPI_F32);
+  e2.bias = m->t_b2;
+  e2.out_f = out;
+  e2.ldo_f = w;
+  if (m->bf16) {
+    st = run_gemm<bf16_t>(&tmp, 0, nullptr, "time1", emb, w, m->t_w1, w, S, w, w, e1);
+    if (st == RAVEL_OK) st = run_gemm<bf16_t>(&tmp, 0, nullptr, "time2", hid, w, m->t_w2, w, S, w, w, e2);
+  } else {
+    st = run_gemm<float>(&tmp, 0, nullptr, "time1", emb, w, m->t_w1, w, S, w, w, e1);
+    if (st == RAVEL_OK) st = run_gemm<float>(&tmp, 0, nullptr, "time2", hid, w, m->t_w2, w, S, w, w, e2);
+  }
+  const hipError_t se = hipDeviceSynchronize();
+  if (st != RAVEL_OK) return done(st);
+  if (se != hipSuccess) return done(fail(RAVEL_E_HIP, hipGetErrorString(se)));
+  return done(RAVEL_OK);
+}
 
 // ---------------------------------------------------------------------------
 // C ABI
@@ -1193,6 +1274,10 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
   ar.want((void**)&m->in_wT, (size_t)w * D * 4);
   ar.want((void**)&m->in_b, (size_t)w * 4);
   ar.want((void**)&m->ctau, (size_t)H * w * 4);
+  ar.want(&m->t_w1, (size_t)w * w * E);
+  ar.want(&m->t_w2, (size_t)w * w * E);
+  ar.want((void**)&m->t_b1, (size_t)w * 4);
+  ar.want((void**)&m->t_b2, (size_t)w * 4);
   ar.want((void**)&m->d_w1, (size_t)w * 4);
   ar.want((void**)&m->d_b1, (size_t)w * 4);
   ar.want((void**)&m->d_w2, (size_t)w * w * E);
@@ -1306,67 +1391,11 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
   }
 
   // flow-time conditioning c_tau(i) = W_t2 silu(W_t1 emb(tau_i) + b_t1) + b_t2, once per model
-  {
-    void *emb = nullptr, *hid = nullptr, *tw1 = nullptr, *tw2 = nullptr;
-    float *tb1 = nullptr, *tb2 = nullptr;
-    Arena ta;
-    void* tarena = nullptr;
-    ta.want(&emb, (size_t)H * w * E);
-    ta.want(&hid, (size_t)H * w * E);
-    ta.want(&tw1, (size_t)w * w * E);
-    ta.want(&tw2, (size_t)w * w * E);
-    ta.want((void**)&tb1, (size_t)w * 4);
-    ta.want((void**)&tb2, (size_t)w * 4);
-    if ((st = ta.commit(&tarena)) != RAVEL_OK) return bail(done(st));
-    auto tdone = [&](ravel_status s2) {
-      (void)hipFree(tarena);
-      return done(s2);
-    };
-    if ((st = up("time.w1", tw1, true)) != RAVEL_OK) return bail(tdone(st));
-    if ((st = up("time.w2", tw2, true)) != RAVEL_OK) return bail(tdone(st));
-    if ((st = up("time.b1", tb1, false)) != RAVEL_OK) return bail(tdone(st));
-    if ((st = up("time.b2", tb2, false)) != RAVEL_OK) return bail(tdone(st));
-    // a throwaway buffer-like context for the GEMM workspace
-    ravel_buffer tmp;
-    tmp.m = m;
-    tmp.B = 1;
-    const GemmPlan p1 = plan_gemm(H, w, w, false);
-    const size_t part = std::max<size_t>(p1.part_elems, 1);
-    tmp.gpart_elems = p1.part_elems;
-    tmp.gcnt_n = std::max(p1.tiles, 1);
-    Arena wa;
-    void* warena = nullptr;
-    wa.want((void**)&tmp.gpart, part * 4);
-    wa.want((void**)&tmp.gcnt, (size_t)std::max(p1.tiles, 1) * 4 * kCounterStride);
-    if ((st = wa.commit(&warena)) != RAVEL_OK) return bail(tdone(st));
-    (void)hipMemset(tmp.gcnt, 0, (size_t)std::max(p1.tiles, 1) * 4 * kCounterStride);
-    hipError_t he = m->bf16 ? launch_time_embedding<bf16_t>(H, w, (bf16_t*)emb, 0)
-                            : launch_time_embedding<float>(H, w, (float*)emb, 0);
-    if (he != hipSuccess) {
-      (void)hipFree(warena);
-      return bail(tdone(fail(RAVEL_E_HIP, hipGetErrorString(he))));
-    }
-    GemmArgs e1 = epi_args(EPI_SILU_T);
-    e1.bias = tb1;
-    e1.out_t = hid;
-    e1.ldo_t = w;
-    GemmArgs e2 = epi_args(EPI_F32);
-    e2.bias = tb2;
-    e2.out_f = m->ctau;
-    e2.ldo_f = w;
-    if (m->bf16) {
-      st = run_gemm<bf16_t>(&tmp, 0, nullptr, "time1", emb, w, tw1, w, H, w, w, e1);
-      if (st == RAVEL_OK) st = run_gemm<bf16_t>(&tmp, 0, nullptr, "time2", hid, w, tw2, w, H, w, w, e2);
-    } else {
-      st = run_gemm<float>(&tmp, 0, nullptr, "time1", emb, w, tw1, w, H, w, w, e1);
-      if (st == RAVEL_OK) st = run_gemm<float>(&tmp, 0, nullptr, "time2", hid, w, tw2, w, H, w, w, e2);
-    }
-    hipError_t se = hipDeviceSynchronize();
-    (void)hipFree(warena);
-    if (st != RAVEL_OK) return bail(tdone(st));
-    if (se != hipSuccess) return bail(tdone(fail(RAVEL_E_HIP, hipGetErrorString(se))));
-    (void)hipFree(tarena);
-  }
+  UP("time.w1", m->t_w1, true);
+  UP("time.w2", m->t_w2, true);
+  UP("time.b1", m->t_b1, false);
+  UP("time.b2", m->t_b2, false);
+  if ((st = flow_time_table(m, H, m->ctau)) != RAVEL_OK) return bail(done(st));
   (void)hipFree(staging);
 #undef UP
   if (hipDeviceSynchronize() != hipSuccess) return bail(fail(RAVEL_E_HIP, "create sync"));
@@ -1538,6 +1567,7 @@ void ravel_buffer_destroy(ravel_buffer* b) {
   }
   if (b->cap_stream) (void)hipStreamDestroy(b->cap_stream);
   for (void* p : b->pallocs) (void)hipFree(p);
+  for (auto& kv : b->full_tables) (void)hipFree(kv.second);
   if (b->arena) (void)hipFree(b->arena);
   delete b;
 }
@@ -1586,6 +1616,62 @@ ravel_status ravel_set_context(ravel_buffer* b, int32_t env, const void* k, cons
   HIP_TRY(hipEventRecord(b->pending[env].ready, ps));
   b->pending[env].valid = true;
   b->pending[env].t_obs = t_obs;
+  return RAVEL_OK;
+}
+
+ravel_status ravel_full_denoise(ravel_buffer* b, int32_t steps, const void* fop, const float* noise, float* chunk,
+                                void* stream) {
+  if (!b || !noise || !chunk) return fail(RAVEL_E_INVALID, "null argument");
+  ravel_model* m = b->m;
+  const ravel_config& c = m->cfg;
+  const int B = b->B, H = c.horizon, D = c.action_dim;
+  if (steps < 1 || steps > kMaxFullSteps) return fail(RAVEL_E_SHAPE, "steps must be in 1..1024");
+  if (c.model_kind == RAVEL_TRANSFORMER && m->n_ad > 0 && !fop)
+    return fail(RAVEL_E_INVALID, "fop_tokens required: the model has FOP adapters");
+  if (fop && ((uintptr_t)fop % 16)) return fail(RAVEL_E_INVALID, "fop_tokens must be 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  std::lock_guard<std::mutex> lk(b->mu);
+  const float* table = nullptr;
+  if (c.model_kind == RAVEL_TRANSFORMER) {
+    // contexts: the latest available ones, published exactly as a rolling step would
+    RV_TRY(apply_publishes(b, s));
+    for (int e = 0; e < B; ++e)
+      if (!b->has_ctx[e]) return fail(RAVEL_E_STATE, "env " + std::to_string(e) + " has no context yet");
+    auto it = b->full_tables.find(steps);
+    if (it == b->full_tables.end()) {
+      float* t = nullptr;
+      HIP_TRY(hipMalloc(&t, (size_t)steps * c.width * 4));
+      const ravel_status st = flow_time_table(m, steps, t);
+      if (st != RAVEL_OK) {
+        (void)hipFree(t);
+        return st;
+      }
+      it = b->full_tables.emplace(steps, t).first;
+    }
+    table = it->second;
+  }
+  const size_t bytes = (size_t)B * H * D * 4;
+  if (chunk != noise) HIP_TRY(hipMemcpyAsync(chunk, noise, bytes, hipMemcpyDeviceToDevice, s));
+  const float dt = 1.0f / (float)steps;
+  for (int k = 0; k < steps; ++k) {
+    // step k: every slot at tau = (steps - k) / steps, row steps - 1 - k of the table
+    if (c.model_kind == RAVEL_TRANSFORMER) {
+      PassIn pin;
+      pin.X = chunk;
+      pin.ctau = table;
+      pin.tau_row = steps - 1 - k;
+      if (b->persistent)
+        RV_TRY(enqueue_persistent_pass(b, fop, s, nullptr, pin));
+      else if (m->bf16)
+        RV_TRY(enqueue_transformer<bf16_t>(b, fop, s, nullptr, pin));
+      else
+        RV_TRY(enqueue_transformer<float>(b, fop, s, nullptr, pin));
+    } else {
+      HIP_TRY(launch_analytic_velocity(c.model_kind, chunk, nullptr, B, H, D, m->analytic,
+                                       (float)(steps - k) / (float)steps, b->v, s));
+    }
+    HIP_TRY(launch_euler_chunk(chunk, b->v, B, H, D, dt, s));
+  }
   return RAVEL_OK;
 }
 
