@@ -100,8 +100,12 @@ def _counter_means(pmc_dir, counter, regex):
             per[key][disp] += float(_col(r, "Counter_Value"))
     if "copy" not in per or "kernel" not in per:
         raise RuntimeError(f"{counter}: missing copy or kernel dispatches in {pmc_dir}")
+    # the calibration copies are the largest copy dispatches (the program's own
+    # small copies -- uploads, context publications -- are left out)
+    big = max(per["copy"].values())
+    cal = [v for v in per["copy"].values() if v >= 0.5 * big]
     mean = lambda d: sum(d.values()) / len(d)
-    return mean(per["kernel"]), len(per["kernel"]), mean(per["copy"])
+    return mean(per["kernel"]), len(per["kernel"]), sum(cal) / len(cal)
 
 
 def traffic(fetch_dir, write_dir, kernel, workload, regex, algo_bytes, cmd_fetch, cmd_write, avg_us=None):
