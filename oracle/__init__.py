@@ -16,6 +16,8 @@ Modules:
               context publication and temporal offset.
   full     -- the full-horizon synchronous baseline (all slots share one flow
               time, S Euler steps per chunk).
+  training -- the streaming-aligned training objective (buffer at the rolling
+              profile, offset p / K, flow-matching loss).
 
 Parity status: model output beyond the pins in tests/test_oracle_*.py is
 "parity unpinned" -- no trained weights or worked numeric example exist, so
@@ -26,3 +28,4 @@ from .expert import Expert, fop_encode  # noqa: F401
 from .philox import philox4x32_10, ring_noise  # noqa: F401
 from .rolling import OracleRavel  # noqa: F401
 from .full import expert_velocity, full_denoise  # noqa: F401
+from .training import training_buffer, training_loss  # noqa: F401
