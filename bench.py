@@ -18,6 +18,8 @@ Prints ONE JSON line.  Extra measurements:
   * step_roofline -- the whole step: algorithmic bytes per step / step time;
   * cpu_baseline -- the numpy oracle (fp32) on a bounded sample of the same
                   workload on the host cores;
+  * batch64.train_forward -- the streaming-aligned training objective (forward
+                  and loss) over the batch of 64 with random context ages;
   * full_denoise -- the full-horizon synchronous baseline on the same kernels
                   (batch-1 workloads): ms per chunk of 10 and of H Euler steps
                   and its first-action time relative to one rolling step;
@@ -128,11 +130,11 @@ def modulation_rows(s, batch) -> int:
     return groups * H
 
 
-def algorithmic_flops(s, batch) -> float:
+def algorithmic_flops(s, batch, mod_rows=None) -> float:
     w, H, F = s.width, s.horizon, s.mlp_dim
     qd, kvd = s.n_q_heads * s.head_dim, s.n_kv_heads * s.head_dim
     M = batch * H
-    Mm = modulation_rows(s, batch)
+    Mm = modulation_rows(s, batch) if mod_rows is None else mod_rows
     f = 2.0 * batch * w * w  # offset MLP
     f += 2.0 * M * w * s.action_dim * 2  # in / out projections
     per_layer = 2.0 * Mm * w * 6 * w + 2.0 * M * w * (qd + 2 * kvd) + 2.0 * M * qd * w + 2.0 * M * w * 3 * F
@@ -234,6 +236,28 @@ class Workload:
             torch.cuda.synchronize()
             res.append((S, e0.elapsed_time(e1) / reps))
         return res
+
+    def train_timing(self, steps, warmup=3, max_age=10):
+        """Streaming-aligned training forward + loss over the batch (random targets, noise
+        and context ages 0 .. max_age-1): ms per batch."""
+        torch = self.torch
+        s = self.s
+        g = torch.Generator(device="cuda").manual_seed(1)
+        shape = (self.B, s.horizon, s.action_dim)
+        target = torch.randn(shape, dtype=torch.float32, device="cuda", generator=g)
+        noise = torch.randn(shape, dtype=torch.float32, device="cuda", generator=g)
+        ages = torch.randint(0, max_age, (self.B,), dtype=torch.int64, device="cuda", generator=g)
+        loss = torch.empty(self.B, dtype=torch.float32, device="cuda")
+        for _ in range(warmup):
+            self.buf.train_loss(target, noise, ages, self.fop, loss)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(self.stream)
+        for _ in range(steps):
+            self.buf.train_loss(target, noise, ages, self.fop, loss)
+        e1.record(self.stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps, int(torch.unique(ages).numel())
 
     def latencies(self, n):
         torch = self.torch
@@ -413,6 +437,14 @@ def main():
                                for k, v in sorted(agg64.items(), key=lambda kv: -kv[1][3])[:8]},
         }
         log(f"[pi_b64] {1000.0 / ms64:.1f} steps/s")
+        # streaming-aligned training forward + loss on the same batch of 64 (Sec. 3.3)
+        tms, n_ages = w64.train_timing(max(5, steps64 // 4))
+        tfl = algorithmic_flops(s64, 64, mod_rows=n_ages * s64.horizon)
+        out["batch64"]["train_forward"] = {
+            "ms_per_batch": round(tms, 4), "samples_per_s": round(64 * 1000.0 / tms, 1),
+            "distinct_context_ages": n_ages, "mfma_TFLOPs": round(tfl / (tms * 1e-3) / 1e12, 1),
+            "mfma_frac": round(tfl / (tms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4)}
+        log(f"[pi_b64] training forward + loss {tms:.3f} ms per batch of 64")
         del w64
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(args.workload, W, args.cpu_seconds)

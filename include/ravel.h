@@ -214,6 +214,24 @@ ravel_status ravel_buffer_load(ravel_buffer* buf, const void* host_blob, size_t 
 ravel_status ravel_full_denoise(ravel_buffer* buf, int32_t steps, const void* fop_tokens, const float* noise,
                                 float* chunk_out, void* stream);
 
+/* Streaming-aligned training objective, forward and loss (Sec. 3.3, Eq. 5 and 6): for
+ * every sample e of the batch, the training buffer at the rolling flow-time profile,
+ * slot i = tau_i * noise + (1 - tau_i) * target with tau_i = (i+1)/H (this build's time
+ * direction: the paper's (1 - tau_k) eps + tau_k a_hat), one expert pass with the buffer's
+ * context of sample e as the observation-time context and offset delta = ages[e] / H
+ * (no lead bias delta_0), and loss[e] = (1/H) sum_i ||v_i - (noise_i - target_i)||^2 (the
+ * paper's ||v - (a_hat - eps)||^2 with velocities of the opposite sign).
+ *   target, noise: [B, H, D_a] fp32, device (slot i = the action i+1 steps after t_a);
+ *   ages: [B] int64, device, context age p = t_a - t_o per sample;
+ *   fop_tokens: as ravel_step; loss_out: [B] fp32, device;
+ *   v_out: optional [B, H, D_a] fp32, device: the predicted velocities (NULL: none).
+ * Context publications are applied first as ravel_step applies them.  Does not touch the
+ * ring or t; shares the buffer's activations with ravel_step (no overlap on one buffer).
+ * No backward pass.  Errors: RAVEL_E_INVALID (null pointers, missing FOP tokens),
+ * RAVEL_E_STATE (a sample without a context). */
+ravel_status ravel_train_loss(ravel_buffer* buf, const float* target, const float* noise, const int64_t* ages,
+                              const void* fop_tokens, float* loss_out, float* v_out, void* stream);
+
 /* Per-kernel timing of one eagerly launched step (HIP events around every
  * launch on `stream`; synchronises).  Each record: kernel class name,
  * algorithmic bytes and flops of that launch, and its duration.  With the

@@ -168,27 +168,28 @@ hipError_t launch_cond_groups(const int64_t* t_obs, int B, int H, int* grp, int*
 // Offset conditioning hidden layer
 // ---------------------------------------------------------------------------
 template <typename T>
-__global__ void delta_hidden_kernel(const int64_t* t, const int64_t* t_obs, int B, int H, float delta_bias,
-                                    const float* wd1, const float* bd1, int w, T* h1) {
+__global__ void delta_hidden_kernel(const int64_t* t, const int64_t* t_obs, const int64_t* ages, int B, int H,
+                                    float delta_bias, const float* wd1, const float* bd1, int w, T* h1) {
   const int e = blockIdx.y;
   const int n = blockIdx.x * blockDim.x + threadIdx.x;
   if (n >= w || e >= B) return;
-  const float p = t ? (float)(*t - t_obs[e]) : 0.f;  // no step counter: context age 0
+  // context age: given per env, or t - t_obs, or 0 without a step counter
+  const float p = ages ? (float)ages[e] : (t ? (float)(*t - t_obs[e]) : 0.f);
   const float delta = p / (float)H + delta_bias;
   h1[(size_t)e * w + n] = act<T>::from_f(silu_f(wd1[n] * delta + bd1[n]));
 }
 
 template <typename T>
-hipError_t launch_delta_hidden(const int64_t* t, const int64_t* t_obs, int B, int H, float delta_bias,
-                               const float* wd1, const float* bd1, int w, T* h1, hipStream_t s) {
-  hipLaunchKernelGGL(delta_hidden_kernel<T>, dim3((w + 255) / 256, B), dim3(256), 0, s, t, t_obs, B, H,
+hipError_t launch_delta_hidden(const int64_t* t, const int64_t* t_obs, const int64_t* ages, int B, int H,
+                               float delta_bias, const float* wd1, const float* bd1, int w, T* h1, hipStream_t s) {
+  hipLaunchKernelGGL(delta_hidden_kernel<T>, dim3((w + 255) / 256, B), dim3(256), 0, s, t, t_obs, ages, B, H,
                      delta_bias, wd1, bd1, w, h1);
   return hipGetLastError();
 }
-template hipError_t launch_delta_hidden<float>(const int64_t*, const int64_t*, int, int, float, const float*,
-                                               const float*, int, float*, hipStream_t);
-template hipError_t launch_delta_hidden<bf16_t>(const int64_t*, const int64_t*, int, int, float, const float*,
-                                                const float*, int, bf16_t*, hipStream_t);
+template hipError_t launch_delta_hidden<float>(const int64_t*, const int64_t*, const int64_t*, int, int, float,
+                                               const float*, const float*, int, float*, hipStream_t);
+template hipError_t launch_delta_hidden<bf16_t>(const int64_t*, const int64_t*, const int64_t*, int, int, float,
+                                                const float*, const float*, int, bf16_t*, hipStream_t);
 
 // ---------------------------------------------------------------------------
 // Offset conditioning rows: cond[blk*H + i, n] = T(silu(ctau[i, n] + d[e, n]))
@@ -351,6 +352,51 @@ __global__ void euler_chunk_kernel(float* __restrict__ X, const float* __restric
 hipError_t launch_euler_chunk(float* X, const float* v, int B, int H, int D, float dt, hipStream_t s) {
   const int n = B * H * D;
   hipLaunchKernelGGL(euler_chunk_kernel, dim3((n + 255) / 256), dim3(256), 0, s, X, v, n, dt);
+  return hipGetLastError();
+}
+
+// Training buffer at the rolling flow-time profile: X[e, i, :] = tau_i * noise + (1 - tau_i) * target,
+// tau_i = (i+1)/H, each product rounded on its own (the definition's operation order).
+__global__ void train_buffer_kernel(const float* __restrict__ target, const float* __restrict__ noise, int B, int H,
+                                    int D, float* __restrict__ X) {
+#pragma clang fp contract(off)
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= B * H * D) return;
+  const int i = (idx / D) % H;
+  const float tau = (float)(i + 1) / (float)H;
+  const float a = tau * noise[idx];
+  const float c = (1.0f - tau) * target[idx];
+  X[idx] = a + c;
+}
+
+hipError_t launch_train_buffer(const float* target, const float* noise, int B, int H, int D, float* X, hipStream_t s) {
+  const int n = B * H * D;
+  hipLaunchKernelGGL(train_buffer_kernel, dim3((n + 255) / 256), dim3(256), 0, s, target, noise, B, H, D, X);
+  return hipGetLastError();
+}
+
+// Flow-matching loss per sample: loss[e] = (1/H) sum_i ||v[e*H+i] - (noise - target)[e, i]||^2.
+// One block per sample, a fixed reduction order (deterministic).
+__global__ __launch_bounds__(256) void train_loss_kernel(const float* __restrict__ v, const float* __restrict__ target,
+                                                         const float* __restrict__ noise, int H, int D,
+                                                         float* __restrict__ loss) {
+  __shared__ float part[4];
+  const int e = blockIdx.x, tid = threadIdx.x;
+  const size_t base = (size_t)e * H * D;
+  float acc = 0.f;
+  for (int k = tid; k < H * D; k += 256) {
+    const float r = v[base + k] - (noise[base + k] - target[base + k]);
+    acc += r * r;
+  }
+  acc = wave_sum(acc);
+  if ((tid & 63) == 0) part[tid >> 6] = acc;
+  __syncthreads();
+  if (tid == 0) loss[e] = ((part[0] + part[1]) + (part[2] + part[3])) / (float)H;
+}
+
+hipError_t launch_train_loss(const float* v, const float* target, const float* noise, int B, int H, int D, float* loss,
+                             hipStream_t s) {
+  hipLaunchKernelGGL(train_loss_kernel, dim3(B), dim3(256), 0, s, v, target, noise, H, D, loss);
   return hipGetLastError();
 }
 

@@ -114,10 +114,17 @@ hipError_t launch_cond_groups(const int64_t* t_obs, int B, int H, int* grp, int*
                               hipStream_t s);
 
 // Offset conditioning hidden layer: h1[e,n] = T(silu(wd1[n]*delta_e + bd1[n])),
-// delta_e = (t - t_obs[e]) / H + delta_bias.
+// delta_e = p_e / H + delta_bias with context age p_e = ages[e] if ages is given, else
+// t - t_obs[e], or 0 when t is NULL too.
 template <typename T>
-hipError_t launch_delta_hidden(const int64_t* t, const int64_t* t_obs, int B, int H, float delta_bias,
-                               const float* wd1, const float* bd1, int w, T* h1, hipStream_t s);
+hipError_t launch_delta_hidden(const int64_t* t, const int64_t* t_obs, const int64_t* ages, int B, int H,
+                               float delta_bias, const float* wd1, const float* bd1, int w, T* h1, hipStream_t s);
+
+// Training buffer at the rolling profile: X[e,i,:] = tau_i noise + (1 - tau_i) target, tau_i = (i+1)/H.
+hipError_t launch_train_buffer(const float* target, const float* noise, int B, int H, int D, float* X, hipStream_t s);
+// Flow-matching loss per sample: loss[e] = (1/H) sum_i ||v[e*H+i,:] - (noise - target)[e,i,:]||^2.
+hipError_t launch_train_loss(const float* v, const float* target, const float* noise, int B, int H, int D, float* loss,
+                             hipStream_t s);
 
 // Offset conditioning rows: cond[blk*H + i, n] = T(silu(ctau[r, n] + d[e, n])) for every env e
 // with blk = grp[e] (>= 0; envs with grp[e] < 0 write nothing) or blk = e without grp, and

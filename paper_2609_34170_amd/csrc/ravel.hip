@@ -372,6 +372,7 @@ struct ravel_buffer {
   hipStream_t cap_stream = nullptr;
   std::vector<GraphEntry> graphs;
   std::map<int, float*> full_tables;  // flow-time conditioning per full-horizon step count
+  float* trainX = nullptr;  // [B, H, D] training buffer of ravel_train_loss
 };
 
 namespace {
@@ -493,6 +494,8 @@ struct PassIn {
   const float* X = nullptr;     // [B, H, D] chunk in logical order; NULL: the ring
   const float* ctau = nullptr;  // conditioning table; NULL: the model's rolling table
   int tau_row = -1;             // every slot uses this table row; -1: slot i uses row i
+  const int64_t* ages = nullptr;  // [B] context age per env (device) instead of t - t_obs / 0
+  bool lead_bias = true;          // add delta_0 to the offset (inference); training uses p / H alone
 };
 
 template <typename T>
@@ -510,8 +513,8 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
   // 1. offset conditioning: delta_e = p/H + delta_0, d = W_d2 silu(W_d1 delta + b_d1) + b_d2,
   //    cond[e,i] = silu(c_tau(i) + d)
   REC_BEGIN("delta_hidden", (double)B * w * (8 + elt), (double)B * w * 4);
-  HIP_TRY(launch_delta_hidden<T>(pin.X ? nullptr : b->t, b->t_obs, B, H, c.delta_bias, m->d_w1, m->d_b1, w,
-                                 (T*)b->h1, s));
+  HIP_TRY(launch_delta_hidden<T>(pin.X ? nullptr : b->t, b->t_obs, pin.ages, B, H, pin.lead_bias ? c.delta_bias : 0.f,
+                                 m->d_w1, m->d_b1, w, (T*)b->h1, s));
   REC_END();
   // Envs with equal t_obs have equal delta, so equal cond rows and modulation
   // rows: cond is written once per group (compacted) and the modulation GEMM
@@ -519,7 +522,8 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
   const int* rowmap = b->cgroups ? b->crowmap : nullptr;
   if (b->cgroups) {
     REC_BEGIN("cond_groups", (double)B * 8 + (double)BH * 4, 0.0);
-    HIP_TRY(launch_cond_groups(b->t_obs, B, H, b->cgrp, b->crowmap, b->crows, s));
+    // equal context ages give equal offsets (the shared t makes equal t_obs equal ages)
+    HIP_TRY(launch_cond_groups(pin.ages ? pin.ages : b->t_obs, B, H, b->cgrp, b->crowmap, b->crows, s));
     REC_END();
   }
   {
@@ -1037,8 +1041,8 @@ ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream
   const int kvd = c.n_kv_heads * c.head_dim;
   const double elt = (double)m->elt;
   REC_BEGIN("delta_hidden", (double)B * w * (8 + elt), (double)B * w * 4);
-  HIP_TRY(launch_delta_hidden<bf16_t>(pin.X ? nullptr : b->t, b->t_obs, B, H, c.delta_bias, m->d_w1, m->d_b1, w,
-                                      (bf16_t*)b->h1, s));
+  HIP_TRY(launch_delta_hidden<bf16_t>(pin.X ? nullptr : b->t, b->t_obs, pin.ages, B, H,
+                                      pin.lead_bias ? c.delta_bias : 0.f, m->d_w1, m->d_b1, w, (bf16_t*)b->h1, s));
   REC_END();
   {
     GemmArgs e = epi_args(EPI_F32);
@@ -1435,6 +1439,7 @@ ravel_status ravel_buffer_create(ravel_model* m, int32_t batch, uint64_t seed, r
   ar.want((void**)&b->slot, (size_t)B * 4);
   ar.want((void**)&b->ticket, 4);
   ar.want((void**)&b->v, (size_t)BH * D * 4);
+  ar.want((void**)&b->trainX, (size_t)BH * D * 4);
   ar.want((void**)&b->dbg_flag, 4);
   size_t part_elems = 0, cnt = 1;
   if (c.model_kind == RAVEL_TRANSFORMER) {
@@ -1672,6 +1677,42 @@ ravel_status ravel_full_denoise(ravel_buffer* b, int32_t steps, const void* fop,
     }
     HIP_TRY(launch_euler_chunk(chunk, b->v, B, H, D, dt, s));
   }
+  return RAVEL_OK;
+}
+
+ravel_status ravel_train_loss(ravel_buffer* b, const float* target, const float* noise, const int64_t* ages,
+                              const void* fop, float* loss, float* v_out, void* stream) {
+  if (!b || !target || !noise || !ages || !loss) return fail(RAVEL_E_INVALID, "null argument");
+  ravel_model* m = b->m;
+  const ravel_config& c = m->cfg;
+  const int B = b->B, H = c.horizon, D = c.action_dim;
+  if (c.model_kind == RAVEL_TRANSFORMER && m->n_ad > 0 && !fop)
+    return fail(RAVEL_E_INVALID, "fop_tokens required: the model has FOP adapters");
+  if (fop && ((uintptr_t)fop % 16)) return fail(RAVEL_E_INVALID, "fop_tokens must be 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  std::lock_guard<std::mutex> lk(b->mu);
+  if (c.model_kind == RAVEL_TRANSFORMER) {
+    RV_TRY(apply_publishes(b, s));
+    for (int e = 0; e < B; ++e)
+      if (!b->has_ctx[e]) return fail(RAVEL_E_STATE, "env " + std::to_string(e) + " has no context yet");
+  }
+  HIP_TRY(launch_train_buffer(target, noise, B, H, D, b->trainX, s));
+  if (c.model_kind == RAVEL_TRANSFORMER) {
+    PassIn pin;
+    pin.X = b->trainX;
+    pin.ages = ages;
+    pin.lead_bias = false;
+    if (b->persistent)
+      RV_TRY(enqueue_persistent_pass(b, fop, s, nullptr, pin));
+    else if (m->bf16)
+      RV_TRY(enqueue_transformer<bf16_t>(b, fop, s, nullptr, pin));
+    else
+      RV_TRY(enqueue_transformer<float>(b, fop, s, nullptr, pin));
+  } else {
+    HIP_TRY(launch_analytic_velocity(c.model_kind, b->trainX, nullptr, B, H, D, m->analytic, 0.f, b->v, s));
+  }
+  HIP_TRY(launch_train_loss(b->v, target, noise, B, H, D, loss, s));
+  if (v_out) HIP_TRY(hipMemcpyAsync(v_out, b->v, (size_t)B * H * D * 4, hipMemcpyDeviceToDevice, s));
   return RAVEL_OK;
 }
 

@@ -50,7 +50,8 @@ class KernelRecord(ctypes.Structure):
 SYMBOLS = [
     "ravel_create", "ravel_destroy", "ravel_model_weight_bytes", "ravel_buffer_create",
     "ravel_buffer_destroy", "ravel_buffer_set_option", "ravel_context_acquire", "ravel_set_context",
-    "ravel_step", "ravel_full_denoise", "ravel_fop_encode", "ravel_buffer_sync", "ravel_debug_state",
+    "ravel_step", "ravel_full_denoise", "ravel_train_loss", "ravel_fop_encode", "ravel_buffer_sync",
+    "ravel_debug_state",
     "ravel_publish_log",
     "ravel_buffer_save", "ravel_buffer_load", "ravel_profile_step", "ravel_last_error",
 ]
@@ -77,6 +78,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "ravel_set_context": ([vp, i32, vp, vp, i64, vp], i32),
         "ravel_step": ([vp, vp, vp, vp], i32),
         "ravel_full_denoise": ([vp, i32, vp, vp, vp, vp], i32),
+        "ravel_train_loss": ([vp, vp, vp, vp, vp, vp, vp, vp], i32),
         "ravel_fop_encode": ([vp, vp, vp, vp], i32),
         "ravel_buffer_sync": ([vp], i32),
         "ravel_debug_state": ([vp, vp, vp, vp], i32),
@@ -205,6 +207,10 @@ class Buffer:
     def full_denoise(self, steps: int, fop_tokens, noise, chunk_out, stream=None):
         _check(load_library().ravel_full_denoise(self.h, int(steps), _ptr(fop_tokens), _ptr(noise), _ptr(chunk_out),
                                                  _stream(stream)))
+
+    def train_loss(self, target, noise, ages, fop_tokens, loss_out, v_out=None, stream=None):
+        _check(load_library().ravel_train_loss(self.h, _ptr(target), _ptr(noise), _ptr(ages), _ptr(fop_tokens),
+                                               _ptr(loss_out), _ptr(v_out), _stream(stream)))
 
     def fop_encode(self, obs, fop_tokens, stream=None):
         _check(load_library().ravel_fop_encode(self.h, _ptr(obs), _ptr(fop_tokens), _stream(stream)))
