@@ -262,8 +262,19 @@ __global__ __launch_bounds__(256) void in_proj_kernel(const float* __restrict__ 
     const int ph = t ? (int)((tt + i) % H) : i;
     const float* a = X + ((size_t)e * H + ph) * D;
     float acc = bias;
-    if (n < w)
-      for (int d = 0; d < D; ++d) acc += w_inT[(size_t)d * w + n] * a[d];
+    // 16 weights and inputs per batch of loads, then their products (a loop with one
+    // multiply-add per load would wait for every load in turn)
+    for (int d0 = 0; d0 < D; d0 += 16) {
+      float wv[16], av[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const bool ok = n < w && d0 + j < D;
+        wv[j] = ok ? w_inT[(size_t)(d0 + j) * w + n] : 0.f;
+        av[j] = d0 + j < D ? a[d0 + j] : 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < 16; ++j) acc += wv[j] * av[j];
+    }
     if (n < w) x[(size_t)row * w + n] = acc;
     if (!nrm.p) continue;
     // first adaptive norm of the persistent step: p = bf16((1 + scale) x), the
