@@ -25,6 +25,24 @@ t_obs it was computed from).  One call of ``step``:
    fresh noise for action index r = t + H into its physical slot;
 6. t <- t + 1.
 
+Relative actions (App. B.1 for pi0.5 on RoboTwin 2.0, App. B.3 for DynamicVLA): a
+model that predicts actions relative to the robot state cannot reuse its buffer
+as the state moves.  The paper keeps the clean targets absolute, converts them
+relative to the latest state before each expert pass and back afterwards, and
+leaves the paired noise in model coordinates.  Written on the buffer of noisy
+actions (slot i = tau_i eps_i + (1 - tau_i) a_rel_i), re-expressing the clean
+part against a new state s moves every slot by (1 - tau_i) (s_prev - s) on the
+relative dimensions, where s_prev is the state the buffer was last expressed
+against -- the same for every slot, since every slot is re-expressed each step
+(a slot appended at tau = 1 carries no clean part).  With relative dimensions
+set, ``step`` takes the state [B, D_a]: it shifts the buffer by
+(1 - tau_i)(s_prev - s) (no shift at an env's first step: the cold-start noise is
+taken relative to the first state), runs the ordinary update, and releases the
+absolute action a_0 + s.  Readings: the state comes in the actions' normalised
+units; dimensions outside the mask (e.g. a gripper command) stay absolute; for
+the analytic OT field the target a* is absolute, so the field aims at
+a* - s on the relative dimensions.
+
 This is test infrastructure: only the tests, the smoke check and the bench's
 CPU-baseline leg may import it.
 """
@@ -70,6 +88,15 @@ class OracleRavel:
         self.has_ctx = np.zeros(batch, dtype=bool)
         self.pending = {}
         self.log = []  # (env, t_apply, t_obs)
+        self.rel = None  # [D_a] 1.0 on relative dimensions (None: absolute actions)
+        self.s_prev = np.zeros((batch, D), dtype=dtype)
+        self.has_prev = np.zeros(batch, dtype=bool)
+        self.state = None
+
+    def set_relative_dims(self, mask):
+        """Mark the relative action dimensions (before the first step)."""
+        assert self.t == 0
+        self.rel = np.asarray(mask, dtype=self.dt)
 
     # -- context plane (Sec. 3.2) ----------------------------------------
     def set_context(self, env: int, k, v, t_obs: int):
@@ -99,8 +126,12 @@ class OracleRavel:
 
     def velocity(self, env: int, a_logical, z=None, hooks=None):
         if self.kind == ANALYTIC_OT:
-            # Conditional OT field towards a fixed target a*: v = (x - a*) / tau.
-            return (a_logical - self.params["analytic.target"][None, :]) / self._taus()[:, None]
+            # Conditional OT field towards a fixed target a*: v = (x - a*) / tau (a* absolute:
+            # relative to the current state on relative dimensions).
+            target = self.params["analytic.target"]
+            if self.rel is not None:
+                target = target - self.rel * self.state[env]
+            return (a_logical - target[None, :]) / self._taus()[:, None]
         if self.kind == ANALYTIC_LINEAR:
             return self.params["analytic.lambda"][0] * a_logical
         k, v = self.ctx[env]
@@ -108,20 +139,34 @@ class OracleRavel:
         return self.expert.velocity(a_logical, k, v, self.offset(env), zz, hooks)
 
     # -- one control step ----------------------------------------------------
-    def step(self, fop_tokens=None, hooks=None):
-        """Advance every env by one control step; returns released actions [B, D_a]."""
+    def step(self, fop_tokens=None, hooks=None, state=None):
+        """Advance every env by one control step; returns released actions [B, D_a].
+        With relative dimensions, state [B, D_a] is the latest robot state."""
         self._apply_pending()
         H, t = self.H, self.t
         if self.kind == TRANSFORMER and not self.has_ctx.all():
             raise RuntimeError("every env needs a context before its first step")
+        if (self.rel is None) != (state is None):
+            raise ValueError("a state is given exactly when relative dimensions are set")
         dtau = self.dt(1) / self.dt(H)
         phys = (t + np.arange(H)) % H
         out = np.empty((self.B, self.s.action_dim), dtype=self.dt)
+        if state is not None:
+            self.state = np.asarray(state, dtype=self.dt)
+            for e in range(self.B):
+                if self.has_prev[e]:
+                    # re-express every slot's clean part against the new state
+                    shift = self.rel * (self.s_prev[e] - self.state[e])
+                    self.X[e, phys] = self.X[e, phys] + (self.dt(1) - self._taus())[:, None] * shift[None, :]
+                self.s_prev[e] = self.state[e]
+                self.has_prev[e] = True
         for e in range(self.B):
             a = self.X[e, phys]
             vel = np.asarray(self.velocity(e, a, fop_tokens, hooks), dtype=self.dt)
             self.X[e, phys] = a - dtau * vel
             out[e] = self.X[e, t % H]
+            if state is not None:
+                out[e] = out[e] + self.rel * self.state[e]
             self.X[e, t % H] = ring_noise(self.seed, self.env_ids[e], t + H, self.s.action_dim)
         self.t += 1
         return out
