@@ -20,6 +20,8 @@ Prints ONE JSON line.  Extra measurements:
                   workload on the host cores;
   * batch64.train_forward -- the streaming-aligned training objective (forward
                   and loss) over the batch of 64 with random context ages;
+  * relative_actions -- the step with every action dimension relative to a
+                  moving robot state (batch-1 workloads);
   * full_denoise -- the full-horizon synchronous baseline on the same kernels
                   (batch-1 workloads): ms per chunk of 10 and of H Euler steps
                   and its first-action time relative to one rolling step;
@@ -259,6 +261,32 @@ class Workload:
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / steps, int(torch.unique(ages).numel())
 
+    def relative_timing(self, steps, warmup=20):
+        """Relative actions (every action dimension relative to a random-walk state): a
+        second buffer on the same model and context, ms per step."""
+        torch = self.torch
+        from paper_2609_34170_amd import ravel
+        s = self.s
+        buf = ravel.Buffer(self.model, self.B, 1)
+        buf.set_relative_dims(np.ones(s.action_dim, dtype=np.int32))
+        k, v = self.ctx[0]
+        for e in range(self.B):
+            buf.set_context(e, k[e], v[e], 0)
+        g = torch.Generator(device="cuda").manual_seed(2)
+        walk = torch.cumsum(0.05 * torch.randn((steps + warmup, self.B, s.action_dim), dtype=torch.float32,
+                                               device="cuda", generator=g), dim=0).contiguous()
+        for i in range(warmup):
+            buf.step_state(self.fop, walk[i], self.action)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(self.stream)
+        for i in range(steps):
+            buf.step_state(self.fop, walk[warmup + i], self.action)
+        e1.record(self.stream)
+        torch.cuda.synchronize()
+        buf.close()
+        return e0.elapsed_time(e1) / steps
+
     def latencies(self, n):
         torch = self.torch
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
@@ -408,6 +436,11 @@ def main():
             for k, v in sorted(wl.phases.items(), key=lambda kv: -kv[1][3])}
     log(f"[{s.name}] {1000.0 / ms:.1f} steps/s, {ms * 1e3:.1f} us/step")
     if not args.no_full and wl.B == 1:
+        # relative actions (state conversion around each pass) on the same model
+        rms = wl.relative_timing(max(20, min(200, args.steps // 2)))
+        out["relative_actions"] = {"ms_per_step": round(rms, 4), "steps_per_s": round(1000.0 / rms, 2),
+                                   "vs_absolute_step": round(rms / ms, 4)}
+        log(f"[{s.name}] relative actions: {rms * 1e3:.1f} us/step")
         # the synchronous baseline on the same kernels: a chunk needs `steps` expert
         # passes before its first action, a rolling step one (Sec. 4.1 latency table)
         out["full_denoise"] = [

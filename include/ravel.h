@@ -191,6 +191,23 @@ ravel_status ravel_publish_log(ravel_buffer* buf, int64_t* entries, int32_t* n);
 ravel_status ravel_buffer_save(ravel_buffer* buf, void* host_blob, size_t* n);
 ravel_status ravel_buffer_load(ravel_buffer* buf, const void* host_blob, size_t n);
 
+/* Relative actions (App. B.1, pi0.5 on RoboTwin 2.0; App. B.3, DynamicVLA): a model that
+ * predicts actions relative to the robot state keeps its buffer across a moving state by
+ * holding the clean targets absolute, converting them relative to the latest state before
+ * each expert pass and back afterwards, with the paired noise in model coordinates.  On the
+ * buffer of noisy actions this is a shift of every slot i by (1 - tau_i) * (s_prev - s) on
+ * the relative dimensions before the pass (s_prev: the state of the env's previous step; no
+ * shift at its first step), and the released action is slot 0 plus s on those dimensions.
+ * ravel_set_relative_dims marks the relative dimensions: mask [D_a] host int32, nonzero =
+ * relative (NULL or all zero: absolute actions, the default); only before the first step
+ * (RAVEL_E_STATE after).  With relative dimensions set, every step is ravel_step_state:
+ * ravel_step with state [B, D_a] fp32 device, the latest robot state in the actions'
+ * normalised units (ravel_step is then RAVEL_E_STATE, as is ravel_step_state without
+ * relative dimensions).  The analytic OT field's target is then absolute. */
+ravel_status ravel_set_relative_dims(ravel_buffer* buf, const int32_t* mask);
+ravel_status ravel_step_state(ravel_buffer* buf, const void* fop_tokens, const float* state, float* action_out,
+                              void* stream);
+
 /* Full-horizon synchronous denoising: the baseline rolling inference is compared with
  * (Sec. 4.1 synchronous evaluation and App. B.1: the same budget of expert passes spent on
  * full-horizon denoising steps, and the first-action latency table of Sec. 4.1).  A fresh

@@ -318,6 +318,7 @@ hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D,
 // ---------------------------------------------------------------------------
 __global__ void analytic_velocity_kernel(int kind, const float* __restrict__ X, const int64_t* t, int B,
                                          int H, int D, const float* __restrict__ param, float tau_all,
+                                         const float* __restrict__ state, const float* __restrict__ mask,
                                          float* __restrict__ v) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= B * H * D) return;
@@ -327,7 +328,9 @@ __global__ void analytic_velocity_kernel(int kind, const float* __restrict__ X, 
   float out;
   if (kind == 1) {  // OT: (x - a*) / tau, tau_i = (i+1)/H on the ring, tau_all for a chunk
     const float tau = tau_all > 0.f ? tau_all : (float)(i + 1) / (float)H;
-    out = (x - param[d]) / tau;
+    // an absolute target is aimed at relative to the state on relative dimensions
+    const float target = state ? param[d] - mask[d] * state[(size_t)e * D + d] : param[d];
+    out = (x - target) / tau;
   } else {  // LINEAR: lambda * x
     out = param[0] * x;
   }
@@ -335,10 +338,46 @@ __global__ void analytic_velocity_kernel(int kind, const float* __restrict__ X, 
 }
 
 hipError_t launch_analytic_velocity(int kind, const float* X, const int64_t* t, int B, int H, int D,
-                                    const float* param, float tau_all, float* v, hipStream_t s) {
+                                    const float* param, float tau_all, const float* state, const float* mask,
+                                    float* v, hipStream_t s) {
   const int n = B * H * D;
   hipLaunchKernelGGL(analytic_velocity_kernel, dim3((n + 255) / 256), dim3(256), 0, s, kind, X, t, B, H, D,
-                     param, tau_all, v);
+                     param, tau_all, state, mask, v);
+  return hipGetLastError();
+}
+
+// Relative actions: re-express every slot's clean part against the new state,
+// X[e, (t+i) mod H, d] += (1 - tau_i) * mask[d] * (s_prev[e, d] - state[e, d]) (no shift at an
+// env's first step), then s_prev = state.  One block per env.
+__global__ __launch_bounds__(256) void relative_shift_kernel(float* __restrict__ X, const int64_t* t, int H, int D,
+                                                             const float* __restrict__ mask,
+                                                             const float* __restrict__ state,
+                                                             float* __restrict__ s_prev, int* __restrict__ has_prev) {
+#pragma clang fp contract(off)
+  const int e = blockIdx.x;
+  const int h0 = (int)(*t % H);
+  const float* st = state + (size_t)e * D;
+  float* sp = s_prev + (size_t)e * D;
+  if (has_prev[e]) {
+    for (int k = threadIdx.x; k < H * D; k += blockDim.x) {
+      const int i = k / D, d = k % D;
+      int ph = h0 + i;
+      if (ph >= H) ph -= H;
+      const float tau = (float)(i + 1) / (float)H;
+      const float shift = mask[d] * (sp[d] - st[d]);
+      const float step = (1.0f - tau) * shift;
+      float* xp = X + ((size_t)e * H + ph) * D + d;
+      *xp = *xp + step;
+    }
+  }
+  __syncthreads();
+  for (int d = threadIdx.x; d < D; d += blockDim.x) sp[d] = st[d];
+  if (threadIdx.x == 0) has_prev[e] = 1;
+}
+
+hipError_t launch_relative_shift(float* X, const int64_t* t, int B, int H, int D, const float* mask,
+                                 const float* state, float* s_prev, int* has_prev, hipStream_t s) {
+  hipLaunchKernelGGL(relative_shift_kernel, dim3(B), dim3(256), 0, s, X, t, H, D, mask, state, s_prev, has_prev);
   return hipGetLastError();
 }
 
@@ -417,7 +456,9 @@ hipError_t launch_train_loss(const float* v, const float* target, const float* n
 // and its increment ordered by block barriers alone.
 __global__ __launch_bounds__(1024) void euler_release_kernel(float* __restrict__ X, const float* __restrict__ v,
                                                              int64_t* t, int B, int H, int D, uint64_t seed,
-                                                             float* __restrict__ action) {
+                                                             float* __restrict__ action,
+                                                             const float* __restrict__ state,
+                                                             const float* __restrict__ mask) {
   const int64_t tt = *t;
   const float dt = 1.0f / (float)H;
   const int h0 = (int)(tt % H);
@@ -439,7 +480,8 @@ __global__ __launch_bounds__(1024) void euler_release_kernel(float* __restrict__
     for (int q = 0; q < 4; ++q) {
       const int d = c * 4 + q;
       if (d < D) {
-        action[(size_t)e * D + d] = xs[d];
+        // relative dimensions: the released action in absolute coordinates
+        action[(size_t)e * D + d] = state ? xs[d] + mask[d] * state[(size_t)e * D + d] : xs[d];
         xs[d] = z[q];
       }
     }
@@ -449,9 +491,10 @@ __global__ __launch_bounds__(1024) void euler_release_kernel(float* __restrict__
 }
 
 hipError_t launch_euler_release(float* X, const float* v, int64_t* t, int B, int H, int D, uint64_t seed,
-                                float* action, unsigned* ticket, hipStream_t s) {
+                                float* action, unsigned* ticket, const float* state, const float* mask,
+                                hipStream_t s) {
   (void)ticket;
-  hipLaunchKernelGGL(euler_release_kernel, dim3(1), dim3(1024), 0, s, X, v, t, B, H, D, seed, action);
+  hipLaunchKernelGGL(euler_release_kernel, dim3(1), dim3(1024), 0, s, X, v, t, B, H, D, seed, action, state, mask);
   return hipGetLastError();
 }
 

@@ -159,16 +159,26 @@ hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D,
 // Analytic velocity fields (logical order): OT v = (x - a*)/tau, LINEAR v = lambda x, with
 // tau = tau_i = (i+1)/H of the ring (rotated by t), or tau_all for every slot of a chunk
 // (t = NULL: X in logical order).
+// With state (relative actions, [B, D] with mask [D] of 0/1), the OT field's absolute target
+// a* is aimed at as a* - mask * state.
 hipError_t launch_analytic_velocity(int kind, const float* X, const int64_t* t, int B, int H, int D,
-                                    const float* param, float tau_all, float* v, hipStream_t s);
+                                    const float* param, float tau_all, const float* state, const float* mask,
+                                    float* v, hipStream_t s);
+
+// Relative actions: X[e, (t+i) mod H, :] += (1 - tau_i) mask * (s_prev[e] - state[e]) unless
+// has_prev[e] is 0 (the env's first step), then s_prev[e] = state[e], has_prev[e] = 1.
+hipError_t launch_relative_shift(float* X, const int64_t* t, int B, int H, int D, const float* mask,
+                                 const float* state, float* s_prev, int* has_prev, hipStream_t s);
 
 // Euler step of a full-horizon chunk: X[e, i, :] -= dt * v[e*H + i, :].
 hipError_t launch_euler_chunk(float* X, const float* v, int B, int H, int D, float dt, hipStream_t s);
 
-// Euler update of every slot, release of logical slot 0 into action[e,:], Philox
+// Euler update of every slot, release of logical slot 0 into action[e,:] (plus mask * state[e]
+// when state is given: relative dimensions released in absolute coordinates), Philox
 // noise for action index r = t + H into the released physical slot, t += 1.
 hipError_t launch_euler_release(float* X, const float* v, int64_t* t, int B, int H, int D,
-                                uint64_t seed, float* action, unsigned* ticket, hipStream_t s);
+                                uint64_t seed, float* action, unsigned* ticket, const float* state,
+                                const float* mask, hipStream_t s);
 
 // Fill X[e, r mod H, :] with the Philox noise of action r, for r = 0..H-1.
 hipError_t launch_ring_init(float* X, int B, int H, int D, uint64_t seed, hipStream_t s);

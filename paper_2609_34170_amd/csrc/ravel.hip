@@ -291,6 +291,7 @@ struct PendingCtx {
 
 struct GraphEntry {
   const void* fop;
+  const float* state;
   float* action;
   hipGraph_t graph;
   hipGraphExec_t exec;
@@ -373,6 +374,12 @@ struct ravel_buffer {
   std::vector<GraphEntry> graphs;
   std::map<int, float*> full_tables;  // flow-time conditioning per full-horizon step count
   float* trainX = nullptr;  // [B, H, D] training buffer of ravel_train_loss
+  // relative actions: mask [D] (1 = relative dimension), state the buffer was last
+  // expressed against [B, D], whether an env has one [B]
+  bool relative = false;
+  float* rel_mask = nullptr;
+  float* s_prev = nullptr;
+  int* has_prev = nullptr;
 };
 
 namespace {
@@ -691,10 +698,16 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
   return RAVEL_OK;
 }
 
-ravel_status enqueue_step(ravel_buffer* b, const void* fop, float* action, hipStream_t s, KernelRecorder* rec) {
+ravel_status enqueue_step(ravel_buffer* b, const void* fop, const float* state, float* action, hipStream_t s,
+                          KernelRecorder* rec) {
   ravel_model* m = b->m;
   const ravel_config& c = m->cfg;
   const int B = b->B, H = c.horizon, D = c.action_dim;
+  if (state) {
+    REC_BEGIN("relative_shift", (double)B * H * D * 8 + (double)B * D * 8, (double)B * H * D * 3);
+    HIP_TRY(launch_relative_shift(b->X, b->t, B, H, D, b->rel_mask, state, b->s_prev, b->has_prev, s));
+    REC_END();
+  }
   if (c.model_kind == RAVEL_TRANSFORMER) {
     if (m->bf16)
       RV_TRY(enqueue_transformer<bf16_t>(b, fop, s, rec, PassIn{}));
@@ -702,11 +715,12 @@ ravel_status enqueue_step(ravel_buffer* b, const void* fop, float* action, hipSt
       RV_TRY(enqueue_transformer<float>(b, fop, s, rec, PassIn{}));
   } else {
     REC_BEGIN("analytic_velocity", (double)B * H * D * 8, (double)B * H * D * 2);
-    HIP_TRY(launch_analytic_velocity(c.model_kind, b->X, b->t, B, H, D, m->analytic, 0.f, b->v, s));
+    HIP_TRY(launch_analytic_velocity(c.model_kind, b->X, b->t, B, H, D, m->analytic, 0.f, state, b->rel_mask, b->v,
+                                     s));
     REC_END();
   }
   REC_BEGIN("euler_release", (double)B * H * D * 12 + (double)B * D * 4, (double)B * H * D * 2);
-  HIP_TRY(launch_euler_release(b->X, b->v, b->t, B, H, D, b->seed, action, b->ticket, s));
+  HIP_TRY(launch_euler_release(b->X, b->v, b->t, B, H, D, b->seed, action, b->ticket, state, b->rel_mask, s));
   REC_END();
   return RAVEL_OK;
 }
@@ -1095,13 +1109,18 @@ ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream
   return RAVEL_OK;
 }
 
-ravel_status enqueue_persistent_step(ravel_buffer* b, const void* fop, float* action, hipStream_t s,
-                                     KernelRecorder* rec) {
-  RV_TRY(enqueue_persistent_pass(b, fop, s, rec, PassIn{}));
+ravel_status enqueue_persistent_step(ravel_buffer* b, const void* fop, const float* state, float* action,
+                                     hipStream_t s, KernelRecorder* rec) {
   const ravel_config& c = b->m->cfg;
   const int B = b->B, H = c.horizon, D = c.action_dim;
+  if (state) {
+    REC_BEGIN("relative_shift", (double)B * H * D * 8 + (double)B * D * 8, (double)B * H * D * 3);
+    HIP_TRY(launch_relative_shift(b->X, b->t, B, H, D, b->rel_mask, state, b->s_prev, b->has_prev, s));
+    REC_END();
+  }
+  RV_TRY(enqueue_persistent_pass(b, fop, s, rec, PassIn{}));
   REC_BEGIN("euler_release", (double)B * H * D * 12 + (double)B * D * 4, (double)B * H * D * 2);
-  HIP_TRY(launch_euler_release(b->X, b->v, b->t, B, H, D, b->seed, action, b->ticket, s));
+  HIP_TRY(launch_euler_release(b->X, b->v, b->t, B, H, D, b->seed, action, b->ticket, state, b->rel_mask, s));
   REC_END();
   return RAVEL_OK;
 }
@@ -1440,6 +1459,9 @@ ravel_status ravel_buffer_create(ravel_model* m, int32_t batch, uint64_t seed, r
   ar.want((void**)&b->ticket, 4);
   ar.want((void**)&b->v, (size_t)BH * D * 4);
   ar.want((void**)&b->trainX, (size_t)BH * D * 4);
+  ar.want((void**)&b->rel_mask, (size_t)D * 4);
+  ar.want((void**)&b->s_prev, (size_t)B * D * 4);
+  ar.want((void**)&b->has_prev, (size_t)B * 4);
   ar.want((void**)&b->dbg_flag, 4);
   size_t part_elems = 0, cnt = 1;
   if (c.model_kind == RAVEL_TRANSFORMER) {
@@ -1673,7 +1695,7 @@ ravel_status ravel_full_denoise(ravel_buffer* b, int32_t steps, const void* fop,
         RV_TRY(enqueue_transformer<float>(b, fop, s, nullptr, pin));
     } else {
       HIP_TRY(launch_analytic_velocity(c.model_kind, chunk, nullptr, B, H, D, m->analytic,
-                                       (float)(steps - k) / (float)steps, b->v, s));
+                                       (float)(steps - k) / (float)steps, nullptr, nullptr, b->v, s));
     }
     HIP_TRY(launch_euler_chunk(chunk, b->v, B, H, D, dt, s));
   }
@@ -1709,15 +1731,18 @@ ravel_status ravel_train_loss(ravel_buffer* b, const float* target, const float*
     else
       RV_TRY(enqueue_transformer<float>(b, fop, s, nullptr, pin));
   } else {
-    HIP_TRY(launch_analytic_velocity(c.model_kind, b->trainX, nullptr, B, H, D, m->analytic, 0.f, b->v, s));
+    HIP_TRY(launch_analytic_velocity(c.model_kind, b->trainX, nullptr, B, H, D, m->analytic, 0.f, nullptr, nullptr,
+                                     b->v, s));
   }
   HIP_TRY(launch_train_loss(b->v, target, noise, B, H, D, loss, s));
   if (v_out) HIP_TRY(hipMemcpyAsync(v_out, b->v, (size_t)B * H * D * 4, hipMemcpyDeviceToDevice, s));
   return RAVEL_OK;
 }
 
-ravel_status ravel_step(ravel_buffer* b, const void* fop, float* action, void* stream) {
+static ravel_status step_impl(ravel_buffer* b, const void* fop, const float* state, float* action, void* stream) {
   if (!b || !action) return fail(RAVEL_E_INVALID, "null argument");
+  if (b->relative && !state) return fail(RAVEL_E_STATE, "relative actions: use ravel_step_state with the robot state");
+  if (!b->relative && state) return fail(RAVEL_E_STATE, "no relative dimensions set (ravel_set_relative_dims)");
   ravel_model* m = b->m;
   const ravel_config& c = m->cfg;
   if (c.model_kind == RAVEL_TRANSFORMER && m->n_ad > 0 && !fop)
@@ -1731,15 +1756,15 @@ ravel_status ravel_step(ravel_buffer* b, const void* fop, float* action, void* s
       if (!b->has_ctx[e]) return fail(RAVEL_E_STATE, "env " + std::to_string(e) + " has no context yet");
   }
   if (b->persistent) {
-    RV_TRY(enqueue_persistent_step(b, fop, action, s, nullptr));
+    RV_TRY(enqueue_persistent_step(b, fop, state, action, s, nullptr));
   } else if (b->use_graph) {
     GraphEntry* ge = nullptr;
     for (auto& g : b->graphs)
-      if (g.fop == fop && g.action == action) ge = &g;
+      if (g.fop == fop && g.state == state && g.action == action) ge = &g;
     if (!ge) {
-      GraphEntry g{fop, action, nullptr, nullptr};
+      GraphEntry g{fop, state, action, nullptr, nullptr};
       HIP_TRY(hipStreamBeginCapture(b->cap_stream, hipStreamCaptureModeRelaxed));
-      ravel_status st = enqueue_step(b, fop, action, b->cap_stream, nullptr);
+      ravel_status st = enqueue_step(b, fop, state, action, b->cap_stream, nullptr);
       hipGraph_t graph = nullptr;
       hipError_t he = hipStreamEndCapture(b->cap_stream, &graph);
       if (st != RAVEL_OK) return st;
@@ -1751,7 +1776,7 @@ ravel_status ravel_step(ravel_buffer* b, const void* fop, float* action, void* s
     }
     HIP_TRY(hipGraphLaunch(ge->exec, s));
   } else {
-    RV_TRY(enqueue_step(b, fop, action, s, nullptr));
+    RV_TRY(enqueue_step(b, fop, state, action, s, nullptr));
   }
   b->t_host += 1;
   if (b->debug) {
@@ -1763,6 +1788,33 @@ ravel_status ravel_step(ravel_buffer* b, const void* fop, float* action, void* s
     HIP_TRY(hipMemcpy(&flag, b->dbg_flag, 4, hipMemcpyDeviceToHost));
     if (flag) return fail(RAVEL_E_STATE, "non-finite values after step " + std::to_string(b->t_host - 1));
   }
+  return RAVEL_OK;
+}
+
+ravel_status ravel_step(ravel_buffer* b, const void* fop, float* action, void* stream) {
+  return step_impl(b, fop, nullptr, action, stream);
+}
+
+ravel_status ravel_step_state(ravel_buffer* b, const void* fop, const float* state, float* action, void* stream) {
+  if (!state) return fail(RAVEL_E_INVALID, "null state");
+  return step_impl(b, fop, state, action, stream);
+}
+
+ravel_status ravel_set_relative_dims(ravel_buffer* b, const int32_t* mask) {
+  if (!b) return fail(RAVEL_E_INVALID, "null buffer");
+  std::lock_guard<std::mutex> lk(b->mu);
+  if (b->t_host != 0) return fail(RAVEL_E_STATE, "relative dimensions must be set before the first step");
+  const int D = b->m->cfg.action_dim;
+  std::vector<float> mk(D, 0.f);
+  bool any = false;
+  for (int d = 0; mask && d < D; ++d) {
+    mk[d] = mask[d] ? 1.f : 0.f;
+    any = any || mask[d];
+  }
+  HIP_TRY(hipMemcpy(b->rel_mask, mk.data(), (size_t)D * 4, hipMemcpyHostToDevice));
+  HIP_TRY(hipMemset(b->has_prev, 0, (size_t)b->B * 4));
+  HIP_TRY(hipMemset(b->s_prev, 0, (size_t)b->B * D * 4));
+  b->relative = any;
   return RAVEL_OK;
 }
 
@@ -1849,6 +1901,7 @@ struct BlobHeader {
   int32_t B, H, D, L, P, kvd, dtype, kind;
   uint64_t seed;
   int64_t t;
+  int32_t relative, pad;  // relative actions: mask [D], s_prev [B, D], has_prev [B] follow the contexts
 };
 const uint64_t kMagic = 0x5241564C53544154ull;  // "RAVLSTAT"
 }  // namespace
@@ -1858,7 +1911,8 @@ ravel_status ravel_buffer_save(ravel_buffer* b, void* blob, size_t* n) {
   const ravel_config& c = b->m->cfg;
   const size_t xs = (size_t)b->B * c.horizon * c.action_dim * 4;
   const size_t cs = b->ctx_elems * b->m->elt;
-  const size_t need = sizeof(BlobHeader) + (size_t)b->B * (8 + 4 + 4) + xs + (size_t)b->B * 2 * cs;
+  const size_t rs = b->relative ? (size_t)c.action_dim * 4 + (size_t)b->B * c.action_dim * 4 + (size_t)b->B * 4 : 0;
+  const size_t need = sizeof(BlobHeader) + (size_t)b->B * (8 + 4 + 4) + xs + (size_t)b->B * 2 * cs + rs;
   if (!blob) {
     *n = need;
     return RAVEL_OK;
@@ -1868,7 +1922,7 @@ ravel_status ravel_buffer_save(ravel_buffer* b, void* blob, size_t* n) {
   HIP_TRY(hipDeviceSynchronize());
   char* p = (char*)blob;
   BlobHeader h{kMagic, b->B, c.horizon, c.action_dim, c.layers, c.prefix_len,
-               c.n_kv_heads * c.head_dim, c.dtype, c.model_kind, b->seed, 0};
+               c.n_kv_heads * c.head_dim, c.dtype, c.model_kind, b->seed, 0, b->relative ? 1 : 0, 0};
   HIP_TRY(hipMemcpy(&h.t, b->t, 8, hipMemcpyDeviceToHost));
   memcpy(p, &h, sizeof h);
   p += sizeof h;
@@ -1889,6 +1943,12 @@ ravel_status ravel_buffer_save(ravel_buffer* b, void* blob, size_t* n) {
     }
     p += 2 * cs;
   }
+  if (b->relative) {
+    const size_t D = c.action_dim;
+    HIP_TRY(hipMemcpy(p, b->rel_mask, D * 4, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(p + D * 4, b->s_prev, (size_t)b->B * D * 4, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(p + D * 4 + (size_t)b->B * D * 4, b->has_prev, (size_t)b->B * 4, hipMemcpyDeviceToHost));
+  }
   *n = need;
   return RAVEL_OK;
 }
@@ -1898,10 +1958,12 @@ ravel_status ravel_buffer_load(ravel_buffer* b, const void* blob, size_t n) {
   const ravel_config& c = b->m->cfg;
   const size_t xs = (size_t)b->B * c.horizon * c.action_dim * 4;
   const size_t cs = b->ctx_elems * b->m->elt;
-  const size_t need = sizeof(BlobHeader) + (size_t)b->B * (8 + 4 + 4) + xs + (size_t)b->B * 2 * cs;
-  if (n < need) return fail(RAVEL_E_INVALID, "blob too small");
+  if (n < sizeof(BlobHeader)) return fail(RAVEL_E_INVALID, "blob too small");
   BlobHeader h;
   memcpy(&h, blob, sizeof h);
+  const size_t rs = h.relative ? (size_t)c.action_dim * 4 + (size_t)b->B * c.action_dim * 4 + (size_t)b->B * 4 : 0;
+  const size_t need = sizeof(BlobHeader) + (size_t)b->B * (8 + 4 + 4) + xs + (size_t)b->B * 2 * cs + rs;
+  if (n < need) return fail(RAVEL_E_INVALID, "blob too small");
   if (h.magic != kMagic || h.B != b->B || h.H != c.horizon || h.D != c.action_dim || h.L != c.layers ||
       h.P != c.prefix_len || h.kvd != c.n_kv_heads * c.head_dim || h.dtype != c.dtype || h.kind != c.model_kind)
     return fail(RAVEL_E_SHAPE, "checkpoint does not match this model/batch");
@@ -1932,6 +1994,13 @@ ravel_status ravel_buffer_load(ravel_buffer* b, const void* blob, size_t n) {
     }
     p += 2 * cs;
   }
+  b->relative = h.relative != 0;
+  if (b->relative) {
+    const size_t D = c.action_dim;
+    HIP_TRY(hipMemcpy(b->rel_mask, p, D * 4, hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(b->s_prev, p + D * 4, (size_t)b->B * D * 4, hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(b->has_prev, p + D * 4 + (size_t)b->B * D * 4, (size_t)b->B * 4, hipMemcpyHostToDevice));
+  }
   // graphs bake in the seed as a kernel argument: rebuild them
   for (auto& g : b->graphs) {
     (void)hipGraphExecDestroy(g.exec);
@@ -1952,10 +2021,11 @@ ravel_status ravel_profile_step(ravel_buffer* b, const void* fop, float* action,
     for (int e = 0; e < b->B; ++e)
       if (!b->has_ctx[e]) return fail(RAVEL_E_STATE, "env " + std::to_string(e) + " has no context yet");
   }
+  if (b->relative) return fail(RAVEL_E_STATE, "profiling covers absolute actions only");
   KernelRecorder rec;
   rec.stream = s;
-  ravel_status st = b->persistent ? enqueue_persistent_step(b, fop, action, s, &rec)
-                                  : enqueue_step(b, fop, action, s, &rec);
+  ravel_status st = b->persistent ? enqueue_persistent_step(b, fop, nullptr, action, s, &rec)
+                                  : enqueue_step(b, fop, nullptr, action, s, &rec);
   b->t_host += 1;
   hipError_t he = hipStreamSynchronize(s);
   const int32_t cap = *n;

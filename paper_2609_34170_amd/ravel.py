@@ -50,8 +50,8 @@ class KernelRecord(ctypes.Structure):
 SYMBOLS = [
     "ravel_create", "ravel_destroy", "ravel_model_weight_bytes", "ravel_buffer_create",
     "ravel_buffer_destroy", "ravel_buffer_set_option", "ravel_context_acquire", "ravel_set_context",
-    "ravel_step", "ravel_full_denoise", "ravel_train_loss", "ravel_fop_encode", "ravel_buffer_sync",
-    "ravel_debug_state",
+    "ravel_step", "ravel_step_state", "ravel_set_relative_dims", "ravel_full_denoise", "ravel_train_loss",
+    "ravel_fop_encode", "ravel_buffer_sync", "ravel_debug_state",
     "ravel_publish_log",
     "ravel_buffer_save", "ravel_buffer_load", "ravel_profile_step", "ravel_last_error",
 ]
@@ -79,6 +79,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "ravel_step": ([vp, vp, vp, vp], i32),
         "ravel_full_denoise": ([vp, i32, vp, vp, vp, vp], i32),
         "ravel_train_loss": ([vp, vp, vp, vp, vp, vp, vp, vp], i32),
+        "ravel_set_relative_dims": ([vp, vp], i32),
+        "ravel_step_state": ([vp, vp, vp, vp, vp], i32),
         "ravel_fop_encode": ([vp, vp, vp, vp], i32),
         "ravel_buffer_sync": ([vp], i32),
         "ravel_debug_state": ([vp, vp, vp, vp], i32),
@@ -203,6 +205,17 @@ class Buffer:
     # -- hot path ----------------------------------------------------------
     def step(self, fop_tokens, action_out, stream=None):
         _check(load_library().ravel_step(self.h, _ptr(fop_tokens), _ptr(action_out), _stream(stream)))
+
+    def set_relative_dims(self, mask):
+        m = None
+        if mask is not None:
+            m = np.ascontiguousarray(np.asarray(mask, dtype=np.int32))
+            self._mask = m
+        _check(load_library().ravel_set_relative_dims(self.h, None if m is None else m.ctypes.data))
+
+    def step_state(self, fop_tokens, state, action_out, stream=None):
+        _check(load_library().ravel_step_state(self.h, _ptr(fop_tokens), _ptr(state), _ptr(action_out),
+                                               _stream(stream)))
 
     def full_denoise(self, steps: int, fop_tokens, noise, chunk_out, stream=None):
         _check(load_library().ravel_full_denoise(self.h, int(steps), _ptr(fop_tokens), _ptr(noise), _ptr(chunk_out),
