@@ -181,6 +181,9 @@ class Workload:
         k, v = self.ctx[0]
         for e in range(self.B):
             self.buf.set_context(e, k[e], v[e], 0)
+        # the initial contexts are in place before the first step (their copies are
+        # asynchronous, and a step publishes only copies that have completed)
+        self.buf.sync()
         self.t = 0
         self.gen = [0] * self.B
         log(f"[{name}] ready in {time.time() - t0:.1f}s")
@@ -272,6 +275,7 @@ class Workload:
         k, v = self.ctx[0]
         for e in range(self.B):
             buf.set_context(e, k[e], v[e], 0)
+        buf.sync()
         g = torch.Generator(device="cuda").manual_seed(2)
         walk = torch.cumsum(0.05 * torch.randn((steps + warmup, self.B, s.action_dim), dtype=torch.float32,
                                                device="cuda", generator=g), dim=0).contiguous()

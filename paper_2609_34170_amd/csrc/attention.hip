@@ -284,8 +284,9 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 // (env, KV head) and streams all keys once, so each K/V tile is staged in LDS
 // once for every query head of the group.  With 8 waves two share each SIMD:
 // one wave's MFMAs run while the other does its softmax or waits on LDS.  K/V
-// tiles are double-buffered in LDS (one barrier per tile) and the next tile's
-// global loads are in flight during the current tile's MFMAs.  V is written
+// tiles are double-buffered in LDS (one barrier per tile); their global loads
+// are issued two tiles ahead into registers, so about two tiles of MFMA time
+// cover each load's latency.  V is written
 // transposed with 8 keys x 4-lane groups per row so that the stores (row stride
 // 18 dwords) and the MFMA operand reads are free of bank conflicts.
 //
@@ -352,15 +353,21 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
   constexpr int KCHUNKS = TK * (HD / 8), VITEMS = (TK / 4) * (HD / 8);
   constexpr int KCH = (KCHUNKS + NT - 1) / NT;
   constexpr int VIT = (VITEMS + NT - 1) / NT;
-  u32x4_t kreg[KCH];
-  u32x4_t vreg[VIT][4];
-  auto load_tile = [&](int k0) {
+  // Two register sets: tile j is fetched into set j % 2 two tiles ahead of its
+  // MFMAs and written to LDS one tile ahead, so each load has about two tiles
+  // of MFMA time to arrive.
+  struct Stage {
+    u32x4_t k[KCH];
+    u32x4_t v[VIT][4];
+  };
+  Stage st0, st1;
+  auto load_tile = [&](int k0, Stage& sg) {
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
       const int c = tid + i * NT;
       if (KCHUNKS % NT == 0 || c < KCHUNKS) {
         const int kidx = min(k0 + c / (HD / 8), nkeys - 1);
-        kreg[i] = *(const u32x4_t*)(key_base(a, pk, sk, e, kidx, g, HD) + (c % (HD / 8)) * 8);
+        sg.k[i] = *(const u32x4_t*)(key_base(a, pk, sk, e, kidx, g, HD) + (c % (HD / 8)) * 8);
       }
     }
 #pragma unroll
@@ -371,16 +378,16 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int kidx = min(k0 + kq * 4 + i, nkeys - 1);
-          vreg[it][i] = *(const u32x4_t*)(key_base(a, pv, sv, e, kidx, g, HD) + dc);
+          sg.v[it][i] = *(const u32x4_t*)(key_base(a, pv, sv, e, kidx, g, HD) + dc);
         }
       }
     }
   };
-  auto store_tile = [&](int buf) {
+  auto store_tile = [&](int buf, const Stage& sg) {
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
       const int c = tid + i * NT;
-      if (KCHUNKS % NT == 0 || c < KCHUNKS) *(u32x4_t*)&Ks[buf][c / (HD / 8)][(c % (HD / 8)) * 8] = kreg[i];
+      if (KCHUNKS % NT == 0 || c < KCHUNKS) *(u32x4_t*)&Ks[buf][c / (HD / 8)][(c % (HD / 8)) * 8] = sg.k[i];
     }
 #pragma unroll
     for (int it = 0; it < VIT; ++it) {
@@ -389,8 +396,8 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
         const int kq = c % (TK / 4), dc = (c / (TK / 4)) * 8;
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
-          const uint32_t a0 = vreg[it][0][m], a1 = vreg[it][1][m];
-          const uint32_t a2 = vreg[it][2][m], a3 = vreg[it][3][m];
+          const uint32_t a0 = sg.v[it][0][m], a1 = sg.v[it][1][m];
+          const uint32_t a2 = sg.v[it][2][m], a3 = sg.v[it][3][m];
           u32x2_t lo, hi;  // dims dc+2m (low halves) and dc+2m+1 (high halves)
           lo[0] = (a0 & 0xFFFFu) | (a1 << 16);
           lo[1] = (a2 & 0xFFFFu) | (a3 << 16);
@@ -404,12 +411,15 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
   };
 
   const int ntile = (nkeys + TK - 1) / TK;
-  load_tile(0);
-  store_tile(0);
+  load_tile(0, st0);
+  if (1 < ntile) load_tile(TK, st1);
+  store_tile(0, st0);
   __syncthreads();
-  for (int t = 0; t < ntile; ++t) {
+  // tile t: fetch tile t + 2 into the set tile t came from, MFMAs on LDS buffer
+  // t & 1, write tile t + 1 (the other set) into the other buffer
+  auto tile_step = [&](int t, Stage& s_next2, const Stage& s_next1) {
     const int k0 = t * TK, buf = t & 1;
-    if (t + 1 < ntile) load_tile(k0 + TK);
+    if (t + 2 < ntile) load_tile(k0 + 2 * TK, s_next2);
     // S^T[key][row] for two 16-key sub-tiles, each summed in two independent
     // MFMA chains (even / odd k-steps)
     f32x4_t sa0 = {0.f, 0.f, 0.f, 0.f}, sa1 = sa0, sb0 = sa0, sb1 = sa0;
@@ -425,15 +435,6 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
         sb0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k2f, qf[ks + 1], sb0, 0, 0, 0);
         sb1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k3f, qf[ks + 1], sb1, 0, 0, 0);
       }
-    }
-    // the V^T operands of the whole tile, read ahead of the softmax
-    u32x4_t vv[DT];
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const bf16_t* vrow = &Vt[buf][dt * 16 + l16][0];
-      const u32x2_t lo = *(const u32x2_t*)(vrow + grp * 4);
-      const u32x2_t hi = *(const u32x2_t*)(vrow + 16 + grp * 4);
-      vv[dt] = u32x4_t{lo[0], lo[1], hi[0], hi[1]};
     }
     float x[8];
 #pragma unroll
@@ -477,11 +478,21 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
     const u32x4_t pw = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
                         pack_bf16x2(p[6], p[7])};
     const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pw);
+    // V^T operands read per 16-dim block (the MFMA chain covers the LDS latency)
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-      o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vv[dt]), pf, o[dt], 0, 0, 0);
-    if (t + 1 < ntile) store_tile(buf ^ 1);
+    for (int dt = 0; dt < DT; ++dt) {
+      const bf16_t* vrow = &Vt[buf][dt * 16 + l16][0];
+      const u32x2_t lo = *(const u32x2_t*)(vrow + grp * 4);
+      const u32x2_t hi = *(const u32x2_t*)(vrow + 16 + grp * 4);
+      const u32x4_t vv = {lo[0], lo[1], hi[0], hi[1]};
+      o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vv), pf, o[dt], 0, 0, 0);
+    }
+    if (t + 1 < ntile) store_tile(buf ^ 1, s_next1);
     __syncthreads();
+  };
+  for (int t = 0; t < ntile; t += 2) {
+    tile_step(t, st0, st1);
+    if (t + 1 < ntile) tile_step(t + 1, st1, st0);
   }
 
   // o[dt][r] = O^T[d = dt*16 + 4grp + r][row]

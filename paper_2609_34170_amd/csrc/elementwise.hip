@@ -62,8 +62,12 @@ RAVEL_DEV void store4<bf16_t>(bf16_t* p, float v0, float v1, float v2, float v3)
   *(u32x2_t*)p = u32x2_t{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
 }
 
-// One wavefront per row, 4 consecutive features per lane and access.
-template <typename T>
+// One wavefront per row, 4 consecutive features per lane and access.  For
+// w <= 256 * NCH the row stays in registers: the row, its modulation-row index
+// and (once that is known) its scale and shift are all requested before the
+// reduction, so a row costs two memory round trips.  NCH = 0: any width, the
+// row is read twice.
+template <typename T, int NCH>
 __global__ __launch_bounds__(256) void adarms_kernel(const float* __restrict__ x, int ldx, int M, int w,
                                                      const float* __restrict__ scale,
                                                      const float* __restrict__ shift, int ldm, int mode,
@@ -73,6 +77,38 @@ __global__ __launch_bounds__(256) void adarms_kernel(const float* __restrict__ x
   const int lane = threadIdx.x & 63;
   if (row >= M) return;
   const float* xr = x + (size_t)row * ldx;
+  T* yr = y + (size_t)row * ldy;
+  if constexpr (NCH > 0) {
+    const size_t mrow = rowmap ? (size_t)rowmap[row] : (size_t)row;
+    f32x4_t v[NCH], sc[NCH], sh[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int n = lane * 4 + c * 256;
+      v[c] = n < w ? *(const f32x4_t*)(xr + n) : f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int n = lane * 4 + c * 256;
+      const f32x4_t z = {0.f, 0.f, 0.f, 0.f};
+      sc[c] = n < w ? *(const f32x4_t*)(scale + (mode == 0 ? mrow * ldm : 0) + n) : z;
+      sh[c] = (n < w && mode == 0) ? *(const f32x4_t*)(shift + mrow * ldm + n) : z;
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) ss += v[c][0] * v[c][0] + v[c][1] * v[c][1] + v[c][2] * v[c][2] + v[c][3] * v[c][3];
+    ss = wave_sum(ss);
+    const float r = 1.0f / sqrtf(ss / (float)w + eps);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int n = lane * 4 + c * 256;
+      if (n >= w) continue;
+      float o[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[i] = v[c][i] * r * (1.0f + sc[c][i]) + sh[c][i];
+      store4<T>(yr + n, o[0], o[1], o[2], o[3]);
+    }
+    return;
+  }
   float ss = 0.f;
   for (int n = lane * 4; n < w; n += 256) {
     const f32x4_t v = *(const f32x4_t*)(xr + n);
@@ -81,7 +117,6 @@ __global__ __launch_bounds__(256) void adarms_kernel(const float* __restrict__ x
   ss = wave_sum(ss);
   const float r = 1.0f / sqrtf(ss / (float)w + eps);
   const size_t mrow = rowmap ? (size_t)rowmap[row] : (size_t)row;
-  T* yr = y + (size_t)row * ldy;
   for (int n = lane * 4; n < w; n += 256) {
     const f32x4_t v = *(const f32x4_t*)(xr + n);
     float o[4];
@@ -106,8 +141,17 @@ hipError_t launch_adarms(const float* x, int ldx, int M, int w, const float* sca
   if (w % 4 || ldx % 4 || ldy % 4 || (mode == 0 && ldm % 4) || ((uintptr_t)x | (uintptr_t)scale) % 16 ||
       (mode == 0 && (uintptr_t)shift % 16) || (uintptr_t)y % (4 * sizeof(T)))
     return hipErrorInvalidValue;
-  hipLaunchKernelGGL(adarms_kernel<T>, dim3((M + 3) / 4), dim3(256), 0, s, x, ldx, M, w, scale, shift,
-                     ldm, mode, rowmap, eps, y, ldy);
+  const dim3 grid((M + 3) / 4), block(256);
+  if (w <= 256)
+    hipLaunchKernelGGL((adarms_kernel<T, 1>), grid, block, 0, s, x, ldx, M, w, scale, shift, ldm, mode, rowmap, eps, y, ldy);
+  else if (w <= 512)
+    hipLaunchKernelGGL((adarms_kernel<T, 2>), grid, block, 0, s, x, ldx, M, w, scale, shift, ldm, mode, rowmap, eps, y, ldy);
+  else if (w <= 1024)
+    hipLaunchKernelGGL((adarms_kernel<T, 4>), grid, block, 0, s, x, ldx, M, w, scale, shift, ldm, mode, rowmap, eps, y, ldy);
+  else if (w <= 2048)
+    hipLaunchKernelGGL((adarms_kernel<T, 8>), grid, block, 0, s, x, ldx, M, w, scale, shift, ldm, mode, rowmap, eps, y, ldy);
+  else
+    hipLaunchKernelGGL((adarms_kernel<T, 0>), grid, block, 0, s, x, ldx, M, w, scale, shift, ldm, mode, rowmap, eps, y, ldy);
   return hipGetLastError();
 }
 template hipError_t launch_adarms<float>(const float*, int, int, int, const float*, const float*, int, int,
@@ -244,43 +288,65 @@ hipError_t launch_transpose_f32(const float* src, int R, int C, float* dst, hipS
 }
 
 // Block = 4 waves over 256 consecutive columns (one 64-column tile per wave) and
-// kInProjRows rows.  The weights are read transposed (w_inT[d, n]: consecutive
-// lanes, consecutive addresses); the ring row of each slot is wave-uniform.
-constexpr int kInProjRows = 1;
+// rpb <= kInProjRows rows.  The weights are read transposed (w_inT[d, n]:
+// consecutive lanes, consecutive addresses) once per block and kept in registers
+// for all of its rows; the rows' ring entries are staged in LDS 16 features at a
+// time, so a block costs one round of loads per 16 features whatever its row
+// count.  Every output is bias + sum over d in increasing order.
+constexpr int kInProjRows = 16;
 __global__ __launch_bounds__(256) void in_proj_kernel(const float* __restrict__ X, const int64_t* t, int B, int H, int D,
                                                       const float* __restrict__ w_inT, const float* __restrict__ b_in,
-                                                      int w, float* __restrict__ x, InProjNorm nrm) {
-  const int n = blockIdx.x * 256 + threadIdx.x;
-  const int lane = threadIdx.x & 63;
+                                                      int w, float* __restrict__ x, InProjNorm nrm, int rpb) {
+  __shared__ float xs[kInProjRows][16];
+  const int tid = threadIdx.x;
+  const int n = blockIdx.x * 256 + tid;
+  const int lane = tid & 63;
   const int BH = B * H;
-  const int64_t tt = t ? *t : 0;  // no step counter: X is a chunk in logical order
+  const int h0 = t ? (int)(*t % H) : 0;  // no step counter: X is a chunk in logical order
+  const int row0 = blockIdx.y * rpb;
+  const int nrows = min(rpb, BH - row0);
+  // the first norm's scales of this thread's column, requested up front
+  float scv[kInProjRows];
+#pragma unroll
+  for (int rr = 0; rr < kInProjRows; ++rr)
+    scv[rr] = (nrm.p && rr < nrows && n < w) ? nrm.scale[(size_t)(row0 + rr) * nrm.ldm + n] : 0.f;
+  // thread (sr, sj) stages feature d0 + sj of row row0 + sr
+  const int sr = tid >> 4, sj = tid & 15;
+  const float* srow = nullptr;
+  if (sr < nrows) {
+    const int row = row0 + sr, e = row / H, i = row % H;
+    const int ph = h0 + i < H ? h0 + i : h0 + i - H;
+    srow = X + ((size_t)e * H + ph) * D;
+  }
+  float acc[kInProjRows];
   const float bias = n < w ? b_in[n] : 0.f;
-  for (int rr = 0; rr < kInProjRows; ++rr) {
-    const int row = blockIdx.y * kInProjRows + rr;
-    if (row >= BH) break;
-    const int e = row / H, i = row % H;
-    const int ph = t ? (int)((tt + i) % H) : i;
-    const float* a = X + ((size_t)e * H + ph) * D;
-    float acc = bias;
-    // 16 weights and inputs per batch of loads, then their products (a loop with one
-    // multiply-add per load would wait for every load in turn)
-    for (int d0 = 0; d0 < D; d0 += 16) {
-      float wv[16], av[16];
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const bool ok = n < w && d0 + j < D;
-        wv[j] = ok ? w_inT[(size_t)(d0 + j) * w + n] : 0.f;
-        av[j] = d0 + j < D ? a[d0 + j] : 0.f;
+  for (int rr = 0; rr < kInProjRows; ++rr) acc[rr] = bias;
+  for (int d0 = 0; d0 < D; d0 += 16) {
+    float wv[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) wv[j] = (n < w && d0 + j < D) ? w_inT[(size_t)(d0 + j) * w + n] : 0.f;
+    const float xv = (srow && d0 + sj < D) ? srow[d0 + sj] : 0.f;
+    __syncthreads();  // the previous chunk's reads are done
+    xs[sr][sj] = xv;
+    __syncthreads();
+#pragma unroll
+    for (int rr = 0; rr < kInProjRows; ++rr)
+      if (rr < nrows) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) acc[rr] += wv[j] * xs[rr][j];
       }
+  }
 #pragma unroll
-      for (int j = 0; j < 16; ++j) acc += wv[j] * av[j];
-    }
-    if (n < w) x[(size_t)row * w + n] = acc;
+  for (int rr = 0; rr < kInProjRows; ++rr) {
+    if (rr >= nrows) break;
+    const int row = row0 + rr;
+    if (n < w) x[(size_t)row * w + n] = acc[rr];
     if (!nrm.p) continue;
     // first adaptive norm of the persistent step: p = bf16((1 + scale) x), the
     // 64-column tile's sum of squares of the row, and the bf16 shift copies
-    float v = n < w ? acc : 0.f;
-    if (n < w) nrm.p[(size_t)row * w + n] = f32_to_bf16((1.f + nrm.scale[(size_t)row * nrm.ldm + n]) * acc);
+    const float v = n < w ? acc[rr] : 0.f;
+    if (n < w) nrm.p[(size_t)row * w + n] = f32_to_bf16((1.f + scv[rr]) * v);
     const float sq = wave_sum(v * v);
     if (lane == 0 && n < w) nrm.sumsq[(size_t)(n >> 6) * 64 + row] = sq;
   }
@@ -304,8 +370,11 @@ __global__ __launch_bounds__(256) void shift_copy_kernel(int M, int w, InProjNor
 hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D, const float* w_inT,
                           const float* b_in, int w, float* x, const InProjNorm& nrm, hipStream_t s) {
   if (nrm.p && (B * H > 64 || (w % 64) != 0)) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(in_proj_kernel, dim3((w + 255) / 256, (B * H + kInProjRows - 1) / kInProjRows), dim3(256), 0, s,
-                     X, t, B, H, D, w_inT, b_in, w, x, nrm);
+  // many rows: 16 per block; few rows: one per block (more blocks, same chain per block)
+  const int BH = B * H;
+  const int rpb = BH >= 1024 ? kInProjRows : (BH >= 256 ? 4 : 1);
+  hipLaunchKernelGGL(in_proj_kernel, dim3((w + 255) / 256, (BH + rpb - 1) / rpb), dim3(256), 0, s, X, t, B, H, D,
+                     w_inT, b_in, w, x, nrm, rpb);
   if (nrm.p && nrm.cvt_chunks > 0) {
     const size_t total = (size_t)nrm.cvt_chunks * B * H * (w / 8);
     hipLaunchKernelGGL(shift_copy_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, B * H, w, nrm);
@@ -454,27 +523,44 @@ hipError_t launch_train_loss(const float* v, const float* target, const float* n
 // elements (memory-level parallel), then the released slot is copied out and
 // refilled with noise, then t advances.  A single block makes the read of t
 // and its increment ordered by block barriers alone.
-__global__ __launch_bounds__(1024) void euler_release_kernel(float* __restrict__ X, const float* __restrict__ v,
-                                                             int64_t* t, int B, int H, int D, uint64_t seed,
-                                                             float* __restrict__ action,
-                                                             const float* __restrict__ state,
-                                                             const float* __restrict__ mask) {
+// One block per env.  Every block reads the step counter at its start; the last
+// block to take the ticket (so every block has read it) re-arms the ticket and
+// advances the counter.
+__global__ __launch_bounds__(256) void euler_release_kernel(float* __restrict__ X, const float* __restrict__ v,
+                                                            int64_t* t, int H, int D, uint64_t seed,
+                                                            float* __restrict__ action,
+                                                            const float* __restrict__ state,
+                                                            const float* __restrict__ mask, unsigned* ticket) {
   const int64_t tt = *t;
   const float dt = 1.0f / (float)H;
   const int h0 = (int)(tt % H);
-  const int total = B * H * D;
-  for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
-    const int d = idx % D, i = (idx / D) % H, e = idx / (D * H);  // logical slot i
-    int ph = h0 + i;
-    if (ph >= H) ph -= H;
-    float* xp = X + ((size_t)e * H + ph) * D + d;
-    *xp = euler_sub(*xp, dt, v[idx]);
+  const int e = blockIdx.x;
+  const int n = H * D;
+  float* Xe = X + (size_t)e * H * D;
+  const float* ve = v + (size_t)e * H * D;
+  // logical slot i of element k = i * D + d sits in physical slot (h0 + i) mod H;
+  // 4 elements per thread per batch, loads first
+  for (int k0 = 0; k0 < n; k0 += 4 * 256) {
+    float xv[4], vv[4];
+    int off[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int k = k0 + u * 256 + (int)threadIdx.x;
+      const int i = k / D, d = k - i * D;
+      int ph = h0 + i;
+      if (ph >= H) ph -= H;
+      off[u] = k < n ? ph * D + d : -1;
+      xv[u] = k < n ? Xe[off[u]] : 0.f;
+      vv[u] = k < n ? ve[k] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (off[u] >= 0) Xe[off[u]] = euler_sub(xv[u], dt, vv[u]);
   }
   __syncthreads();
   const int NG = (D + 3) / 4;
-  for (int idx = threadIdx.x; idx < B * NG; idx += blockDim.x) {
-    const int e = idx / NG, c = idx % NG;
-    float* xs = X + ((size_t)e * H + h0) * D;
+  float* xs = Xe + (size_t)h0 * D;
+  for (int c = threadIdx.x; c < NG; c += blockDim.x) {
     float z[4];
     ring_noise4(seed, e, tt + H, c, z);
     for (int q = 0; q < 4; ++q) {
@@ -487,14 +573,21 @@ __global__ __launch_bounds__(1024) void euler_release_kernel(float* __restrict__
     }
   }
   __syncthreads();
-  if (threadIdx.x == 0) *t = tt + 1;
+  if (threadIdx.x == 0) {
+    const unsigned prev = atomicAdd(ticket, 1u);
+    if (prev == gridDim.x - 1) {
+      *ticket = 0u;
+      *t = tt + 1;
+    }
+  }
 }
 
 hipError_t launch_euler_release(float* X, const float* v, int64_t* t, int B, int H, int D, uint64_t seed,
                                 float* action, unsigned* ticket, const float* state, const float* mask,
                                 hipStream_t s) {
-  (void)ticket;
-  hipLaunchKernelGGL(euler_release_kernel, dim3(1), dim3(1024), 0, s, X, v, t, B, H, D, seed, action, state, mask);
+  if (!ticket) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(euler_release_kernel, dim3(B), dim3(256), 0, s, X, v, t, H, D, seed, action, state, mask,
+                     ticket);
   return hipGetLastError();
 }
 

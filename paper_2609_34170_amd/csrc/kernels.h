@@ -175,7 +175,8 @@ hipError_t launch_euler_chunk(float* X, const float* v, int B, int H, int D, flo
 
 // Euler update of every slot, release of logical slot 0 into action[e,:] (plus mask * state[e]
 // when state is given: relative dimensions released in absolute coordinates), Philox
-// noise for action index r = t + H into the released physical slot, t += 1.
+// noise for action index r = t + H into the released physical slot, t += 1.  One block per
+// env; ticket is a device word that is zero between launches (the last block re-arms it).
 hipError_t launch_euler_release(float* X, const float* v, int64_t* t, int B, int H, int D,
                                 uint64_t seed, float* action, unsigned* ticket, const float* state,
                                 const float* mask, hipStream_t s);
