@@ -287,8 +287,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 // tiles are double-buffered in LDS (one barrier per tile); their global loads
 // are issued two tiles ahead into registers, so about two tiles of MFMA time
 // cover each load's latency.  V is written
-// transposed with 8 keys x 4-lane groups per row so that the stores (row stride
-// 18 dwords) and the MFMA operand reads are free of bank conflicts.
+// transposed with 8 keys x 4-lane groups per row.
 //
 // Softmax rescaling is lazy: the running maximum m of a row only moves when a
 // tile raises it by more than kLazy (log2 units), so between moves exp2(s - m)
@@ -305,6 +304,7 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
   constexpr int KS = HD / 32;
   constexpr int DT = HD / 16;
   constexpr int KLD = HD + 8;
+  // V^T row stride 18 dwords (a stride of 20 measured slower)
   constexpr int VLD = TK + 4;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2][TK][KLD];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[2][HD][VLD];
@@ -322,7 +322,6 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
   const int l16 = lane & 15, grp = lane >> 4;
   const int G = a.nq / a.nkv;
   const int R = G * a.Hq;
-  const int nkeys = a.P + a.S;
   const int row = (chunk * NW + wave) * 16 + l16;  // this lane's row
 
   const bf16_t* q = (const bf16_t*)a.q;
@@ -361,13 +360,26 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
     u32x4_t v[VIT][4];
   };
   Stage st0, st1;
+  // Key tiles: the prefix rows padded to a multiple of TK, then the buffer's own
+  // rows, so that every tile reads one part from one uniform base.  Rows past a
+  // part's end are clamped to its last row (finite values) and masked out of
+  // the softmax.
+  const int Ppad = ((a.P + TK - 1) / TK) * TK;
+  const bf16_t* sk_e = sk + (size_t)e * a.S * a.s_ld;
+  const bf16_t* sv_e = sv + (size_t)e * a.S * a.s_ld;
   auto load_tile = [&](int k0, Stage& sg) {
+    const bool pre = k0 < Ppad;  // uniform
+    const int r0 = pre ? k0 : k0 - Ppad;
+    const int last = (pre ? a.P : a.S) - 1;
+    const int ld = pre ? a.p_ld : a.s_ld;
+    const bf16_t* kb = (pre ? pk : sk_e) + g * HD;
+    const bf16_t* vb = (pre ? pv : sv_e) + g * HD;
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
       const int c = tid + i * NT;
       if (KCHUNKS % NT == 0 || c < KCHUNKS) {
-        const int kidx = min(k0 + c / (HD / 8), nkeys - 1);
-        sg.k[i] = *(const u32x4_t*)(key_base(a, pk, sk, e, kidx, g, HD) + (c % (HD / 8)) * 8);
+        const int r = min(r0 + c / (HD / 8), last);
+        sg.k[i] = *(const u32x4_t*)(kb + (size_t)r * ld + (c % (HD / 8)) * 8);
       }
     }
 #pragma unroll
@@ -377,8 +389,8 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
         const int kq = c % (TK / 4), dc = (c / (TK / 4)) * 8;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int kidx = min(k0 + kq * 4 + i, nkeys - 1);
-          sg.v[it][i] = *(const u32x4_t*)(key_base(a, pv, sv, e, kidx, g, HD) + dc);
+          const int r = min(r0 + kq * 4 + i, last);
+          sg.v[it][i] = *(const u32x4_t*)(vb + (size_t)r * ld + dc);
         }
       }
     }
@@ -398,11 +410,13 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
         for (int m = 0; m < 4; ++m) {
           const uint32_t a0 = sg.v[it][0][m], a1 = sg.v[it][1][m];
           const uint32_t a2 = sg.v[it][2][m], a3 = sg.v[it][3][m];
-          u32x2_t lo, hi;  // dims dc+2m (low halves) and dc+2m+1 (high halves)
-          lo[0] = (a0 & 0xFFFFu) | (a1 << 16);
-          lo[1] = (a2 & 0xFFFFu) | (a3 << 16);
-          hi[0] = (a0 >> 16) | (a1 & 0xFFFF0000u);
-          hi[1] = (a2 >> 16) | (a3 & 0xFFFF0000u);
+          // dims dc+2m (low halves of a0..a3) and dc+2m+1 (high halves), one byte
+          // permute per output word
+          u32x2_t lo, hi;
+          lo[0] = __builtin_amdgcn_perm(a1, a0, 0x05040100u);
+          lo[1] = __builtin_amdgcn_perm(a3, a2, 0x05040100u);
+          hi[0] = __builtin_amdgcn_perm(a1, a0, 0x07060302u);
+          hi[1] = __builtin_amdgcn_perm(a3, a2, 0x07060302u);
           *(u32x2_t*)&Vt[buf][dc + 2 * m][kq * 4] = lo;
           *(u32x2_t*)&Vt[buf][dc + 2 * m + 1][kq * 4] = hi;
         }
@@ -410,7 +424,7 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
     }
   };
 
-  const int ntile = (nkeys + TK - 1) / TK;
+  const int ntile = Ppad / TK + (a.S + TK - 1) / TK;
   load_tile(0, st0);
   if (1 < ntile) load_tile(TK, st1);
   store_tile(0, st0);
@@ -442,11 +456,13 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
       x[r] = (sa0[r] + sb0[r]) * sl2;
       x[4 + r] = (sa1[r] + sb1[r]) * sl2;
     }
-    if (k0 + TK > nkeys) {  // uniform: the ragged last tile
+    // valid keys of the tile (uniform): the last tile of each part is ragged
+    const int nvalid = k0 < Ppad ? a.P - k0 : a.S - (k0 - Ppad);
+    if (nvalid < TK) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        if (k0 + grp * 4 + r >= nkeys) x[r] = -INFINITY;
-        if (k0 + 16 + grp * 4 + r >= nkeys) x[4 + r] = -INFINITY;
+        if (grp * 4 + r >= nvalid) x[r] = -INFINITY;
+        if (16 + grp * 4 + r >= nvalid) x[4 + r] = -INFINITY;
       }
     }
     // The row maximum needs the 4 lane groups only when some lane of the wave
@@ -469,9 +485,11 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
         o[dt][3] *= corr;
       }
     }
+    // x - mrow <= kLazy: the hardware exp2 (no denormal range handling: results
+    // below 2^-126 flush to zero, far below the bf16 resolution of P)
     float p[8];
 #pragma unroll
-    for (int r = 0; r < 8; ++r) p[r] = exp2f(x[r] - mrow);
+    for (int r = 0; r < 8; ++r) p[r] = __builtin_amdgcn_exp2f(x[r] - mrow);
     // the row sum stays split over the 4 lane groups until the end
     lrow += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
     // P^T as the B operand: slot jj of group grp is key (jj<4 ? 4grp+jj : 16+4grp+jj-4)

@@ -39,10 +39,14 @@ template <> struct act<bf16_t> {
 
 RAVEL_DEV float silu_f(float x) { return x / (1.0f + __expf(-x)); }
 
+// gelu_tanh(x) = 0.5 x (1 + tanh(u)) with u = sqrt(2/pi) (x + 0.044715 x^3), written
+// as x / (1 + exp(-2u)) (the same function: 1 + tanh(u) = 2 / (1 + exp(-2u))) and
+// evaluated with the hardware exp2 and reciprocal, a few ulp; large |x| saturate to
+// x and to -0.
 RAVEL_DEV float gelu_tanh_f(float x) {
-  const float c = 0.7978845608028654f;  // sqrt(2/pi)
-  float u = c * (x + 0.044715f * x * x * x);
-  return 0.5f * x * (1.0f + tanhf(u));
+  const float c = -2.0f * 0.7978845608028654f * 1.4426950408889634f;  // -2 sqrt(2/pi) log2(e)
+  const float t = c * x * (1.0f + 0.044715f * x * x);
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(t));
 }
 
 // Sum across the 64 lanes of a wavefront.

@@ -519,11 +519,8 @@ hipError_t launch_train_loss(const float* v, const float* target, const float* n
   return hipGetLastError();
 }
 
-// One block: every thread first applies the Euler update to independent ring
-// elements (memory-level parallel), then the released slot is copied out and
-// refilled with noise, then t advances.  A single block makes the read of t
-// and its increment ordered by block barriers alone.
-// One block per env.  Every block reads the step counter at its start; the last
+// One block per env: its threads first apply the Euler update to independent
+// ring elements, then the released slot is copied out and refilled with noise.  Every block reads the step counter at its start; the last
 // block to take the ticket (so every block has read it) re-arms the ticket and
 // advances the counter.
 __global__ __launch_bounds__(256) void euler_release_kernel(float* __restrict__ X, const float* __restrict__ v,
