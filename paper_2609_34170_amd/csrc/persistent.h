@@ -14,6 +14,11 @@ enum PAMode : int {
   // p = bf16((1 + scale) * x) written by whoever produced the residual x, and
   // r[m] = 1 / sqrt(mean_k x[m][k]^2 + eps) from the per-64-column row sums of squares of x
   PA_NORM = 1,
+  // the FOP cross-attention output of one head, computed by the item itself from
+  // the adapter queries A = qa (bf16): the item's K range is exactly one head
+  // (hd = 256, kw = 1), the head's keys and values are rows [x_nf][x_ld] of
+  // xk / xv (x_nf <= 16) at column (head / x_group) * 256, scores scaled by x_scale
+  PA_XATTN = 2,
 };
 enum PEMode : int { PE_BF16 = 0, PE_F32 = 1, PE_GEGLU = 2, PE_RESID = 3 };
 // scale of the next norm, applied to a new residual x to form p: per (row, column)
@@ -57,6 +62,9 @@ struct PGemm {
   // 1: the ksplit blocks of a tile meet and each finishes a slice of its rows
   // (needs one item per block); 0: the last block to arrive finishes the tile
   int coop;
+  const bf16_t* xk; const bf16_t* xv;  // PA_XATTN: FOP keys and values of the adapter
+  int x_ld, x_nf, x_group;
+  float x_scale;
 };
 
 struct alignas(16) Phase {

@@ -64,8 +64,10 @@ struct PSmem {
   };
   float rscale[64];
   float rowsq[64][17];
+  bf16_t xvt[256 * 20];  // PA_XATTN: the head's FOP values transposed, [dim][key], row stride kXLD
   int flag;
 };
+constexpr int kXLD = 20;
 
 RAVEL_DEV int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
@@ -244,8 +246,34 @@ RAVEL_DEV void load_w(const PGemm& g, int item, u32x4_t (&wf)[16]) {
   }
 }
 
+// PA_XATTN weight fragments: the same rows, with the K slots of lane group grp
+// holding dims 32f + 4grp .. +3 and 32f + 16 + 4grp .. +3 of the wave's quarter --
+// the order in which the item's attention output leaves its MFMAs.
+RAVEL_DEV void load_w_xattn(const PGemm& g, int item, u32x4_t (&wf)[16]) {
+  const int tid = local_tid();
+  const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, grp = lane >> 4;
+  const int tiles = (g.N + 63) >> 6, tile = item % tiles, z = item / tiles;
+  const int n0 = tile * 64, kb = z * 256 + wave * 64;
+  const rsrc_t rw = rsrc(g.W);
+#pragma unroll
+  for (int f = 0; f < 4; ++f) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int n = n0 + c * 16 + l16;
+      const bool ok = f < 2 && n < g.N;
+      const int k = kb + f * 32 + grp * 4;
+      const auto lo = __builtin_amdgcn_raw_buffer_load_b64(rw, boff(ok && k < g.K, ((size_t)n * g.ldw + k) * 2), 0, PLAIN);
+      const auto hi =
+          __builtin_amdgcn_raw_buffer_load_b64(rw, boff(ok && k + 16 < g.K, ((size_t)n * g.ldw + k + 16) * 2), 0, PLAIN);
+      wf[c * 4 + f] = u32x4_t{lo[0], lo[1], hi[0], hi[1]};
+    }
+  }
+}
+
 RAVEL_DEV void load_weights(const PGemm& g, int item, u32x4_t (&wf)[16]) {
-  if (g.kw == 2)
+  if (g.a_mode == PA_XATTN)
+    load_w_xattn(g, item, wf);
+  else if (g.kw == 2)
     load_w<2>(g, item, wf);
   else
     load_w<1>(g, item, wf);
@@ -261,6 +289,94 @@ template <int MT>
 RAVEL_DEV CoopOps coop_operands(const PGemm& g, int tile, int z, int s0, bool use);
 template <int MT>
 RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& sm, const CoopOps& first);
+
+// PA_XATTN: the item's activation operand is head z's cross-attention output
+// o = softmax(q k^T * scale) v over the FOP tokens, computed here from the query
+// fragments af (this wave's 64 dims of the head, rows i*16 + l16).  Each wave
+// forms its partial scores S^T = K Q^T over its dims; the four partials are added
+// through LDS in wave order; each lane then holds rows l16 and keys 4grp .. +3, the
+// row softmax is reduced over the four lane groups, and P^T (bf16) feeds
+// O^T = V^T P^T (16x16x16 MFMAs, V^T staged transposed in LDS) for the wave's
+// four 16-dim tiles.  The normalised outputs become the GEMM's B fragments in
+// the K-slot order of load_w_xattn.  Templated on the KW = 1 fragment shape.
+template <int MT>
+RAVEL_DEV void xattn_operands(const PGemm& g, const bf16x8_t (&xkf)[2], const u32x4_t (&xvc)[2],
+                              bf16x8_t (&af)[MT][2], PSmem& sm) {
+  typedef __attribute__((ext_vector_type(4))) short s16x4_t;
+  const int tid = local_tid(), lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, grp = lane >> 4;
+  f32x4_t sp[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    sp[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int f = 0; f < 2; ++f) sp[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xkf[f], af[i][f], sp[i], 0, 0, 0);
+  }
+  __syncthreads();  // LDS may still be read by this block's previous item
+#pragma unroll
+  for (int i = 0; i < MT; ++i) *(f32x4_t*)&sm.red[wave][i][lane][0] = sp[i];
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int c = tid + r * 256, key = c >> 5, d0 = (c & 31) * 8;
+    const bf16_t* h = reinterpret_cast<const bf16_t*>(&xvc[r]);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sm.xvt[(d0 + j) * kXLD + key] = h[j];
+  }
+  __syncthreads();
+  const float sl2 = g.x_scale * 1.4426950408889634f;
+  s16x4_t pb[MT];
+  float inv[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    f32x4_t s = *(const f32x4_t*)&sm.red[0][i][lane][0];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) {
+      const f32x4_t t = *(const f32x4_t*)&sm.red[w][i][lane][0];
+      s[0] += t[0];
+      s[1] += t[1];
+      s[2] += t[2];
+      s[3] += t[3];
+    }
+    float x[4], mx = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      x[r] = grp * 4 + r < g.x_nf ? s[r] * sl2 : -INFINITY;
+      mx = fmaxf(mx, x[r]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    float p[4], l = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      p[r] = __builtin_amdgcn_exp2f(x[r] - mx);
+      l += p[r];
+    }
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    inv[i] = 1.f / l;
+    const u32x2_t pw = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])};
+    pb[i] = __builtin_bit_cast(s16x4_t, pw);
+  }
+#pragma unroll
+  for (int f = 0; f < 2; ++f) {
+    f32x4_t ot[2][MT];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int d = wave * 64 + (2 * f + h) * 16 + l16;
+      const s16x4_t vf = __builtin_bit_cast(s16x4_t, *(const u32x2_t*)&sm.xvt[d * kXLD + grp * 4]);
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+        ot[h][i] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vf, pb[i], f32x4_t{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const float r = inv[i];
+      const u32x4_t w = {pack_bf16x2(ot[0][i][0] * r, ot[0][i][1] * r), pack_bf16x2(ot[0][i][2] * r, ot[0][i][3] * r),
+                         pack_bf16x2(ot[1][i][0] * r, ot[1][i][1] * r), pack_bf16x2(ot[1][i][2] * r, ot[1][i][3] * r)};
+      af[i][f] = __builtin_bit_cast(bf16x8_t, w);
+    }
+  }
+}
 
 template <int MT, int KW, class AfterLoads>
 RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int* err, PSmem& sm,
@@ -298,6 +414,23 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int
       const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
       af[i][f] = ld_b8<COH>(rA, boff(m < g.M && k < g.K, ((size_t)m * g.lda + k) * 2));
     }
+  // PA_XATTN: the head's keys (this wave's 64 dims; lane: key l16) and its values
+  // (16-byte chunks c = tid, tid + 256: key c / 32, dims (c % 32) * 8), plain loads
+  const bool xattn = g.a_mode == PA_XATTN;
+  const int xoff = xattn ? (z / g.x_group) * 256 : 0;
+  bf16x8_t xkf[2];
+  u32x4_t xvc[2];
+  if (xattn) {
+    const rsrc_t rK = rsrc(g.xk), rV = rsrc(g.xv);
+#pragma unroll
+    for (int f = 0; f < 2; ++f)
+      xkf[f] = ld_b8<PLAIN>(rK, boff(l16 < g.x_nf, ((size_t)l16 * g.x_ld + xoff + wave * 64 + f * 32 + grp * 8) * 2));
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int c = tid + r * 256, key = c >> 5;
+      xvc[r] = ld16<PLAIN>(rV, boff(key < g.x_nf, ((size_t)key * g.x_ld + xoff + (c & 31) * 8) * 2));
+    }
+  }
   float sq[16];
   const int row = tid & 63, part = tid >> 6, nt = g.K >> 6;
   if (norm) {
@@ -311,6 +444,9 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int
   // a cooperative split tile's epilogue operands of this block's first slots
   const CoopOps ops = coop_operands<MT>(g, tile, z, 0, g.ksplit > 1 && g.coop);
   after_loads();
+  if constexpr (KW == 1) {
+    if (xattn) xattn_operands<MT>(g, xkf, xvc, af, sm);
+  }
 
   // The norm's operand is h = r p + shift (r = 1 / rms(x) per row), so
   // W h = r (W p + W shift / r): the shift product runs while p is in flight,

@@ -911,6 +911,8 @@ ravel_status build_persistent(ravel_buffer* b) {
     return ph;
   };
   const size_t ctx_layer = (size_t)c.prefix_len * kvd;
+  bool xattn_fused = B == 1 && hd == 256 && c.n_fop >= 1 && c.n_fop <= 16 && c.n_q_heads % c.n_kv_heads == 0;
+  if (const char* ev = getenv("RAVEL_NO_FUSED_XATTN")) xattn_fused = xattn_fused && atoi(ev) == 0;
   for (int l = 0; l < c.layers; ++l) {
     const LayerW& L = m->layers[l];
     const float* mod = b->mod + (size_t)l * 6 * w;
@@ -957,10 +959,24 @@ ravel_status build_persistent(ravel_buffer* b) {
         ph.g.ldo = qd;
         push(ph, "q_adapter");
       }
-      {
+      // one env, heads of 256 dims, at most 16 FOP tokens: the output projection's
+      // items compute their head's cross-attention themselves (no attention phase)
+      const int ld = m->n_ad * 2 * kvd;
+      Phase fused = gemm(b->qa, qd, nullptr, false, L.oa_w, w, qd, PE_RESID);
+      if (xattn_fused && fused.g.kw == 1) {
+        resid(fused, nullptr, L.alpha, NS_ROW, mod + 3 * w);
+        PGemm& g = fused.g;
+        g.a_mode = PA_XATTN;
+        g.xk = (const bf16_t*)b->kva + (size_t)L.adapter * 2 * kvd;
+        g.xv = g.xk + kvd;
+        g.x_ld = ld;
+        g.x_nf = c.n_fop;
+        g.x_group = c.n_q_heads / c.n_kv_heads;
+        g.x_scale = 1.0f / sqrtf((float)hd);
+        push(fused, "o_adapter");
+      } else {
         AttnArgs a;
         memset(&a, 0, sizeof a);
-        const int ld = m->n_ad * 2 * kvd;
         a.q = b->qa;
         a.ldq = qd;
         a.Hq = H;
@@ -973,8 +989,6 @@ ravel_status build_persistent(ravel_buffer* b) {
         a.out = b->att;
         a.ldo = qd;
         push(attn_phase(a), "cross_attn");
-      }
-      {
         Phase ph = gemm(b->att, qd, nullptr, false, L.oa_w, w, qd, PE_RESID);
         resid(ph, nullptr, L.alpha, NS_ROW, mod + 3 * w);
         push(ph, "o_adapter");
@@ -1033,6 +1047,10 @@ ravel_status build_persistent(ravel_buffer* b) {
     if (ph.type == PH_GEMM) {
       b->ph_bytes[i] = (double)ph.g.N * ph.g.K * 2;
       b->ph_flops[i] = 2.0 * ph.g.M * ph.g.N * ph.g.K;
+      if (ph.g.a_mode == PA_XATTN) {  // plus the cross-attention it computes: FOP keys and values
+        b->ph_bytes[i] += (double)B * ph.g.x_nf * kvd * 4;
+        b->ph_flops[i] += 4.0 * B * c.n_q_heads * H * ph.g.x_nf * hd;
+      }
     } else if (ph.type == PH_ATTN) {
       const int nk = ph.at.P + ph.at.S;
       b->ph_bytes[i] = (double)B * nk * kvd * 4;

@@ -58,3 +58,41 @@ def test_persistent_is_deterministic():
     a1, _ = _roll(s, wts, 2, 10, True)
     a2, _ = _roll(s, wts, 2, 10, True)
     assert np.array_equal(a1, a2)
+
+
+def _phase_classes(shape, wts):
+    """Phase classes of the persistent kernel's list for one env (from the profile records)."""
+    from tests.harness import GpuRoll
+    g = GpuRoll(shape, wts, 1, seed=3)
+    k, v = synth.draw_context(shape, 0, 0, 0)
+    g.set_context(0, k, v, 0)
+    g.fop.copy_(g.to_dev(synth.draw_fop_tokens(shape, 0, 0, batch=1)))
+    recs = g.buf.profile_step(g.fop, g.action)
+    return {r[0].split("/", 1)[1] for r in recs if r[0].startswith("persistent/")}
+
+
+@pytest.mark.parametrize("n_fop", [16, 5])
+def test_fused_cross_attention_matches_the_attention_phase_and_oracle(n_fop, monkeypatch):
+    """One env with 256-dim heads: the adapter output projection computes its head's
+    cross-attention itself (no attention phase); against the separate attention
+    phase and the oracle, with every FOP slot used and with a ragged key count."""
+    s = synth.RavelShape(layers=2, width=512, n_q_heads=4, n_kv_heads=1, head_dim=256, mlp_dim=1024, horizon=20,
+                         action_dim=9, prefix_len=70, n_fop=n_fop, fop_obs_dim=16, dtype=W.BF16, batch=1,
+                         name="xattn")
+    wts = synth.draw_weights(s, seed=7, stress=True)
+    steps = 6
+    assert "cross_attn" not in _phase_classes(s, wts)
+    a_f, X_f = _roll(s, wts, 1, steps, True)
+    monkeypatch.setenv("RAVEL_NO_FUSED_XATTN", "1")
+    assert "cross_attn" in _phase_classes(s, wts)
+    a_u, X_u = _roll(s, wts, 1, steps, True)
+    o = OracleRavel(s, wts, batch=1, seed=3)
+    k, v = synth.draw_context(s, 0, 0, 0)
+    o.set_context(0, k, v, 0)
+    a_o = np.stack([o.step(synth.draw_fop_tokens(s, 0, st, batch=1)) for st in range(steps)])
+    print(f"fused vs attention phase {rel_err(a_f, a_u):.2e}, fused vs oracle {rel_err(a_f, a_o):.2e}, "
+          f"attention phase vs oracle {rel_err(a_u, a_o):.2e}")
+    assert rel_err(a_f, a_o) < 2e-2
+    assert rel_err(X_f, o.X) < 2e-2
+    assert rel_err(a_u, a_o) < 2e-2
+    assert rel_err(a_f, a_u) < 2e-2
