@@ -76,12 +76,23 @@ typedef struct {
   int32_t model_kind;  /* RAVEL_TRANSFORMER / RAVEL_ANALYTIC_OT / _LINEAR        */
   float delta_bias;    /* delta_0 added to the offset p/H (Sec. 4.4, App. B.1)   */
   float rms_eps;       /* RMSNorm epsilon (1e-6)                                 */
+  int32_t offset_mode; /* how the offset delta enters the expert (App. A.1):
+                          RAVEL_OFFSET_MLP    an MLP of delta added to the flow-time
+                                              embedding (the pi0.5 expert);
+                          RAVEL_OFFSET_CONCAT delta concatenated to every slot's noisy
+                                              action at the action encoder (the X-VLA
+                                              expert): in.w is [w, D_a + 1], its last
+                                              column multiplies delta, and the
+                                              conditioning is silu(c_tau(i)) alone   */
 } ravel_config;
+
+enum { RAVEL_OFFSET_MLP = 0, RAVEL_OFFSET_CONCAT = 1 };
 
 /* A named host or device tensor, row-major, [out, in] for linear layers.
  * dtype RAVEL_F32 or RAVEL_BF16 (raw bf16 bits).  Names and shapes:
- *   in.w [w,D_a]  in.b [w]  time.w1 [w,w] time.b1 [w] time.w2 [w,w] time.b2 [w]
- *   delta.w1 [w,1] delta.b1 [w] delta.w2 [w,w] delta.b2 [w]
+ *   in.w [w,D_a] ([w,D_a+1] with RAVEL_OFFSET_CONCAT)  in.b [w]
+ *   time.w1 [w,w] time.b1 [w] time.w2 [w,w] time.b2 [w]
+ *   delta.w1 [w,1] delta.b1 [w] delta.w2 [w,w] delta.b2 [w]  (RAVEL_OFFSET_MLP only)
  *   layers.<l>.mod.w [6w,w] .mod.b [6w] .qkv.w [(nq+2nkv)hd,w] .o.w [w,nq hd]
  *   layers.<l>.gate.w [F,w] .up.w [F,w] .down.w [w,F]
  *   adapter layers: layers.<l>.fop.gamma [w] .fop.q.w [nq hd,w]

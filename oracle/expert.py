@@ -14,7 +14,10 @@ here (fixed for the whole repository) are:
 * conditioning: cond_i = silu(c_tau(i) + d), with
   c_tau(i) = W_t2 silu(W_t1 emb(tau_i) + b_t1) + b_t2 and
   d = W_d2 silu(W_d1 delta + b_d1) + b_d2 (the delta MLP added to the time
-  embedding before the shared final silu);
+  embedding before the shared final silu); or, for the X-VLA way of App. A.1
+  (offset_mode 1: delta concatenated to the noisy action at the action
+  encoder, every slot the same delta), cond_i = silu(c_tau(i)) and the input
+  projection takes [a_i ; delta];
 * emb(tau) = [sin(1000 tau w_j), cos(1000 tau w_j)], w_j = 10000^(-j/(w/2)),
   j < w/2;
 * every block: adaptive RMSNorm whose scale/shift/gate come from
@@ -136,8 +139,21 @@ class Expert:
         h = silu(W["delta.w1"][:, 0] * dl[0] + W["delta.b1"])
         return W["delta.w2"] @ h + W["delta.b2"]
 
+    def concat_offset(self) -> bool:
+        return getattr(self.s, "offset_mode", 0) == 1
+
     def conditioning(self, delta: float, taus=None) -> np.ndarray:
+        if self.concat_offset():  # the offset enters at the action encoder instead
+            return silu(self.tau_conditioning(taus))
         return silu(self.tau_conditioning(taus) + self.delta_conditioning(delta)[None, :])
+
+    def encode_actions(self, a, delta: float) -> np.ndarray:
+        """Action encoder: h_i = W_in a_i + b_in; with the offset concatenated (the X-VLA
+        expert, App. A.1), h_i = W_in [a_i ; delta] + b_in for every slot i."""
+        W = self.W
+        if self.concat_offset():
+            a = np.concatenate([a, np.full((a.shape[0], 1), delta, dtype=a.dtype)], axis=1)
+        return linear(a, W["in.w"], W["in.b"])
 
     # -- one pass ---------------------------------------------------------
     def velocity(self, a_slots, ctx_k, ctx_v, delta: float, z=None, hooks=None, taus=None) -> np.ndarray:
@@ -156,8 +172,9 @@ class Expert:
         qd, kvd = nq * hd, nkv * hd
         eps = s.rms_eps
         a = np.asarray(a_slots, dtype=dt)
-        cond = self.conditioning(0.0 if "delta" in hooks else delta, taus)
-        h = linear(a, W["in.w"], W["in.b"])
+        d_eff = 0.0 if "delta" in hooks else delta
+        cond = self.conditioning(d_eff, taus)
+        h = self.encode_actions(a, d_eff)
         adapters = set(s.adapter_layers())
         for l in range(s.layers):
             p = f"layers.{l}."

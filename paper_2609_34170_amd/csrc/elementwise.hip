@@ -235,6 +235,22 @@ template hipError_t launch_delta_hidden<float>(const int64_t*, const int64_t*, c
 template hipError_t launch_delta_hidden<bf16_t>(const int64_t*, const int64_t*, const int64_t*, int, int, float,
                                                 const float*, const float*, int, bf16_t*, hipStream_t);
 
+// Offset of every env (concatenated to its slots' inputs): same age rule as the MLP's.
+__global__ void offset_value_kernel(const int64_t* t, const int64_t* t_obs, const int64_t* ages, int B, int H,
+                                    float delta_bias, float* dval) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= B) return;
+  const float p = ages ? (float)ages[e] : (t ? (float)(*t - t_obs[e]) : 0.f);
+  dval[e] = p / (float)H + delta_bias;
+}
+
+hipError_t launch_offset_value(const int64_t* t, const int64_t* t_obs, const int64_t* ages, int B, int H,
+                               float delta_bias, float* dval, hipStream_t s) {
+  hipLaunchKernelGGL(offset_value_kernel, dim3((B + 255) / 256), dim3(256), 0, s, t, t_obs, ages, B, H, delta_bias,
+                     dval);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------------------
 // Offset conditioning rows: cond[blk*H + i, n] = T(silu(ctau[i, n] + d[e, n]))
 // ---------------------------------------------------------------------------
@@ -250,14 +266,14 @@ __global__ void cond_expand_kernel(const float* __restrict__ d, int B, int H, in
   if (n >= w) return;
   T* o = cond + ((size_t)blk * H + i) * w;
   if (n + 4 <= w && (w % 4) == 0) {
-    const f32x4_t dv = *(const f32x4_t*)(d + (size_t)e * w + n);
+    const f32x4_t dv = d ? *(const f32x4_t*)(d + (size_t)e * w + n) : f32x4_t{0.f, 0.f, 0.f, 0.f};
     const f32x4_t c = *(const f32x4_t*)(ctau + (size_t)ti * w + n);
 #pragma unroll
     for (int r = 0; r < 4; ++r) o[n + r] = act<T>::from_f(silu_f(c[r] + dv[r]));
     return;
   }
   for (int r = 0; r < 4 && n + r < w; ++r)
-    o[n + r] = act<T>::from_f(silu_f(ctau[(size_t)ti * w + n + r] + d[(size_t)e * w + n + r]));
+    o[n + r] = act<T>::from_f(silu_f(ctau[(size_t)ti * w + n + r] + (d ? d[(size_t)e * w + n + r] : 0.f)));
 }
 
 template <typename T>
@@ -296,7 +312,8 @@ hipError_t launch_transpose_f32(const float* src, int R, int C, float* dst, hipS
 constexpr int kInProjRows = 16;
 __global__ __launch_bounds__(256) void in_proj_kernel(const float* __restrict__ X, const int64_t* t, int B, int H, int D,
                                                       const float* __restrict__ w_inT, const float* __restrict__ b_in,
-                                                      int w, float* __restrict__ x, InProjNorm nrm, int rpb) {
+                                                      int w, float* __restrict__ x, InProjNorm nrm,
+                                                      const float* __restrict__ dval, int rpb) {
   __shared__ float xs[kInProjRows][16];
   const int tid = threadIdx.x;
   const int n = blockIdx.x * 256 + tid;
@@ -337,6 +354,12 @@ __global__ __launch_bounds__(256) void in_proj_kernel(const float* __restrict__ 
         for (int j = 0; j < 16; ++j) acc[rr] += wv[j] * xs[rr][j];
       }
   }
+  if (dval) {  // the offset as input feature D of every slot
+    const float wd = n < w ? w_inT[(size_t)D * w + n] : 0.f;
+#pragma unroll
+    for (int rr = 0; rr < kInProjRows; ++rr)
+      if (rr < nrows) acc[rr] += wd * dval[(row0 + rr) / H];
+  }
 #pragma unroll
   for (int rr = 0; rr < kInProjRows; ++rr) {
     if (rr >= nrows) break;
@@ -368,13 +391,14 @@ __global__ __launch_bounds__(256) void shift_copy_kernel(int M, int w, InProjNor
 }
 
 hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D, const float* w_inT,
-                          const float* b_in, int w, float* x, const InProjNorm& nrm, hipStream_t s) {
+                          const float* b_in, int w, float* x, const InProjNorm& nrm, const float* dval,
+                          hipStream_t s) {
   if (nrm.p && (B * H > 64 || (w % 64) != 0)) return hipErrorInvalidValue;
   // many rows: 16 per block; few rows: one per block (more blocks, same chain per block)
   const int BH = B * H;
   const int rpb = BH >= 1024 ? kInProjRows : (BH >= 256 ? 4 : 1);
   hipLaunchKernelGGL(in_proj_kernel, dim3((w + 255) / 256, (BH + rpb - 1) / rpb), dim3(256), 0, s, X, t, B, H, D,
-                     w_inT, b_in, w, x, nrm, rpb);
+                     w_inT, b_in, w, x, nrm, dval, rpb);
   if (nrm.p && nrm.cvt_chunks > 0) {
     const size_t total = (size_t)nrm.cvt_chunks * B * H * (w / 8);
     hipLaunchKernelGGL(shift_copy_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, B * H, w, nrm);

@@ -697,6 +697,14 @@ __global__ __launch_bounds__(64 * NW) void gemm_regstream_kernel(GemmArgs a) {
   const bf16_t* __restrict__ A = (const bf16_t*)a.A;
   const bf16_t* __restrict__ B = (const bf16_t*)a.B;
 
+  // buffer loads: a lane with nothing to load passes an offset past the
+  // resource's range and reads zeros, so every load is issued unconditionally
+  // and all of them are in flight together
+  const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(A), (short)0, 0x7fffffff,
+                                                                       0x00020000);
+  const __amdgpu_buffer_rsrc_t rB = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(B), (short)0, 0x7fffffff,
+                                                                       0x00020000);
+  constexpr int kOOR = (int)0x80000000u;
   bf16x8_t wf[NC][2], xf[MT][2];
 #pragma unroll
   for (int f = 0; f < 2; ++f) {
@@ -704,12 +712,14 @@ __global__ __launch_bounds__(64 * NW) void gemm_regstream_kernel(GemmArgs a) {
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const int n = n0 + c * 16 + l16;
-      wf[c][f] = (n < a.N && k < a.K) ? *(const bf16x8_t*)(B + (size_t)n * a.ldb + k) : bf16x8_t{};
+      const int off = (n < a.N && k < a.K) ? (int)(((size_t)n * a.ldb + k) * 2) : kOOR;
+      wf[c][f] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rB, off, 0, 0));
     }
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
       const int m = i * 16 + l16;
-      xf[i][f] = (m < a.M && k < a.K) ? *(const bf16x8_t*)(A + (size_t)m * a.lda + k) : bf16x8_t{};
+      const int off = (m < a.M && k < a.K) ? (int)(((size_t)m * a.lda + k) * 2) : kOOR;
+      xf[i][f] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rA, off, 0, 0));
     }
   }
   f32x4_t acc[NC][MT];
@@ -840,9 +850,14 @@ static hipError_t launch_regstream_m(const GemmArgs& a, hipStream_t s) {
   }
 }
 
+// operands addressed through buffer resources with 32-bit byte offsets
+static bool fits_buffer(const GemmArgs& a) {
+  return (size_t)a.N * a.ldb * 2 < 0x7fffffffull && (size_t)a.M * a.lda * 2 < 0x7fffffffull;
+}
+
 hipError_t launch_gemm_regstream(const GemmArgs& a, hipStream_t s) {
   if (a.M > 64 || (a.mode == EPI_GEGLU && a.N % 32)) return hipErrorInvalidValue;
-  if (a.ksplit * a.kchunk < a.K) return hipErrorInvalidValue;
+  if (a.ksplit * a.kchunk < a.K || !fits_buffer(a)) return hipErrorInvalidValue;
   switch ((a.M + 15) / 16) {
     case 1: return launch_regstream_m<1>(a, s);
     case 2: return launch_regstream_m<2>(a, s);

@@ -128,7 +128,8 @@ hipError_t launch_train_loss(const float* v, const float* target, const float* n
 
 // Offset conditioning rows: cond[blk*H + i, n] = T(silu(ctau[r, n] + d[e, n])) for every env e
 // with blk = grp[e] (>= 0; envs with grp[e] < 0 write nothing) or blk = e without grp, and
-// table row r = i (tau_row < 0: each slot its own flow time) or r = tau_row (every slot).
+// table row r = i (tau_row < 0: each slot its own flow time) or r = tau_row (every slot);
+// d = NULL: no offset term.
 template <typename T>
 hipError_t launch_cond_expand(const float* d, int B, int H, int w, const float* ctau, int tau_row, const int* grp,
                               T* cond, hipStream_t s);
@@ -153,8 +154,15 @@ struct InProjNorm {
 // with the weights given transposed (w_inT[d, n] = W_in[n, d]); t = NULL: X is a chunk
 // already in logical order (row i of env e).  The offset MLP's hidden layer likewise takes
 // t = NULL for context age 0.
+// dval: NULL, or [B] offsets delta_e concatenated to every slot's input: w_inT then has
+// D + 1 rows and row D multiplies delta_e.
 hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D, const float* w_inT,
-                          const float* b_in, int w, float* x, const InProjNorm& nrm, hipStream_t s);
+                          const float* b_in, int w, float* x, const InProjNorm& nrm, const float* dval,
+                          hipStream_t s);
+
+// dval[e] = p_e / H + delta_bias with p_e = ages[e], or *t - t_obs[e], or 0 (no step counter).
+hipError_t launch_offset_value(const int64_t* t, const int64_t* t_obs, const int64_t* ages, int B, int H,
+                               float delta_bias, float* dval, hipStream_t s);
 
 // Analytic velocity fields (logical order): OT v = (x - a*)/tau, LINEAR v = lambda x, with
 // tau = tau_i = (i+1)/H of the ring (rotated by t), or tau_all for every slot of a chunk

@@ -105,7 +105,7 @@ struct ravel_model {
   size_t arena_bytes = 0;
   int64_t weight_bytes = 0;
   float *in_w = nullptr, *in_b = nullptr;
-  float* in_wT = nullptr;  // [D, w]: in_w transposed (input projection reads it)
+  float* in_wT = nullptr;  // [D_in, w]: in_w transposed (input projection reads it); D_in = D (+1: offset column)
   float* ctau = nullptr;  // [H, w]
   void *t_w1 = nullptr, *t_w2 = nullptr;  // flow-time MLP (model dtype), kept for other step counts
   float *t_b1 = nullptr, *t_b2 = nullptr;
@@ -316,6 +316,7 @@ struct ravel_buffer {
   void* cond = nullptr;
   void* h1 = nullptr;
   float* dvec = nullptr;  // [B, w] offset embedding d = W_d2 h1 + b_d2
+  float* dval = nullptr;  // [B] offsets, concatenated to the slots' inputs (RAVEL_OFFSET_CONCAT)
   bf16_t* pshift = nullptr;  // persistent step: bf16 copies of the norm shifts
   float* mod = nullptr;
   void* y = nullptr;
@@ -518,11 +519,20 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
   const double elt = (double)m->elt;
 
   // 1. offset conditioning: delta_e = p/H + delta_0, d = W_d2 silu(W_d1 delta + b_d1) + b_d2,
-  //    cond[e,i] = silu(c_tau(i) + d)
-  REC_BEGIN("delta_hidden", (double)B * w * (8 + elt), (double)B * w * 4);
-  HIP_TRY(launch_delta_hidden<T>(pin.X ? nullptr : b->t, b->t_obs, pin.ages, B, H, pin.lead_bias ? c.delta_bias : 0.f,
-                                 m->d_w1, m->d_b1, w, (T*)b->h1, s));
-  REC_END();
+  //    cond[e,i] = silu(c_tau(i) + d); or, with the offset concatenated to the inputs,
+  //    cond[e,i] = silu(c_tau(i)) and delta_e goes to the input projection
+  const bool concat = c.offset_mode == RAVEL_OFFSET_CONCAT;
+  const float dbias = pin.lead_bias ? c.delta_bias : 0.f;
+  if (concat) {
+    REC_BEGIN("offset_value", (double)B * 12, 0.0);
+    HIP_TRY(launch_offset_value(pin.X ? nullptr : b->t, b->t_obs, pin.ages, B, H, dbias, b->dval, s));
+    REC_END();
+  } else {
+    REC_BEGIN("delta_hidden", (double)B * w * (8 + elt), (double)B * w * 4);
+    HIP_TRY(launch_delta_hidden<T>(pin.X ? nullptr : b->t, b->t_obs, pin.ages, B, H, dbias, m->d_w1, m->d_b1, w,
+                                   (T*)b->h1, s));
+    REC_END();
+  }
   // Envs with equal t_obs have equal delta, so equal cond rows and modulation
   // rows: cond is written once per group (compacted) and the modulation GEMM
   // runs on the groups' rows only.
@@ -533,7 +543,7 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
     HIP_TRY(launch_cond_groups(pin.ages ? pin.ages : b->t_obs, B, H, b->cgrp, b->crowmap, b->crows, s));
     REC_END();
   }
-  {
+  if (!concat) {
     GemmArgs e = epi_args(EPI_F32);
     e.bias = m->d_b2;
     e.out_f = b->dvec;
@@ -541,13 +551,13 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
     RV_TRY(run_gemm<T>(b, s, rec, "cond", b->h1, w, m->d_w2, w, B, w, w, e));
   }
   REC_BEGIN("cond_expand", (double)B * w * 4 + (double)H * w * 4 + (double)BH * w * elt, (double)BH * w * 4);
-  HIP_TRY(launch_cond_expand<T>(b->dvec, B, H, w, pin.ctau ? pin.ctau : m->ctau, pin.tau_row,
+  HIP_TRY(launch_cond_expand<T>(concat ? nullptr : b->dvec, B, H, w, pin.ctau ? pin.ctau : m->ctau, pin.tau_row,
                                 b->cgroups ? b->cgrp : nullptr, (T*)b->cond, s));
   REC_END();
   // 2. input projection of the buffer in logical order
   REC_BEGIN("in_proj", (double)BH * (D + w) * 4, 2.0 * BH * w * D);
   HIP_TRY(launch_in_proj(pin.X ? pin.X : b->X, pin.X ? nullptr : b->t, B, H, D, m->in_wT, m->in_b, w, b->x,
-                         InProjNorm{}, s));
+                         InProjNorm{}, concat ? b->dval : nullptr, s));
   REC_END();
   // FOP adapter keys/values of every adapter layer at once
   if (m->n_ad > 0) {
@@ -1072,11 +1082,17 @@ ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream
   const int B = b->B, H = c.horizon, w = c.width, D = c.action_dim, BH = B * H;
   const int kvd = c.n_kv_heads * c.head_dim;
   const double elt = (double)m->elt;
-  REC_BEGIN("delta_hidden", (double)B * w * (8 + elt), (double)B * w * 4);
-  HIP_TRY(launch_delta_hidden<bf16_t>(pin.X ? nullptr : b->t, b->t_obs, pin.ages, B, H,
-                                      pin.lead_bias ? c.delta_bias : 0.f, m->d_w1, m->d_b1, w, (bf16_t*)b->h1, s));
-  REC_END();
-  {
+  const bool concat = c.offset_mode == RAVEL_OFFSET_CONCAT;
+  const float dbias = pin.lead_bias ? c.delta_bias : 0.f;
+  if (concat) {
+    REC_BEGIN("offset_value", (double)B * 12, 0.0);
+    HIP_TRY(launch_offset_value(pin.X ? nullptr : b->t, b->t_obs, pin.ages, B, H, dbias, b->dval, s));
+    REC_END();
+  } else {
+    REC_BEGIN("delta_hidden", (double)B * w * (8 + elt), (double)B * w * 4);
+    HIP_TRY(launch_delta_hidden<bf16_t>(pin.X ? nullptr : b->t, b->t_obs, pin.ages, B, H, dbias, m->d_w1, m->d_b1, w,
+                                        (bf16_t*)b->h1, s));
+    REC_END();
     GemmArgs e = epi_args(EPI_F32);
     e.bias = m->d_b2;
     e.out_f = b->dvec;
@@ -1084,8 +1100,8 @@ ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream
     RV_TRY(run_gemm<bf16_t>(b, s, rec, "cond", b->h1, w, m->d_w2, w, B, w, w, e));
   }
   REC_BEGIN("cond_expand", (double)B * w * 4 + (double)H * w * 4 + (double)BH * w * elt, (double)BH * w * 4);
-  HIP_TRY(launch_cond_expand<bf16_t>(b->dvec, B, H, w, pin.ctau ? pin.ctau : m->ctau, pin.tau_row, nullptr,
-                                     (bf16_t*)b->cond, s));
+  HIP_TRY(launch_cond_expand<bf16_t>(concat ? nullptr : b->dvec, B, H, w, pin.ctau ? pin.ctau : m->ctau, pin.tau_row,
+                                     nullptr, (bf16_t*)b->cond, s));
   REC_END();
   {
     GemmArgs e = epi_args(EPI_F32);
@@ -1111,7 +1127,7 @@ ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream
     nrm.cvt_out = b->pshift;
     REC_BEGIN("in_proj", (double)BH * (D + w) * 4 + (double)BH * w * (6 + nrm.cvt_chunks * 6), 2.0 * BH * w * D);
     HIP_TRY(launch_in_proj(pin.X ? pin.X : b->X, pin.X ? nullptr : b->t, B, H, D, m->in_wT, m->in_b, w, b->x, nrm,
-                           s));
+                           concat ? b->dval : nullptr, s));
     REC_END();
   }
   if (m->n_ad > 0) {
@@ -1247,6 +1263,10 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
     return RAVEL_OK;
   }
   if (c.model_kind != RAVEL_TRANSFORMER) return bail(fail(RAVEL_E_INVALID, "model_kind"));
+  if (c.offset_mode != RAVEL_OFFSET_MLP && c.offset_mode != RAVEL_OFFSET_CONCAT)
+    return bail(fail(RAVEL_E_INVALID, "offset_mode"));
+  const bool concat = c.offset_mode == RAVEL_OFFSET_CONCAT;
+  const int Din = D + (concat ? 1 : 0);  // input features of the action encoder
   const int nq = c.n_q_heads, nkv = c.n_kv_heads, hd = c.head_dim, F = c.mlp_dim, L = c.layers;
   if (w <= 0 || w % 8 || nq <= 0 || nkv <= 0 || nq % nkv || hd % 32 || hd > 256 || F <= 0 || F % 16 ||
       L <= 0 || c.prefix_len < 0 || c.n_fop < 0)
@@ -1268,16 +1288,18 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
   do {                                                             \
     if ((st = check_shape(tm.get(name), name, {__VA_ARGS__})) != RAVEL_OK) return bail(st); \
   } while (0)
-  CHK("in.w", w, D);
+  CHK("in.w", w, Din);
   CHK("in.b", w);
   CHK("time.w1", w, w);
   CHK("time.b1", w);
   CHK("time.w2", w, w);
   CHK("time.b2", w);
-  CHK("delta.w1", w, 1);
-  CHK("delta.b1", w);
-  CHK("delta.w2", w, w);
-  CHK("delta.b2", w);
+  if (!concat) {
+    CHK("delta.w1", w, 1);
+    CHK("delta.b1", w);
+    CHK("delta.w2", w, w);
+    CHK("delta.b2", w);
+  }
   CHK("final.mod.w", 3 * w, w);
   CHK("final.mod.b", 3 * w);
   CHK("out.w", D, w);
@@ -1311,8 +1333,8 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
   // device layout
   const size_t E = m->elt;
   Arena ar;
-  ar.want((void**)&m->in_w, (size_t)w * D * 4);
-  ar.want((void**)&m->in_wT, (size_t)w * D * 4);
+  ar.want((void**)&m->in_w, (size_t)w * Din * 4);
+  ar.want((void**)&m->in_wT, (size_t)w * Din * 4);
   ar.want((void**)&m->in_b, (size_t)w * 4);
   ar.want((void**)&m->ctau, (size_t)H * w * 4);
   ar.want(&m->t_w1, (size_t)w * w * E);
@@ -1378,12 +1400,15 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
     if ((st = up(name, dst, md)) != RAVEL_OK) return bail(done(st)); \
   } while (0)
   UP("in.w", m->in_w, false);
-  if (launch_transpose_f32(m->in_w, w, D, m->in_wT, 0) != hipSuccess) return bail(done(fail(RAVEL_E_HIP, "in.w transpose")));
+  if (launch_transpose_f32(m->in_w, w, Din, m->in_wT, 0) != hipSuccess)
+    return bail(done(fail(RAVEL_E_HIP, "in.w transpose")));
   UP("in.b", m->in_b, false);
-  UP("delta.w1", m->d_w1, false);
-  UP("delta.b1", m->d_b1, false);
-  UP("delta.w2", m->d_w2, true);
-  UP("delta.b2", m->d_b2, false);
+  if (!concat) {
+    UP("delta.w1", m->d_w1, false);
+    UP("delta.b1", m->d_b1, false);
+    UP("delta.w2", m->d_w2, true);
+    UP("delta.b2", m->d_b2, false);
+  }
   for (int l = 0; l < L; ++l) {
     LayerW& Lw = m->layers[l];
     const std::string p = "layers." + std::to_string(l) + ".";
@@ -1441,7 +1466,7 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
 #undef UP
   if (hipDeviceSynchronize() != hipSuccess) return bail(fail(RAVEL_E_HIP, "create sync"));
   // algorithmic weight bytes streamed by one step (time MLP excluded: precomputed)
-  int64_t wb = (int64_t)w * D * 4 + (int64_t)w * w * E;
+  int64_t wb = (int64_t)w * Din * 4 + (concat ? 0 : (int64_t)w * w * E);
   for (int l = 0; l < L; ++l) {
     wb += (int64_t)(6 * w + qkvd) * w * E + (int64_t)w * qd * E + (int64_t)3 * F * w * E + 6 * w * 4;
     if (ad_of[l] >= 0) wb += (int64_t)(2 * qd + 2 * kvd) * w * E;
@@ -1492,6 +1517,7 @@ ravel_status ravel_buffer_create(ravel_model* m, int32_t batch, uint64_t seed, r
     ar.want(&b->cond, (size_t)BH * w * E);
     ar.want(&b->h1, (size_t)B * w * E);
     ar.want((void**)&b->dvec, (size_t)B * w * 4);
+    ar.want((void**)&b->dval, (size_t)B * 4);
     // few rows: every layer's modulation comes from one GEMM at the start of the step
     // Few rows, or rows grouped by offset conditioning: every layer's modulation
     // comes from one GEMM at the start of the step (on the groups' rows only).

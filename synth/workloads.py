@@ -38,6 +38,11 @@ TRANSFORMER = 0
 ANALYTIC_OT = 1
 ANALYTIC_LINEAR = 2
 
+# how the context-age offset enters the expert: an MLP of it added to the
+# flow-time embedding, or concatenated to every slot's action input
+OFFSET_MLP = 0
+OFFSET_CONCAT = 1
+
 
 @dataclasses.dataclass(frozen=True)
 class RavelShape:
@@ -59,6 +64,7 @@ class RavelShape:
     model_kind: int = TRANSFORMER
     delta_bias: float = 0.0
     rms_eps: float = 1e-6
+    offset_mode: int = OFFSET_MLP
     # workload (not model) fields
     batch: int = 1
     steps: int = 200
@@ -115,13 +121,14 @@ def weight_shapes(s: RavelShape, with_fop_encoder: bool = True) -> List[Tuple[st
         return [("analytic.target", (da,))]
     if s.model_kind == ANALYTIC_LINEAR:
         return [("analytic.lambda", (1,))]
+    concat = s.offset_mode == OFFSET_CONCAT
     out: List[Tuple[str, Tuple[int, ...]]] = [
-        ("in.w", (w, da)), ("in.b", (w,)),
+        ("in.w", (w, da + 1 if concat else da)), ("in.b", (w,)),
         ("time.w1", (w, w)), ("time.b1", (w,)),
         ("time.w2", (w, w)), ("time.b2", (w,)),
-        ("delta.w1", (w, 1)), ("delta.b1", (w,)),
-        ("delta.w2", (w, w)), ("delta.b2", (w,)),
     ]
+    if not concat:
+        out += [("delta.w1", (w, 1)), ("delta.b1", (w,)), ("delta.w2", (w, w)), ("delta.b2", (w,))]
     qd = s.n_q_heads * s.head_dim
     kvd = s.n_kv_heads * s.head_dim
     adapters = set(s.adapter_layers())
