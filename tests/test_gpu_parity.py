@@ -157,6 +157,17 @@ def test_pi_b64_sampled_envs():
     print(f"pi_b64: action err {ea:.2e}, state err {ex:.2e}")
 
 
+def test_large_b16_shapes_sampled_envs():
+    """The large expert's layer shapes (width 2048, 16 query / 4 KV heads of 128, MLP 8192,
+    2048 prefix tokens, 100 slots, 32 FOP tokens) at batch 16 with the refresh at step 3;
+    4 of its 24 layers (two with adapters), so that the CPU oracle finishes in seconds."""
+    s = synth.get_config("large_b16").replace(layers=4)
+    wts = synth.draw_weights(s, seed=0)
+    ea, ex, n = run_parity(s, wts, batch=16, seed=0, steps=4, env_sample=[0, 15], oracle_dtype=np.float32,
+                           check_every=2)
+    print(f"large_b16: action err {ea:.2e}, state err {ex:.2e}")
+
+
 # ---------------------------------------------------------------------------
 # runtime behaviour
 # ---------------------------------------------------------------------------
