@@ -437,6 +437,9 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
     // S^T[key][row] for two 16-key sub-tiles, each summed in two independent
     // MFMA chains (even / odd k-steps)
     f32x4_t sa0 = {0.f, 0.f, 0.f, 0.f}, sa1 = sa0, sb0 = sa0, sb1 = sa0;
+    // the wave issuing MFMAs goes first; the SIMD's other wave fills the gaps
+    // with its softmax or staging work
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int ks = 0; ks < KS; ks += 2) {
       const bf16x8_t k0f = *(const bf16x8_t*)&Ks[buf][l16][ks * 32 + grp * 8];
@@ -450,6 +453,7 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
         sb1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k3f, qf[ks + 1], sb1, 0, 0, 0);
       }
     }
+    __builtin_amdgcn_s_setprio(0);
     float x[8];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -497,6 +501,7 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
                         pack_bf16x2(p[6], p[7])};
     const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pw);
     // V^T operands read per 16-dim block (the MFMA chain covers the LDS latency)
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
       const bf16_t* vrow = &Vt[buf][dt * 16 + l16][0];
@@ -505,6 +510,7 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
       const u32x4_t vv = {lo[0], lo[1], hi[0], hi[1]};
       o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vv), pf, o[dt], 0, 0, 0);
     }
+    __builtin_amdgcn_s_setprio(0);
     if (t + 1 < ntile) store_tile(buf ^ 1, s_next1);
     __syncthreads();
   };
