@@ -130,7 +130,13 @@ int64_t ravel_model_weight_bytes(const ravel_model* model);
  * slot r mod H and is Philox noise for (seed, e, r) (App. A.1: no additional
  * initialisation).  Noise is Philox4x32-10 (Salmon et al., SC'11) keyed by
  * (seed lo, seed hi) with counter (j/4, env, r lo, r hi) and Box-Muller in
- * float64 rounded to float32.  Synchronous. */
+ * float64 rounded to float32.  Synchronous.
+ * Environment variables read here (each "1" to apply), for tests and comparisons:
+ *   RAVEL_NO_PERSISTENT   the per-kernel path even where the persistent kernel fits;
+ *   RAVEL_NO_FUSED_XATTN  a separate attention phase for the FOP adapters in the
+ *                         persistent kernel (default for one env with 256-dim heads
+ *                         and <= 16 FOP tokens: computed inside the output projection);
+ *   RAVEL_SYNC_CONTEXT    RAVEL_OPT_SYNC_CONTEXT on;  RAVEL_NO_GRAPH  RAVEL_OPT_USE_GRAPH off. */
 ravel_status ravel_buffer_create(ravel_model* model, int32_t batch, uint64_t seed, ravel_buffer** out);
 void ravel_buffer_destroy(ravel_buffer* buf);
 
