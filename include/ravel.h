@@ -136,7 +136,10 @@ int64_t ravel_model_weight_bytes(const ravel_model* model);
  *   RAVEL_NO_FUSED_XATTN  a separate attention phase for the FOP adapters in the
  *                         persistent kernel (default for one env with 256-dim heads
  *                         and <= 16 FOP tokens: computed inside the output projection);
- *   RAVEL_SYNC_CONTEXT    RAVEL_OPT_SYNC_CONTEXT on;  RAVEL_NO_GRAPH  RAVEL_OPT_USE_GRAPH off. */
+ *   RAVEL_SYNC_CONTEXT    RAVEL_OPT_SYNC_CONTEXT on;  RAVEL_NO_GRAPH  RAVEL_OPT_USE_GRAPH off;
+ *   RAVEL_COOPERATIVE     launch the persistent kernel cooperatively (residency of
+ *                         its whole grid guaranteed up front, e.g. on a GPU shared
+ *                         with other processes; read once per process). */
 ravel_status ravel_buffer_create(ravel_model* model, int32_t batch, uint64_t seed, ravel_buffer** out);
 void ravel_buffer_destroy(ravel_buffer* buf);
 

@@ -1,7 +1,7 @@
 // Persistent few-row step: the transformer layers of a batch whose B*H rows fit
 // one 64-row MFMA tile (B*H <= 64, e.g. one env with 50 slots) run inside ONE
-// cooperative kernel that walks a host-built list of phases separated by
-// hierarchical grid barriers.
+// kernel (one block per CU, all co-resident) that walks a host-built list of
+// phases separated by hierarchical grid barriers.
 //
 // At these sizes every phase is a chain of memory round trips rather than a
 // bandwidth problem, so the kernel is laid out to keep that chain short:
@@ -36,6 +36,8 @@
 // read with plain loads.  Producers drain their stores before arriving at a
 // barrier or ticket.  Spins are bounded: a barrier that does not complete sets
 // the error flag and every wave exits.
+#include <cstdlib>
+
 #include "kernels.h"
 #include "persistent.h"
 
@@ -1210,7 +1212,17 @@ hipError_t launch_persistent(const Phase* phases, int nphase, const int* env_slo
   if (!fn || nenv > 64 || nphase < 1) return hipErrorInvalidValue;
   void* args[] = {(void*)&phases, (void*)&nphase, (void*)&env_slot, (void*)&nenv,
                   (void*)&bar,    (void*)&err,    (void*)&times};
-  return hipLaunchCooperativeKernel(fn, dim3(blocks), dim3(256), args, 0, s);
+  // An ordinary launch: the grid (one block per CU, at most the occupancy limit)
+  // is co-resident as soon as the CUs are free, and every wait in the kernel is
+  // bounded, so a block held back by other work only delays the first barrier.
+  // The cooperative launch guarantees residency up front but adds ~11 us of idle
+  // device time on each side of the kernel; it is used when asked for.
+  static const bool coop = [] {
+    const char* ev = getenv("RAVEL_COOPERATIVE");
+    return ev && atoi(ev) != 0;
+  }();
+  if (coop) return hipLaunchCooperativeKernel(fn, dim3(blocks), dim3(256), args, 0, s);
+  return hipLaunchKernel(fn, dim3(blocks), dim3(256), args, 0, s);
 }
 
 int persistent_max_blocks(int mt, int hd) {
