@@ -289,6 +289,99 @@ template hipError_t launch_cond_expand<bf16_t>(const float*, int, int, int, cons
                                                hipStream_t);
 
 // ---------------------------------------------------------------------------
+// Offset conditioning of a few envs in one kernel: delta_e, h1 = silu(W_d1 delta +
+// b_d1) (bf16, as the GEMM operand of the three-kernel path), d = W_d2 h1 + b_d2
+// and cond[e*H + i, n] = bf16(silu(ctau[r, n] + d[n])).  Block = 4 waves over 16
+// columns of one env; wave w owns columns 4w .. 4w+3 and its lanes split K in
+// 8-element chunks (a wave reduction per column); h1 is formed by every block in
+// LDS.  All of a block's loads are issued together at its start.
+// ---------------------------------------------------------------------------
+constexpr int kCondCols = 16;
+constexpr int kCondMaxW = 2048;  // w <= 2048: 8 chunks of K per lane, 8 h1 values per thread
+constexpr int kCondMaxH = 128;   // H <= 128: 8 conditioning entries per thread
+__global__ __launch_bounds__(256) void offset_cond_kernel(const int64_t* t, const int64_t* t_obs,
+                                                          const int64_t* ages, int H, float delta_bias,
+                                                          const float* __restrict__ wd1,
+                                                          const float* __restrict__ bd1,
+                                                          const bf16_t* __restrict__ wd2,
+                                                          const float* __restrict__ bd2, int w,
+                                                          const float* __restrict__ ctau, int tau_row,
+                                                          bf16_t* __restrict__ cond) {
+  __shared__ bf16_t h1[kCondMaxW];
+  __shared__ float dcol[kCondCols];
+  constexpr int MAXJ = kCondMaxW / 512, MAXK = kCondMaxW / 256, MAXC = kCondMaxH * kCondCols / 256;
+  const int e = blockIdx.y, n0 = blockIdx.x * kCondCols;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // every load of the block is issued before any is used: the offset MLP's first
+  // layer, this wave's four rows of W_d2, the conditioning table entries and bias
+  float a1[MAXK], c1[MAXK];
+#pragma unroll
+  for (int q = 0; q < MAXK; ++q) {
+    const int k = tid + 256 * q;
+    a1[q] = k < w ? wd1[k] : 0.f;
+    c1[q] = k < w ? bd1[k] : 0.f;
+  }
+  u32x4_t wv[4][MAXJ];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int n = n0 + wave * 4 + c;
+#pragma unroll
+    for (int j = 0; j < MAXJ; ++j) {
+      const int k = 8 * (lane + 64 * j);
+      wv[c][j] = (n < w && k < w) ? *(const u32x4_t*)(wd2 + (size_t)n * w + k) : u32x4_t{0, 0, 0, 0};
+    }
+  }
+  float cv[MAXC];
+#pragma unroll
+  for (int q = 0; q < MAXC; ++q) {
+    const int idx = tid + 256 * q, i = idx / kCondCols, n = n0 + idx % kCondCols;
+    const int ti = tau_row >= 0 ? tau_row : i;
+    cv[q] = (i < H && n < w) ? ctau[(size_t)ti * w + n] : 0.f;
+  }
+  const float bias = (lane < 4 && n0 + wave * 4 + lane < w) ? bd2[n0 + wave * 4 + lane] : 0.f;
+  const float p = ages ? (float)ages[e] : (t ? (float)(*t - t_obs[e]) : 0.f);
+  const float delta = p / (float)H + delta_bias;
+#pragma unroll
+  for (int q = 0; q < MAXK; ++q) {
+    const int k = tid + 256 * q;
+    if (k < w) h1[k] = f32_to_bf16(silu_f(a1[q] * delta + c1[q]));
+  }
+  __syncthreads();
+  // column n = n0 + 4 wave + c: lanes take 8-element chunks k = 8 (lane + 64 j)
+  float acc[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    float sacc = 0.f;
+#pragma unroll
+    for (int j = 0; j < MAXJ; ++j) {
+      const int k = 8 * (lane + 64 * j);
+      if (k >= w) break;
+      const bf16_t* wb = reinterpret_cast<const bf16_t*>(&wv[c][j]);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) sacc += bf16_to_f32(wb[q]) * bf16_to_f32(h1[k + q]);
+    }
+    acc[c] = wave_sum(sacc);
+  }
+  if (lane < 4) dcol[wave * 4 + lane] = (lane == 0 ? acc[0] : lane == 1 ? acc[1] : lane == 2 ? acc[2] : acc[3]) + bias;
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < MAXC; ++q) {
+    const int idx = tid + 256 * q, i = idx / kCondCols, cc = idx % kCondCols, n = n0 + cc;
+    if (i < H && n < w) cond[((size_t)e * H + i) * w + n] = f32_to_bf16(silu_f(cv[q] + dcol[cc]));
+  }
+}
+
+hipError_t launch_offset_cond(const int64_t* t, const int64_t* t_obs, const int64_t* ages, int B, int H,
+                              float delta_bias, const float* wd1, const float* bd1, const bf16_t* wd2,
+                              const float* bd2, int w, const float* ctau, int tau_row, bf16_t* cond,
+                              hipStream_t s) {
+  if (w > kCondMaxW || w % 8 || B < 1 || H > kCondMaxH) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(offset_cond_kernel, dim3((w + kCondCols - 1) / kCondCols, B), dim3(256), 0, s, t, t_obs, ages, H,
+                     delta_bias, wd1, bd1, wd2, bd2, w, ctau, tau_row, cond);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Input projection (logical slot order)
 // ---------------------------------------------------------------------------
 __global__ void transpose_f32_kernel(const float* __restrict__ src, int R, int C, float* __restrict__ dst) {
@@ -303,19 +396,38 @@ hipError_t launch_transpose_f32(const float* src, int R, int C, float* dst, hipS
   return hipGetLastError();
 }
 
+// bf16 copies of the norm shifts: item = 8 consecutive columns of one (chunk, row)
+RAVEL_DEV void shift_copy_item(size_t idx, int M, int w, const InProjNorm& nrm) {
+  const int per_row = w / 8;
+  const size_t total = (size_t)nrm.cvt_chunks * M * per_row;
+  if (idx >= total) return;
+  const int n = (int)(idx % per_row) * 8;
+  const int row = (int)((idx / per_row) % M);
+  const int c = (int)(idx / ((size_t)per_row * M));
+  const float* src = nrm.cvt_in + (size_t)row * nrm.cvt_ld + (size_t)c * nrm.cvt_stride + n;
+  const f32x4_t a = *(const f32x4_t*)src, b = *(const f32x4_t*)(src + 4);
+  const u32x4_t o = {pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3])};
+  *(u32x4_t*)(nrm.cvt_out + ((size_t)c * M + row) * w + n) = o;
+}
+
 // Block = 4 waves over 256 consecutive columns (one 64-column tile per wave) and
 // rpb <= kInProjRows rows.  The weights are read transposed (w_inT[d, n]:
 // consecutive lanes, consecutive addresses) once per block and kept in registers
 // for all of its rows; the rows' ring entries are staged in LDS 16 features at a
 // time, so a block costs one round of loads per 16 features whatever its row
-// count.  Every output is bias + sum over d in increasing order.
+// count.  Every output is bias + sum over d in increasing order.  Blocks past the
+// row blocks (blockIdx.y >= nrowblk) make the bf16 shift copies instead.
 constexpr int kInProjRows = 16;
 __global__ __launch_bounds__(256) void in_proj_kernel(const float* __restrict__ X, const int64_t* t, int B, int H, int D,
                                                       const float* __restrict__ w_inT, const float* __restrict__ b_in,
                                                       int w, float* __restrict__ x, InProjNorm nrm,
-                                                      const float* __restrict__ dval, int rpb) {
+                                                      const float* __restrict__ dval, int rpb, int nrowblk) {
   __shared__ float xs[kInProjRows][16];
   const int tid = threadIdx.x;
+  if ((int)blockIdx.y >= nrowblk) {
+    shift_copy_item(((size_t)(blockIdx.y - nrowblk) * gridDim.x + blockIdx.x) * 256 + tid, B * H, w, nrm);
+    return;
+  }
   const int n = blockIdx.x * 256 + tid;
   const int lane = tid & 63;
   const int BH = B * H;
@@ -375,21 +487,6 @@ __global__ __launch_bounds__(256) void in_proj_kernel(const float* __restrict__ 
   }
 }
 
-// bf16 copies of the norm shifts: thread = 8 consecutive columns of one (chunk, row)
-__global__ __launch_bounds__(256) void shift_copy_kernel(int M, int w, InProjNorm nrm) {
-  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
-  const int per_row = w / 8;
-  const size_t total = (size_t)nrm.cvt_chunks * M * per_row;
-  if (idx >= total) return;
-  const int n = (int)(idx % per_row) * 8;
-  const int row = (int)((idx / per_row) % M);
-  const int c = (int)(idx / ((size_t)per_row * M));
-  const float* src = nrm.cvt_in + (size_t)row * nrm.cvt_ld + (size_t)c * nrm.cvt_stride + n;
-  const f32x4_t a = *(const f32x4_t*)src, b = *(const f32x4_t*)(src + 4);
-  const u32x4_t o = {pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3])};
-  *(u32x4_t*)(nrm.cvt_out + ((size_t)c * M + row) * w + n) = o;
-}
-
 hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D, const float* w_inT,
                           const float* b_in, int w, float* x, const InProjNorm& nrm, const float* dval,
                           hipStream_t s) {
@@ -397,12 +494,15 @@ hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D,
   // many rows: 16 per block; few rows: one per block (more blocks, same chain per block)
   const int BH = B * H;
   const int rpb = BH >= 1024 ? kInProjRows : (BH >= 256 ? 4 : 1);
-  hipLaunchKernelGGL(in_proj_kernel, dim3((w + 255) / 256, (BH + rpb - 1) / rpb), dim3(256), 0, s, X, t, B, H, D,
-                     w_inT, b_in, w, x, nrm, dval, rpb);
+  const int cols = (w + 255) / 256, nrowblk = (BH + rpb - 1) / rpb;
+  // the shift copies ride along in extra row blocks of the same launch
+  int extra = 0;
   if (nrm.p && nrm.cvt_chunks > 0) {
-    const size_t total = (size_t)nrm.cvt_chunks * B * H * (w / 8);
-    hipLaunchKernelGGL(shift_copy_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, B * H, w, nrm);
+    const size_t total = (size_t)nrm.cvt_chunks * BH * (w / 8);
+    extra = (int)((total + (size_t)cols * 256 - 1) / ((size_t)cols * 256));
   }
+  hipLaunchKernelGGL(in_proj_kernel, dim3(cols, nrowblk + extra), dim3(256), 0, s, X, t, B, H, D, w_inT, b_in, w, x, nrm,
+                     dval, rpb, nrowblk);
   return hipGetLastError();
 }
 

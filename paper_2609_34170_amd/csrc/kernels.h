@@ -154,6 +154,15 @@ struct InProjNorm {
 // with the weights given transposed (w_inT[d, n] = W_in[n, d]); t = NULL: X is a chunk
 // already in logical order (row i of env e).  The offset MLP's hidden layer likewise takes
 // t = NULL for context age 0.
+// The offset conditioning of a few envs in one launch (bf16 models): delta_e as for
+// launch_delta_hidden, h1 = bf16(silu(wd1 delta_e + bd1)), d = wd2 h1 + bd2 (wd2 bf16
+// [w, w]), cond[e*H + i, n] = bf16(silu(ctau[r, n] + d[n])) with r as for
+// launch_cond_expand.  w <= 2048, a multiple of 8; H <= 128.
+hipError_t launch_offset_cond(const int64_t* t, const int64_t* t_obs, const int64_t* ages, int B, int H,
+                              float delta_bias, const float* wd1, const float* bd1, const bf16_t* wd2,
+                              const float* bd2, int w, const float* ctau, int tau_row, bf16_t* cond,
+                              hipStream_t s);
+
 // dval: NULL, or [B] offsets delta_e concatenated to every slot's input: w_inT then has
 // D + 1 rows and row D multiplies delta_e.
 hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D, const float* w_inT,

@@ -1088,21 +1088,19 @@ ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream
     REC_BEGIN("offset_value", (double)B * 12, 0.0);
     HIP_TRY(launch_offset_value(pin.X ? nullptr : b->t, b->t_obs, pin.ages, B, H, dbias, b->dval, s));
     REC_END();
-  } else {
-    REC_BEGIN("delta_hidden", (double)B * w * (8 + elt), (double)B * w * 4);
-    HIP_TRY(launch_delta_hidden<bf16_t>(pin.X ? nullptr : b->t, b->t_obs, pin.ages, B, H, dbias, m->d_w1, m->d_b1, w,
-                                        (bf16_t*)b->h1, s));
+    REC_BEGIN("cond_expand", (double)H * w * 4 + (double)BH * w * elt, (double)BH * w * 4);
+    HIP_TRY(launch_cond_expand<bf16_t>(nullptr, B, H, w, pin.ctau ? pin.ctau : m->ctau, pin.tau_row, nullptr,
+                                       (bf16_t*)b->cond, s));
     REC_END();
-    GemmArgs e = epi_args(EPI_F32);
-    e.bias = m->d_b2;
-    e.out_f = b->dvec;
-    e.ldo_f = w;
-    RV_TRY(run_gemm<bf16_t>(b, s, rec, "cond", b->h1, w, m->d_w2, w, B, w, w, e));
+  } else {
+    // offset MLP and conditioning rows in one launch
+    REC_BEGIN("offset_cond", (double)w * w * elt + (double)H * w * 4 + (double)BH * w * elt,
+              2.0 * B * w * w + (double)BH * w * 4);
+    HIP_TRY(launch_offset_cond(pin.X ? nullptr : b->t, b->t_obs, pin.ages, B, H, dbias, m->d_w1, m->d_b1,
+                               (const bf16_t*)m->d_w2, m->d_b2, w, pin.ctau ? pin.ctau : m->ctau, pin.tau_row,
+                               (bf16_t*)b->cond, s));
+    REC_END();
   }
-  REC_BEGIN("cond_expand", (double)B * w * 4 + (double)H * w * 4 + (double)BH * w * elt, (double)BH * w * 4);
-  HIP_TRY(launch_cond_expand<bf16_t>(concat ? nullptr : b->dvec, B, H, w, pin.ctau ? pin.ctau : m->ctau, pin.tau_row,
-                                     nullptr, (bf16_t*)b->cond, s));
-  REC_END();
   {
     GemmArgs e = epi_args(EPI_F32);
     e.bias = m->mod_all_b;

@@ -149,6 +149,38 @@ def test_pi_b1_full_size_steps():
     print(f"pi_b1: action err {ea:.2e}, state err {ex:.2e}")
 
 
+def test_pi_b1_after_1000_steps_from_the_same_state():
+    """The pi-style workload rolled 1000 steps on the GPU (ring indices wrapped 20 times,
+    noise counters past 1000), then three more steps on both sides from the GPU's state:
+    the step at late t matches the oracle's step from the same buffer."""
+    s = synth.get_config("pi_b1")
+    wts = synth.draw_weights(s, seed=0)
+    g = GpuRoll(s, wts, 1, seed=0)
+    k, v = synth.draw_context(s, 0, 0, 0)
+    g.set_context(0, k, v, 0)
+    z = synth.draw_fop_tokens(s, 0, 0, batch=1)
+    g.fop.copy_(g.to_dev(z))
+    for _ in range(1000):
+        g.buf.step(g.fop, g.action)
+    g.buf.sync()
+    X, t, t_obs = g.state()
+    assert t == 1000 and t_obs[0] == 0
+    o = OracleRavel(s, wts, batch=1, seed=0, dtype=np.float32)
+    o.X = X.astype(np.float32).copy()
+    o.t = t
+    o.set_context(0, k, v, 0)
+    for st in range(3):
+        zz = synth.draw_fop_tokens(s, 0, 1000 + st, batch=1)
+        ga = g.step(zz)
+        oa = o.step(zz)
+        err = rel_err(ga, oa)
+        print(f"step {1000 + st}: action err {err:.2e}")
+        assert err < 2e-2
+    Xg, tg, _ = g.state()
+    assert tg == 1003
+    assert rel_err(Xg, o.X) < 2e-2
+
+
 def test_pi_b64_sampled_envs():
     s = synth.get_config("pi_b64")
     wts = synth.draw_weights(s, seed=0)
