@@ -248,7 +248,8 @@ GemmPlan plan_gemm(int M, int N, int K, bool geglu) {
     }
     p.regstream = true;
     p.tiles = tiles64;
-    p.kchunk = K >= 512 ? 512 : 256;
+    // K ranges of 512 (8 waves per block), or of 256 when that leaves fewer blocks than CUs
+    p.kchunk = (K >= 512 && (size_t)tiles64 * ((K + 511) / 512) >= 256) ? 512 : 256;
     p.ksplit = (K + p.kchunk - 1) / p.kchunk;
     const size_t tile_elems = (size_t)((M + 15) / 16) * 1024;
     p.part_elems = p.ksplit > 1 ? (size_t)p.ksplit * p.tiles * tile_elems : 0;
