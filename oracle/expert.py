@@ -17,7 +17,14 @@ here (fixed for the whole repository) are:
   embedding before the shared final silu); or, for the X-VLA way of App. A.1
   (offset_mode 1: delta concatenated to the noisy action at the action
   encoder, every slot the same delta), cond_i = silu(c_tau(i)) and the input
-  projection takes [a_i ; delta];
+  projection takes [a_i ; delta]; or, for the DynamicVLA way of App. A.1
+  (offset_mode 2), cond_i = silu(c_tau(i)) and the action encoder becomes
+  e_i = W_in a_i + b_in, g_i = W_a2 silu(W_a1 [e_i ; emb(tau_i) ; delta] + b_a1)
+  + b_a2 (the action-time MLP with delta concatenated to the action and
+  flow-time embeddings), then a gated residual adapter conditioned on the
+  offset's sinusoidal embedding: h_i = g_i + tanh(beta) W_r2 silu(W_r1 [g_i ;
+  emb(delta)] + b_r1), with a bottleneck of w/4 and emb the same sinusoid as
+  the flow time's;
 * emb(tau) = [sin(1000 tau w_j), cos(1000 tau w_j)], w_j = 10000^(-j/(w/2)),
   j < w/2;
 * every block: adaptive RMSNorm whose scale/shift/gate come from
@@ -142,18 +149,35 @@ class Expert:
     def concat_offset(self) -> bool:
         return getattr(self.s, "offset_mode", 0) == 1
 
+    def adapter_offset(self) -> bool:
+        return getattr(self.s, "offset_mode", 0) == 2
+
     def conditioning(self, delta: float, taus=None) -> np.ndarray:
-        if self.concat_offset():  # the offset enters at the action encoder instead
+        if self.concat_offset() or self.adapter_offset():  # the offset enters at the action encoder
             return silu(self.tau_conditioning(taus))
         return silu(self.tau_conditioning(taus) + self.delta_conditioning(delta)[None, :])
 
-    def encode_actions(self, a, delta: float) -> np.ndarray:
+    def encode_actions(self, a, delta: float, taus=None) -> np.ndarray:
         """Action encoder: h_i = W_in a_i + b_in; with the offset concatenated (the X-VLA
-        expert, App. A.1), h_i = W_in [a_i ; delta] + b_in for every slot i."""
+        expert, App. A.1), h_i = W_in [a_i ; delta] + b_in for every slot i; in the
+        DynamicVLA form (App. A.1) the action-time MLP over [e_i ; emb(tau_i) ; delta]
+        followed by the offset-conditioned gated residual adapter."""
         W = self.W
         if self.concat_offset():
             a = np.concatenate([a, np.full((a.shape[0], 1), delta, dtype=a.dtype)], axis=1)
-        return linear(a, W["in.w"], W["in.b"])
+        h = linear(a, W["in.w"], W["in.b"])
+        if not self.adapter_offset():
+            return h
+        n = h.shape[0]
+        t = flow_times(self.s.horizon) if taus is None else np.asarray(taus, dtype=np.float64)
+        # action-time MLP: action embedding, flow-time embedding and the offset side by side
+        z = np.concatenate([h, time_embedding(t, self.s.width).astype(self.dt),
+                            np.full((n, 1), delta, dtype=self.dt)], axis=1)
+        g = linear(silu(linear(z, W["at.w1"], W["at.b1"])), W["at.w2"], W["at.b2"])
+        # gated residual adapter on the action tokens, conditioned on emb(delta)
+        ed = np.repeat(time_embedding([delta], self.s.width).astype(self.dt), n, axis=0)
+        r = silu(linear(np.concatenate([g, ed], axis=1), W["ta.w1"], W["ta.b1"]))
+        return g + np.tanh(W["ta.alpha"][0]) * linear(r, W["ta.w2"])
 
     # -- one pass ---------------------------------------------------------
     def velocity(self, a_slots, ctx_k, ctx_v, delta: float, z=None, hooks=None, taus=None) -> np.ndarray:
@@ -174,7 +198,7 @@ class Expert:
         a = np.asarray(a_slots, dtype=dt)
         d_eff = 0.0 if "delta" in hooks else delta
         cond = self.conditioning(d_eff, taus)
-        h = self.encode_actions(a, d_eff)
+        h = self.encode_actions(a, d_eff, taus)
         adapters = set(s.adapter_layers())
         for l in range(s.layers):
             p = f"layers.{l}."

@@ -39,9 +39,12 @@ ANALYTIC_OT = 1
 ANALYTIC_LINEAR = 2
 
 # how the context-age offset enters the expert: an MLP of it added to the
-# flow-time embedding, or concatenated to every slot's action input
+# flow-time embedding, concatenated to every slot's action input, or (the
+# DynamicVLA way) concatenated before the action-time MLP plus a gated residual
+# adapter conditioned on its sinusoidal embedding
 OFFSET_MLP = 0
 OFFSET_CONCAT = 1
+OFFSET_ADAPTER = 2
 
 
 @dataclasses.dataclass(frozen=True)
@@ -85,6 +88,10 @@ class RavelShape:
         s = self.fop_stride
         return [l for l in range(self.layers) if l % s == s - 1]
 
+    def adapter_rank(self) -> int:
+        """Bottleneck width of the offset adapter (OFFSET_ADAPTER): a quarter of the width."""
+        return self.width // 4
+
 
 CONFIGS: Dict[str, RavelShape] = {
     "tiny_fp32": RavelShape(
@@ -127,8 +134,12 @@ def weight_shapes(s: RavelShape, with_fop_encoder: bool = True) -> List[Tuple[st
         ("time.w1", (w, w)), ("time.b1", (w,)),
         ("time.w2", (w, w)), ("time.b2", (w,)),
     ]
-    if not concat:
+    if s.offset_mode == OFFSET_MLP:
         out += [("delta.w1", (w, 1)), ("delta.b1", (w,)), ("delta.w2", (w, w)), ("delta.b2", (w,))]
+    if s.offset_mode == OFFSET_ADAPTER:
+        r = s.adapter_rank()
+        out += [("at.w1", (w, 2 * w + 1)), ("at.b1", (w,)), ("at.w2", (w, w)), ("at.b2", (w,)),
+                ("ta.w1", (r, 2 * w)), ("ta.b1", (r,)), ("ta.w2", (w, r)), ("ta.alpha", (1,))]
     qd = s.n_q_heads * s.head_dim
     kvd = s.n_kv_heads * s.head_dim
     adapters = set(s.adapter_layers())
@@ -211,7 +222,7 @@ def draw_weights(s: RavelShape, seed: int = 0, stress: bool = False,
             std = 1.0 / np.sqrt(shp[1])
         a = _normal(_rng(seed, name), shp, std)
         if stress:
-            if name.endswith("fop.alpha"):
+            if name.endswith("alpha"):
                 a[:] = 1.0
             if name.endswith(".mod.b") and not name.startswith("final"):
                 a[2 * w:3 * w] += 1.0
