@@ -83,16 +83,32 @@ typedef struct {
                                               action at the action encoder (the X-VLA
                                               expert): in.w is [w, D_a + 1], its last
                                               column multiplies delta, and the
-                                              conditioning is silu(c_tau(i)) alone   */
+                                              conditioning is silu(c_tau(i)) alone;
+                          RAVEL_OFFSET_ADAPTER delta concatenated with the action and
+                                              flow-time embeddings before an
+                                              action-time MLP, whose tokens then pass
+                                              a gated residual adapter conditioned on
+                                              delta's sinusoidal embedding (the
+                                              DynamicVLA expert, App. A.1):
+                                              e_i = in.w a_i + in.b,
+                                              g_i = at.w2 silu(at.w1 [e_i; emb(tau_i);
+                                              delta] + at.b1) + at.b2,
+                                              h_i = g_i + tanh(ta.alpha) ta.w2
+                                              silu(ta.w1 [g_i; emb(delta)] + ta.b1),
+                                              emb the flow-time sinusoid; the
+                                              conditioning is silu(c_tau(i)) alone;
+                                              w a multiple of 32                     */
 } ravel_config;
 
-enum { RAVEL_OFFSET_MLP = 0, RAVEL_OFFSET_CONCAT = 1 };
+enum { RAVEL_OFFSET_MLP = 0, RAVEL_OFFSET_CONCAT = 1, RAVEL_OFFSET_ADAPTER = 2 };
 
 /* A named host or device tensor, row-major, [out, in] for linear layers.
  * dtype RAVEL_F32 or RAVEL_BF16 (raw bf16 bits).  Names and shapes:
  *   in.w [w,D_a] ([w,D_a+1] with RAVEL_OFFSET_CONCAT)  in.b [w]
  *   time.w1 [w,w] time.b1 [w] time.w2 [w,w] time.b2 [w]
  *   delta.w1 [w,1] delta.b1 [w] delta.w2 [w,w] delta.b2 [w]  (RAVEL_OFFSET_MLP only)
+ *   at.w1 [w,2w+1] at.b1 [w] at.w2 [w,w] at.b2 [w]
+ *   ta.w1 [w/4,2w] ta.b1 [w/4] ta.w2 [w,w/4] ta.alpha [1]     (RAVEL_OFFSET_ADAPTER only)
  *   layers.<l>.mod.w [6w,w] .mod.b [6w] .qkv.w [(nq+2nkv)hd,w] .o.w [w,nq hd]
  *   layers.<l>.gate.w [F,w] .up.w [F,w] .down.w [w,F]
  *   adapter layers: layers.<l>.fop.gamma [w] .fop.q.w [nq hd,w]

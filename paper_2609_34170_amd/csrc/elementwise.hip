@@ -237,15 +237,15 @@ template hipError_t launch_delta_hidden<bf16_t>(const int64_t*, const int64_t*, 
 
 // Offset of every env (concatenated to its slots' inputs): same age rule as the MLP's.
 __global__ void offset_value_kernel(const int64_t* t, const int64_t* t_obs, const int64_t* ages, int B, int H,
-                                    float delta_bias, float* dval) {
+                                    float delta_bias, double* dval) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= B) return;
-  const float p = ages ? (float)ages[e] : (t ? (float)(*t - t_obs[e]) : 0.f);
-  dval[e] = p / (float)H + delta_bias;
+  const double p = ages ? (double)ages[e] : (t ? (double)(*t - t_obs[e]) : 0.0);
+  dval[e] = p / (double)H + (double)delta_bias;
 }
 
 hipError_t launch_offset_value(const int64_t* t, const int64_t* t_obs, const int64_t* ages, int B, int H,
-                               float delta_bias, float* dval, hipStream_t s) {
+                               float delta_bias, double* dval, hipStream_t s) {
   hipLaunchKernelGGL(offset_value_kernel, dim3((B + 255) / 256), dim3(256), 0, s, t, t_obs, ages, B, H, delta_bias,
                      dval);
   return hipGetLastError();
@@ -421,7 +421,7 @@ constexpr int kInProjRows = 16;
 __global__ __launch_bounds__(256) void in_proj_kernel(const float* __restrict__ X, const int64_t* t, int B, int H, int D,
                                                       const float* __restrict__ w_inT, const float* __restrict__ b_in,
                                                       int w, float* __restrict__ x, InProjNorm nrm,
-                                                      const float* __restrict__ dval, int rpb, int nrowblk) {
+                                                      const double* __restrict__ dval, int rpb, int nrowblk) {
   __shared__ float xs[kInProjRows][16];
   const int tid = threadIdx.x;
   if ((int)blockIdx.y >= nrowblk) {
@@ -470,7 +470,7 @@ __global__ __launch_bounds__(256) void in_proj_kernel(const float* __restrict__ 
     const float wd = n < w ? w_inT[(size_t)D * w + n] : 0.f;
 #pragma unroll
     for (int rr = 0; rr < kInProjRows; ++rr)
-      if (rr < nrows) acc[rr] += wd * dval[(row0 + rr) / H];
+      if (rr < nrows) acc[rr] += wd * (float)dval[(row0 + rr) / H];
   }
 #pragma unroll
   for (int rr = 0; rr < kInProjRows; ++rr) {
@@ -488,7 +488,7 @@ __global__ __launch_bounds__(256) void in_proj_kernel(const float* __restrict__ 
 }
 
 hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D, const float* w_inT,
-                          const float* b_in, int w, float* x, const InProjNorm& nrm, const float* dval,
+                          const float* b_in, int w, float* x, const InProjNorm& nrm, const double* dval,
                           hipStream_t s) {
   if (nrm.p && (B * H > 64 || (w % 64) != 0)) return hipErrorInvalidValue;
   // many rows: 16 per block; few rows: one per block (more blocks, same chain per block)
@@ -505,6 +505,84 @@ hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D,
                      dval, rpb, nrowblk);
   return hipGetLastError();
 }
+
+// Block = 4 waves over 256 consecutive columns of one row (blockIdx.y < BH), or
+// shift copies (blockIdx.y >= BH): the in_proj_kernel epilogue for rows that
+// were produced elsewhere.
+__global__ __launch_bounds__(256) void norm_operands_kernel(const float* __restrict__ x, int BH, int w,
+                                                            InProjNorm nrm) {
+  const int tid = threadIdx.x;
+  if ((int)blockIdx.y >= BH) {
+    shift_copy_item(((size_t)(blockIdx.y - BH) * gridDim.x + blockIdx.x) * 256 + tid, BH, w, nrm);
+    return;
+  }
+  const int row = blockIdx.y, n = blockIdx.x * 256 + tid;
+  // w is a multiple of 64: a wave is wholly inside or wholly outside the row
+  if (n >= w) return;
+  const float v = x[(size_t)row * w + n];
+  nrm.p[(size_t)row * w + n] = f32_to_bf16((1.f + nrm.scale[(size_t)row * nrm.ldm + n]) * v);
+  const float sq = wave_sum(v * v);
+  if ((tid & 63) == 0) nrm.sumsq[(size_t)(n >> 6) * 64 + row] = sq;
+}
+
+hipError_t launch_norm_operands(const float* x, int BH, int w, const InProjNorm& nrm, hipStream_t s) {
+  if (!nrm.p || BH <= 0 || BH > 64 || (w % 64) != 0) return hipErrorInvalidValue;
+  const int cols = (w + 255) / 256;
+  int extra = 0;
+  if (nrm.cvt_chunks > 0) {
+    const size_t total = (size_t)nrm.cvt_chunks * BH * (w / 8);
+    extra = (int)((total + (size_t)cols * 256 - 1) / ((size_t)cols * 256));
+  }
+  hipLaunchKernelGGL(norm_operands_kernel, dim3(cols, BH + extra), dim3(256), 0, s, x, BH, w, nrm);
+  return hipGetLastError();
+}
+
+// Sinusoid of value v at column c of a w-wide embedding (c < w/2: sine, else
+// cosine), as the flow-time embedding, in float64.
+RAVEL_DEV float sinusoid_at(double v, int c, int w) {
+  const int half = w / 2;
+  const int jj = c < half ? c : c - half;
+  const double arg = 1000.0 * v * pow(10000.0, -(double)jj / (double)half);
+  return (float)(c < half ? sin(arg) : cos(arg));
+}
+
+// One block column range of one row; grid (ceil(ldz / 256), B * H).
+template <typename T>
+__global__ __launch_bounds__(256) void offset_rows_kernel(int mode, const float* __restrict__ x,
+                                                          const double* __restrict__ dval, int H, int w, int tau_row,
+                                                          int tau_den, T* __restrict__ z, int ldz) {
+  const int row = blockIdx.y, e = row / H, i = row % H;
+  const double dv = dval[e];
+  // mode 0: the slot's flow time; mode 1: the env's offset
+  const double tv = mode == 1 ? dv : (tau_row < 0 ? (double)(i + 1) / (double)H
+                                                  : (double)(tau_row + 1) / (double)tau_den);
+  const float* xr = x + (size_t)row * w;
+  T* zr = z + (size_t)row * ldz;
+  for (int c = blockIdx.x * 256 + threadIdx.x; c < ldz; c += gridDim.x * 256) {
+    float v = 0.f;
+    if (c < w)
+      v = xr[c];
+    else if (c < 2 * w)
+      v = sinusoid_at(tv, c - w, w);
+    else if (mode == 0 && c == 2 * w)
+      v = (float)dv;
+    zr[c] = act<T>::from_f(v);
+  }
+}
+
+template <typename T>
+hipError_t launch_offset_rows(int mode, const float* x, const double* dval, int B, int H, int w, int tau_row,
+                              int tau_den, T* z, int ldz, hipStream_t s) {
+  if (B <= 0 || (w % 2) || ldz < 2 * w + (mode == 0 ? 1 : 0) || (tau_row >= 0 && tau_den <= 0))
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(offset_rows_kernel<T>, dim3((ldz + 255) / 256, B * H), dim3(256), 0, s, mode, x, dval, H, w,
+                     tau_row, tau_den, z, ldz);
+  return hipGetLastError();
+}
+template hipError_t launch_offset_rows<float>(int, const float*, const double*, int, int, int, int, int, float*, int,
+                                              hipStream_t);
+template hipError_t launch_offset_rows<bf16_t>(int, const float*, const double*, int, int, int, int, int, bf16_t*,
+                                               int, hipStream_t);
 
 // ---------------------------------------------------------------------------
 // Analytic velocity fields

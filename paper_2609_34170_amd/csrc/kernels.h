@@ -166,12 +166,23 @@ hipError_t launch_offset_cond(const int64_t* t, const int64_t* t_obs, const int6
 // dval: NULL, or [B] offsets delta_e concatenated to every slot's input: w_inT then has
 // D + 1 rows and row D multiplies delta_e.
 hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D, const float* w_inT,
-                          const float* b_in, int w, float* x, const InProjNorm& nrm, const float* dval,
+                          const float* b_in, int w, float* x, const InProjNorm& nrm, const double* dval,
                           hipStream_t s);
+// The norm operands of InProjNorm (p, sums of squares, shift copies; nrm.p required)
+// for rows x [BH, w] produced by other kernels.  BH <= 64, w a multiple of 64.
+hipError_t launch_norm_operands(const float* x, int BH, int w, const InProjNorm& nrm, hipStream_t s);
 
-// dval[e] = p_e / H + delta_bias with p_e = ages[e], or *t - t_obs[e], or 0 (no step counter).
+// dval[e] = p_e / H + delta_bias (float64) with p_e = ages[e], or *t - t_obs[e], or 0 (no step counter).
 hipError_t launch_offset_value(const int64_t* t, const int64_t* t_obs, const int64_t* ages, int B, int H,
-                               float delta_bias, float* dval, hipStream_t s);
+                               float delta_bias, double* dval, hipStream_t s);
+// Inputs of the DynamicVLA-style offset form, row = e*H + i in logical order, emb the
+// flow-time sinusoid (launch_time_embedding's, evaluated in float64):
+//   mode 0, the action-time MLP: z[row] = [x[row] ; emb(tau) ; dval[e] ; 0 ...] up to ldz,
+//           tau = (i + 1) / H, or (tau_row + 1) / tau_den for every slot when tau_row >= 0;
+//   mode 1, the offset adapter:  z[row] = [x[row] ; emb(dval[e])] (columns >= 2w zero).
+template <typename T>
+hipError_t launch_offset_rows(int mode, const float* x, const double* dval, int B, int H, int w, int tau_row,
+                              int tau_den, T* z, int ldz, hipStream_t s);
 
 // Analytic velocity fields (logical order): OT v = (x - a*)/tau, LINEAR v = lambda x, with
 // tau = tau_i = (i+1)/H of the ring (rotated by t), or tau_all for every slot of a chunk

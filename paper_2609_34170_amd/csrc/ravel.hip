@@ -126,6 +126,11 @@ struct ravel_model {
   void* f_w2 = nullptr;
   float* f_b2 = nullptr;
   float* analytic = nullptr;
+  // DynamicVLA-style offset form: action-time MLP (first layer's inputs padded to at_kz
+  // columns: [e ; emb(tau) ; delta ; 0 ...]) and the offset adapter (bottleneck w/4)
+  void *at_w1 = nullptr, *at_w2 = nullptr, *ta_w1 = nullptr, *ta_w2 = nullptr;
+  float *at_b1 = nullptr, *at_b2 = nullptr, *ta_b1 = nullptr, *ta_alpha = nullptr;
+  int at_kz = 0;
 };
 
 namespace {
@@ -317,7 +322,9 @@ struct ravel_buffer {
   void* cond = nullptr;
   void* h1 = nullptr;
   float* dvec = nullptr;  // [B, w] offset embedding d = W_d2 h1 + b_d2
-  float* dval = nullptr;  // [B] offsets, concatenated to the slots' inputs (RAVEL_OFFSET_CONCAT)
+  double* dval = nullptr;  // [B] offsets delta_e (RAVEL_OFFSET_CONCAT, RAVEL_OFFSET_ADAPTER)
+  void* tz = nullptr;      // [BH, at_kz] inputs of the offset form's action-time MLP and adapter
+  void* th = nullptr;      // [BH, w] their hidden rows
   bf16_t* pshift = nullptr;  // persistent step: bf16 copies of the norm shifts
   float* mod = nullptr;
   void* y = nullptr;
@@ -504,8 +511,47 @@ struct PassIn {
   const float* ctau = nullptr;  // conditioning table; NULL: the model's rolling table
   int tau_row = -1;             // every slot uses this table row; -1: slot i uses row i
   const int64_t* ages = nullptr;  // [B] context age per env (device) instead of t - t_obs / 0
+  int tau_den = 0;                // with tau_row >= 0: that row's flow time is (tau_row + 1) / tau_den
   bool lead_bias = true;          // add delta_0 to the offset (inference); training uses p / H alone
 };
+
+// DynamicVLA-style offset form (App. A.1) on the encoded actions x = W_in a + b_in:
+// x = W_a2 silu(W_a1 [x ; emb(tau) ; delta] + b_a1) + b_a2 (the action-time MLP), then
+// x += tanh(beta) W_r2 silu(W_r1 [x ; emb(delta)] + b_r1) (the gated residual adapter).
+template <typename T>
+ravel_status enqueue_offset_adapter(ravel_buffer* b, hipStream_t s, KernelRecorder* rec, const PassIn& pin) {
+  ravel_model* m = b->m;
+  const ravel_config& c = m->cfg;
+  const int B = b->B, H = c.horizon, w = c.width, BH = B * H, Kz = m->at_kz, r = w / 4;
+  const double elt = (double)m->elt;
+  REC_BEGIN("offset_rows", (double)BH * w * 4 + (double)BH * Kz * elt, 0.0);
+  HIP_TRY(launch_offset_rows<T>(0, b->x, b->dval, B, H, w, pin.tau_row, pin.tau_den, (T*)b->tz, Kz, s));
+  REC_END();
+  GemmArgs e1 = epi_args(EPI_SILU_T);
+  e1.bias = m->at_b1;
+  e1.out_t = b->th;
+  e1.ldo_t = w;
+  RV_TRY(run_gemm<T>(b, s, rec, "action_time1", b->tz, Kz, m->at_w1, Kz, BH, w, Kz, e1));
+  GemmArgs e2 = epi_args(EPI_F32);
+  e2.bias = m->at_b2;
+  e2.out_f = b->x;
+  e2.ldo_f = w;
+  RV_TRY(run_gemm<T>(b, s, rec, "action_time2", b->th, w, m->at_w2, w, BH, w, w, e2));
+  REC_BEGIN("offset_rows", (double)BH * w * 4 + (double)BH * 2 * w * elt, 0.0);
+  HIP_TRY(launch_offset_rows<T>(1, b->x, b->dval, B, H, w, -1, 0, (T*)b->tz, Kz, s));
+  REC_END();
+  GemmArgs e3 = epi_args(EPI_SILU_T);
+  e3.bias = m->ta_b1;
+  e3.out_t = b->th;
+  e3.ldo_t = r;
+  RV_TRY(run_gemm<T>(b, s, rec, "offset_adapter1", b->tz, Kz, m->ta_w1, 2 * w, BH, r, 2 * w, e3));
+  GemmArgs e4 = epi_args(EPI_RESID_TANH);
+  e4.gate_scalar = m->ta_alpha;
+  e4.out_f = b->x;
+  e4.ldo_f = w;
+  RV_TRY(run_gemm<T>(b, s, rec, "offset_adapter2", b->th, r, m->ta_w2, r, BH, w, r, e4));
+  return RAVEL_OK;
+}
 
 template <typename T>
 ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s, KernelRecorder* rec,
@@ -520,11 +566,13 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
   const double elt = (double)m->elt;
 
   // 1. offset conditioning: delta_e = p/H + delta_0, d = W_d2 silu(W_d1 delta + b_d1) + b_d2,
-  //    cond[e,i] = silu(c_tau(i) + d); or, with the offset concatenated to the inputs,
-  //    cond[e,i] = silu(c_tau(i)) and delta_e goes to the input projection
+  //    cond[e,i] = silu(c_tau(i) + d); or, with the offset concatenated to the inputs (or
+  //    fed to the action-time MLP and adapter), cond[e,i] = silu(c_tau(i)) and delta_e
+  //    goes to the action encoder
   const bool concat = c.offset_mode == RAVEL_OFFSET_CONCAT;
+  const bool no_mlp = c.offset_mode != RAVEL_OFFSET_MLP;
   const float dbias = pin.lead_bias ? c.delta_bias : 0.f;
-  if (concat) {
+  if (no_mlp) {
     REC_BEGIN("offset_value", (double)B * 12, 0.0);
     HIP_TRY(launch_offset_value(pin.X ? nullptr : b->t, b->t_obs, pin.ages, B, H, dbias, b->dval, s));
     REC_END();
@@ -544,7 +592,7 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
     HIP_TRY(launch_cond_groups(pin.ages ? pin.ages : b->t_obs, B, H, b->cgrp, b->crowmap, b->crows, s));
     REC_END();
   }
-  if (!concat) {
+  if (!no_mlp) {
     GemmArgs e = epi_args(EPI_F32);
     e.bias = m->d_b2;
     e.out_f = b->dvec;
@@ -552,7 +600,7 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
     RV_TRY(run_gemm<T>(b, s, rec, "cond", b->h1, w, m->d_w2, w, B, w, w, e));
   }
   REC_BEGIN("cond_expand", (double)B * w * 4 + (double)H * w * 4 + (double)BH * w * elt, (double)BH * w * 4);
-  HIP_TRY(launch_cond_expand<T>(concat ? nullptr : b->dvec, B, H, w, pin.ctau ? pin.ctau : m->ctau, pin.tau_row,
+  HIP_TRY(launch_cond_expand<T>(no_mlp ? nullptr : b->dvec, B, H, w, pin.ctau ? pin.ctau : m->ctau, pin.tau_row,
                                 b->cgroups ? b->cgrp : nullptr, (T*)b->cond, s));
   REC_END();
   // 2. input projection of the buffer in logical order
@@ -560,6 +608,7 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
   HIP_TRY(launch_in_proj(pin.X ? pin.X : b->X, pin.X ? nullptr : b->t, B, H, D, m->in_wT, m->in_b, w, b->x,
                          InProjNorm{}, concat ? b->dval : nullptr, s));
   REC_END();
+  if (c.offset_mode == RAVEL_OFFSET_ADAPTER) RV_TRY(enqueue_offset_adapter<T>(b, s, rec, pin));
   // FOP adapter keys/values of every adapter layer at once
   if (m->n_ad > 0) {
     GemmArgs e = epi_args(EPI_T);
@@ -1084,8 +1133,9 @@ ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream
   const int kvd = c.n_kv_heads * c.head_dim;
   const double elt = (double)m->elt;
   const bool concat = c.offset_mode == RAVEL_OFFSET_CONCAT;
+  const bool adapter = c.offset_mode == RAVEL_OFFSET_ADAPTER;
   const float dbias = pin.lead_bias ? c.delta_bias : 0.f;
-  if (concat) {
+  if (concat || adapter) {
     REC_BEGIN("offset_value", (double)B * 12, 0.0);
     HIP_TRY(launch_offset_value(pin.X ? nullptr : b->t, b->t_obs, pin.ages, B, H, dbias, b->dval, s));
     REC_END();
@@ -1124,10 +1174,23 @@ ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream
     nrm.cvt_stride = 3 * w;
     nrm.cvt_chunks = 2 * c.layers + 1;
     nrm.cvt_out = b->pshift;
-    REC_BEGIN("in_proj", (double)BH * (D + w) * 4 + (double)BH * w * (6 + nrm.cvt_chunks * 6), 2.0 * BH * w * D);
-    HIP_TRY(launch_in_proj(pin.X ? pin.X : b->X, pin.X ? nullptr : b->t, B, H, D, m->in_wT, m->in_b, w, b->x, nrm,
-                           concat ? b->dval : nullptr, s));
-    REC_END();
+    if (adapter) {
+      // the first norm's operands come from the offset form's tokens
+      REC_BEGIN("in_proj", (double)BH * (D + w) * 4, 2.0 * BH * w * D);
+      HIP_TRY(launch_in_proj(pin.X ? pin.X : b->X, pin.X ? nullptr : b->t, B, H, D, m->in_wT, m->in_b, w, b->x,
+                             InProjNorm{}, nullptr, s));
+      REC_END();
+      RV_TRY(enqueue_offset_adapter<bf16_t>(b, s, rec, pin));
+      REC_BEGIN("norm_operands", (double)BH * w * (10 + nrm.cvt_chunks * 6), 0.0);
+      HIP_TRY(launch_norm_operands(b->x, BH, w, nrm, s));
+      REC_END();
+    } else {
+      REC_BEGIN("in_proj", (double)BH * (D + w) * 4 + (double)BH * w * (6 + nrm.cvt_chunks * 6),
+                2.0 * BH * w * D);
+      HIP_TRY(launch_in_proj(pin.X ? pin.X : b->X, pin.X ? nullptr : b->t, B, H, D, m->in_wT, m->in_b, w, b->x,
+                             nrm, concat ? b->dval : nullptr, s));
+      REC_END();
+    }
   }
   if (m->n_ad > 0) {
     GemmArgs e = epi_args(EPI_T);
@@ -1262,9 +1325,13 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
     return RAVEL_OK;
   }
   if (c.model_kind != RAVEL_TRANSFORMER) return bail(fail(RAVEL_E_INVALID, "model_kind"));
-  if (c.offset_mode != RAVEL_OFFSET_MLP && c.offset_mode != RAVEL_OFFSET_CONCAT)
+  if (c.offset_mode != RAVEL_OFFSET_MLP && c.offset_mode != RAVEL_OFFSET_CONCAT &&
+      c.offset_mode != RAVEL_OFFSET_ADAPTER)
     return bail(fail(RAVEL_E_INVALID, "offset_mode"));
   const bool concat = c.offset_mode == RAVEL_OFFSET_CONCAT;
+  const bool oadapter = c.offset_mode == RAVEL_OFFSET_ADAPTER;
+  if (oadapter && w % 32)
+    return bail(fail(RAVEL_E_SHAPE, "RAVEL_OFFSET_ADAPTER needs a width that is a multiple of 32"));
   const int Din = D + (concat ? 1 : 0);  // input features of the action encoder
   const int nq = c.n_q_heads, nkv = c.n_kv_heads, hd = c.head_dim, F = c.mlp_dim, L = c.layers;
   if (w <= 0 || w % 8 || nq <= 0 || nkv <= 0 || nq % nkv || hd % 32 || hd > 256 || F <= 0 || F % 16 ||
@@ -1293,11 +1360,21 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
   CHK("time.b1", w);
   CHK("time.w2", w, w);
   CHK("time.b2", w);
-  if (!concat) {
+  if (c.offset_mode == RAVEL_OFFSET_MLP) {
     CHK("delta.w1", w, 1);
     CHK("delta.b1", w);
     CHK("delta.w2", w, w);
     CHK("delta.b2", w);
+  }
+  if (oadapter) {
+    CHK("at.w1", w, 2 * w + 1);
+    CHK("at.b1", w);
+    CHK("at.w2", w, w);
+    CHK("at.b2", w);
+    CHK("ta.w1", w / 4, 2 * w);
+    CHK("ta.b1", w / 4);
+    CHK("ta.w2", w, w / 4);
+    CHK("ta.alpha", 1);
   }
   CHK("final.mod.w", 3 * w, w);
   CHK("final.mod.b", 3 * w);
@@ -1361,6 +1438,17 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
     }
   }
   if (n_ad > 0) ar.want(&m->kva_w, (size_t)n_ad * 2 * kvd * w * E);
+  if (oadapter) {
+    m->at_kz = 2 * w + 64;
+    ar.want(&m->at_w1, (size_t)w * m->at_kz * E);
+    ar.want(&m->at_w2, (size_t)w * w * E);
+    ar.want(&m->ta_w1, (size_t)(w / 4) * 2 * w * E);
+    ar.want(&m->ta_w2, (size_t)w * (w / 4) * E);
+    ar.want((void**)&m->at_b1, (size_t)w * 4);
+    ar.want((void**)&m->at_b2, (size_t)w * 4);
+    ar.want((void**)&m->ta_b1, (size_t)(w / 4) * 4);
+    ar.want((void**)&m->ta_alpha, 4);
+  }
   ar.want(&m->out_w, (size_t)D * w * E);
   ar.want((void**)&m->out_b, (size_t)D * 4);
   if (m->has_fop_encoder) {
@@ -1402,7 +1490,27 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
   if (launch_transpose_f32(m->in_w, w, Din, m->in_wT, 0) != hipSuccess)
     return bail(done(fail(RAVEL_E_HIP, "in.w transpose")));
   UP("in.b", m->in_b, false);
-  if (!concat) {
+  if (oadapter) {
+    // action-time MLP, first layer: [w, 2w + 1] rows placed in [w, at_kz] with zero padding
+    const size_t src_row = (size_t)(2 * w + 1) * E, dst_row = (size_t)m->at_kz * E;
+    void* tmp = nullptr;
+    if (hipMalloc(&tmp, (size_t)w * src_row) != hipSuccess) return bail(done(fail(RAVEL_E_NOMEM, "at.w1 staging")));
+    st = up("at.w1", tmp, true);
+    if (st == RAVEL_OK && (hipMemset(m->at_w1, 0, (size_t)w * dst_row) != hipSuccess ||
+                           hipMemcpy2D(m->at_w1, dst_row, tmp, src_row, src_row, w, hipMemcpyDeviceToDevice) !=
+                               hipSuccess))
+      st = fail(RAVEL_E_HIP, "at.w1 upload");
+    (void)hipFree(tmp);
+    if (st != RAVEL_OK) return bail(done(st));
+    UP("at.b1", m->at_b1, false);
+    UP("at.w2", m->at_w2, true);
+    UP("at.b2", m->at_b2, false);
+    UP("ta.w1", m->ta_w1, true);
+    UP("ta.b1", m->ta_b1, false);
+    UP("ta.w2", m->ta_w2, true);
+    UP("ta.alpha", m->ta_alpha, false);
+  }
+  if (c.offset_mode == RAVEL_OFFSET_MLP) {
     UP("delta.w1", m->d_w1, false);
     UP("delta.b1", m->d_b1, false);
     UP("delta.w2", m->d_w2, true);
@@ -1465,7 +1573,8 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
 #undef UP
   if (hipDeviceSynchronize() != hipSuccess) return bail(fail(RAVEL_E_HIP, "create sync"));
   // algorithmic weight bytes streamed by one step (time MLP excluded: precomputed)
-  int64_t wb = (int64_t)w * Din * 4 + (concat ? 0 : (int64_t)w * w * E);
+  int64_t wb = (int64_t)w * Din * 4 + (c.offset_mode == RAVEL_OFFSET_MLP ? (int64_t)w * w * E : 0);
+  if (oadapter) wb += ((int64_t)w * m->at_kz + (int64_t)w * w + (int64_t)w * w / 2 + (int64_t)w * w / 4) * E;
   for (int l = 0; l < L; ++l) {
     wb += (int64_t)(6 * w + qkvd) * w * E + (int64_t)w * qd * E + (int64_t)3 * F * w * E + 6 * w * 4;
     if (ad_of[l] >= 0) wb += (int64_t)(2 * qd + 2 * kvd) * w * E;
@@ -1516,7 +1625,11 @@ ravel_status ravel_buffer_create(ravel_model* m, int32_t batch, uint64_t seed, r
     ar.want(&b->cond, (size_t)BH * w * E);
     ar.want(&b->h1, (size_t)B * w * E);
     ar.want((void**)&b->dvec, (size_t)B * w * 4);
-    ar.want((void**)&b->dval, (size_t)B * 4);
+    ar.want((void**)&b->dval, (size_t)B * 8);
+    if (m->at_kz > 0) {
+      ar.want(&b->tz, (size_t)BH * m->at_kz * E);
+      ar.want(&b->th, (size_t)BH * w * E);
+    }
     // few rows: every layer's modulation comes from one GEMM at the start of the step
     // Few rows, or rows grouped by offset conditioning: every layer's modulation
     // comes from one GEMM at the start of the step (on the groups' rows only).
@@ -1546,6 +1659,11 @@ ravel_status ravel_buffer_create(ravel_model* m, int32_t batch, uint64_t seed, r
                                  {BH, w, F, false}, {BH, 2 * w, w, false}, {BH, D, w, false},
                                  {B, w, std::max(c.fop_obs_dim, 8), false}, {B, c.n_fop * w, w, false}};
     if (m->n_ad > 0) shapes.push_back({B * c.n_fop, m->n_ad * 2 * kvd, w, false});
+    if (m->at_kz > 0) {
+      shapes.push_back({BH, w, m->at_kz, false});
+      shapes.push_back({BH, w / 4, 2 * w, false});
+      shapes.push_back({BH, w, w / 4, false});
+    }
     for (auto& s : shapes) {
       if (s.N <= 0 || s.M <= 0) continue;
       const GemmPlan p = plan_gemm(s.M, s.N, s.K, s.geglu);
@@ -1730,6 +1848,7 @@ ravel_status ravel_full_denoise(ravel_buffer* b, int32_t steps, const void* fop,
       pin.X = chunk;
       pin.ctau = table;
       pin.tau_row = steps - 1 - k;
+      pin.tau_den = steps;
       if (b->persistent)
         RV_TRY(enqueue_persistent_pass(b, fop, s, nullptr, pin));
       else if (m->bf16)
