@@ -22,6 +22,9 @@ Prints ONE JSON line.  Extra measurements:
                   and loss) over the batch of 64 with random context ages;
   * relative_actions -- the step with every action dimension relative to a
                   moving robot state (batch-1 workloads);
+  * offset_forms -- the step with the offset fed the X-VLA way (concatenated to
+                  the action input) and the DynamicVLA way (action-time MLP plus
+                  offset-conditioned adapter), batch-1 workloads;
   * full_denoise -- the full-horizon synchronous baseline on the same kernels
                   (batch-1 workloads): ms per chunk of 10 and of H Euler steps
                   and its first-action time relative to one rolling step;
@@ -291,6 +294,42 @@ class Workload:
         buf.close()
         return e0.elapsed_time(e1) / steps
 
+    def offset_form_timing(self, mode, steps, warmup=20):
+        """The step with the offset fed the X-VLA way (mode 1: concatenated to the
+        action input) or the DynamicVLA way (mode 2: in the action-time MLP plus the
+        offset-conditioned adapter): a model of the same widths that shares every
+        other weight, on the same context; ms per step."""
+        torch = self.torch
+        import synth
+        from paper_2609_34170_amd import ravel
+        WL = synth.workloads
+        s = self.s.replace(offset_mode=mode)
+        shapes = dict(WL.weight_shapes(s))
+        W = {k: v for k, v in self.W.items() if k in shapes and tuple(v.shape) == tuple(shapes[k])}
+        rng = np.random.default_rng(7 + mode)
+        for k, shp in shapes.items():
+            if k not in W:
+                a = (0.02 * rng.standard_normal(shp)).astype(np.float32)
+                W[k] = WL.bf16_round(a) if s.dtype == WL.BF16 else a
+        model = ravel.Model(s, W)
+        buf = ravel.Buffer(model, self.B, 1)
+        k, v = self.ctx[0]
+        for e in range(self.B):
+            buf.set_context(e, k[e], v[e], 0)
+        buf.sync()
+        for _ in range(warmup):
+            buf.step(self.fop, self.action)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(self.stream)
+        for _ in range(steps):
+            buf.step(self.fop, self.action)
+        e1.record(self.stream)
+        torch.cuda.synchronize()
+        buf.close()
+        model.close()
+        return e0.elapsed_time(e1) / steps
+
     def latencies(self, n):
         torch = self.torch
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
@@ -445,6 +484,13 @@ def main():
         out["relative_actions"] = {"ms_per_step": round(rms, 4), "steps_per_s": round(1000.0 / rms, 2),
                                    "vs_absolute_step": round(rms / ms, 4)}
         log(f"[{s.name}] relative actions: {rms * 1e3:.1f} us/step")
+        # the other two ways of feeding the offset (App. A.1) on models of the same widths
+        out["offset_forms"] = {}
+        for mode, key in ((1, "concat_xvla"), (2, "adapter_dynamicvla")):
+            oms = wl.offset_form_timing(mode, max(20, min(200, args.steps // 2)))
+            out["offset_forms"][key] = {"ms_per_step": round(oms, 4), "steps_per_s": round(1000.0 / oms, 2),
+                                        "vs_mlp_step": round(oms / ms, 4)}
+            log(f"[{s.name}] offset form {key}: {oms * 1e3:.1f} us/step")
         # the synchronous baseline on the same kernels: a chunk needs `steps` expert
         # passes before its first action, a rolling step one (Sec. 4.1 latency table)
         out["full_denoise"] = [
