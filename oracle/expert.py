@@ -31,7 +31,8 @@ here (fixed for the whole repository) are:
   Linear(cond) per token (six chunks per layer, three for the final norm of
   which the third is unused); residual updates are gated x += g * f(.);
 * attention: bidirectional over [prefix tokens ; buffer tokens], no mask, no
-  positional encoding, grouped-query heads (query head j uses KV head
+  positional encoding (optionally a rotary one on the buffer tokens, see
+  rope_rotate), grouped-query heads (query head j uses KV head
   floor(j * n_kv / n_q)), scale 1/sqrt(hd), no biases on attention/MLP linears;
 * MLP: gated GeLU (tanh form), down(gelu_tanh(gate y) * up y);
 * FOP adapter in layers l with l % stride == stride - 1: rms(x) (1 + gamma) ->
@@ -84,6 +85,28 @@ def time_embedding(tau, width: int) -> np.ndarray:
     omega = 10000.0 ** (-j / half)
     arg = 1000.0 * np.asarray(tau, dtype=np.float64)[:, None] * omega[None, :]
     return np.concatenate([np.sin(arg), np.cos(arg)], axis=1)
+
+
+def rope_rotate(x, pos, n_heads: int, hd: int, base: float):
+    """Rotary position embedding, rotate-half pairing: in every head, the pair
+    (x_d, x_{d + hd/2}), d < hd/2, turns by the angle pos * base^(-2d/hd).
+
+    x: [T, n_heads * hd]; pos: [T] positions.  The paper uses no positional
+    encoding of the buffer tokens; this optional variant places logical slot i at
+    position P + i, after the P prefix tokens, whose cached keys are taken as
+    already encoded by the VLM and are used as given.
+    """
+    half = hd // 2
+    theta = np.asarray(base, dtype=np.float64) ** (-2.0 * np.arange(half, dtype=np.float64) / hd)
+    ang = np.asarray(pos, dtype=np.float64)[:, None] * theta[None, :]
+    c, s_ = np.cos(ang).astype(x.dtype), np.sin(ang).astype(x.dtype)
+    out = np.empty_like(x)
+    for j in range(n_heads):
+        a = x[:, j * hd:j * hd + half]
+        b = x[:, j * hd + half:(j + 1) * hd]
+        out[:, j * hd:j * hd + half] = a * c - b * s_
+        out[:, j * hd + half:(j + 1) * hd] = b * c + a * s_
+    return out
 
 
 def linear(x, w, b=None):
@@ -180,7 +203,8 @@ class Expert:
         return g + np.tanh(W["ta.alpha"][0]) * linear(r, W["ta.w2"])
 
     # -- one pass ---------------------------------------------------------
-    def velocity(self, a_slots, ctx_k, ctx_v, delta: float, z=None, hooks=None, taus=None) -> np.ndarray:
+    def velocity(self, a_slots, ctx_k, ctx_v, delta: float, z=None, hooks=None, taus=None,
+                 pos0=None) -> np.ndarray:
         """Velocity of every slot.
 
         a_slots: [H, D_a] noisy actions in logical order (slot i has tau_i, the
@@ -189,6 +213,7 @@ class Expert:
         z: [n_fop, w] FOP tokens (ignored when the expert has no adapters).
         hooks: optional set of sub-block names to switch off ("attn",
         "adapter", "mlp", "delta") for sensitivity checks.
+        pos0: rotary position of slot 0 (default P, the prefix length).
         """
         s, W, dt = self.s, self.W, self.dt
         hooks = hooks or set()
@@ -209,6 +234,10 @@ class Expert:
             qkv = linear(y, W[p + "qkv.w"])
             q, k, v = qkv[:, :qd], qkv[:, qd:qd + kvd], qkv[:, qd + kvd:]
             P = ctx_k.shape[1] if ctx_k is not None else 0
+            if getattr(s, "rope_base", 0.0):
+                pos = (P if pos0 is None else pos0) + np.arange(a.shape[0])
+                q = rope_rotate(q, pos, nq, hd, s.rope_base)
+                k = rope_rotate(k, pos, nkv, hd, s.rope_base)
             if P:
                 kp = np.asarray(ctx_k[l], dtype=dt).reshape(P, kvd)
                 vp = np.asarray(ctx_v[l], dtype=dt).reshape(P, kvd)

@@ -68,6 +68,9 @@ class RavelShape:
     delta_bias: float = 0.0
     rms_eps: float = 1e-6
     offset_mode: int = OFFSET_MLP
+    # rotary position embedding of the buffer tokens' self-attention queries and
+    # keys at positions P + i (0: none)
+    rope_base: float = 0.0
     # workload (not model) fields
     batch: int = 1
     steps: int = 200
