@@ -584,6 +584,31 @@ template hipError_t launch_offset_rows<float>(int, const float*, const double*, 
 template hipError_t launch_offset_rows<bf16_t>(int, const float*, const double*, int, int, int, int, int, bf16_t*,
                                                int, hipStream_t);
 
+// Rotary position embedding in place; grid (ceil(nh * hd/2 / 256), B * H), one thread per pair.
+template <typename T>
+__global__ __launch_bounds__(256) void rope_kernel(T* __restrict__ qkv, int ld, int H, int nh, int hd,
+                                                   const float* __restrict__ cs) {
+  const int row = blockIdx.y, i = row % H, half = hd / 2;
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= nh * half) return;
+  const int h = idx / half, d = idx - h * half;
+  T* p = qkv + (size_t)row * ld + (size_t)h * hd + d;
+  const float c = cs[((size_t)i * half + d) * 2], sn = cs[((size_t)i * half + d) * 2 + 1];
+  const float a = act<T>::to_f(p[0]), b = act<T>::to_f(p[half]);
+  p[0] = act<T>::from_f(a * c - b * sn);
+  p[half] = act<T>::from_f(b * c + a * sn);
+}
+
+template <typename T>
+hipError_t launch_rope(T* qkv, int ld, int BH, int H, int nq, int nkv, int hd, const float* cs, hipStream_t s) {
+  const int nh = nq + nkv;
+  if (BH <= 0 || H <= 0 || BH % H || (hd % 2) || ld < nh * hd) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rope_kernel<T>, dim3((nh * (hd / 2) + 255) / 256, BH), dim3(256), 0, s, qkv, ld, H, nh, hd, cs);
+  return hipGetLastError();
+}
+template hipError_t launch_rope<float>(float*, int, int, int, int, int, int, const float*, hipStream_t);
+template hipError_t launch_rope<bf16_t>(bf16_t*, int, int, int, int, int, int, const float*, hipStream_t);
+
 // ---------------------------------------------------------------------------
 // Analytic velocity fields
 // ---------------------------------------------------------------------------

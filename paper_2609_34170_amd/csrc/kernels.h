@@ -172,6 +172,13 @@ hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D,
 // for rows x [BH, w] produced by other kernels.  BH <= 64, w a multiple of 64.
 hipError_t launch_norm_operands(const float* x, int BH, int w, const InProjNorm& nrm, hipStream_t s);
 
+// Rotary position embedding of the buffer rows' self-attention queries and keys, in place:
+// row e*H + i of qkv (row stride ld) holds nq query heads then nkv key heads of hd columns;
+// in each, the pair (d, d + hd/2) turns by the angle whose cosine and sine are
+// cs[(i * hd/2 + d) * 2 + {0, 1}] (slot i's table row).
+template <typename T>
+hipError_t launch_rope(T* qkv, int ld, int BH, int H, int nq, int nkv, int hd, const float* cs, hipStream_t s);
+
 // dval[e] = p_e / H + delta_bias (float64) with p_e = ages[e], or *t - t_obs[e], or 0 (no step counter).
 hipError_t launch_offset_value(const int64_t* t, const int64_t* t_obs, const int64_t* ages, int B, int H,
                                float delta_bias, double* dval, hipStream_t s);

@@ -131,6 +131,7 @@ struct ravel_model {
   void *at_w1 = nullptr, *at_w2 = nullptr, *ta_w1 = nullptr, *ta_w2 = nullptr;
   float *at_b1 = nullptr, *at_b2 = nullptr, *ta_b1 = nullptr, *ta_alpha = nullptr;
   int at_kz = 0;
+  float* rope_cs = nullptr;  // [H][hd/2][2] cos, sin of slot i's rotary angles (rope_base > 0)
 };
 
 namespace {
@@ -646,6 +647,11 @@ ravel_status enqueue_transformer(ravel_buffer* b, const void* fop, hipStream_t s
       e.ldo_t = qkvd;
       RV_TRY(run_gemm<T>(b, s, rec, "qkv", b->y, w, L.qkv_w, w, BH, qkvd, w, e));
     }
+    if (m->rope_cs) {
+      REC_BEGIN("rope", (double)BH * (qd + kvd) * 2 * elt + (double)H * c.head_dim * 4, 0.0);
+      HIP_TRY(launch_rope<T>((T*)b->qkv, qkvd, BH, H, c.n_q_heads, c.n_kv_heads, c.head_dim, m->rope_cs, s));
+      REC_END();
+    }
     {
       AttnArgs a;
       memset(&a, 0, sizeof a);
@@ -838,7 +844,7 @@ ravel_status acquire_locked(ravel_buffer* b, int env, void** k, void** v, hipStr
 bool persistent_eligible(const ravel_buffer* b) {
   const ravel_model* m = b->m;
   const ravel_config& c = m->cfg;
-  if (!m->bf16 || c.model_kind != RAVEL_TRANSFORMER || !b->mod_all) return false;
+  if (!m->bf16 || c.model_kind != RAVEL_TRANSFORMER || !b->mod_all || m->rope_cs) return false;
   const int BH = b->B * c.horizon, hd = c.head_dim;
   const int qd = c.n_q_heads * hd, kvd = c.n_kv_heads * hd;
   if (BH > 64 || b->B > 64) return false;
@@ -1438,6 +1444,8 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
     }
   }
   if (n_ad > 0) ar.want(&m->kva_w, (size_t)n_ad * 2 * kvd * w * E);
+  if (c.rope_base < 0.f || c.rope_base != c.rope_base) return bail(fail(RAVEL_E_INVALID, "rope_base must be >= 0"));
+  if (c.rope_base > 0.f) ar.want((void**)&m->rope_cs, (size_t)H * hd * 4);
   if (oadapter) {
     m->at_kz = 2 * w + 64;
     ar.want(&m->at_w1, (size_t)w * m->at_kz * E);
@@ -1490,6 +1498,18 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
   if (launch_transpose_f32(m->in_w, w, Din, m->in_wT, 0) != hipSuccess)
     return bail(done(fail(RAVEL_E_HIP, "in.w transpose")));
   UP("in.b", m->in_b, false);
+  if (m->rope_cs) {
+    // rotary table: slot i at position P + i, pair d at base^(-2d/hd), in float64
+    std::vector<float> cs((size_t)H * hd);
+    for (int i = 0; i < H; ++i)
+      for (int d = 0; d < hd / 2; ++d) {
+        const double ang = (double)(c.prefix_len + i) * pow((double)c.rope_base, -2.0 * d / hd);
+        cs[((size_t)i * (hd / 2) + d) * 2] = (float)cos(ang);
+        cs[((size_t)i * (hd / 2) + d) * 2 + 1] = (float)sin(ang);
+      }
+    if (hipMemcpy(m->rope_cs, cs.data(), cs.size() * 4, hipMemcpyHostToDevice) != hipSuccess)
+      return bail(done(fail(RAVEL_E_HIP, "rope table")));
+  }
   if (oadapter) {
     // action-time MLP, first layer: [w, 2w + 1] rows placed in [w, at_kz] with zero padding
     const size_t src_row = (size_t)(2 * w + 1) * E, dst_row = (size_t)m->at_kz * E;

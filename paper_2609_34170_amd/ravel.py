@@ -34,7 +34,8 @@ class RavelConfig(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "layers", "width", "n_q_heads", "n_kv_heads", "head_dim", "mlp_dim", "horizon", "action_dim",
         "prefix_len", "n_fop", "fop_obs_dim", "fop_stride", "dtype", "model_kind")] + [
-        ("delta_bias", ctypes.c_float), ("rms_eps", ctypes.c_float), ("offset_mode", ctypes.c_int32)]
+        ("delta_bias", ctypes.c_float), ("rms_eps", ctypes.c_float), ("offset_mode", ctypes.c_int32),
+        ("rope_base", ctypes.c_float)]
 
 
 class RavelTensor(ctypes.Structure):
