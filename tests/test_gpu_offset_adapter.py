@@ -74,3 +74,17 @@ def test_training_loss_with_the_adapter_form():
     print("tiny_fp32 adapter training", _case("tiny_fp32", 3, [0, 4, 11], np.float64, offset_mode=W.OFFSET_ADAPTER))
     print("small_bf16 adapter training", _case("small_bf16", 4, [0, 2, 5, 9], np.float64, layers=2,
                                                offset_mode=W.OFFSET_ADAPTER))
+
+
+def test_ragged_shapes_with_the_adapter_form_and_rotary_positions():
+    """63 rows (3 envs x 21 slots), 77 prefix tokens, 32-dim heads, width 256 (adapter
+    bottleneck 64): the adapter form on the persistent path, then with rotary positions
+    on the per-kernel path."""
+    base = dict(layers=2, width=256, n_q_heads=4, n_kv_heads=2, head_dim=32, mlp_dim=512, horizon=21,
+                action_dim=5, prefix_len=77, n_fop=3, fop_obs_dim=16, dtype=W.BF16, batch=3,
+                offset_mode=W.OFFSET_ADAPTER, context_period=3, stagger=True, delta_bias=0.1, name="ragged_ada")
+    for rope in (0.0, 1000.0):
+        s = synth.RavelShape(rope_base=rope, **base)
+        wts = synth.draw_weights(s, seed=25, stress=True)
+        ea, ex, n = run_parity(s, wts, batch=3, seed=9, steps=9, oracle_dtype=np.float64, check_every=3)
+        print(f"ragged adapter rope={rope}: action err {ea:.2e}, state err {ex:.2e}")
