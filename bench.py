@@ -25,6 +25,8 @@ Prints ONE JSON line.  Extra measurements:
   * offset_forms -- the step with the offset fed the X-VLA way (concatenated to
                   the action input) and the DynamicVLA way (action-time MLP plus
                   offset-conditioned adapter), batch-1 workloads;
+  * rotary_positions -- the step with rotary positions of the buffer tokens
+                  (per-kernel path), batch-1 workloads;
   * full_denoise -- the full-horizon synchronous baseline on the same kernels
                   (batch-1 workloads): ms per chunk of 10 and of H Euler steps
                   and its first-action time relative to one rolling step;
@@ -294,16 +296,17 @@ class Workload:
         buf.close()
         return e0.elapsed_time(e1) / steps
 
-    def offset_form_timing(self, mode, steps, warmup=20):
+    def offset_form_timing(self, mode, steps, warmup=20, rope_base=0.0):
         """The step with the offset fed the X-VLA way (mode 1: concatenated to the
         action input) or the DynamicVLA way (mode 2: in the action-time MLP plus the
-        offset-conditioned adapter): a model of the same widths that shares every
-        other weight, on the same context; ms per step."""
+        offset-conditioned adapter), or with rotary positions of the buffer tokens
+        (rope_base > 0): a model of the same widths that shares every other weight,
+        on the same context; ms per step."""
         torch = self.torch
         import synth
         from paper_2609_34170_amd import ravel
         WL = synth.workloads
-        s = self.s.replace(offset_mode=mode)
+        s = self.s.replace(offset_mode=mode, rope_base=rope_base)
         shapes = dict(WL.weight_shapes(s))
         W = {k: v for k, v in self.W.items() if k in shapes and tuple(v.shape) == tuple(shapes[k])}
         rng = np.random.default_rng(7 + mode)
@@ -491,6 +494,11 @@ def main():
             out["offset_forms"][key] = {"ms_per_step": round(oms, 4), "steps_per_s": round(1000.0 / oms, 2),
                                         "vs_mlp_step": round(oms / ms, 4)}
             log(f"[{s.name}] offset form {key}: {oms * 1e3:.1f} us/step")
+        # rotary positions of the buffer tokens: the per-kernel path (no persistent kernel)
+        rms2 = wl.offset_form_timing(0, max(20, min(200, args.steps // 2)), rope_base=10000.0)
+        out["rotary_positions"] = {"ms_per_step": round(rms2, 4), "steps_per_s": round(1000.0 / rms2, 2),
+                                   "vs_step": round(rms2 / ms, 4), "path": "per-kernel hipGraph"}
+        log(f"[{s.name}] rotary positions: {rms2 * 1e3:.1f} us/step")
         # the synchronous baseline on the same kernels: a chunk needs `steps` expert
         # passes before its first action, a rolling step one (Sec. 4.1 latency table)
         out["full_denoise"] = [
