@@ -25,8 +25,8 @@ Prints ONE JSON line.  Extra measurements:
   * offset_forms -- the step with the offset fed the X-VLA way (concatenated to
                   the action input) and the DynamicVLA way (action-time MLP plus
                   offset-conditioned adapter), batch-1 workloads;
-  * rotary_positions -- the step with rotary positions of the buffer tokens
-                  (per-kernel path), batch-1 workloads;
+  * rotary_positions -- the step with rotary positions of the buffer tokens,
+                  batch-1 workloads;
   * full_denoise -- the full-horizon synchronous baseline on the same kernels
                   (batch-1 workloads): ms per chunk of 10 and of H Euler steps
                   and its first-action time relative to one rolling step;
@@ -494,10 +494,10 @@ def main():
             out["offset_forms"][key] = {"ms_per_step": round(oms, 4), "steps_per_s": round(1000.0 / oms, 2),
                                         "vs_mlp_step": round(oms / ms, 4)}
             log(f"[{s.name}] offset form {key}: {oms * 1e3:.1f} us/step")
-        # rotary positions of the buffer tokens: the per-kernel path (no persistent kernel)
+        # rotary positions of the buffer tokens (a rotary phase after each QKV projection)
         rms2 = wl.offset_form_timing(0, max(20, min(200, args.steps // 2)), rope_base=10000.0)
         out["rotary_positions"] = {"ms_per_step": round(rms2, 4), "steps_per_s": round(1000.0 / rms2, 2),
-                                   "vs_step": round(rms2 / ms, 4), "path": "per-kernel hipGraph"}
+                                   "vs_step": round(rms2 / ms, 4)}
         log(f"[{s.name}] rotary positions: {rms2 * 1e3:.1f} us/step")
         # the synchronous baseline on the same kernels: a chunk needs `steps` expert
         # passes before its first action, a rolling step one (Sec. 4.1 latency table)

@@ -5,7 +5,7 @@
 
 namespace ravel {
 
-enum PhaseType : int { PH_GEMM = 2, PH_ATTN = 3 };
+enum PhaseType : int { PH_GEMM = 2, PH_ATTN = 3, PH_ROPE = 4 };
 
 // GEMM activation operand
 enum PAMode : int {
@@ -67,11 +67,22 @@ struct PGemm {
   float x_scale;
 };
 
+// Rotary positions in place (the rows' queries and keys written by the phase
+// before): item = one row e*H + i of qkv (row stride ld), whose nh = nq + nkv
+// heads of hd columns each turn their pairs (d, d + hd/2) by the angle with
+// cosine cs[(i * hd/2 + d) * 2] and sine cs[(i * hd/2 + d) * 2 + 1]; hd % 8 == 0.
+struct PRope {
+  bf16_t* qkv; int ld;
+  int H, nh, hd;
+  const float* cs;
+};
+
 struct alignas(16) Phase {
   int type, items, pad0, pad1;
   union {
     PGemm g;
     AttnArgs at;
+    PRope r;
   };
 };
 

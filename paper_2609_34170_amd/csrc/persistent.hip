@@ -1086,6 +1086,39 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
 constexpr int kDescChunks = (int)(sizeof(Phase) / 16);
 static_assert(sizeof(Phase) % 16 == 0 && kDescChunks <= 256, "phase descriptor size");
 
+// One row of a rotary phase: each thread turns four consecutive pairs of one head
+// (8-byte device-coherent loads and stores of the bf16 halves; the angle table was
+// written before the launch).
+RAVEL_DEV void rope_item(const PRope& r, int row) {
+  const int i = row % r.H, half = r.hd >> 1, quads = r.nh * (half >> 2);
+  const rsrc_t q = rsrc(r.qkv + (size_t)row * r.ld);
+  const rsrc_t t = rsrc(r.cs + (size_t)i * r.hd);
+  for (int idx = local_tid(); idx < quads; idx += 256) {
+    const int h = idx / (half >> 2), d = (idx - h * (half >> 2)) * 4;
+    const int o0 = (h * r.hd + d) * 2, o1 = o0 + half * 2;
+    const auto a = __builtin_amdgcn_raw_buffer_load_b64(q, o0, 0, COH);
+    const auto b = __builtin_amdgcn_raw_buffer_load_b64(q, o1, 0, COH);
+    const f32x4_t c01 = ld_f4<PLAIN>(t, d * 8), c23 = ld_f4<PLAIN>(t, d * 8 + 16);
+    const float cs[8] = {c01[0], c01[1], c01[2], c01[3], c23[0], c23[1], c23[2], c23[3]};
+    float x[4], y[4];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      x[2 * j] = __uint_as_float(a[j] << 16);
+      x[2 * j + 1] = __uint_as_float(a[j] & 0xFFFF0000u);
+      y[2 * j] = __uint_as_float(b[j] << 16);
+      y[2 * j + 1] = __uint_as_float(b[j] & 0xFFFF0000u);
+    }
+    float u[4], v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      u[j] = x[j] * cs[2 * j] - y[j] * cs[2 * j + 1];
+      v[j] = y[j] * cs[2 * j] + x[j] * cs[2 * j + 1];
+    }
+    st_bf16x4(q, (size_t)o0, u[0], u[1], u[2], u[3]);
+    st_bf16x4(q, (size_t)o1, v[0], v[1], v[2], v[3]);
+  }
+}
+
 template <int MT, int HD>
 __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __restrict__ phases, int nphase,
                                                               const int* __restrict__ env_slot, int nenv,
@@ -1151,6 +1184,9 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
         for (int i = 0; i < 8; ++i) kv[i] = pre[i];
         attn_item<HD>(a, item, slots, err, sm, kv, item == (int)blockIdx.x && kv_ready, none);
       }
+    } else if (type == PH_ROPE) {
+      const PRope r = make_uniform(ph.r);
+      for (int item = blockIdx.x; item < items; item += gridDim.x) rope_item(r, item);
     }
     if (p + 1 == nphase) break;
     // barrier between phases p and p + 1; while waiting, fetch descriptor p + 2

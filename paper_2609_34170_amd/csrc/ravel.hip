@@ -844,7 +844,7 @@ ravel_status acquire_locked(ravel_buffer* b, int env, void** k, void** v, hipStr
 bool persistent_eligible(const ravel_buffer* b) {
   const ravel_model* m = b->m;
   const ravel_config& c = m->cfg;
-  if (!m->bf16 || c.model_kind != RAVEL_TRANSFORMER || !b->mod_all || m->rope_cs) return false;
+  if (!m->bf16 || c.model_kind != RAVEL_TRANSFORMER || !b->mod_all) return false;
   const int BH = b->B * c.horizon, hd = c.head_dim;
   const int qd = c.n_q_heads * hd, kvd = c.n_kv_heads * hd;
   if (BH > 64 || b->B > 64) return false;
@@ -989,6 +989,19 @@ ravel_status build_persistent(ravel_buffer* b) {
       ph.g.ldo = qkvd;
       push(ph, "qkv");
     }
+    if (m->rope_cs) {
+      Phase ph;
+      memset(&ph, 0, sizeof ph);
+      ph.type = PH_ROPE;
+      ph.items = BH;
+      ph.r.qkv = (bf16_t*)b->qkv;
+      ph.r.ld = qkvd;
+      ph.r.H = H;
+      ph.r.nh = c.n_q_heads + c.n_kv_heads;
+      ph.r.hd = hd;
+      ph.r.cs = m->rope_cs;
+      push(ph, "rope");
+    }
     {
       AttnArgs a;
       memset(&a, 0, sizeof a);
@@ -1121,6 +1134,8 @@ ravel_status build_persistent(ravel_buffer* b) {
       const int nk = ph.at.P + ph.at.S;
       b->ph_bytes[i] = (double)B * nk * kvd * 4;
       b->ph_flops[i] = 4.0 * B * c.n_q_heads * H * nk * hd;
+    } else if (ph.type == PH_ROPE) {  // the angle table (the rows stay in L2)
+      b->ph_bytes[i] = (double)H * hd * 4;
     }
     by += b->ph_bytes[i];
     fl += b->ph_flops[i];

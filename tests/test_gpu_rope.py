@@ -21,28 +21,29 @@ def test_tiny_fp32_rope_roll_matches_oracle():
     print(f"tiny_fp32 rope: {n} steps, action err {ea:.2e}, state err {ex:.2e}")
 
 
-def test_small_bf16_rope_roll_matches_oracle():
+@pytest.mark.parametrize("persistent", [True, False])
+def test_small_bf16_rope_roll_matches_oracle_on_both_paths(persistent, monkeypatch):
+    if not persistent:
+        monkeypatch.setenv("RAVEL_NO_PERSISTENT", "1")
     s = synth.get_config("small_bf16").replace(layers=2, rope_base=100.0, context_period=4)
     wts = synth.draw_weights(s, seed=32, stress=True)
     ea, ex, n = run_parity(s, wts, batch=2, seed=6, steps=24, oracle_dtype=np.float64, check_every=8)
-    print(f"small_bf16 rope: action err {ea:.2e}, state err {ex:.2e}")
+    print(f"small_bf16 rope persistent={persistent}: action err {ea:.2e}, state err {ex:.2e}")
 
 
 def test_pi_widths_rope_roll_matches_oracle():
-    """256-dim heads, 816 prefix tokens (positions up to 865), one env: the per-kernel
-    path at batch 1, since the persistent kernel has no rotary step."""
+    """256-dim heads, 816 prefix tokens (positions up to 865), one env: the persistent
+    kernel with its rotary phase after every QKV projection."""
     s = synth.get_config("pi_b1").replace(layers=2, rope_base=10000.0, context_period=2)
     wts = synth.draw_weights(s, seed=33, stress=True)
     ea, ex, n = run_parity(s, wts, batch=1, seed=8, steps=6, oracle_dtype=np.float32, check_every=3)
     print(f"pi widths rope: action err {ea:.2e}, state err {ex:.2e}")
 
 
-def test_rope_models_refuse_the_persistent_path():
-    from paper_2609_34170_amd import ravel
-    s = synth.get_config("small_bf16").replace(layers=2, rope_base=10000.0)
-    g = GpuRoll(s, synth.draw_weights(s, seed=34), 1, 0)
-    with pytest.raises(ravel.RavelError):
-        g.buf.set_option(ravel.OPT_PERSISTENT, 1)
+def test_persistent_kernel_has_a_rotary_phase():
+    from tests.test_gpu_persistent import _phase_classes
+    s = synth.get_config("small_bf16").replace(layers=3, rope_base=10000.0)
+    assert "rope" in _phase_classes(s, synth.draw_weights(s, seed=34))
 
 
 def test_full_horizon_chunk_with_rope():
