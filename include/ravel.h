@@ -102,8 +102,7 @@ typedef struct {
                           paper's expert); > 0: rotary embedding of their
                           self-attention queries and keys, rotate-half pairs
                           (d, d + hd/2) turned by (P + i) base^(-2d/hd) for
-                          logical slot i, the prefix keys used as given; runs on
-                          the per-kernel path (no persistent few-row kernel)    */
+                          logical slot i, the prefix keys used as given        */
 } ravel_config;
 
 enum { RAVEL_OFFSET_MLP = 0, RAVEL_OFFSET_CONCAT = 1, RAVEL_OFFSET_ADAPTER = 2 };
