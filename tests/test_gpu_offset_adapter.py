@@ -88,3 +88,14 @@ def test_ragged_shapes_with_the_adapter_form_and_rotary_positions():
         wts = synth.draw_weights(s, seed=25, stress=True)
         ea, ex, n = run_parity(s, wts, batch=3, seed=9, steps=9, oracle_dtype=np.float64, check_every=3)
         print(f"ragged adapter rope={rope}: action err {ea:.2e}, state err {ex:.2e}")
+
+
+def test_batch64_widths_with_the_adapter_form_sampled_envs():
+    """The pi-style widths at batch 64 (3200 rows: the action-time MLP's 2112-wide inputs
+    through the tiled MFMA GEMMs, conditioning groups, staggered refreshes) with two
+    layers and rotary positions; envs {0, 31, 63} against the oracle."""
+    s = synth.get_config("pi_b64").replace(layers=2, offset_mode=W.OFFSET_ADAPTER, rope_base=10000.0)
+    wts = synth.draw_weights(s, seed=26, stress=True)
+    ea, ex, n = run_parity(s, wts, batch=64, seed=10, steps=6, env_sample=[0, 31, 63], oracle_dtype=np.float32,
+                           check_every=3)
+    print(f"batch 64 adapter + rope: action err {ea:.2e}, state err {ex:.2e}")
