@@ -51,3 +51,32 @@ def test_argument_errors_are_reported_without_a_gpu():
     assert st == -1
     assert b"null" in lib.ravel_last_error()
     assert lib.ravel_step(None, None, None, None) == -1
+
+
+def _struct_fields(name):
+    """(C type, field) pairs of `typedef struct { ... } name;` in the header, in order."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    body = re.search(r"typedef struct\s*\{([^}]*)\}\s*" + name + r"\s*;", text).group(1)
+    return re.findall(r"\b(int32_t|float|int64_t|const char\*|const void\*)\s+(\w+)\s*(?:\[\d+\])?\s*;", body)
+
+
+def test_binding_config_struct_matches_header():
+    """The ctypes mirror of ravel_config has the header's fields, in order and of the same
+    C types (a field added on one side only would shift every later field)."""
+    from paper_2609_34170_amd import ravel
+    ctype = {"int32_t": ctypes.c_int32, "float": ctypes.c_float}
+    fields = _struct_fields("ravel_config")
+    assert [n for _, n in fields] == [n for n, _ in ravel.RavelConfig._fields_]
+    for (ct, n), (_, pt) in zip(fields, ravel.RavelConfig._fields_):
+        assert ctype[ct] is pt, n
+    assert ctypes.sizeof(ravel.RavelConfig) == 4 * len(fields)
+
+
+def test_offset_mode_values_match_the_synthetic_workloads():
+    import synth
+    text = open(HEADER).read()
+    vals = dict(re.findall(r"\b(RAVEL_OFFSET_\w+)\s*=\s*(\d+)", text))
+    W = synth.workloads
+    assert int(vals["RAVEL_OFFSET_MLP"]) == W.OFFSET_MLP
+    assert int(vals["RAVEL_OFFSET_CONCAT"]) == W.OFFSET_CONCAT
+    assert int(vals["RAVEL_OFFSET_ADAPTER"]) == W.OFFSET_ADAPTER
