@@ -26,7 +26,15 @@
  * Errors: every entry point returns a ravel_status and never throws; the
  * message of the calling thread's last failure is in ravel_last_error().
  * Shape and argument errors are returned synchronously.  Asynchronous device
- * faults surface as RAVEL_E_HIP on a later call that synchronises.
+ * faults surface as RAVEL_E_HIP on a later call that synchronises.  A failed
+ * launch of the persistent layers' kernel (a grid barrier or split meeting
+ * that timed out) is not left silent: that step and every step enqueued after
+ * it release NaN actions and leave the ring and t unchanged, and the next
+ * ravel_step / ravel_step_state / ravel_full_denoise / ravel_train_loss call
+ * that finds the release kernel's pinned host flag raised (read without
+ * synchronising), or the next ravel_buffer_sync / ravel_debug_state, waits for
+ * the device, re-arms the kernel's counters and returns RAVEL_E_HIP; the call
+ * after that runs normally from the unchanged state.
  *
  * Streams are hipStream_t values passed as void* (NULL = the default stream).
  */
@@ -158,9 +166,9 @@ int64_t ravel_model_weight_bytes(const ravel_model* model);
  *                         persistent kernel (default for one env with 256-dim heads
  *                         and <= 16 FOP tokens: computed inside the output projection);
  *   RAVEL_SYNC_CONTEXT    RAVEL_OPT_SYNC_CONTEXT on;  RAVEL_NO_GRAPH  RAVEL_OPT_USE_GRAPH off;
- *   RAVEL_COOPERATIVE     launch the persistent kernel cooperatively (residency of
- *                         its whole grid guaranteed up front, e.g. on a GPU shared
- *                         with other processes; read once per process). */
+ *   RAVEL_COOPERATIVE     not supported: set to a nonzero value, buffer creation
+ *                         fails with RAVEL_E_INVALID (the persistent kernel is
+ *                         launched ordinarily; its waits are bounded). */
 ravel_status ravel_buffer_create(ravel_model* model, int32_t batch, uint64_t seed, ravel_buffer** out);
 void ravel_buffer_destroy(ravel_buffer* buf);
 
@@ -169,13 +177,25 @@ void ravel_buffer_destroy(ravel_buffer* buf);
  *                           step, which waits on the GPU (not the host) for its
  *                           data; 0 (default): applied at the first step whose
  *                           host-side event query finds the data ready.
- *   RAVEL_OPT_USE_GRAPH     1 (default): replay a captured hipGraph per step.
+ *   RAVEL_OPT_USE_GRAPH     1 (default): replay a captured hipGraph per step (the
+ *                           whole step after the host's publish check, on either
+ *                           execution path; one graph per pointer set); 0: launch
+ *                           the step's kernels eagerly.
  *   RAVEL_OPT_DEBUG         1: synchronise and check for NaN/Inf after each kernel.
  *   RAVEL_OPT_PERSISTENT    1 (default where available): run the transformer layers
  *                           of a bf16 model whose B*H rows fit one 64-row tile as a
- *                           single cooperative persistent kernel; 0: one kernel per
- *                           operation.  E_STATE if the buffer does not qualify. */
-enum { RAVEL_OPT_SYNC_CONTEXT = 1, RAVEL_OPT_USE_GRAPH = 2, RAVEL_OPT_DEBUG = 3, RAVEL_OPT_PERSISTENT = 4 };
+ *                           single persistent kernel (one block per CU, grid
+ *                           barriers between phases) between the few kernels around
+ *                           it; 0: one kernel per operation.  E_STATE if the buffer
+ *                           does not qualify.
+ *   RAVEL_OPT_FAIL_LAYERS   test hook, 1: mark the persistent layers' kernel as failed
+ *                           (synchronises, then sets its error word as a grid barrier
+ *                           that timed out would; every later launch then returns at
+ *                           once and the error handling described at the top of this
+ *                           file takes over).  E_STATE on a buffer without the
+ *                           persistent kernel. */
+enum { RAVEL_OPT_SYNC_CONTEXT = 1, RAVEL_OPT_USE_GRAPH = 2, RAVEL_OPT_DEBUG = 3, RAVEL_OPT_PERSISTENT = 4,
+       RAVEL_OPT_FAIL_LAYERS = 5 };
 ravel_status ravel_buffer_set_option(ravel_buffer* buf, int32_t option, int64_t value);
 
 /* Context plane (paper Sec. 3.2: the latest available context is reused
@@ -193,7 +213,10 @@ ravel_status ravel_buffer_set_option(ravel_buffer* buf, int32_t option, int64_t 
  * observation of control step t_obs.  With non-NULL k and v (host or device,
  * [L, P, n_kv, hd] model dtype) it first copies them into the inactive slot
  * on `producer` (acquire + copy); the sources must stay valid until that copy
- * has run.  The swap happens at a later ravel_step: the slot index flips in
+ * has run.  env = -1 publishes one context per env at once: k and v are then
+ * [B, L, P, n_kv, hd] (env e's block at offset e * L*P*n_kv*hd) and must not be
+ * NULL; t_obs is checked for every env before anything is copied (E_STATE for
+ * all if one env's would decrease).  The swap happens at a later ravel_step: the slot index flips in
  * device memory and the step's offset becomes p = t - t_obs.  t_obs must not
  * decrease per env (E_STATE).  Never blocks on the GPU. */
 ravel_status ravel_context_acquire(ravel_buffer* buf, int32_t env, void** k_slot, void** v_slot,
@@ -221,6 +244,16 @@ ravel_status ravel_buffer_sync(ravel_buffer* buf);
  *   X_host float [B, H, D_a] ring in PHYSICAL slot order (slot (t+i) mod H is
  *   logical slot i); t = step counter; t_obs_host int64 [B]. */
 ravel_status ravel_debug_state(ravel_buffer* buf, float* X_host, int64_t* t, int64_t* t_obs_host);
+
+/* Facts about a buffer's execution (for tests and tooling):
+ *   RAVEL_Q_GRAPHS      step graphs captured so far (one per (fop, state, action)
+ *                       pointer set and execution path while RAVEL_OPT_USE_GRAPH is on);
+ *   RAVEL_Q_PERSISTENT  1 if the transformer layers run as the persistent kernel;
+ *   RAVEL_Q_PHASES      phases of that kernel's list (0 on the per-kernel path);
+ *   RAVEL_Q_STEPS       steps enqueued (the host's copy of t).
+ * Errors: E_INVALID (null pointer, unknown key). */
+enum { RAVEL_Q_GRAPHS = 1, RAVEL_Q_PERSISTENT = 2, RAVEL_Q_PHASES = 3, RAVEL_Q_STEPS = 4 };
+ravel_status ravel_buffer_query(ravel_buffer* buf, int32_t key, int64_t* value);
 
 /* Publish log: entries (env, t_apply, t_obs) as int64 triples, oldest first.
  * On input *n is the capacity in entries; on output the number written. */

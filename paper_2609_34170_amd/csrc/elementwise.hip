@@ -754,7 +754,17 @@ __global__ __launch_bounds__(256) void euler_release_kernel(float* __restrict__ 
                                                             int64_t* t, int H, int D, uint64_t seed,
                                                             float* __restrict__ action,
                                                             const float* __restrict__ state,
-                                                            const float* __restrict__ mask, unsigned* ticket) {
+                                                            const float* __restrict__ mask, unsigned* ticket,
+                                                            const int* err, int* host_flag) {
+  // The layers' kernel reported a failure (a grid barrier that timed out): v is not
+  // a velocity.  Release NaN actions, leave the ring and t as they were, and raise
+  // the host-visible flag that the next step call checks.
+  if (err && __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+    for (int d = threadIdx.x; d < D; d += blockDim.x) action[(size_t)blockIdx.x * D + d] = __int_as_float(0x7fc00000);
+    if (host_flag && blockIdx.x == 0 && threadIdx.x == 0)
+      __hip_atomic_store(host_flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    return;
+  }
   const int64_t tt = *t;
   const float dt = 1.0f / (float)H;
   const int h0 = (int)(tt % H);
@@ -808,10 +818,10 @@ __global__ __launch_bounds__(256) void euler_release_kernel(float* __restrict__ 
 
 hipError_t launch_euler_release(float* X, const float* v, int64_t* t, int B, int H, int D, uint64_t seed,
                                 float* action, unsigned* ticket, const float* state, const float* mask,
-                                hipStream_t s) {
+                                const int* err, int* host_flag, hipStream_t s) {
   if (!ticket) return hipErrorInvalidValue;
   hipLaunchKernelGGL(euler_release_kernel, dim3(B), dim3(256), 0, s, X, v, t, H, D, seed, action, state, mask,
-                     ticket);
+                     ticket, err, host_flag);
   return hipGetLastError();
 }
 

@@ -214,7 +214,7 @@ hipError_t launch_euler_chunk(float* X, const float* v, int B, int H, int D, flo
 // env; ticket is a device word that is zero between launches (the last block re-arms it).
 hipError_t launch_euler_release(float* X, const float* v, int64_t* t, int B, int H, int D,
                                 uint64_t seed, float* action, unsigned* ticket, const float* state,
-                                const float* mask, hipStream_t s);
+                                const float* mask, const int* err, int* host_flag, hipStream_t s);
 
 // Fill X[e, r mod H, :] with the Philox noise of action r, for r = 0..H-1.
 hipError_t launch_ring_init(float* X, int B, int H, int D, uint64_t seed, hipStream_t s);

@@ -42,22 +42,35 @@ constexpr int kMaxAttnSplit = 32;
 // barrier that opens the phase)
 __host__ __device__ constexpr int attn_keys_per_split_max(int hd) { return (8192 / hd) < 256 ? (8192 / hd) : 256; }
 
+// Activations produced inside the launch are written once per launch (each phase
+// has its own output buffers) and every 128-byte line of them by exactly one block,
+// so the phases after it read them with plain loads, shared through each XCD's L2;
+// a_coh = 1 keeps device-coherent loads for an operand whose lines are shared by
+// several writers (attention outputs of heads narrower than 64 dims).
 struct PGemm {
   int a_mode, e_mode;  // PAMode, PEMode
   int kw, ksplit;      // K per item = 256 * kw; items = tiles(N, 64) * ksplit
   int M, N, K;
   const bf16_t* A; int lda;            // PA_BF16: A; PA_NORM: p
+  int a_t32;                           // PA_BF16: A stored in 32-column tiles [K/32][64 rows][32]
+  int a_coh;                           // 1: device-coherent loads of A
   const bf16_t* shift; int ld_shift;   // PA_NORM: bf16 shift rows or NULL
-  const float* sumsq_in; float eps;    // PA_NORM: [K/64][64]
+  // PA_NORM: row sums of squares of x per 64-column tile, entry (t, row) at
+  // sumsq_in[(t * 64 + row) * sq_in_ld]
+  const float* sumsq_in; int sq_in_ld; float eps;
   const bf16_t* W; int ldw;            // weights [N][ldw]
   const float* bias;                   // PE_F32 (or NULL)
   bf16_t* out_t; int ldo;              // PE_BF16 / PE_GEGLU
-  float* out_f; int ldof;              // PE_F32 output, or the residual x (PE_RESID)
+  int out_t32;                         // PE_GEGLU: output in 32-column tiles [N/64][64 rows][32]
+  float* out_f; int ldof;              // PE_F32 output, or the new residual x (PE_RESID)
+  const float* x_in;                   // PE_RESID: the residual x before the update (stride ldof)
   const float* gate; int ldg;          // PE_RESID: gate rows, or NULL and then
   const float* gate_scalar;            // tanh(*gate_scalar)
   int ns_mode; const float* ns; int ldns;  // PE_RESID: scale of the next norm
   bf16_t* p_out; int ldp;              // PE_RESID: p of the next norm
-  float* sumsq_out;                    // PE_RESID: [N/64][64] row sums of squares of the new x
+  // PE_RESID: row sums of squares of the new x, entry (tile, row) at
+  // sumsq_out[(tile * 64 + row) * sq_out_ld] (32: one 128-byte line per entry)
+  float* sumsq_out; int sq_out_ld;
   float* partial; unsigned* counters;  // split-K partial tiles, per-tile tickets
   // 1: the ksplit blocks of a tile meet and each finishes a slice of its rows
   // (needs one item per block); 0: the last block to arrive finishes the tile
@@ -67,12 +80,13 @@ struct PGemm {
   float x_scale;
 };
 
-// Rotary positions in place (the rows' queries and keys written by the phase
-// before): item = one row e*H + i of qkv (row stride ld), whose nh = nq + nkv
-// heads of hd columns each turn their pairs (d, d + hd/2) by the angle with
-// cosine cs[(i * hd/2 + d) * 2] and sine cs[(i * hd/2 + d) * 2 + 1]; hd % 8 == 0.
+// Rotary positions (the rows' queries and keys written by the phase before): item =
+// one row e*H + i of qkv (row stride ld), whose nh = nq + nkv heads of hd columns
+// each turn their pairs (d, d + hd/2) by the angle with cosine cs[(i * hd/2 + d) * 2]
+// and sine cs[(i * hd/2 + d) * 2 + 1], written to the same place of out (a buffer of
+// the same layout); hd % 8 == 0.
 struct PRope {
-  bf16_t* qkv; int ld;
+  const bf16_t* qkv; bf16_t* out; int ld;
   int H, nh, hd;
   const float* cs;
 };

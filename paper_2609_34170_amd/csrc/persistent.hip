@@ -36,8 +36,6 @@
 // read with plain loads.  Producers drain their stores before arriving at a
 // barrier or ticket.  Spins are bounded: a barrier that does not complete sets
 // the error flag and every wave exits.
-#include <cstdlib>
-
 #include "kernels.h"
 #include "persistent.h"
 
@@ -178,6 +176,11 @@ RAVEL_DEV bool group_meet(unsigned* counter, unsigned arrivals, int* err, int* s
         ok = 0;
         break;
       }
+      // another block gave up: leave instead of waiting out the limit
+      if ((spins & 255) == 0 && __hip_atomic_load(gptr(err), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+        ok = 0;
+        break;
+      }
     }
     *s_flag = ok;
   }
@@ -221,6 +224,8 @@ RAVEL_DEV int barrier_wait(unsigned* bar, unsigned gen, int* err) {
       __hip_atomic_fetch_or(gptr(err), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       return 0;
     }
+    // another block gave up (a barrier or a split meeting timed out): leave now
+    if ((spins & 255) == 0 && __hip_atomic_load(gptr(err), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return 0;
   }
   return 1;
 }
@@ -279,6 +284,22 @@ RAVEL_DEV void load_weights(const PGemm& g, int item, u32x4_t (&wf)[16]) {
     load_w<2>(g, item, wf);
   else
     load_w<1>(g, item, wf);
+}
+
+// Rows of a cooperative split-K tile that block z finishes: [z * rp, (z + 1) * rp)
+// with rp even, so that two rows sharing a 128-byte line of a 32-column-tile
+// output go to one block.
+RAVEL_DEV int coop_rows(const PGemm& g) {
+  const int rp = (g.M + g.ksplit - 1) / g.ksplit;
+  return (rp + 1) & ~1;
+}
+// Byte offset of A[m][k] (bf16): row-major with stride lda, or 32-column tiles.
+RAVEL_DEV size_t a_off(const PGemm& g, int m, int k) {
+  return g.a_t32 ? ((size_t)(k >> 5) * 2048 + (size_t)m * 32 + (k & 31)) * 2 : ((size_t)m * g.lda + k) * 2;
+}
+// Byte offset of output column c (of N / 2) of row m of a gated-GeLU phase.
+RAVEL_DEV size_t geglu_off(const PGemm& g, int m, int c) {
+  return g.out_t32 ? ((size_t)(c >> 5) * 2048 + (size_t)m * 32 + (c & 31)) * 2 : ((size_t)m * g.ldo + c) * 2;
 }
 
 // Epilogue operands of one slot of a cooperative split-K tile: residual x,
@@ -414,7 +435,8 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int
 #pragma unroll
     for (int f = 0; f < NF; ++f) {
       const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
-      af[i][f] = ld_b8<COH>(rA, boff(m < g.M && k < g.K, ((size_t)m * g.lda + k) * 2));
+      const int o = boff(m < g.M && k < g.K, a_off(g, m, k));
+      af[i][f] = g.a_coh ? ld_b8<COH>(rA, o) : ld_b8<PLAIN>(rA, o);
     }
   // PA_XATTN: the head's keys (this wave's 64 dims; lane: key l16) and its values
   // (16-byte chunks c = tid, tid + 256: key c / 32, dims (c % 32) * 8), plain loads
@@ -440,7 +462,7 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const int t = part + 4 * j;
-      sq[j] = ld_f1<COH>(rQ, boff(t < nt && row < g.M, (size_t)(t * 64 + row) * 4));
+      sq[j] = ld_f1<PLAIN>(rQ, boff(t < nt && row < g.M, (size_t)(t * 64 + row) * g.sq_in_ld * 4));
     }
   }
   // a cooperative split tile's epilogue operands of this block's first slots
@@ -538,12 +560,12 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int
   // epilogue operands (residual x, gate, next-norm scale, bias), one batch
   f32x4_t e_x[MT], e_g[MT], e_s[MT], e_b[MT];
   auto load_epilogue = [&]() {
-    const rsrc_t rX = rsrc(g.out_f), rG = rsrc(g.gate), rN = rsrc(g.ns), rB = rsrc(g.bias);
+    const rsrc_t rX = rsrc(g.x_in), rG = rsrc(g.gate), rN = rsrc(g.ns), rB = rsrc(g.bias);
 #pragma unroll
     for (int q = 0; q < MT; ++q) {
       const int m = row_of(q), n = col_of(q);
       const bool ok = m < g.M && n + 4 <= g.N;
-      e_x[q] = ld_f4<COH>(rX, boff(resid && ok, ((size_t)m * g.ldof + n) * 4));
+      e_x[q] = ld_f4<PLAIN>(rX, boff(resid && ok, ((size_t)m * g.ldof + n) * 4));
       e_g[q] = ld_f4<PLAIN>(rG, boff(resid && ok && g.gate, ((size_t)m * g.ldg + n) * 4));
       e_s[q] = ld_f4<PLAIN>(rN, boff(resid && ok, (g.ns_mode == NS_ROW ? (size_t)m * g.ldns + n : (size_t)n) * 4));
       e_b[q] = ld_f4<PLAIN>(rB, boff(!resid && ok && g.bias, (size_t)n * 4));
@@ -609,7 +631,7 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int
       if (m >= g.M || ng >= g.N) continue;
       const f32x4_t u = *(const f32x4_t*)&sm.red[0][(c + 1) * MT + i][ln][0];
       const f32x4_t gt = sum[q];
-      st_bf16x4(rsrc(g.out_t), ((size_t)m * g.ldo + (ng >> 5) * 16 + (ln >> 4) * 4) * 2, gelu_tanh_f(gt[0]) * u[0],
+      st_bf16x4(rsrc(g.out_t), geglu_off(g, m, (ng >> 5) * 16 + (ln >> 4) * 4), gelu_tanh_f(gt[0]) * u[0],
                 gelu_tanh_f(gt[1]) * u[1], gelu_tanh_f(gt[2]) * u[2], gelu_tanh_f(gt[3]) * u[3]);
     }
     __syncthreads();
@@ -660,7 +682,7 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int
       float s = 0.f;
 #pragma unroll
       for (int h = 0; h < 16; ++h) s += sm.rowsq[tid][h];
-      st_f1(rsrc(g.sumsq_out), (size_t)(tile * 64 + tid) * 4, s);
+      st_f1(rsrc(g.sumsq_out), (size_t)(tile * 64 + tid) * g.sq_out_ld * 4, s);
     }
   }
   __syncthreads();
@@ -678,7 +700,7 @@ struct CoopSlot {
 };
 template <int MT>
 RAVEL_DEV CoopSlot coop_slot(const PGemm& g, int tile, int z, int slot) {
-  const int rp = (g.M + g.ksplit - 1) / g.ksplit;
+  const int rp = coop_rows(g);
   const int r0 = z * rp, r1 = min(g.M, r0 + rp);
   const bool geglu = g.e_mode == PE_GEGLU;
   const int per_row = geglu ? 8 : 16;
@@ -702,9 +724,9 @@ RAVEL_DEV CoopOps coop_operands(const PGemm& g, int tile, int z, int s0, bool us
   CoopSlot q = coop_slot<MT>(g, tile, z, s0 + local_tid());
   q.ok = q.ok && use;
   const bool geglu = g.e_mode == PE_GEGLU, resid = g.e_mode == PE_RESID;
-  const rsrc_t rX = rsrc(g.out_f), rG = rsrc(g.gate), rN = rsrc(g.ns), rB = rsrc(g.bias);
+  const rsrc_t rX = rsrc(g.x_in), rG = rsrc(g.gate), rN = rsrc(g.ns), rB = rsrc(g.bias);
   CoopOps o;
-  o.ex = ld_f4<COH>(rX, boff(resid && q.ok, ((size_t)q.row * g.ldof + q.n) * 4));
+  o.ex = ld_f4<PLAIN>(rX, boff(resid && q.ok, ((size_t)q.row * g.ldof + q.n) * 4));
   o.eg = ld_f4<PLAIN>(rG, boff(resid && q.ok && g.gate, ((size_t)q.row * g.ldg + q.n) * 4));
   o.es = ld_f4<PLAIN>(rN, boff(resid && q.ok, (g.ns_mode == NS_ROW ? (size_t)q.row * g.ldns + q.n : (size_t)q.n) * 4));
   o.eb = ld_f4<PLAIN>(rB, boff(!resid && !geglu && q.ok && g.bias, (size_t)q.n * 4));
@@ -719,7 +741,7 @@ template <int MT>
 RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& sm, const CoopOps& first) {
   const int tid = local_tid();
   const int n0 = tile * 64;
-  const int rp = (g.M + g.ksplit - 1) / g.ksplit;
+  const int rp = coop_rows(g);
   const int r0 = z * rp, r1 = min(g.M, r0 + rp);
   const size_t tile_elems = (size_t)MT * 4 * 64 * 4;
   const bool geglu = g.e_mode == PE_GEGLU, resid = g.e_mode == PE_RESID;
@@ -757,7 +779,7 @@ RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& 
     float sq = 0.f;
     if (valid && n < g.N) {
       if (geglu) {
-        st_bf16x4(rsrc(g.out_t), ((size_t)row * g.ldo + (n0 >> 1) + cb * 16 + grp * 4) * 2, gelu_tanh_f(v[0]) * u[0],
+        st_bf16x4(rsrc(g.out_t), geglu_off(g, row, (n0 >> 1) + cb * 16 + grp * 4), gelu_tanh_f(v[0]) * u[0],
                   gelu_tanh_f(v[1]) * u[1], gelu_tanh_f(v[2]) * u[2], gelu_tanh_f(v[3]) * u[3]);
       } else if (g.e_mode == PE_BF16) {
         st_bf16x4(rsrc(g.out_t), ((size_t)row * g.ldo + n) * 2, v[0], v[1], v[2], v[3]);
@@ -789,7 +811,7 @@ RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& 
       float s = 0.f;
 #pragma unroll
       for (int h = 0; h < 16; ++h) s += sm.rowsq[tid][h];
-      st_f1(rsrc(g.sumsq_out), (size_t)(tile * 64 + r0 + tid) * 4, s);
+      st_f1(rsrc(g.sumsq_out), (size_t)(tile * 64 + r0 + tid) * g.sq_out_ld * 4, s);
     }
   }
 }
@@ -839,12 +861,12 @@ RAVEL_DEV void attn_load_kv(const AttnArgs& a, const SplitKeys& k, const int* sl
   for (int r = 0; r < 4; ++r) {
     const int c = tid + r * 256;
     const int o = off(k.kbeg + c / CPR, (c % CPR) * 8);
-    kv[r] = k.self ? ld16<COH>(rK, o) : ld16<PLAIN>(rK, o);
+    kv[r] = ld16<PLAIN>(rK, o);
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int o = off(k.kbeg + (tid / CPR) * 4 + i, (tid % CPR) * 8);
-    kv[4 + i] = k.self ? ld16<COH>(rV, o) : ld16<PLAIN>(rV, o);
+    kv[4 + i] = ld16<PLAIN>(rV, o);
   }
 }
 
@@ -864,8 +886,8 @@ RAVEL_DEV void attn_merge(const AttnArgs& a, int e, int j, int el0, int el1, PSm
     const int t = tid + r * 256, sp = t >> 6, qq = t & 63;
     mlv[r] = ld_f2<COH>(rML, boff(sp < a.nsplit && qq < a.Hq, ((pbase + sp) * Hp + qq) * 2 * 4));
   }
-  // each thread sums one element over the splits, 16 splits per batch of loads
-  constexpr int SB = 16;
+  // each thread sums one element over the splits
+  constexpr int SB = kMaxAttnSplit;  // every split of a head in one batch of loads
   f32x4_t pvl[SB];
   auto load_parts = [&](int el, int sp0) {
     const int qq = el / (HD / 4), d = (el % (HD / 4)) * 4;
@@ -941,7 +963,7 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
   bf16x8_t qf[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks)
-    qf[ks] = ld_b8<COH>(rq, boff(query < a.Hq, ((size_t)(e * a.Hq + query) * a.ldq + j * HD + ks * 32 + grp * 8) * 2));
+    qf[ks] = ld_b8<PLAIN>(rq, boff(query < a.Hq, ((size_t)(e * a.Hq + query) * a.ldq + j * HD + ks * 32 + grp * 8) * 2));
   after_loads();
   __syncthreads();  // LDS may still be read by this block's previous item
 #pragma unroll
@@ -1068,7 +1090,8 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
   if (a.coop) {
     // the splits of this (env, head) meet; each merges a share of the output
     if (group_meet(ctr, (unsigned)a.nsplit, err, &sm.flag)) {
-      const int share = (total + a.nsplit - 1) / a.nsplit;
+      // shares of whole 128-byte lines of the bf16 output (16 elements of 4 dims)
+      const int share = (((total + a.nsplit - 1) / a.nsplit) + 15) & ~15;
       const int el0 = split * share, el1 = min(total, el0 + share);
       attn_merge<HD>(a, e, j, el0, el1, sm);
     }
@@ -1091,13 +1114,13 @@ static_assert(sizeof(Phase) % 16 == 0 && kDescChunks <= 256, "phase descriptor s
 // written before the launch).
 RAVEL_DEV void rope_item(const PRope& r, int row) {
   const int i = row % r.H, half = r.hd >> 1, quads = r.nh * (half >> 2);
-  const rsrc_t q = rsrc(r.qkv + (size_t)row * r.ld);
+  const rsrc_t q = rsrc(r.qkv + (size_t)row * r.ld), qo = rsrc(r.out + (size_t)row * r.ld);
   const rsrc_t t = rsrc(r.cs + (size_t)i * r.hd);
   for (int idx = local_tid(); idx < quads; idx += 256) {
     const int h = idx / (half >> 2), d = (idx - h * (half >> 2)) * 4;
     const int o0 = (h * r.hd + d) * 2, o1 = o0 + half * 2;
-    const auto a = __builtin_amdgcn_raw_buffer_load_b64(q, o0, 0, COH);
-    const auto b = __builtin_amdgcn_raw_buffer_load_b64(q, o1, 0, COH);
+    const auto a = __builtin_amdgcn_raw_buffer_load_b64(q, o0, 0, PLAIN);
+    const auto b = __builtin_amdgcn_raw_buffer_load_b64(q, o1, 0, PLAIN);
     const f32x4_t c01 = ld_f4<PLAIN>(t, d * 8), c23 = ld_f4<PLAIN>(t, d * 8 + 16);
     const float cs[8] = {c01[0], c01[1], c01[2], c01[3], c23[0], c23[1], c23[2], c23[3]};
     float x[4], y[4];
@@ -1114,8 +1137,8 @@ RAVEL_DEV void rope_item(const PRope& r, int row) {
       u[j] = x[j] * cs[2 * j] - y[j] * cs[2 * j + 1];
       v[j] = y[j] * cs[2 * j] + x[j] * cs[2 * j + 1];
     }
-    st_bf16x4(q, (size_t)o0, u[0], u[1], u[2], u[3]);
-    st_bf16x4(q, (size_t)o1, v[0], v[1], v[2], v[3]);
+    st_bf16x4(qo, (size_t)o0, u[0], u[1], u[2], u[3]);
+    st_bf16x4(qo, (size_t)o1, v[0], v[1], v[2], v[3]);
   }
 }
 
@@ -1128,6 +1151,11 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
   __shared__ int slots[64];
   __shared__ int ok;
   const int tid = threadIdx.x;
+  // a barrier of an earlier launch timed out and its counters are stale: do
+  // nothing until the host has re-armed them (the error word is sticky until then)
+  if (tid == 0) ok = __hip_atomic_load(gptr(err), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0;
+  __syncthreads();
+  if (!ok) return;
   const bool stamp = times != nullptr && blockIdx.x == 0 && tid == 0;
   if (stamp) *gptr(times) = wall_clock64();
   for (int d = 0; d < 2 && d < nphase; ++d)
@@ -1162,6 +1190,7 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
     }
   };
   prefetch(desc[0]);
+
   auto none = [] {};
 
   for (int p = 0; p < nphase; ++p) {
@@ -1250,14 +1279,8 @@ hipError_t launch_persistent(const Phase* phases, int nphase, const int* env_slo
                   (void*)&bar,    (void*)&err,    (void*)&times};
   // An ordinary launch: the grid (one block per CU, at most the occupancy limit)
   // is co-resident as soon as the CUs are free, and every wait in the kernel is
-  // bounded, so a block held back by other work only delays the first barrier.
-  // The cooperative launch guarantees residency up front but adds ~11 us of idle
-  // device time on each side of the kernel; it is used when asked for.
-  static const bool coop = [] {
-    const char* ev = getenv("RAVEL_COOPERATIVE");
-    return ev && atoi(ev) != 0;
-  }();
-  if (coop) return hipLaunchCooperativeKernel(fn, dim3(blocks), dim3(256), args, 0, s);
+  // bounded, so a block held back by other work only delays the first barrier; a
+  // wait that never completes sets the error word and every block leaves.
   return hipLaunchKernel(fn, dim3(blocks), dim3(256), args, 0, s);
 }
 

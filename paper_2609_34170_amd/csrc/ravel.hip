@@ -300,6 +300,7 @@ struct GraphEntry {
   const void* fop;
   const float* state;
   float* action;
+  bool persistent;
   hipGraph_t graph;
   hipGraphExec_t exec;
 };
@@ -363,6 +364,14 @@ struct ravel_buffer {
   float* sumsq[2] = {nullptr, nullptr};
   bf16_t* pnorm = nullptr;             // p = bf16((1 + scale) * x) of the next norm, [B*H][w]
   std::vector<void*> pallocs;          // device memory of the persistent path
+  // split tickets of the persistent kernel (re-armed with the barrier after a failure)
+  unsigned* pgcnt = nullptr;
+  unsigned* pacnt = nullptr;
+  size_t pgcnt_bytes = 0, pacnt_bytes = 0;
+  // pinned host word raised by the release kernel when the layers' kernel failed
+  // (read by the next step call without synchronising), and its device address
+  int* hflag = nullptr;
+  int* hflag_dev = nullptr;
   int pblocks = 0, pmt = 4;
   double p_bytes = 0, p_flops = 0;
   // per phase: class name and algorithmic bytes / flops; device time stamps
@@ -786,7 +795,7 @@ ravel_status enqueue_step(ravel_buffer* b, const void* fop, const float* state, 
     REC_END();
   }
   REC_BEGIN("euler_release", (double)B * H * D * 12 + (double)B * D * 4, (double)B * H * D * 2);
-  HIP_TRY(launch_euler_release(b->X, b->v, b->t, B, H, D, b->seed, action, b->ticket, state, b->rel_mask, s));
+  HIP_TRY(launch_euler_release(b->X, b->v, b->t, B, H, D, b->seed, action, b->ticket, state, b->rel_mask, nullptr, nullptr, s));
   REC_END();
   return RAVEL_OK;
 }
@@ -887,18 +896,45 @@ ravel_status build_persistent(ravel_buffer* b) {
   RV_TRY(palloc(b, &b->pbar, kBarrierWords * 4, true));
   RV_TRY(palloc(b, &b->perr, 64, true));
   RV_TRY(palloc(b, &b->sumsq[0], (size_t)(w / 64) * 64 * 4, true));
-  RV_TRY(palloc(b, &b->sumsq[1], (size_t)(w / 64) * 64 * 4, true));
   RV_TRY(palloc(b, &b->pnorm, (size_t)BH * w * 2, true));
   // bf16 copies of the norm shifts: chunk 2l (attention) and 2l + 1 (MLP) of
   // layer l, 2L the final norm; in the modulation rows they sit 3w apart
   // starting at column w
   const int nshift = 2 * c.layers + 1;
   RV_TRY(palloc(b, &b->pshift, (size_t)nshift * BH * w * 2, true));
+  // Every activation a phase writes gets buffers of its own (written once per
+  // launch, read with plain loads by the phases after it): one arena, bumped in
+  // phase order.  Row sums of squares take one 128-byte line per (tile, row).
+  const size_t sq_bytes = (size_t)(w / 64) * 64 * 32 * 4;
+  const size_t resid_bytes = align_up((size_t)BH * w * 4, 256) + align_up((size_t)BH * w * 2, 256) + sq_bytes;
+  const bool rope = m->rope_cs != nullptr;
+  size_t act_bytes = 0;
+  for (int l = 0; l < c.layers; ++l) {
+    const bool ad = m->layers[l].adapter >= 0;
+    act_bytes += align_up((size_t)BH * qkvd * 2, 256) * (rope ? 2 : 1);                   // QKV (+ rotated)
+    act_bytes += align_up((size_t)BH * qd * 2, 256);                                       // attention output
+    act_bytes += resid_bytes * (ad ? 3 : 2);                                               // x, p, sums per update
+    if (ad) act_bytes += align_up((size_t)BH * qd * 2, 256) * 2;  // adapter queries (+ cross-attention output)
+    act_bytes += align_up((size_t)(F / 32) * 2048 * 2, 256);                               // MLP hidden, 32-col tiles
+  }
+  char* act = nullptr;
+  RV_TRY(palloc(b, &act, act_bytes, true));
+  size_t act_off = 0;
+  auto fresh = [&](size_t bytes) -> void* {
+    void* q = act + act_off;
+    act_off += align_up(bytes, 256);
+    return q;
+  };
+  // the current residual, the next norm's p and row sums (the input projection
+  // writes the first ones before the launch, sums unpadded)
+  const float* cur_x = b->x;
+  const bf16_t* cur_p = (const bf16_t*)b->pnorm;
+  const float* cur_sq = b->sumsq[0];
+  int cur_sq_ld = 1;
   const bf16_t* pshift = b->pshift;
   auto shift_of = [&](int chunk) -> const bf16_t* { return pshift + (size_t)chunk * BH * w; };
   size_t part = 0;
   int max_tiles = 1;
-  int cur = 0;
   std::vector<Phase>& P = b->phases;
   P.clear();
   b->pnames.clear();
@@ -916,7 +952,8 @@ ravel_status build_persistent(ravel_buffer* b) {
     g.lda = lda;
     g.shift = shift;
     g.ld_shift = w;
-    g.sumsq_in = b->sumsq[cur];
+    g.sumsq_in = cur_sq;
+    g.sq_in_ld = cur_sq_ld;
     g.eps = c.rms_eps;
     g.W = (const bf16_t*)W;
     g.ldw = K;
@@ -937,7 +974,8 @@ ravel_status build_persistent(ravel_buffer* b) {
   };
   auto resid = [&](Phase& ph, const float* gate, const float* gate_scalar, int ns_mode, const float* ns) {
     PGemm& g = ph.g;
-    g.out_f = b->x;
+    g.x_in = cur_x;
+    g.out_f = (float*)fresh((size_t)BH * w * 4);
     g.ldof = w;
     g.gate = gate;
     g.ldg = ldm;
@@ -945,10 +983,14 @@ ravel_status build_persistent(ravel_buffer* b) {
     g.ns_mode = ns_mode;
     g.ns = ns;
     g.ldns = ldm;
-    g.p_out = (bf16_t*)b->pnorm;
+    g.p_out = (bf16_t*)fresh((size_t)BH * w * 2);
     g.ldp = w;
-    g.sumsq_out = b->sumsq[cur ^ 1];
-    cur ^= 1;
+    g.sumsq_out = (float*)fresh(sq_bytes);
+    g.sq_out_ld = 32;
+    cur_x = g.out_f;
+    cur_p = g.p_out;
+    cur_sq = g.sumsq_out;
+    cur_sq_ld = 32;
   };
   // the input projection writes the first norm's p and row sums of squares
   // (b->sumsq[0]) and the bf16 shifts before the launch
@@ -979,33 +1021,43 @@ ravel_status build_persistent(ravel_buffer* b) {
   const size_t ctx_layer = (size_t)c.prefix_len * kvd;
   bool xattn_fused = B == 1 && hd == 256 && c.n_fop >= 1 && c.n_fop <= 16 && c.n_q_heads % c.n_kv_heads == 0;
   if (const char* ev = getenv("RAVEL_NO_FUSED_XATTN")) xattn_fused = xattn_fused && atoi(ev) == 0;
+  // an attention output is written in (query, head) segments of hd bf16 values by
+  // each head's merge: whole 128-byte lines only when hd >= 64
+  const int att_coh = hd < 64 ? 1 : 0;
   for (int l = 0; l < c.layers; ++l) {
     const LayerW& L = m->layers[l];
     const float* mod = b->mod + (size_t)l * 6 * w;
     const float* next_scale = b->mod + (size_t)(l + 1) * 6 * w;  // next layer's (or the final) chunk 0
+    bf16_t* qkv = (bf16_t*)fresh((size_t)BH * qkvd * 2);
     {
-      Phase ph = gemm(b->pnorm, w, shift_of(2 * l), true, L.qkv_w, qkvd, w, PE_BF16);
-      ph.g.out_t = (bf16_t*)b->qkv;
+      Phase ph = gemm(cur_p, w, shift_of(2 * l), true, L.qkv_w, qkvd, w, PE_BF16);
+      ph.g.out_t = qkv;
       ph.g.ldo = qkvd;
       push(ph, "qkv");
     }
-    if (m->rope_cs) {
+    // queries and keys as attention reads them: rotated into a buffer of their own
+    const bf16_t* qk = qkv;
+    if (rope) {
+      bf16_t* rot = (bf16_t*)fresh((size_t)BH * qkvd * 2);
       Phase ph;
       memset(&ph, 0, sizeof ph);
       ph.type = PH_ROPE;
       ph.items = BH;
-      ph.r.qkv = (bf16_t*)b->qkv;
+      ph.r.qkv = qkv;
+      ph.r.out = rot;
       ph.r.ld = qkvd;
       ph.r.H = H;
       ph.r.nh = c.n_q_heads + c.n_kv_heads;
       ph.r.hd = hd;
       ph.r.cs = m->rope_cs;
       push(ph, "rope");
+      qk = rot;
     }
+    bf16_t* att = (bf16_t*)fresh((size_t)BH * qd * 2);
     {
       AttnArgs a;
       memset(&a, 0, sizeof a);
-      a.q = b->qkv;
+      a.q = qk;
       a.ldq = qkvd;
       a.Hq = H;
       a.pk = (const char*)b->ctx_k + l * ctx_layer * m->elt;
@@ -1015,16 +1067,17 @@ ravel_status build_persistent(ravel_buffer* b) {
       a.slot = b->slot;
       a.P = c.prefix_len;
       a.p_ld = kvd;
-      a.sk = (const char*)b->qkv + (size_t)qd * m->elt;
-      a.sv = (const char*)b->qkv + (size_t)(qd + kvd) * m->elt;
+      a.sk = (const char*)qk + (size_t)qd * m->elt;
+      a.sv = (const char*)qkv + (size_t)(qd + kvd) * m->elt;
       a.S = H;
       a.s_ld = qkvd;
-      a.out = b->att;
+      a.out = att;
       a.ldo = qd;
       push(attn_phase(a), "self_attn");
     }
     {
-      Phase ph = gemm(b->att, qd, nullptr, false, L.o_w, w, qd, PE_RESID);
+      Phase ph = gemm(att, qd, nullptr, false, L.o_w, w, qd, PE_RESID);
+      ph.g.a_coh = att_coh;
       if (L.adapter >= 0)
         resid(ph, mod + 2 * w, nullptr, NS_COL, L.gamma);
       else
@@ -1032,16 +1085,17 @@ ravel_status build_persistent(ravel_buffer* b) {
       push(ph, "o_proj");
     }
     if (L.adapter >= 0) {
+      bf16_t* qa = (bf16_t*)fresh((size_t)BH * qd * 2);
       {
-        Phase ph = gemm(b->pnorm, w, nullptr, true, L.qa_w, qd, w, PE_BF16);
-        ph.g.out_t = (bf16_t*)b->qa;
+        Phase ph = gemm(cur_p, w, nullptr, true, L.qa_w, qd, w, PE_BF16);
+        ph.g.out_t = qa;
         ph.g.ldo = qd;
         push(ph, "q_adapter");
       }
       // one env, heads of 256 dims, at most 16 FOP tokens: the output projection's
       // items compute their head's cross-attention themselves (no attention phase)
       const int ld = m->n_ad * 2 * kvd;
-      Phase fused = gemm(b->qa, qd, nullptr, false, L.oa_w, w, qd, PE_RESID);
+      Phase fused = gemm(qa, qd, nullptr, false, L.oa_w, w, qd, PE_RESID);
       if (xattn_fused && fused.g.kw == 1) {
         resid(fused, nullptr, L.alpha, NS_ROW, mod + 3 * w);
         PGemm& g = fused.g;
@@ -1054,9 +1108,10 @@ ravel_status build_persistent(ravel_buffer* b) {
         g.x_scale = 1.0f / sqrtf((float)hd);
         push(fused, "o_adapter");
       } else {
+        bf16_t* xatt = (bf16_t*)fresh((size_t)BH * qd * 2);
         AttnArgs a;
         memset(&a, 0, sizeof a);
-        a.q = b->qa;
+        a.q = qa;
         a.ldq = qd;
         a.Hq = H;
         a.pk = (const char*)b->kva + (size_t)L.adapter * 2 * kvd * m->elt;
@@ -1065,29 +1120,34 @@ ravel_status build_persistent(ravel_buffer* b) {
         a.P = c.n_fop;
         a.p_ld = ld;
         a.S = 0;
-        a.out = b->att;
+        a.out = xatt;
         a.ldo = qd;
         push(attn_phase(a), "cross_attn");
-        Phase ph = gemm(b->att, qd, nullptr, false, L.oa_w, w, qd, PE_RESID);
+        Phase ph = gemm(xatt, qd, nullptr, false, L.oa_w, w, qd, PE_RESID);
+        ph.g.a_coh = att_coh;
         resid(ph, nullptr, L.alpha, NS_ROW, mod + 3 * w);
         push(ph, "o_adapter");
       }
     }
+    bf16_t* u = (bf16_t*)fresh((size_t)(F / 32) * 2048 * 2);
     {
-      Phase ph = gemm(b->pnorm, w, shift_of(2 * l + 1), true, L.gu_w, 2 * F, w, PE_GEGLU);
-      ph.g.out_t = (bf16_t*)b->u;
+      Phase ph = gemm(cur_p, w, shift_of(2 * l + 1), true, L.gu_w, 2 * F, w, PE_GEGLU);
+      ph.g.out_t = u;
       ph.g.ldo = F;
+      ph.g.out_t32 = 1;
       push(ph, "gate_up");
     }
     {
-      Phase ph = gemm(b->u, F, nullptr, false, L.down_w, w, F, PE_RESID);
+      Phase ph = gemm(u, F, nullptr, false, L.down_w, w, F, PE_RESID);
+      ph.g.a_t32 = 1;
       resid(ph, mod + 5 * w, nullptr, NS_ROW, next_scale);
       push(ph, "down");
     }
   }
+  if (act_off > act_bytes) return fail(RAVEL_E_STATE, "persistent: activation arena too small");
   // final adaptive norm (chunks scale, shift) and output head
   {
-    Phase ph = gemm(b->pnorm, w, shift_of(2 * c.layers), true, m->out_w, D, w, PE_F32);
+    Phase ph = gemm(cur_p, w, shift_of(2 * c.layers), true, m->out_w, D, w, PE_F32);
     ph.g.out_f = b->v;
     ph.g.ldof = D;
     ph.g.bias = m->out_b;
@@ -1100,10 +1160,23 @@ ravel_status build_persistent(ravel_buffer* b) {
   unsigned *gcnt, *acnt;
   const int Hp = ((H + 15) / 16) * 16;
   RV_TRY(palloc(b, &gpart, part * 4, false));
-  RV_TRY(palloc(b, &gcnt, (size_t)max_tiles * 4 * kCounterStride, true));
+  b->pgcnt_bytes = (size_t)max_tiles * 4 * kCounterStride;
+  RV_TRY(palloc(b, &gcnt, b->pgcnt_bytes, true));
   RV_TRY(palloc(b, &ao, (size_t)max_attn_parts * Hp * hd * 4, false));
   RV_TRY(palloc(b, &aml, (size_t)max_attn_parts * Hp * 2 * 4, false));
-  RV_TRY(palloc(b, &acnt, (size_t)max_attn_heads * 4 * kCounterStride, true));
+  b->pacnt_bytes = (size_t)max_attn_heads * 4 * kCounterStride;
+  RV_TRY(palloc(b, &acnt, b->pacnt_bytes, true));
+  b->pgcnt = gcnt;
+  b->pacnt = acnt;
+  if (!b->hflag) {
+    void* h = nullptr;
+    HIP_TRY(hipHostMalloc(&h, 64, hipHostMallocMapped));
+    b->hflag = (int*)h;
+    *b->hflag = 0;
+    void* d = nullptr;
+    HIP_TRY(hipHostGetDevicePointer(&d, h, 0));
+    b->hflag_dev = (int*)d;
+  }
   for (auto& ph : P) {
     if (ph.type == PH_GEMM) {
       ph.g.partial = gpart;
@@ -1237,7 +1310,8 @@ ravel_status enqueue_persistent_step(ravel_buffer* b, const void* fop, const flo
   }
   RV_TRY(enqueue_persistent_pass(b, fop, s, rec, PassIn{}));
   REC_BEGIN("euler_release", (double)B * H * D * 12 + (double)B * D * 4, (double)B * H * D * 2);
-  HIP_TRY(launch_euler_release(b->X, b->v, b->t, B, H, D, b->seed, action, b->ticket, state, b->rel_mask, s));
+  HIP_TRY(launch_euler_release(b->X, b->v, b->t, B, H, D, b->seed, action, b->ticket, state, b->rel_mask, b->perr,
+                               b->hflag_dev, s));
   REC_END();
   return RAVEL_OK;
 }
@@ -1295,6 +1369,35 @@ static ravel_status flow_time_table(ravel_model* m, int S, float* out) {
   if (se != hipSuccess) return done(fail(RAVEL_E_HIP, hipGetErrorString(se)));
   return done(RAVEL_OK);
 }
+
+namespace {
+// The FOP stand-in encoder over a batch (shared by both entry points): obs [B, d]
+// fp32 -> bf16 staging (bf16 models), hidden = gelu_tanh(W1 obs + b1), tokens =
+// W2 hidden + b2; b provides the model, the batch size, the staging rows and the
+// GEMM workspace.
+ravel_status fop_encode_impl(ravel_buffer* b, const float* obs, void* fop_tokens, hipStream_t s) {
+  ravel_model* m = b->m;
+  const ravel_config& c = m->cfg;
+  const int B = b->B, w = c.width, d = c.fop_obs_dim;
+  GemmArgs e1 = epi_args(EPI_GELU_T);
+  e1.bias = m->f_b1;
+  e1.out_t = b->fhid;
+  e1.ldo_t = w;
+  GemmArgs e2 = epi_args(EPI_T);
+  e2.bias = m->f_b2;
+  e2.out_t = fop_tokens;
+  e2.ldo_t = c.n_fop * w;
+  if (m->bf16) {
+    HIP_TRY(launch_convert<bf16_t>(obs, (bf16_t*)b->obs_t, (long long)B * d, s));
+    RV_TRY(run_gemm<bf16_t>(b, s, nullptr, "fop1", b->obs_t, d, m->f_w1, d, B, w, d, e1));
+    RV_TRY(run_gemm<bf16_t>(b, s, nullptr, "fop2", b->fhid, w, m->f_w2, w, B, c.n_fop * w, w, e2));
+  } else {
+    RV_TRY(run_gemm<float>(b, s, nullptr, "fop1", obs, d, m->f_w1, d, B, w, d, e1));
+    RV_TRY(run_gemm<float>(b, s, nullptr, "fop2", b->fhid, w, m->f_w2, w, B, c.n_fop * w, w, e2));
+  }
+  return RAVEL_OK;
+}
+}  // namespace
 
 // ---------------------------------------------------------------------------
 // C ABI
@@ -1630,6 +1733,10 @@ ravel_status ravel_buffer_create(ravel_model* m, int32_t batch, uint64_t seed, r
   if (!m || !out) return fail(RAVEL_E_INVALID, "null argument");
   if (batch < 1) return fail(RAVEL_E_SHAPE, "batch must be >= 1");
   *out = nullptr;
+  if (const char* ev = getenv("RAVEL_COOPERATIVE"))
+    if (atoi(ev) != 0)
+      return fail(RAVEL_E_INVALID, "RAVEL_COOPERATIVE: the cooperative launch of the layers' kernel is not supported "
+                                   "(an ordinary launch with bounded waits is used)");
   const ravel_config& c = m->cfg;
   ravel_buffer* b = new ravel_buffer();
   b->m = m;
@@ -1789,6 +1896,7 @@ void ravel_buffer_destroy(ravel_buffer* b) {
     if (b->retire[e]) (void)hipEventDestroy(b->retire[e]);
   }
   if (b->cap_stream) (void)hipStreamDestroy(b->cap_stream);
+  if (b->hflag) (void)hipHostFree(b->hflag);
   for (void* p : b->pallocs) (void)hipFree(p);
   for (auto& kv : b->full_tables) (void)hipFree(kv.second);
   if (b->arena) (void)hipFree(b->arena);
@@ -1806,6 +1914,13 @@ ravel_status ravel_buffer_set_option(ravel_buffer* b, int32_t option, int64_t va
       if (value != 0 && !b->d_phases) return fail(RAVEL_E_STATE, "persistent path not available for this model/batch");
       b->persistent = value != 0;
       return RAVEL_OK;
+    case RAVEL_OPT_FAIL_LAYERS: {
+      if (!b->perr) return fail(RAVEL_E_STATE, "no persistent layers' kernel on this buffer");
+      HIP_TRY(hipDeviceSynchronize());
+      const int word = value != 0 ? 4 : 0;
+      HIP_TRY(hipMemcpy(b->perr, &word, 4, hipMemcpyHostToDevice));
+      return RAVEL_OK;
+    }
     default: return fail(RAVEL_E_INVALID, "unknown option");
   }
 }
@@ -1822,25 +1937,76 @@ ravel_status ravel_set_context(ravel_buffer* b, int32_t env, const void* k, cons
                                void* producer) {
   if (!b) return fail(RAVEL_E_INVALID, "null buffer");
   if (b->m->cfg.model_kind != RAVEL_TRANSFORMER) return fail(RAVEL_E_STATE, "analytic models have no context");
-  if (env < 0 || env >= b->B) return fail(RAVEL_E_INVALID, "env out of range");
+  if (env < -1 || env >= b->B) return fail(RAVEL_E_INVALID, "env out of range");
   if ((k == nullptr) != (v == nullptr)) return fail(RAVEL_E_INVALID, "k and v must both be given or both NULL");
+  if (env == -1 && !k) return fail(RAVEL_E_INVALID, "env = -1 needs k and v ([B, L, P, n_kv, hd])");
   hipStream_t ps = (hipStream_t)producer;
   std::lock_guard<std::mutex> lk(b->mu);
-  int64_t latest = b->has_ctx[env] ? b->tobs_host[env] : INT64_MIN;
-  if (b->pending[env].valid) latest = std::max(latest, b->pending[env].t_obs);
-  if (t_obs < latest) return fail(RAVEL_E_STATE, "t_obs must not decrease per env");
-  if (k) {
-    void *dk, *dv;
-    RV_TRY(acquire_locked(b, env, &dk, &dv, ps));
-    const size_t bytes = b->ctx_elems * b->m->elt;
-    HIP_TRY(hipMemcpyAsync(dk, k, bytes, hipMemcpyDefault, ps));
-    HIP_TRY(hipMemcpyAsync(dv, v, bytes, hipMemcpyDefault, ps));
+  const int e0 = env < 0 ? 0 : env, e1 = env < 0 ? b->B : env + 1;
+  // every env's t_obs is checked before anything is copied: all or none
+  for (int e = e0; e < e1; ++e) {
+    int64_t latest = b->has_ctx[e] ? b->tobs_host[e] : INT64_MIN;
+    if (b->pending[e].valid) latest = std::max(latest, b->pending[e].t_obs);
+    if (t_obs < latest) return fail(RAVEL_E_STATE, "t_obs must not decrease per env (env " + std::to_string(e) + ")");
   }
-  HIP_TRY(hipEventRecord(b->pending[env].ready, ps));
-  b->pending[env].valid = true;
-  b->pending[env].t_obs = t_obs;
+  const size_t bytes = b->ctx_elems * b->m->elt;
+  for (int e = e0; e < e1; ++e) {
+    if (k) {
+      void *dk, *dv;
+      RV_TRY(acquire_locked(b, e, &dk, &dv, ps));
+      const size_t src = env < 0 ? (size_t)e * bytes : 0;  // [B, L, P, n_kv, hd]: env e's block
+      HIP_TRY(hipMemcpyAsync(dk, (const char*)k + src, bytes, hipMemcpyDefault, ps));
+      HIP_TRY(hipMemcpyAsync(dv, (const char*)v + src, bytes, hipMemcpyDefault, ps));
+    }
+    HIP_TRY(hipEventRecord(b->pending[e].ready, ps));
+    b->pending[e].valid = true;
+    b->pending[e].t_obs = t_obs;
+  }
   return RAVEL_OK;
 }
+
+namespace {
+// After a failed launch of the layers' kernel (device idle): the blocks that gave
+// up left the barrier and split counters behind, and every launch since returned
+// at once (the error word is sticky): re-arm all of them, clear the word and the
+// host flag, and take the step counter back from the device (failed steps did not
+// advance it).
+ravel_status persistent_rearm(ravel_buffer* b) {
+  HIP_TRY(hipMemset(b->pbar, 0, kBarrierWords * 4));
+  if (b->pgcnt) HIP_TRY(hipMemset(b->pgcnt, 0, b->pgcnt_bytes));
+  if (b->pacnt) HIP_TRY(hipMemset(b->pacnt, 0, b->pacnt_bytes));
+  HIP_TRY(hipMemset(b->perr, 0, 64));
+  HIP_TRY(hipDeviceSynchronize());
+  if (b->hflag) __atomic_store_n(b->hflag, 0, __ATOMIC_RELEASE);
+  int64_t t = 0;
+  HIP_TRY(hipMemcpy(&t, b->t, 8, hipMemcpyDeviceToHost));
+  b->t_host = t;
+  return RAVEL_OK;
+}
+
+ravel_status check_persistent_error(ravel_buffer* b) {
+  if (!b->perr) return RAVEL_OK;
+  int e = 0;
+  HIP_TRY(hipMemcpy(&e, b->perr, 4, hipMemcpyDeviceToHost));
+  if (e) {
+    RV_TRY(persistent_rearm(b));
+    return fail(RAVEL_E_HIP, "persistent kernel: a grid barrier timed out; the steps since released NaN actions "
+                             "and left the ring and t unchanged");
+  }
+  return RAVEL_OK;
+}
+
+// Called at the start of every call that enqueues work (caller holds the mutex): a
+// release kernel found the layers' kernel failed and raised the pinned host flag
+// (no synchronisation unless it is up).
+ravel_status check_failed_launch(ravel_buffer* b) {
+  if (!b->hflag || __atomic_load_n(b->hflag, __ATOMIC_ACQUIRE) == 0) return RAVEL_OK;
+  HIP_TRY(hipDeviceSynchronize());
+  RV_TRY(persistent_rearm(b));
+  return fail(RAVEL_E_HIP, "persistent kernel: a grid barrier timed out; the steps since released NaN actions "
+                           "and left the ring and t unchanged");
+}
+}  // namespace
 
 ravel_status ravel_full_denoise(ravel_buffer* b, int32_t steps, const void* fop, const float* noise, float* chunk,
                                 void* stream) {
@@ -1854,6 +2020,7 @@ ravel_status ravel_full_denoise(ravel_buffer* b, int32_t steps, const void* fop,
   if (fop && ((uintptr_t)fop % 16)) return fail(RAVEL_E_INVALID, "fop_tokens must be 16-byte aligned");
   hipStream_t s = (hipStream_t)stream;
   std::lock_guard<std::mutex> lk(b->mu);
+  RV_TRY(check_failed_launch(b));
   const float* table = nullptr;
   if (c.model_kind == RAVEL_TRANSFORMER) {
     // contexts: the latest available ones, published exactly as a rolling step would
@@ -1910,6 +2077,7 @@ ravel_status ravel_train_loss(ravel_buffer* b, const float* target, const float*
   if (fop && ((uintptr_t)fop % 16)) return fail(RAVEL_E_INVALID, "fop_tokens must be 16-byte aligned");
   hipStream_t s = (hipStream_t)stream;
   std::lock_guard<std::mutex> lk(b->mu);
+  RV_TRY(check_failed_launch(b));
   if (c.model_kind == RAVEL_TRANSFORMER) {
     RV_TRY(apply_publishes(b, s));
     for (int e = 0; e < B; ++e)
@@ -1947,21 +2115,22 @@ static ravel_status step_impl(ravel_buffer* b, const void* fop, const float* sta
   if (fop && ((uintptr_t)fop % 16)) return fail(RAVEL_E_INVALID, "fop_tokens must be 16-byte aligned");
   hipStream_t s = (hipStream_t)stream;
   std::lock_guard<std::mutex> lk(b->mu);
+  RV_TRY(check_failed_launch(b));
   if (c.model_kind == RAVEL_TRANSFORMER) {
     RV_TRY(apply_publishes(b, s));
     for (int e = 0; e < b->B; ++e)
       if (!b->has_ctx[e]) return fail(RAVEL_E_STATE, "env " + std::to_string(e) + " has no context yet");
   }
-  if (b->persistent) {
-    RV_TRY(enqueue_persistent_step(b, fop, state, action, s, nullptr));
-  } else if (b->use_graph) {
+  if (b->use_graph) {
+    // one captured graph per (fop, state, action) pointer set and execution path
     GraphEntry* ge = nullptr;
     for (auto& g : b->graphs)
-      if (g.fop == fop && g.state == state && g.action == action) ge = &g;
+      if (g.fop == fop && g.state == state && g.action == action && g.persistent == b->persistent) ge = &g;
     if (!ge) {
-      GraphEntry g{fop, state, action, nullptr, nullptr};
+      GraphEntry g{fop, state, action, b->persistent, nullptr, nullptr};
       HIP_TRY(hipStreamBeginCapture(b->cap_stream, hipStreamCaptureModeRelaxed));
-      ravel_status st = enqueue_step(b, fop, state, action, b->cap_stream, nullptr);
+      ravel_status st = b->persistent ? enqueue_persistent_step(b, fop, state, action, b->cap_stream, nullptr)
+                                      : enqueue_step(b, fop, state, action, b->cap_stream, nullptr);
       hipGraph_t graph = nullptr;
       hipError_t he = hipStreamEndCapture(b->cap_stream, &graph);
       if (st != RAVEL_OK) return st;
@@ -1972,6 +2141,8 @@ static ravel_status step_impl(ravel_buffer* b, const void* fop, const float* sta
       ge = &b->graphs.back();
     }
     HIP_TRY(hipGraphLaunch(ge->exec, s));
+  } else if (b->persistent) {
+    RV_TRY(enqueue_persistent_step(b, fop, state, action, s, nullptr));
   } else {
     RV_TRY(enqueue_step(b, fop, state, action, s, nullptr));
   }
@@ -2017,45 +2188,10 @@ ravel_status ravel_set_relative_dims(ravel_buffer* b, const int32_t* mask) {
 
 ravel_status ravel_fop_encode(ravel_buffer* b, const float* obs, void* fop_tokens, void* stream) {
   if (!b || !obs || !fop_tokens) return fail(RAVEL_E_INVALID, "null argument");
-  ravel_model* m = b->m;
-  const ravel_config& c = m->cfg;
-  if (!m->has_fop_encoder) return fail(RAVEL_E_STATE, "model has no FOP encoder weights");
-  hipStream_t s = (hipStream_t)stream;
-  const int B = b->B, w = c.width, d = c.fop_obs_dim;
+  if (!b->m->has_fop_encoder) return fail(RAVEL_E_STATE, "model has no FOP encoder weights");
   std::lock_guard<std::mutex> lk(b->mu);
-  GemmArgs e1 = epi_args(EPI_GELU_T);
-  e1.bias = m->f_b1;
-  e1.out_t = b->fhid;
-  e1.ldo_t = w;
-  GemmArgs e2 = epi_args(EPI_T);
-  e2.bias = m->f_b2;
-  e2.out_t = fop_tokens;
-  e2.ldo_t = c.n_fop * w;
-  if (m->bf16) {
-    HIP_TRY(launch_convert<bf16_t>(obs, (bf16_t*)b->obs_t, (long long)B * d, s));
-    RV_TRY(run_gemm<bf16_t>(b, s, nullptr, "fop1", b->obs_t, d, m->f_w1, d, B, w, d, e1));
-    RV_TRY(run_gemm<bf16_t>(b, s, nullptr, "fop2", b->fhid, w, m->f_w2, w, B, c.n_fop * w, w, e2));
-  } else {
-    RV_TRY(run_gemm<float>(b, s, nullptr, "fop1", obs, d, m->f_w1, d, B, w, d, e1));
-    RV_TRY(run_gemm<float>(b, s, nullptr, "fop2", b->fhid, w, m->f_w2, w, B, c.n_fop * w, w, e2));
-  }
-  return RAVEL_OK;
+  return fop_encode_impl(b, obs, fop_tokens, (hipStream_t)stream);
 }
-
-namespace {
-ravel_status check_persistent_error(ravel_buffer* b) {
-  if (!b->perr) return RAVEL_OK;
-  int e = 0;
-  HIP_TRY(hipMemcpy(&e, b->perr, 4, hipMemcpyDeviceToHost));
-  if (e) {
-    // the blocks that gave up left the barrier counters behind: re-arm them
-    HIP_TRY(hipMemset(b->pbar, 0, kBarrierWords * 4));
-    HIP_TRY(hipMemset(b->perr, 0, 64));
-    return fail(RAVEL_E_HIP, "persistent kernel: a grid barrier timed out");
-  }
-  return RAVEL_OK;
-}
-}  // namespace
 
 ravel_status ravel_buffer_sync(ravel_buffer* b) {
   if (!b) return fail(RAVEL_E_INVALID, "null buffer");
@@ -2072,6 +2208,18 @@ ravel_status ravel_debug_state(ravel_buffer* b, float* X_host, int64_t* t, int64
   if (t) HIP_TRY(hipMemcpy(t, b->t, 8, hipMemcpyDeviceToHost));
   if (t_obs_host) HIP_TRY(hipMemcpy(t_obs_host, b->t_obs, (size_t)b->B * 8, hipMemcpyDeviceToHost));
   return RAVEL_OK;
+}
+
+ravel_status ravel_buffer_query(ravel_buffer* b, int32_t key, int64_t* value) {
+  if (!b || !value) return fail(RAVEL_E_INVALID, "null argument");
+  std::lock_guard<std::mutex> lk(b->mu);
+  switch (key) {
+    case RAVEL_Q_GRAPHS: *value = (int64_t)b->graphs.size(); return RAVEL_OK;
+    case RAVEL_Q_PERSISTENT: *value = b->persistent ? 1 : 0; return RAVEL_OK;
+    case RAVEL_Q_PHASES: *value = b->persistent ? (int64_t)b->phases.size() : 0; return RAVEL_OK;
+    case RAVEL_Q_STEPS: *value = b->t_host; return RAVEL_OK;
+    default: return fail(RAVEL_E_INVALID, "unknown query key");
+  }
 }
 
 ravel_status ravel_publish_log(ravel_buffer* b, int64_t* entries, int32_t* n) {

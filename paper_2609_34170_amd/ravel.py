@@ -19,7 +19,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libravel.so
 
 F32, BF16 = 0, 1
 TRANSFORMER, ANALYTIC_OT, ANALYTIC_LINEAR = 0, 1, 2
-OPT_SYNC_CONTEXT, OPT_USE_GRAPH, OPT_DEBUG, OPT_PERSISTENT = 1, 2, 3, 4
+OPT_SYNC_CONTEXT, OPT_USE_GRAPH, OPT_DEBUG, OPT_PERSISTENT, OPT_FAIL_LAYERS = 1, 2, 3, 4, 5
+Q_GRAPHS, Q_PERSISTENT, Q_PHASES, Q_STEPS = 1, 2, 3, 4
 
 _STATUS = {0: "OK", -1: "E_INVALID", -2: "E_NOMEM", -3: "E_HIP", -4: "E_SHAPE", -5: "E_STATE"}
 
@@ -53,7 +54,7 @@ SYMBOLS = [
     "ravel_buffer_destroy", "ravel_buffer_set_option", "ravel_context_acquire", "ravel_set_context",
     "ravel_step", "ravel_step_state", "ravel_set_relative_dims", "ravel_full_denoise", "ravel_train_loss",
     "ravel_fop_encode", "ravel_buffer_sync", "ravel_debug_state",
-    "ravel_publish_log",
+    "ravel_publish_log", "ravel_buffer_query",
     "ravel_buffer_save", "ravel_buffer_load", "ravel_profile_step", "ravel_last_error",
 ]
 
@@ -86,6 +87,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "ravel_buffer_sync": ([vp], i32),
         "ravel_debug_state": ([vp, vp, vp, vp], i32),
         "ravel_publish_log": ([vp, vp, ctypes.POINTER(i32)], i32),
+        "ravel_buffer_query": ([vp, i32, ctypes.POINTER(i64)], i32),
         "ravel_buffer_save": ([vp, vp, ctypes.POINTER(ctypes.c_size_t)], i32),
         "ravel_buffer_load": ([vp, vp, ctypes.c_size_t], i32),
         "ravel_profile_step": ([vp, vp, vp, vp, ctypes.POINTER(KernelRecord), ctypes.POINTER(i32)], i32),
@@ -257,6 +259,11 @@ class Buffer:
         n = ctypes.c_int32(cap)
         _check(lib.ravel_publish_log(self.h, buf.ctypes.data, ctypes.byref(n)))
         return [tuple(int(x) for x in buf[i]) for i in range(n.value)]
+
+    def query(self, key: int) -> int:
+        v = ctypes.c_int64(0)
+        _check(load_library().ravel_buffer_query(self.h, int(key), ctypes.byref(v)))
+        return int(v.value)
 
     def save(self) -> bytes:
         lib = load_library()

@@ -189,17 +189,6 @@ def test_pi_b64_sampled_envs():
     print(f"pi_b64: action err {ea:.2e}, state err {ex:.2e}")
 
 
-def test_large_b16_shapes_sampled_envs():
-    """The large expert's layer shapes (width 2048, 16 query / 4 KV heads of 128, MLP 8192,
-    2048 prefix tokens, 100 slots, 32 FOP tokens) at batch 16 with the refresh at step 3;
-    4 of its 24 layers (two with adapters), so that the CPU oracle finishes in seconds."""
-    s = synth.get_config("large_b16").replace(layers=4)
-    wts = synth.draw_weights(s, seed=0)
-    ea, ex, n = run_parity(s, wts, batch=16, seed=0, steps=4, env_sample=[0, 15], oracle_dtype=np.float32,
-                           check_every=2)
-    print(f"large_b16: action err {ea:.2e}, state err {ex:.2e}")
-
-
 # ---------------------------------------------------------------------------
 # runtime behaviour
 # ---------------------------------------------------------------------------
@@ -215,18 +204,6 @@ def _roll(g, s, steps, t0=0):
     for st in range(t0, t0 + steps):
         outs.append(g.step(synth.draw_fop_tokens(s, 0, st, batch=g.B)))
     return np.stack(outs)
-
-
-def test_graph_replay_equals_eager_bitwise():
-    s, wts = _tiny_bf16()
-    rolls = []
-    for graph in (True, False):
-        g = GpuRoll(s, wts, 2, seed=7, use_graph=graph)
-        for e in range(2):
-            k, v = synth.draw_context(s, 0, e, 0)
-            g.set_context(e, k, v, 0)
-        rolls.append(_roll(g, s, 30))
-    assert np.array_equal(rolls[0], rolls[1])
 
 
 def test_save_load_resumes_bit_exact():

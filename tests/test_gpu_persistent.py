@@ -1,4 +1,4 @@
-"""The persistent few-row path (one cooperative kernel for all layers) against
+"""The persistent few-row path (one kernel for all layers) against
 the per-kernel path and the oracle."""
 
 import numpy as np

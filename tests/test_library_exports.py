@@ -80,3 +80,12 @@ def test_offset_mode_values_match_the_synthetic_workloads():
     assert int(vals["RAVEL_OFFSET_MLP"]) == W.OFFSET_MLP
     assert int(vals["RAVEL_OFFSET_CONCAT"]) == W.OFFSET_CONCAT
     assert int(vals["RAVEL_OFFSET_ADAPTER"]) == W.OFFSET_ADAPTER
+
+
+def test_option_and_query_values_match_the_header():
+    from paper_2609_34170_amd import ravel
+    text = open(HEADER).read()
+    vals = {k: int(v) for k, v in re.findall(r"\b(RAVEL_(?:OPT|Q)_\w+)\s*=\s*(\d+)", text)}
+    for name, v in vals.items():
+        assert getattr(ravel, name[len("RAVEL_"):]) == v, name
+    assert len(vals) == 9
