@@ -29,6 +29,9 @@ import dataclasses
 import zlib
 from typing import Dict, List, Tuple
 
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 F32 = 0
@@ -195,6 +198,20 @@ def bf16_round(a: np.ndarray) -> np.ndarray:
     return out
 
 
+def _bf16_round_inplace(a: np.ndarray, chunk: int = 1 << 22) -> None:
+    """bf16_round on a float32 array in place, a chunk at a time (no full-size temporaries)."""
+    u = a.reshape(-1).view(np.uint32)
+    for i in range(0, u.size, chunk):
+        c = u[i:i + chunk]
+        r = ((c >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
+        c += r
+        c &= np.uint32(0xFFFF0000)
+
+
+def _draw_threads() -> int:
+    return max(1, min(16, os.cpu_count() or 1))
+
+
 def _normal(rng: np.random.Generator, shape, std: float) -> np.ndarray:
     a = rng.standard_normal(size=shape, dtype=np.float32)
     if std != 1.0:
@@ -219,7 +236,9 @@ def draw_weights(s: RavelShape, seed: int = 0, stress: bool = False,
         out["analytic.lambda"] = np.array([analytic_lambda], dtype=np.float32)
         return out
     w = s.width
-    for name, shp in weight_shapes(s, with_fop_encoder):
+
+    def draw(item):
+        name, shp = item
         std = 0.02
         if stress and len(shp) == 2:
             std = 1.0 / np.sqrt(shp[1])
@@ -231,8 +250,15 @@ def draw_weights(s: RavelShape, seed: int = 0, stress: bool = False,
                 a[2 * w:3 * w] += 1.0
                 a[5 * w:6 * w] += 1.0
         if s.dtype == BF16:
-            a = bf16_round(a)
-        out[name] = a
+            _bf16_round_inplace(a)
+        return name, a
+
+    # every tensor has its own seeded stream, so drawing them on several threads
+    # (numpy's generators release the GIL) gives the same values in any order
+    items = weight_shapes(s, with_fop_encoder)
+    with ThreadPoolExecutor(max_workers=_draw_threads()) as ex:
+        for name, a in ex.map(draw, items):
+            out[name] = a
     return out
 
 

@@ -121,3 +121,90 @@ def run_parity(shape, weights, batch, seed, steps, env_sample=None, fop_mode="to
             assert ex <= tol, f"step {st}: ring-state error {ex:.3e} > {tol:.1e}"
         n += 1
     return worst_a, worst_x, n
+
+
+def recovered_velocity(X0, X1, action, t):
+    """Velocity of every slot of one GPU step, from the ring before (X0) and after (X1)
+    the step at t and the released action: the step moves logical slot i by -v_i / H
+    (slot 0 is then released and its physical slot refilled with noise), so
+    v_i = H (X0_i - X1_i) for i >= 1 and v_0 = H (X0_0 - action).  Float64 differences
+    of float32 values: exact up to the float32 rounding of the update itself."""
+    H = X0.shape[1]
+    phys = (t + np.arange(H)) % H
+    L0 = X0[:, phys].astype(np.float64)
+    v = np.empty_like(L0)
+    v[:, 1:] = H * (L0[:, 1:] - X1[:, phys[1:]].astype(np.float64))
+    v[:, 0] = H * (L0[:, 0] - np.asarray(action, np.float64))
+    return L0, v
+
+
+def velocity_parity(shape, weights, batch, envs, captures, *, tol, oracle_dtype=np.float64, init_tobs=0,
+                    lag=0, period=0, stagger=False, seed=0, ctx_seed=0, persistent=None, sens_assert=(),
+                    sens_report=("attn", "adapter", "mlp", "delta"), v_scale=1.0, log=print):
+    """Roll the GPU library; at each step in `captures`, recover its velocity of every
+    slot (recovered_velocity) and compare it element by element with the oracle's
+    Expert.velocity on the GPU's own buffer before that step, with the same context,
+    offset delta = (t - t_obs) / H + delta_0 and FOP tokens, for the envs in `envs`.
+
+    Contexts: refresh 0 of every env, t_obs = init_tobs, before step 0; with period > 0,
+    env e publishes its next refresh before step st >= 1 when (st [+ e]) % period == 0,
+    with t_obs = st - lag (synchronous publish).  At the first capture, the oracle's
+    velocity with each sub-block of `sens_report` switched off is compared with the
+    full one; the sub-blocks in `sens_assert` must move it by at least 10x `tol`.
+    v_scale multiplies every prefix value (a power of two keeps bf16 values exact).
+    Returns the worst velocity error and the sensitivities."""
+    from oracle.expert import Expert
+    from paper_2609_34170_amd import ravel
+    H = shape.horizon
+    g = GpuRoll(shape, weights, batch, seed)
+    if persistent is not None:
+        g.buf.set_option(ravel.OPT_PERSISTENT, 1 if persistent else 0)
+    ex = Expert(shape, weights, oracle_dtype)
+    active = {}
+    worst, sens = 0.0, {}
+
+    def context(e, r):
+        k, v = synth.draw_context(shape, ctx_seed, e, r)
+        return k, (v * np.float32(v_scale) if v_scale != 1.0 else v)
+
+    for st in range(max(captures) + 1):
+        pubs = []
+        if st == 0:
+            pubs = [(e, 0, init_tobs) for e in range(batch)]
+        elif period > 0:
+            pubs = [(e, active[e][0] + 1, st - lag) for e in range(batch)
+                    if ((st + e) if stagger else st) % period == 0 and st - lag >= active[e][1]]
+        for e, r, tob in pubs:
+            k, v = context(e, r)
+            g.set_context(e, k, v, tob)
+            active[e] = (r, tob)
+        z = synth.draw_fop_tokens(shape, ctx_seed, st, batch=batch) if shape.n_fop > 0 else None
+        if st not in captures:
+            g.step(z)
+            continue
+        X0, t, _ = g.state()
+        assert t == st
+        a = g.step(z)
+        X1, t1, _ = g.state()
+        assert t1 == st + 1
+        L0, vg = recovered_velocity(X0, X1, a, st)
+        for e in envs:
+            r, tob = active[e]
+            k, v = context(e, r)
+            delta = (st - tob) / H + shape.delta_bias
+            ze = None if z is None else z[e]
+            vo = ex.velocity(L0[e], k, v, delta, ze)
+            err = rel_err(vg[e], vo)
+            worst = max(worst, err)
+            log(f"step {st} env {e} (delta {delta:.3f}): velocity error {err:.3e}")
+            assert np.all(np.isfinite(vg[e])), f"step {st} env {e}: non-finite GPU velocity"
+            assert err <= tol, f"step {st} env {e}: velocity error {err:.3e} > {tol:.1e}"
+            if st == captures[0] and e == envs[0]:
+                for h in sens_report:
+                    if h == "adapter" and shape.n_fop == 0:
+                        continue
+                    sens[h] = rel_err(ex.velocity(L0[e], k, v, delta, ze, hooks={h}), vo)
+                    log(f"  without {h}: the velocity moves by {sens[h]:.3e} ({sens[h] / tol:.1f}x tolerance)")
+                for h in sens_assert:
+                    assert sens[h] >= 10 * tol, f"{h} moves the velocity by only {sens[h]:.3e} (< 10x {tol:.1e})"
+    return worst, sens
