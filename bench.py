@@ -66,6 +66,8 @@ def parse():
     p.add_argument("--no-full", action="store_true", help="skip the full-horizon denoising baseline")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
     p.add_argument("--profile-steps", type=int, default=3)
+    p.add_argument("--no-configs", action="store_true",
+                   help="skip the other workloads (tiny fp32, small bf16, large expert at batch 16)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="first run 5 plain device copies of MIB MiB (counter calibration under rocprofv3)")
     return p.parse_args()
@@ -191,6 +193,10 @@ class Workload:
         self.buf.sync()
         self.t = 0
         self.gen = [0] * self.B
+        # refreshes come from the VLM worker's own stream (the paper's separate VLM and
+        # action-expert workers): their copies run beside the steps, and a step applies a
+        # refresh once its copy has completed
+        self.producer = torch.cuda.Stream()
         log(f"[{name}] ready in {time.time() - t0:.1f}s")
 
     def refresh(self):
@@ -203,7 +209,7 @@ class Workload:
             if phase % s.context_period == 0 and self.t >= s.context_period:
                 self.gen[e] ^= 1
                 k, v = self.ctx[self.gen[e]]
-                self.buf.set_context(e, k[e], v[e], self.t - s.context_period)
+                self.buf.set_context(e, k[e], v[e], self.t - s.context_period, stream=self.producer)
 
     def step(self):
         self.refresh()
@@ -333,6 +339,24 @@ class Workload:
         model.close()
         return e0.elapsed_time(e1) / steps
 
+    def fop_timing(self, n=200, warmup=10):
+        """ms per ravel_fop_encode call (the FOP stand-in encoder over the batch's
+        observation vectors), timed with HIP events; not part of the step."""
+        import synth
+        torch = self.torch
+        obs = torch.from_numpy(synth.draw_observation(self.s, 0, 0, batch=self.B)).to("cuda:0").contiguous()
+        z = torch.empty_like(self.fop)
+        for _ in range(warmup):
+            self.buf.fop_encode(obs, z)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(self.stream)
+        for _ in range(n):
+            self.buf.fop_encode(obs, z)
+        e1.record(self.stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
     def latencies(self, n):
         torch = self.torch
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
@@ -410,10 +434,12 @@ def cpu_baseline(name, W, seconds):
     try:
         import threadpoolctl
         info = threadpoolctl.threadpool_info()
-        cores = max([i.get("num_threads", 1) for i in info] + [1])
+        blas = max([i.get("num_threads", 1) for i in info] + [1])
     except Exception:
-        cores = os.cpu_count()
-    return {"value": round(env_steps_per_s / s.batch, 4), "unit": "steps/s", "cores": cores, "kind": "oracle",
+        blas = None
+    cores = blas if blas else os.cpu_count()
+    return {"value": round(env_steps_per_s / s.batch, 4), "unit": "steps/s", "cores": cores,
+            "cpu_count": os.cpu_count(), "blas_threads": blas, "kind": "oracle",
             "sample": f"{n} steps of env 0 of {name} with the float32 numpy oracle in {el:.1f}s "
                       f"(steps/s = env-steps/s / batch {s.batch})"}
 
@@ -507,9 +533,38 @@ def main():
             for S, fm in wl.full_denoise_timing(sorted({10, s.horizon}))]
         log(f"[{s.name}] full denoise: " + ", ".join(f"{d['steps']} steps {d['ms_per_chunk']} ms"
                                                        for d in out["full_denoise"]))
+    out["fop_encode"] = {"ms_per_call": round(wl.fop_timing(), 4), "batch": wl.B,
+                         "note": "FOP stand-in encoder, separate from the step"}
+    log(f"[{s.name}] FOP encoder {out['fop_encode']['ms_per_call'] * 1e3:.1f} us per call")
     W = wl.W
+    if not args.no_configs and args.workload == "pi_b1":
+        # the other workloads: tiny fp32 (latency-bound), small bf16 (its 81 MB of
+        # weights and contexts stay in the 256 MB Infinity Cache, so its HBM fraction
+        # is quoted with that caveat), the large expert at batch 16 (MFMA-bound)
+        wl = None
+        torch.cuda.synchronize()
+        out["configs"] = {}
+        for name, steps_c in (("tiny_fp32", 400), ("small_bf16", 400), ("large_b16", 30)):
+            wc = Workload(name)
+            sc = wc.s
+            msc, _ = wc.timed(steps_c, 10)
+            d = {"steps": steps_c, "us_per_step": round(msc * 1e3, 2), "steps_per_s": round(1000.0 / msc, 2),
+                 "batch": wc.B}
+            if name == "small_bf16":
+                by = algorithmic_bytes(sc, wc.B)
+                d["hbm_frac"] = round(by / (msc * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+                d["note"] = "bytes per step fit the 256 MB Infinity Cache: not an HBM-streaming figure"
+            if name == "large_b16":
+                fl = algorithmic_flops(sc, wc.B)
+                d["mfma_TFLOPs"] = round(fl / (msc * 1e-3) / 1e12, 1)
+                d["mfma_frac"] = round(fl / (msc * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4)
+                d["env_steps_per_s"] = round(wc.B * 1000.0 / msc, 1)
+            out["configs"][name] = d
+            log(f"[{name}] {d['us_per_step']} us/step")
+            del wc
+            torch.cuda.synchronize()
     if not args.no_batch64 and args.workload == "pi_b1":
-        del wl
+        wl = None
         torch.cuda.synchronize()
         w64 = Workload("pi_b64", weights=W)  # the same model at batch 64
         s64 = w64.s
