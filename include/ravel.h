@@ -237,6 +237,24 @@ ravel_status ravel_step(ravel_buffer* buf, const void* fop_tokens, float* action
  *   obs: device float [B, d_obs]; fop_tokens: device [B, n_fop, w] model dtype. */
 ravel_status ravel_fop_encode(ravel_buffer* buf, const float* obs, void* fop_tokens, void* stream);
 
+/* ravel_fop_encode for callers that cannot allocate device memory -- code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc: the
+ * same encoder (same kernels, same results as ravel_fop_encode on a buffer of
+ * `batch` envs) without a buffer, its staging rows, split-K partials and tickets
+ * kept in a fixed device array of 16 MiB that the library holds on every GPU it
+ * runs on until the process ends (set up by ravel_create on the device current
+ * then).  Calls no allocating routine; enqueued on `stream` (its tickets are
+ * cleared with a kernel, not a memset).
+ *   obs: device float [batch, d_obs]; fop_tokens: device [batch, n_fop, w] model dtype.
+ * Every call on one GPU shares that GPU's array (the last call's contents stay):
+ * calls that overlap on one GPU (different streams or threads without ordering)
+ * race and must be serialised by the caller.  Errors: E_INVALID (null pointer, or
+ * a batch whose workspace exceeds the fixed array -- the message gives both sizes),
+ * E_SHAPE (batch < 1), E_STATE (no FOP encoder weights, or no model created on
+ * the current device). */
+ravel_status ravel_fop_encode_noalloc(const ravel_model* model, int32_t batch, const float* obs, void* fop_tokens,
+                                      void* stream);
+
 /* Wait until every enqueued step and context copy of this buffer finished. */
 ravel_status ravel_buffer_sync(ravel_buffer* buf);
 

@@ -825,6 +825,18 @@ hipError_t launch_euler_release(float* X, const float* v, int64_t* t, int B, int
   return hipGetLastError();
 }
 
+__global__ void zero_u32_kernel(unsigned* __restrict__ p, long long n) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0u;
+}
+
+// Zero n words with a kernel (a memset node recorded into a captured graph is avoided).
+hipError_t launch_zero_u32(unsigned* p, long long n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(zero_u32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, p, n);
+  return hipGetLastError();
+}
+
 __global__ void ring_init_kernel(float* X, int B, int H, int D, uint64_t seed) {
   const int NG = (D + 3) / 4;
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;

@@ -216,6 +216,9 @@ hipError_t launch_euler_release(float* X, const float* v, int64_t* t, int B, int
                                 uint64_t seed, float* action, unsigned* ticket, const float* state,
                                 const float* mask, const int* err, int* host_flag, hipStream_t s);
 
+// Zero n 32-bit words on stream s with a kernel.
+hipError_t launch_zero_u32(unsigned* p, long long n, hipStream_t s);
+
 // Fill X[e, r mod H, :] with the Philox noise of action r, for r = 0..H-1.
 hipError_t launch_ring_init(float* X, int B, int H, int D, uint64_t seed, hipStream_t s);
 

@@ -1370,7 +1370,38 @@ static ravel_status flow_time_table(ravel_model* m, int S, float* out) {
   return done(RAVEL_OK);
 }
 
+// ---------------------------------------------------------------------------
+// Fixed device scratch of the allocation-free FOP encoder entry point
+// ---------------------------------------------------------------------------
+// Staging rows, split-K partials and tickets of ravel_fop_encode_noalloc live in
+// this array; every GPU the library runs on holds its own copy until the process
+// ends.  Host code never passes the array's name to a kernel: it takes the
+// device address from hipGetSymbolAddress, once per device, at model creation.
+constexpr size_t kNoAllocScratchBytes = (size_t)16 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
 namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch` (looked up and cleared on first use).
+ravel_status scratch_init_current_device() {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(RAVEL_E_STATE, "device index beyond the scratch table");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev]) return RAVEL_OK;
+  void* ptr = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+  if (e != hipSuccess || !ptr)
+    return fail(RAVEL_E_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+  HIP_TRY(hipMemset(ptr, 0, kNoAllocScratchBytes));
+  HIP_TRY(hipDeviceSynchronize());
+  g_scratch_ptr[dev] = ptr;
+  return RAVEL_OK;
+}
+
 // The FOP stand-in encoder over a batch (shared by both entry points): obs [B, d]
 // fp32 -> bf16 staging (bf16 models), hidden = gelu_tanh(W1 obs + b1), tokens =
 // W2 hidden + b2; b provides the model, the batch size, the staging rows and the
@@ -1445,6 +1476,10 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
     if (hipMemcpy(m->analytic, t->data, n * 4, hipMemcpyDefault) != hipSuccess)
       return bail(fail(RAVEL_E_HIP, "upload analytic parameter"));
     m->weight_bytes = n * 4;
+    {
+      const ravel_status si = scratch_init_current_device();
+      if (si != RAVEL_OK) return bail(si);
+    }
     *out = m;
     return RAVEL_OK;
   }
@@ -1719,6 +1754,10 @@ ravel_status ravel_create(const ravel_config* cfgp, const ravel_tensor* weights,
   }
   wb += (int64_t)2 * w * w * E + (int64_t)D * w * E;
   m->weight_bytes = wb;
+  {
+    const ravel_status si = scratch_init_current_device();
+    if (si != RAVEL_OK) return bail(si);
+  }
   *out = m;
   return RAVEL_OK;
 }
@@ -2191,6 +2230,56 @@ ravel_status ravel_fop_encode(ravel_buffer* b, const float* obs, void* fop_token
   if (!b->m->has_fop_encoder) return fail(RAVEL_E_STATE, "model has no FOP encoder weights");
   std::lock_guard<std::mutex> lk(b->mu);
   return fop_encode_impl(b, obs, fop_tokens, (hipStream_t)stream);
+}
+
+ravel_status ravel_fop_encode_noalloc(const ravel_model* mc, int32_t batch, const float* obs, void* fop_tokens,
+                                      void* stream) {
+  if (!mc || !obs || !fop_tokens) return fail(RAVEL_E_INVALID, "null argument");
+  ravel_model* m = const_cast<ravel_model*>(mc);
+  if (!m->has_fop_encoder) return fail(RAVEL_E_STATE, "model has no FOP encoder weights");
+  if (batch < 1) return fail(RAVEL_E_SHAPE, "batch must be >= 1");
+  const ravel_config& c = m->cfg;
+  const int w = c.width, d = c.fop_obs_dim;
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  void* base = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (dev >= 0 && dev < kMaxDevices) base = g_scratch_ptr[dev];
+  }
+  if (!base) return fail(RAVEL_E_STATE, "no model was created on the current device (its scratch is not set up)");
+  // workspace of the two GEMMs, then the staging rows, 256-byte aligned
+  size_t part_elems = 0;
+  int tiles = 1;
+  if (m->bf16) {
+    const GemmPlan p1 = plan_gemm(batch, w, d, false), p2 = plan_gemm(batch, c.n_fop * w, w, false);
+    part_elems = std::max(p1.part_elems, p2.part_elems);
+    tiles = std::max(std::max(p1.tiles, p2.tiles), 1);
+  }
+  const size_t cnt_bytes = align_up((size_t)tiles * kCounterStride * 4, 256);
+  const size_t part_bytes = align_up(std::max<size_t>(part_elems, 1) * 4, 256);
+  const size_t obs_bytes = align_up((size_t)batch * std::max(d, 1) * m->elt, 256);
+  const size_t hid_bytes = align_up((size_t)batch * w * m->elt, 256);
+  const size_t need = cnt_bytes + part_bytes + obs_bytes + hid_bytes;
+  if (need > kNoAllocScratchBytes)
+    return fail(RAVEL_E_INVALID, "ravel_fop_encode_noalloc: batch " + std::to_string(batch) + " needs " +
+                                     std::to_string(need) + " bytes of scratch; the fixed scratch holds " +
+                                     std::to_string(kNoAllocScratchBytes));
+  char* q = (char*)base;
+  ravel_buffer ws;  // views into the scratch only: nothing is allocated
+  ws.m = m;
+  ws.B = batch;
+  ws.gcnt = (unsigned*)q;
+  ws.gcnt_n = tiles;
+  ws.gpart = (float*)(q + cnt_bytes);
+  ws.gpart_elems = part_elems;
+  ws.obs_t = q + cnt_bytes + part_bytes;
+  ws.fhid = q + cnt_bytes + part_bytes + obs_bytes;
+  hipStream_t s = (hipStream_t)stream;
+  // the tickets must start at zero (an earlier call re-arms them, but a call that
+  // failed half-way may not have)
+  HIP_TRY(launch_zero_u32(ws.gcnt, (long long)tiles * kCounterStride, s));
+  return fop_encode_impl(&ws, obs, fop_tokens, s);
 }
 
 ravel_status ravel_buffer_sync(ravel_buffer* b) {

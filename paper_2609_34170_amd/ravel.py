@@ -53,7 +53,7 @@ SYMBOLS = [
     "ravel_create", "ravel_destroy", "ravel_model_weight_bytes", "ravel_buffer_create",
     "ravel_buffer_destroy", "ravel_buffer_set_option", "ravel_context_acquire", "ravel_set_context",
     "ravel_step", "ravel_step_state", "ravel_set_relative_dims", "ravel_full_denoise", "ravel_train_loss",
-    "ravel_fop_encode", "ravel_buffer_sync", "ravel_debug_state",
+    "ravel_fop_encode", "ravel_fop_encode_noalloc", "ravel_buffer_sync", "ravel_debug_state",
     "ravel_publish_log", "ravel_buffer_query",
     "ravel_buffer_save", "ravel_buffer_load", "ravel_profile_step", "ravel_last_error",
 ]
@@ -84,6 +84,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "ravel_set_relative_dims": ([vp, vp], i32),
         "ravel_step_state": ([vp, vp, vp, vp, vp], i32),
         "ravel_fop_encode": ([vp, vp, vp, vp], i32),
+        "ravel_fop_encode_noalloc": ([vp, i32, vp, vp, vp], i32),
         "ravel_buffer_sync": ([vp], i32),
         "ravel_debug_state": ([vp, vp, vp, vp], i32),
         "ravel_publish_log": ([vp, vp, ctypes.POINTER(i32)], i32),
@@ -162,6 +163,11 @@ class Model:
         h = ctypes.c_void_p()
         _check(lib.ravel_create(ctypes.byref(self.cfg), arr, len(weights), ctypes.byref(h)))
         self.h = h
+
+    def fop_encode_noalloc(self, batch: int, obs, fop_tokens, stream=None):
+        """The FOP encoder without a buffer and without allocating (fixed device scratch)."""
+        _check(load_library().ravel_fop_encode_noalloc(self.h, int(batch), _ptr(obs), _ptr(fop_tokens),
+                                                        _stream(stream)))
 
     @property
     def weight_bytes(self) -> int:
