@@ -3,8 +3,13 @@
     python -m paper_2609_34170_amd.profiling stats <kernel_stats.csv> <out.md> --title T --command C [--bench-line F]
     python -m paper_2609_34170_amd.profiling traffic <fetch_dir> <write_dir> --kernel K --workload W
                                                      --regex R --algorithmic-bytes B --command-fetch C1 --command-write C2
+    python -m paper_2609_34170_amd.profiling counters <pmc_dir> <out.md> --title T --command C
 
 ``stats`` turns a ``--kernel-trace --stats`` kernel table into a markdown table.
+``counters`` summarises a ``--pmc`` pass of SQ_VALU_MFMA_BUSY_CYCLES, GRBM_GUI_ACTIVE,
+SQ_LDS_IDX_ACTIVE, SQ_LDS_BANK_CONFLICT, SQ_INSTS_VALU and SQ_INSTS_VALU_MFMA_MOPS_BF16
+per kernel: MFMA busy = busy cycles summed over SIMDs / (GUI-active cycles x SIMDs),
+the GUI-active cycles of a dispatch being the largest over the XCDs.
 ``traffic`` reads two ``--pmc`` runs (FETCH_SIZE, then WRITE_SIZE, in KiB per
 dispatch) of a program that also ran plain device copies of 512 MiB
 (``bench.py --copy-calibration 512``): each counter is scaled by the bytes a
@@ -148,6 +153,49 @@ def traffic(fetch_dir, write_dir, kernel, workload, regex, algo_bytes, cmd_fetch
     return entry, "\n".join(md) + "\n"
 
 
+# MI355X: 256 compute units of 4 SIMDs in 8 XCDs
+CUS, SIMDS, XCDS = 256, 1024, 8
+
+
+def counters_markdown(pmc_dir, title, command):
+    """Per kernel: dispatches, MFMA busy, LDS active, LDS bank conflicts per LDS-active cycle,
+    VALU instructions per bf16 MFMA op (the counters are summed over the XCDs' instances;
+    GRBM_GUI_ACTIVE, the same on every XCD, is divided by their count)."""
+    files = glob.glob(os.path.join(pmc_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise FileNotFoundError(f"no counter_collection.csv under {pmc_dir}")
+    agg, disp = {}, {}
+    for f in files:
+        for r in _rows(f):
+            name = _col(r, "Kernel_Name")
+            name = name if len(name) <= 70 else name[:68] + ".."
+            c = _col(r, "Counter_Name")
+            agg.setdefault(name, {}).setdefault(c, 0.0)
+            agg[name][c] += float(_col(r, "Counter_Value"))
+            disp.setdefault(name, set()).add(_col(r, "Dispatch_Id"))
+    out = [f"# {title}", "", "Command (from the repository root, on one MI355X):", "", "    " + command, "",
+           "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE per XCD x 1024 SIMDs); LDS active =",
+           "SQ_LDS_IDX_ACTIVE / (GRBM_GUI_ACTIVE per XCD x 256 CUs); conflicts = SQ_LDS_BANK_CONFLICT /",
+           "SQ_LDS_IDX_ACTIVE; GRBM_GUI_ACTIVE is reported summed over the 8 XCDs.", "",
+           "| kernel | dispatches | GPU-active us / dispatch | MFMA busy | LDS active | LDS bank conflicts | VALU instr / bf16 MFMA op |",
+           "|---|---:|---:|---:|---:|---:|---:|"]
+    for name, d in sorted(agg.items(), key=lambda kv: -kv[1].get("GRBM_GUI_ACTIVE", 0.0)):
+        n = len(disp[name])
+        gui = d.get("GRBM_GUI_ACTIVE", 0.0) / XCDS  # cycles, summed over dispatches
+        if gui <= 0:
+            continue
+        mfma = d.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (gui * SIMDS)
+        lds = d.get("SQ_LDS_IDX_ACTIVE", 0.0) / (gui * CUS)
+        conf = d.get("SQ_LDS_BANK_CONFLICT", 0.0) / max(d.get("SQ_LDS_IDX_ACTIVE", 0.0), 1.0)
+        ops = d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0)
+        valu = d.get("SQ_INSTS_VALU", 0.0) / ops if ops > 0 else float("nan")
+        out.append(f"| `{name}` | {n} | {gui / n / 2400.0:.1f} | {mfma * 100:.1f}% | {lds * 100:.1f}% | "
+                   f"{conf * 100:.1f}% | {valu:.3f} |")
+    out.append("")
+    out.append("GPU-active microseconds assume the 2.4 GHz clock.")
+    return "\n".join(out) + "\n"
+
+
 def main(argv=None):
     p = argparse.ArgumentParser()
     sub = p.add_subparsers(dest="cmd", required=True)
@@ -168,8 +216,16 @@ def main(argv=None):
     t.add_argument("--command-fetch", required=True)
     t.add_argument("--command-write", required=True)
     t.add_argument("--avg-us", type=float)
+    c = sub.add_parser("counters")
+    c.add_argument("pmc_dir")
+    c.add_argument("out")
+    c.add_argument("--title", required=True)
+    c.add_argument("--command", required=True)
     a = p.parse_args(argv)
-    if a.cmd == "stats":
+    if a.cmd == "counters":
+        with open(a.out, "w") as fh:
+            fh.write(counters_markdown(a.pmc_dir, a.title, a.command))
+    elif a.cmd == "stats":
         with open(a.out, "w") as fh:
             fh.write(stats_markdown(a.csv, a.title, a.command, a.bench_line))
     else:
