@@ -323,6 +323,9 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
   const int G = a.nq / a.nkv;
   const int R = G * a.Hq;
   const int row = (chunk * NW + wave) * 16 + l16;  // this lane's row
+  // a wave whose 16 rows all lie past the group stages tiles and meets the
+  // barriers but does no MFMA or softmax work (uniform per wave)
+  const bool active = (chunk * NW + wave) * 16 < R;
 
   const bf16_t* q = (const bf16_t*)a.q;
   const int slot = a.slot ? a.slot[e] : 0;
@@ -434,6 +437,7 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
   auto tile_step = [&](int t, Stage& s_next2, const Stage& s_next1) {
     const int k0 = t * TK, buf = t & 1;
     if (t + 2 < ntile) load_tile(k0 + 2 * TK, s_next2);
+    if (active) {
     // S^T[key][row] for two 16-key sub-tiles, each summed in two independent
     // MFMA chains (even / odd k-steps)
     f32x4_t sa0 = {0.f, 0.f, 0.f, 0.f}, sa1 = sa0, sb0 = sa0, sb1 = sa0;
@@ -511,6 +515,7 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
       o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vv), pf, o[dt], 0, 0, 0);
     }
     __builtin_amdgcn_s_setprio(0);
+    }
     if (t + 1 < ntile) store_tile(buf ^ 1, s_next1);
     __syncthreads();
   };

@@ -886,8 +886,8 @@ RAVEL_DEV void attn_merge(const AttnArgs& a, int e, int j, int el0, int el1, PSm
     const int t = tid + r * 256, sp = t >> 6, qq = t & 63;
     mlv[r] = ld_f2<COH>(rML, boff(sp < a.nsplit && qq < a.Hq, ((pbase + sp) * Hp + qq) * 2 * 4));
   }
-  // each thread sums one element over the splits
-  constexpr int SB = kMaxAttnSplit;  // every split of a head in one batch of loads
+  // each thread sums one element over the splits, 16 splits per batch of loads
+  constexpr int SB = 16;
   f32x4_t pvl[SB];
   auto load_parts = [&](int el, int sp0) {
     const int qq = el / (HD / 4), d = (el % (HD / 4)) * 4;
@@ -1142,6 +1142,53 @@ RAVEL_DEV void rope_item(const PRope& r, int row) {
   }
 }
 
+// L2 warm-up by the blocks without an item: while the other blocks work on phase p, a
+// block that has no item in it touches one dword of every 128-byte line that the
+// items of phase p + 1 on its XCD (item j runs on block j, XCD j % 8) read from memory
+// written before the launch -- the item's weight rows, or the keys and values of a
+// prefix attention split -- so that those items' loads at the barrier find the lines
+// in the XCD's L2.  The idle blocks of an XCD share its items round-robin; a block
+// with an item of its own never issues these loads, so none of its waits include them.
+template <int HD>
+RAVEL_DEV void idle_warm(const Phase& nx, int items_now, const int* slots) {
+  const int b = blockIdx.x, G = gridDim.x;
+  if (b < items_now) return;
+  const int x = b & 7;
+  const int first = items_now + ((x - (items_now & 7)) + 8) % 8;  // this XCD's first idle block
+  if (first >= G) return;
+  const int rank = (b - first) >> 3, count = (G - 1 - first) / 8 + 1;
+  const int ntype = uni(nx.type);
+  const int nitems = min(uni(nx.items), G);
+  const int tid = local_tid();
+  unsigned acc = 0;
+  for (int j = x; j < nitems; j += 8) {
+    if (((j >> 3) % count) != rank) continue;
+    if (ntype == PH_GEMM) {
+      const PGemm g = make_uniform(nx.g);
+      const int tiles = (g.N + 63) >> 6, tile = j % tiles, z = j / tiles;
+      const int n0 = tile * 64, kb = z * 256 * g.kw, lpr = 4 * g.kw;  // 64-column lines per row
+      const rsrc_t rw = rsrc(g.W);
+      for (int l = tid; l < 64 * lpr; l += 256) {
+        const int n = n0 + l / lpr, k = kb + (l % lpr) * 64;
+        acc += __builtin_amdgcn_raw_buffer_load_b32(rw, boff(n < g.N && k < g.K, ((size_t)n * g.ldw + k) * 2), 0,
+                                                    PLAIN);
+      }
+    } else if (ntype == PH_ATTN) {
+      const AttnArgs a = make_uniform(nx.at);
+      const SplitKeys k = split_keys(a, j);
+      if (k.self) continue;
+      constexpr int LPK = HD / 64 > 0 ? HD / 64 : 1;  // lines per key row of one head
+      const int slot = a.slot ? slots[k.e] : 0;
+      const int half = uni(tid >> 7);  // waves 0-1: keys, waves 2-3: values
+      const bf16_t* base = (const bf16_t*)(half ? a.pv : a.pk) + slot * a.p_slot_stride + k.e * a.p_env_stride;
+      const int l = tid & 127, key = k.kbeg + l / LPK, dc = (l % LPK) * 64;
+      acc += __builtin_amdgcn_raw_buffer_load_b32(
+          rsrc(base), boff(key < k.kend && dc < HD, ((size_t)key * a.p_ld + k.g * HD + dc) * 2), 0, PLAIN);
+    }
+  }
+  asm volatile("" ::"v"(acc));
+}
+
 template <int MT, int HD>
 __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __restrict__ phases, int nphase,
                                                               const int* __restrict__ env_slot, int nenv,
@@ -1218,6 +1265,7 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
       for (int item = blockIdx.x; item < items; item += gridDim.x) rope_item(r, item);
     }
     if (p + 1 == nphase) break;
+    idle_warm<HD>(desc[(p + 1) % 3], items, slots);
     // barrier between phases p and p + 1; while waiting, fetch descriptor p + 2
     // and what this block's item of phase p + 1 reads from before the launch
     wait_memory();
