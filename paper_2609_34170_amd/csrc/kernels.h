@@ -89,6 +89,7 @@ struct AttnArgs {
   float* part_ml;                  // [B*nq*nsplit][Hq_pad][2]
   unsigned* counters;              // [B*nq]
   int coop;                        // persistent kernel: the splits of a head merge together
+  int coh;                         // persistent kernel: device-coherent loads of q and the self rows
 };
 
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s);

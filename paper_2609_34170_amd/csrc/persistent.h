@@ -78,6 +78,13 @@ struct PGemm {
   const bf16_t* xk; const bf16_t* xv;  // PA_XATTN: FOP keys and values of the adapter
   int x_ld, x_nf, x_group;
   float x_scale;
+  // whole-K items (wk = column blocks of 16 per item, 1 or 2; 0: K ranges of 256 * kw
+  // with split tiles): item t covers columns [16 wk t, 16 wk (t + 1)) over the whole K,
+  // wave w its K quarter [w K/4, (w + 1) K/4) (K/4 a multiple of 32, at most 256); the
+  // quarters are added through LDS, so no tile is split across blocks.  PA_BF16 /
+  // PA_NORM operands, PE_BF16 / PE_GEGLU (wk = 2: a 16-column gate block and its up
+  // block) / PE_F32 epilogues.
+  int wk;
 };
 
 // Rotary positions (the rows' queries and keys written by the phase before): item =
@@ -87,6 +94,7 @@ struct PGemm {
 // the same layout); hd % 8 == 0.
 struct PRope {
   const bf16_t* qkv; bf16_t* out; int ld;
+  int coh;  // 1: device-coherent loads of qkv (written by whole-K items in 16-column pieces)
   int H, nh, hd;
   const float* cs;
 };

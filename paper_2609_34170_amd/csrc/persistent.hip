@@ -21,7 +21,9 @@
 //    from the row sums; split-K ranges are added in fixed order by the last
 //    block to arrive at the tile's ticket, whose epilogue writes bf16 / fp32
 //    outputs, gelu(gate) * up, or a gated residual update of x that also
-//    writes the next norm's p and the new row sums of squares;
+//    writes the next norm's p and the new row sums of squares; a K of at most
+//    1024 that the output tiles would split across blocks is instead covered
+//    whole by items of 16 (GeGLU: 2 x 16) columns, which need no meet;
 //  * ATTN: an item is one (env, head, key split): its keys and values are
 //    staged in LDS in one batch, the four waves take 16 queries each, and the
 //    splits are merged by the last item of the (env, head) to arrive.
@@ -277,8 +279,26 @@ RAVEL_DEV void load_w_xattn(const PGemm& g, int item, u32x4_t (&wf)[16]) {
   }
 }
 
+// Whole-K item fragments: wave w holds rows n0 + 16c + (lane & 15), c < wk, and the
+// K range w K/4 + 32f + 8(lane >> 4) .. +7, f < K/128 (fragment c * 8 + f).
+RAVEL_DEV void load_w_wk(const PGemm& g, int item, u32x4_t (&wf)[16]) {
+  const int tid = local_tid();
+  const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, grp = lane >> 4;
+  const int n0 = item * 16 * g.wk, kq = g.K >> 2, kb = wave * kq;
+  const rsrc_t rw = rsrc(g.W);
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+      const int n = n0 + c * 16 + l16, k = kb + f * 32 + grp * 8;
+      wf[c * 8 + f] = ld16<PLAIN>(rw, boff(c < g.wk && f * 32 < kq && n < g.N, ((size_t)n * g.ldw + k) * 2));
+    }
+}
+
 RAVEL_DEV void load_weights(const PGemm& g, int item, u32x4_t (&wf)[16]) {
-  if (g.a_mode == PA_XATTN)
+  if (g.wk)
+    load_w_wk(g, item, wf);
+  else if (g.a_mode == PA_XATTN)
     load_w_xattn(g, item, wf);
   else if (g.kw == 2)
     load_w<2>(g, item, wf);
@@ -688,6 +708,164 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int
   __syncthreads();
 }
 
+// A whole-K item: 16 * WK output columns of every row over the whole K, so the
+// item owns its outputs and no other block meets it.  The four waves take K
+// quarters of the item (all their loads -- shift rows, activations, row sums --
+// issued as one batch), are added through LDS in wave order, and thread
+// (i, lane) of the first MT * 64 writes row i*16 + (lane & 15), columns
+// n0 + 16c + 4(lane >> 4) .. +3 of every block c: bf16, fp32 plus bias, or
+// gelu(gate) * up of the block pair (gate block c = 0, up block c = 1).  The
+// norm's operand h = r p + shift is applied as in the split item.  Outputs
+// are narrower than a 128-byte line, so the phases that read them use
+// device-coherent loads.
+template <int MT, int WK>
+RAVEL_DEV void gemm_item_wk(const PGemm& g, int item, const u32x4_t (&w16)[16], PSmem& sm) {
+  bf16x8_t wf[WK][8];
+#pragma unroll
+  for (int c = 0; c < WK; ++c)
+#pragma unroll
+    for (int f = 0; f < 8; ++f) wf[c][f] = __builtin_bit_cast(bf16x8_t, w16[c * 8 + f]);
+  const int tid = local_tid(), lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, grp = lane >> 4;
+  const int n0 = item * 16 * WK, kq = g.K >> 2, kb = wave * kq;
+  const bool norm = g.a_mode == PA_NORM;
+  const bool has_shift = norm && g.shift != nullptr;
+  const rsrc_t rA = rsrc(g.A), rS = rsrc(g.shift);
+  bf16x8_t sh[MT][8], af[MT][8];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+      const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
+      sh[i][f] = ld_b8<PLAIN>(rS, boff(has_shift && m < g.M && f * 32 < kq, ((size_t)m * g.ld_shift + k) * 2));
+    }
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+      const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
+      const int o = boff(m < g.M && f * 32 < kq, a_off(g, m, k));
+      af[i][f] = g.a_coh ? ld_b8<COH>(rA, o) : ld_b8<PLAIN>(rA, o);
+    }
+  float sq[16];
+  const int row = tid & 63, part = tid >> 6, nt = g.K >> 6;
+  if (norm) {
+    const rsrc_t rQ = rsrc(g.sumsq_in);
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int t = part + 4 * j;
+      sq[j] = ld_f1<PLAIN>(rQ, boff(t < nt && row < g.M, (size_t)(t * 64 + row) * g.sq_in_ld * 4));
+    }
+  }
+  f32x4_t bias4 = {0.f, 0.f, 0.f, 0.f};
+  {
+    const int n = n0 + 4 * ((tid & 63) >> 4);
+    bias4 = ld_f4<PLAIN>(rsrc(g.bias), boff(g.e_mode == PE_F32 && g.bias && n + 4 <= g.N, (size_t)n * 4));
+  }
+
+  f32x4_t acc[WK][MT];
+#pragma unroll
+  for (int c = 0; c < WK; ++c)
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      acc[c][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      if (has_shift) {
+#pragma unroll
+        for (int f = 0; f < 8; ++f)
+          acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[c][f], sh[i][f], acc[c][i], 0, 0, 0);
+      }
+    }
+  if (norm) {
+    float ssum = 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) ssum += sq[j];
+    sm.rowsq[row][part] = ssum;
+    __syncthreads();
+    if (tid < 64) {
+      const float t = (sm.rowsq[tid][0] + sm.rowsq[tid][1]) + (sm.rowsq[tid][2] + sm.rowsq[tid][3]);
+      const float ms = t / (float)g.K + g.eps;
+      sm.rscale[tid] = 1.0f / sqrtf(ms);
+      sm.rowsq[tid][16] = sqrtf(ms);
+    }
+    __syncthreads();
+    if (has_shift) {
+#pragma unroll
+      for (int i = 0; i < MT; ++i) {
+        const float rms = sm.rowsq[i * 16 + l16][16];
+#pragma unroll
+        for (int c = 0; c < WK; ++c)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) acc[c][i][q] *= rms;
+      }
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < WK; ++c)
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int f = 0; f < 8; ++f)
+        acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[c][f], af[i][f], acc[c][i], 0, 0, 0);
+  if (norm) {
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const float r = sm.rscale[i * 16 + l16];
+#pragma unroll
+      for (int c = 0; c < WK; ++c)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[c][i][q] *= r;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < WK; ++c)
+#pragma unroll
+    for (int i = 0; i < MT; ++i) *(f32x4_t*)&sm.red[wave][c * MT + i][lane][0] = acc[c][i];
+  __syncthreads();
+  if (tid < MT * 64) {
+    const int i = tid >> 6, ln = tid & 63;
+    const int m = i * 16 + (ln & 15), cg = 4 * (ln >> 4);
+    f32x4_t s[WK];
+#pragma unroll
+    for (int c = 0; c < WK; ++c) {
+      s[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const f32x4_t v = *(const f32x4_t*)&sm.red[w][c * MT + i][ln][0];
+        s[c][0] += v[0];
+        s[c][1] += v[1];
+        s[c][2] += v[2];
+        s[c][3] += v[3];
+      }
+    }
+    if (m < g.M) {
+      if constexpr (WK == 2) {
+        if (g.e_mode == PE_GEGLU) {
+          st_bf16x4(rsrc(g.out_t), geglu_off(g, m, item * 16 + cg), gelu_tanh_f(s[0][0]) * s[1][0],
+                    gelu_tanh_f(s[0][1]) * s[1][1], gelu_tanh_f(s[0][2]) * s[1][2], gelu_tanh_f(s[0][3]) * s[1][3]);
+        }
+      }
+      if (g.e_mode == PE_BF16) {
+#pragma unroll
+        for (int c = 0; c < WK; ++c) {
+          const int n = n0 + 16 * c + cg;
+          if (n < g.N) st_bf16x4(rsrc(g.out_t), ((size_t)m * g.ldo + n) * 2, s[c][0], s[c][1], s[c][2], s[c][3]);
+        }
+      } else if (g.e_mode == PE_F32) {
+        const int n = n0 + cg;  // PE_F32 items have one column block
+        if (n + 4 <= g.N) {
+          st_f4(rsrc(g.out_f), ((size_t)m * g.ldof + n) * 4,
+                f32x4_t{s[0][0] + bias4[0], s[0][1] + bias4[1], s[0][2] + bias4[2], s[0][3] + bias4[3]});
+        } else {
+          for (int r = 0; n + r < g.N; ++r)
+            st_f1(rsrc(g.out_f), ((size_t)m * g.ldof + n + r) * 4, s[0][r] + (g.bias ? *gptr(g.bias + n + r) : 0.f));
+        }
+      }
+    }
+  }
+  __syncthreads();
+}
+
 // A split-K tile finished by its ksplit blocks together: block z takes rows
 // [z*rp, min(M, (z+1)*rp)), rp = ceil(M / ksplit), adds the partials of each of its
 // (row, 4-column) slots in split order and applies the epilogue; the new rows' sums
@@ -854,6 +1032,7 @@ RAVEL_DEV void attn_load_kv(const AttnArgs& a, const SplitKeys& k, const int* sl
   const rsrc_t rV = k.self ? rsrc((const bf16_t*)a.sv + (size_t)k.e * a.S * a.s_ld) : rsrc(pv);
   const int ld_row = k.self ? a.s_ld : a.p_ld;
   const int k_row0 = k.self ? a.P : 0;
+  const bool coh = k.self && a.coh;
   auto off = [&](int kidx, int dc) {
     return boff(kidx < k.kend, ((size_t)(kidx - k_row0) * ld_row + k.g * HD + dc) * 2);
   };
@@ -861,12 +1040,12 @@ RAVEL_DEV void attn_load_kv(const AttnArgs& a, const SplitKeys& k, const int* sl
   for (int r = 0; r < 4; ++r) {
     const int c = tid + r * 256;
     const int o = off(k.kbeg + c / CPR, (c % CPR) * 8);
-    kv[r] = ld16<PLAIN>(rK, o);
+    kv[r] = coh ? ld16<COH>(rK, o) : ld16<PLAIN>(rK, o);
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int o = off(k.kbeg + (tid / CPR) * 4 + i, (tid % CPR) * 8);
-    kv[4 + i] = ld16<PLAIN>(rV, o);
+    kv[4 + i] = coh ? ld16<COH>(rV, o) : ld16<PLAIN>(rV, o);
   }
 }
 
@@ -962,8 +1141,10 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
   const bool active = wave < QB;
   bf16x8_t qf[KS];
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks)
-    qf[ks] = ld_b8<PLAIN>(rq, boff(query < a.Hq, ((size_t)(e * a.Hq + query) * a.ldq + j * HD + ks * 32 + grp * 8) * 2));
+  for (int ks = 0; ks < KS; ++ks) {
+    const int o = boff(query < a.Hq, ((size_t)(e * a.Hq + query) * a.ldq + j * HD + ks * 32 + grp * 8) * 2);
+    qf[ks] = a.coh ? ld_b8<COH>(rq, o) : ld_b8<PLAIN>(rq, o);
+  }
   after_loads();
   __syncthreads();  // LDS may still be read by this block's previous item
 #pragma unroll
@@ -1110,8 +1291,9 @@ constexpr int kDescChunks = (int)(sizeof(Phase) / 16);
 static_assert(sizeof(Phase) % 16 == 0 && kDescChunks <= 256, "phase descriptor size");
 
 // One row of a rotary phase: each thread turns four consecutive pairs of one head
-// (8-byte device-coherent loads and stores of the bf16 halves; the angle table was
-// written before the launch).
+// (8-byte loads and stores of the bf16 halves, the loads device-coherent when the
+// rows were written in pieces narrower than a line; the angle table was written
+// before the launch).
 RAVEL_DEV void rope_item(const PRope& r, int row) {
   const int i = row % r.H, half = r.hd >> 1, quads = r.nh * (half >> 2);
   const rsrc_t q = rsrc(r.qkv + (size_t)row * r.ld), qo = rsrc(r.out + (size_t)row * r.ld);
@@ -1119,8 +1301,10 @@ RAVEL_DEV void rope_item(const PRope& r, int row) {
   for (int idx = local_tid(); idx < quads; idx += 256) {
     const int h = idx / (half >> 2), d = (idx - h * (half >> 2)) * 4;
     const int o0 = (h * r.hd + d) * 2, o1 = o0 + half * 2;
-    const auto a = __builtin_amdgcn_raw_buffer_load_b64(q, o0, 0, PLAIN);
-    const auto b = __builtin_amdgcn_raw_buffer_load_b64(q, o1, 0, PLAIN);
+    const auto a = r.coh ? __builtin_amdgcn_raw_buffer_load_b64(q, o0, 0, COH)
+                         : __builtin_amdgcn_raw_buffer_load_b64(q, o0, 0, PLAIN);
+    const auto b = r.coh ? __builtin_amdgcn_raw_buffer_load_b64(q, o1, 0, COH)
+                         : __builtin_amdgcn_raw_buffer_load_b64(q, o1, 0, PLAIN);
     const f32x4_t c01 = ld_f4<PLAIN>(t, d * 8), c23 = ld_f4<PLAIN>(t, d * 8 + 16);
     const float cs[8] = {c01[0], c01[1], c01[2], c01[3], c23[0], c23[1], c23[2], c23[3]};
     float x[4], y[4];
@@ -1166,9 +1350,11 @@ RAVEL_DEV void idle_warm(const Phase& nx, int items_now, const int* slots) {
     if (ntype == PH_GEMM) {
       const PGemm g = make_uniform(nx.g);
       const int tiles = (g.N + 63) >> 6, tile = j % tiles, z = j / tiles;
-      const int n0 = tile * 64, kb = z * 256 * g.kw, lpr = 4 * g.kw;  // 64-column lines per row
+      // rows and 64-column lines per row of the item's weights
+      const int rows = g.wk ? 16 * g.wk : 64, lpr = g.wk ? g.K >> 6 : 4 * g.kw;
+      const int n0 = g.wk ? j * rows : tile * 64, kb = g.wk ? 0 : z * 256 * g.kw;
       const rsrc_t rw = rsrc(g.W);
-      for (int l = tid; l < 64 * lpr; l += 256) {
+      for (int l = tid; l < rows * lpr; l += 256) {
         const int n = n0 + l / lpr, k = kb + (l % lpr) * 64;
         acc += __builtin_amdgcn_raw_buffer_load_b32(rw, boff(n < g.N && k < g.K, ((size_t)n * g.ldw + k) * 2), 0,
                                                     PLAIN);
@@ -1247,7 +1433,11 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
       const PGemm g = make_uniform(ph.g);
       for (int item = blockIdx.x; item < items; item += gridDim.x) {
         if (item != (int)blockIdx.x) load_weights(g, item, pre);
-        if (g.kw == 2)
+        if (g.wk == 2)
+          gemm_item_wk<MT, 2>(g, item, pre, sm);
+        else if (g.wk == 1)
+          gemm_item_wk<MT, 1>(g, item, pre, sm);
+        else if (g.kw == 2)
           gemm_item<MT, 2>(g, item, pre, err, sm, none);
         else
           gemm_item<MT, 1>(g, item, pre, err, sm, none);

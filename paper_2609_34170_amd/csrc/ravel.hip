@@ -942,6 +942,8 @@ ravel_status build_persistent(ravel_buffer* b) {
     P.push_back(ph);
     b->pnames.push_back(name);
   };
+  bool whole_k = true;
+  if (const char* ev = getenv("RAVEL_NO_WHOLE_K")) whole_k = atoi(ev) == 0;
   auto gemm = [&](const void* A, int lda, const bf16_t* shift, bool norm, const void* W, int N, int K, int e_mode) {
     Phase ph;
     memset(&ph, 0, sizeof ph);
@@ -966,6 +968,17 @@ ravel_status build_persistent(ravel_buffer* b) {
     g.ksplit = (K + 256 * g.kw - 1) / (256 * g.kw);
     g.e_mode = e_mode;
     g.counters = nullptr;  // patched below
+    // a K that would be split over blocks and fits four waves' quarters of at most
+    // 256: whole-K items of 16 columns (a gate block and its up block for GeGLU)
+    const int wk = e_mode == PE_GEGLU ? 2 : 1;
+    if (whole_k && g.ksplit > 1 && K % 128 == 0 && K <= 1024 && N % (16 * wk) == 0 &&
+        (e_mode == PE_BF16 || e_mode == PE_F32 || e_mode == PE_GEGLU)) {
+      g.wk = wk;
+      g.kw = 1;
+      g.ksplit = 1;
+      ph.items = N / (16 * wk);
+      return ph;
+    }
     ph.items = tiles(N) * g.ksplit;
     g.coop = g.ksplit > 1 && ph.items <= b->pblocks;
     part = std::max(part, (size_t)g.ksplit * tiles(N) * mt * 4 * 64 * 4);
@@ -1024,6 +1037,9 @@ ravel_status build_persistent(ravel_buffer* b) {
   // an attention output is written in (query, head) segments of hd bf16 values by
   // each head's merge: whole 128-byte lines only when hd >= 64
   const int att_coh = hd < 64 ? 1 : 0;
+  // outputs of whole-K items are written in 16-column pieces (several writers per
+  // 128-byte line): their readers use device-coherent loads
+  bool qkv_pieces = false, qa_pieces = false, u_pieces = false;
   for (int l = 0; l < c.layers; ++l) {
     const LayerW& L = m->layers[l];
     const float* mod = b->mod + (size_t)l * 6 * w;
@@ -1033,6 +1049,7 @@ ravel_status build_persistent(ravel_buffer* b) {
       Phase ph = gemm(cur_p, w, shift_of(2 * l), true, L.qkv_w, qkvd, w, PE_BF16);
       ph.g.out_t = qkv;
       ph.g.ldo = qkvd;
+      qkv_pieces = ph.g.wk != 0;
       push(ph, "qkv");
     }
     // queries and keys as attention reads them: rotated into a buffer of their own
@@ -1050,6 +1067,7 @@ ravel_status build_persistent(ravel_buffer* b) {
       ph.r.nh = c.n_q_heads + c.n_kv_heads;
       ph.r.hd = hd;
       ph.r.cs = m->rope_cs;
+      ph.r.coh = qkv_pieces ? 1 : 0;
       push(ph, "rope");
       qk = rot;
     }
@@ -1073,6 +1091,7 @@ ravel_status build_persistent(ravel_buffer* b) {
       a.s_ld = qkvd;
       a.out = att;
       a.ldo = qd;
+      a.coh = qkv_pieces ? 1 : 0;
       push(attn_phase(a), "self_attn");
     }
     {
@@ -1090,6 +1109,7 @@ ravel_status build_persistent(ravel_buffer* b) {
         Phase ph = gemm(cur_p, w, nullptr, true, L.qa_w, qd, w, PE_BF16);
         ph.g.out_t = qa;
         ph.g.ldo = qd;
+        qa_pieces = ph.g.wk != 0;
         push(ph, "q_adapter");
       }
       // one env, heads of 256 dims, at most 16 FOP tokens: the output projection's
@@ -1106,6 +1126,7 @@ ravel_status build_persistent(ravel_buffer* b) {
         g.x_nf = c.n_fop;
         g.x_group = c.n_q_heads / c.n_kv_heads;
         g.x_scale = 1.0f / sqrtf((float)hd);
+        g.a_coh = qa_pieces ? 1 : 0;
         push(fused, "o_adapter");
       } else {
         bf16_t* xatt = (bf16_t*)fresh((size_t)BH * qd * 2);
@@ -1122,6 +1143,7 @@ ravel_status build_persistent(ravel_buffer* b) {
         a.S = 0;
         a.out = xatt;
         a.ldo = qd;
+        a.coh = qa_pieces ? 1 : 0;
         push(attn_phase(a), "cross_attn");
         Phase ph = gemm(xatt, qd, nullptr, false, L.oa_w, w, qd, PE_RESID);
         ph.g.a_coh = att_coh;
@@ -1135,11 +1157,13 @@ ravel_status build_persistent(ravel_buffer* b) {
       ph.g.out_t = u;
       ph.g.ldo = F;
       ph.g.out_t32 = 1;
+      u_pieces = ph.g.wk != 0;
       push(ph, "gate_up");
     }
     {
       Phase ph = gemm(u, F, nullptr, false, L.down_w, w, F, PE_RESID);
       ph.g.a_t32 = 1;
+      ph.g.a_coh = u_pieces ? 1 : 0;
       resid(ph, mod + 5 * w, nullptr, NS_ROW, next_scale);
       push(ph, "down");
     }
