@@ -396,6 +396,9 @@ hipError_t launch_transpose_f32(const float* src, int R, int C, float* dst, hipS
   return hipGetLastError();
 }
 
+// Element (row, n) of a [w/32][64 rows][32] tile layout (rows < 64).
+RAVEL_DEV size_t t32_index(int row, int n) { return ((size_t)(n >> 5) * 64 + row) * 32 + (n & 31); }
+
 // bf16 copies of the norm shifts: item = 8 consecutive columns of one (chunk, row)
 RAVEL_DEV void shift_copy_item(size_t idx, int M, int w, const InProjNorm& nrm) {
   const int per_row = w / 8;
@@ -407,7 +410,7 @@ RAVEL_DEV void shift_copy_item(size_t idx, int M, int w, const InProjNorm& nrm) 
   const float* src = nrm.cvt_in + (size_t)row * nrm.cvt_ld + (size_t)c * nrm.cvt_stride + n;
   const f32x4_t a = *(const f32x4_t*)src, b = *(const f32x4_t*)(src + 4);
   const u32x4_t o = {pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3])};
-  *(u32x4_t*)(nrm.cvt_out + ((size_t)c * M + row) * w + n) = o;
+  *(u32x4_t*)(nrm.cvt_out + (size_t)c * 64 * w + t32_index(row, n)) = o;
 }
 
 // Block = 4 waves over 256 consecutive columns (one 64-column tile per wave) and
@@ -481,7 +484,7 @@ __global__ __launch_bounds__(256) void in_proj_kernel(const float* __restrict__ 
     // first adaptive norm of the persistent step: p = bf16((1 + scale) x), the
     // 64-column tile's sum of squares of the row, and the bf16 shift copies
     const float v = n < w ? acc[rr] : 0.f;
-    if (n < w) nrm.p[(size_t)row * w + n] = f32_to_bf16((1.f + scv[rr]) * v);
+    if (n < w) nrm.p[t32_index(row, n)] = f32_to_bf16((1.f + scv[rr]) * v);
     const float sq = wave_sum(v * v);
     if (lane == 0 && n < w) nrm.sumsq[(size_t)(n >> 6) * 64 + row] = sq;
   }
@@ -520,7 +523,7 @@ __global__ __launch_bounds__(256) void norm_operands_kernel(const float* __restr
   // w is a multiple of 64: a wave is wholly inside or wholly outside the row
   if (n >= w) return;
   const float v = x[(size_t)row * w + n];
-  nrm.p[(size_t)row * w + n] = f32_to_bf16((1.f + nrm.scale[(size_t)row * nrm.ldm + n]) * v);
+  nrm.p[t32_index(row, n)] = f32_to_bf16((1.f + nrm.scale[(size_t)row * nrm.ldm + n]) * v);
   const float sq = wave_sum(v * v);
   if ((tid & 63) == 0) nrm.sumsq[(size_t)(n >> 6) * 64 + row] = sq;
 }

@@ -143,6 +143,9 @@ hipError_t launch_transpose_f32(const float* src, int R, int C, float* dst, hipS
 // the rows' sums of squares per 64-column tile sumsq[(n/64)*64 + row], and bf16 copies
 // cvt_out[c][row][n] = bf16(cvt_in[row*cvt_ld + c*cvt_stride + n]) for c < cvt_chunks.
 // p = NULL: none of these.
+// First adaptive norm of the persistent step (B*H <= 64 rows): p = bf16((1 + scale) x)
+// and the bf16 shift copies (chunk c at cvt_out + c * 64 * w) in 32-column tiles
+// [w/32][64 rows][32]; sumsq[(n / 64) * 64 + row] the 64-column tiles' sums of squares.
 struct InProjNorm {
   const float* scale; int ldm;
   bf16_t* p;

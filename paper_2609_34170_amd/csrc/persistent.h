@@ -55,6 +55,7 @@ struct PGemm {
   int a_t32;                           // PA_BF16: A stored in 32-column tiles [K/32][64 rows][32]
   int a_coh;                           // 1: device-coherent loads of A
   const bf16_t* shift; int ld_shift;   // PA_NORM: bf16 shift rows or NULL
+  int sh_t32;                          // PA_NORM: shift in 32-column tiles [K/32][64 rows][32]
   // PA_NORM: row sums of squares of x per 64-column tile, entry (t, row) at
   // sumsq_in[(t * 64 + row) * sq_in_ld]
   const float* sumsq_in; int sq_in_ld; float eps;
@@ -68,6 +69,7 @@ struct PGemm {
   const float* gate_scalar;            // tanh(*gate_scalar)
   int ns_mode; const float* ns; int ldns;  // PE_RESID: scale of the next norm
   bf16_t* p_out; int ldp;              // PE_RESID: p of the next norm
+  int p_t32;                           // PE_RESID: p in 32-column tiles [N/32][64 rows][32]
   // PE_RESID: row sums of squares of the new x, entry (tile, row) at
   // sumsq_out[(tile * 64 + row) * sq_out_ld] (32: one 128-byte line per entry)
   float* sumsq_out; int sq_out_ld;

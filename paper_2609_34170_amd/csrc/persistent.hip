@@ -317,6 +317,14 @@ RAVEL_DEV int coop_rows(const PGemm& g) {
 RAVEL_DEV size_t a_off(const PGemm& g, int m, int k) {
   return g.a_t32 ? ((size_t)(k >> 5) * 2048 + (size_t)m * 32 + (k & 31)) * 2 : ((size_t)m * g.lda + k) * 2;
 }
+// Byte offset of shift[m][k] (bf16): row-major with stride ld_shift, or 32-column tiles.
+RAVEL_DEV size_t sh_off(const PGemm& g, int m, int k) {
+  return g.sh_t32 ? ((size_t)(k >> 5) * 2048 + (size_t)m * 32 + (k & 31)) * 2 : ((size_t)m * g.ld_shift + k) * 2;
+}
+// Byte offset of p_out[m][n] (bf16) of a residual update.
+RAVEL_DEV size_t p_off(const PGemm& g, int m, int n) {
+  return g.p_t32 ? ((size_t)(n >> 5) * 2048 + (size_t)m * 32 + (n & 31)) * 2 : ((size_t)m * g.ldp + n) * 2;
+}
 // Byte offset of output column c (of N / 2) of row m of a gated-GeLU phase.
 RAVEL_DEV size_t geglu_off(const PGemm& g, int m, int c) {
   return g.out_t32 ? ((size_t)(c >> 5) * 2048 + (size_t)m * 32 + (c & 31)) * 2 : ((size_t)m * g.ldo + c) * 2;
@@ -448,7 +456,7 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int
 #pragma unroll
     for (int f = 0; f < NF; ++f) {
       const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
-      sh[i][f] = ld_b8<PLAIN>(rS, boff(has_shift && m < g.M && k < g.K, ((size_t)m * g.ld_shift + k) * 2));
+      sh[i][f] = ld_b8<PLAIN>(rS, boff(has_shift && m < g.M && k < g.K, sh_off(g, m, k)));
     }
 #pragma unroll
   for (int i = 0; i < MT; ++i)
@@ -688,7 +696,7 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int
         xn[2] = e_x[q][2] + gt[2] * v[2];
         xn[3] = e_x[q][3] + gt[3] * v[3];
         st_f4(rsrc(g.out_f), ((size_t)m * g.ldof + n) * 4, xn);
-        st_bf16x4(rsrc(g.p_out), ((size_t)m * g.ldp + n) * 2, (1.f + e_s[q][0]) * xn[0], (1.f + e_s[q][1]) * xn[1],
+        st_bf16x4(rsrc(g.p_out), p_off(g, m, n), (1.f + e_s[q][0]) * xn[0], (1.f + e_s[q][1]) * xn[1],
                   (1.f + e_s[q][2]) * xn[2], (1.f + e_s[q][3]) * xn[3]);
         sq = xn[0] * xn[0] + xn[1] * xn[1] + xn[2] * xn[2] + xn[3] * xn[3];
       }
@@ -737,7 +745,7 @@ RAVEL_DEV void gemm_item_wk(const PGemm& g, int item, const u32x4_t (&w16)[16], 
 #pragma unroll
     for (int f = 0; f < 8; ++f) {
       const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
-      sh[i][f] = ld_b8<PLAIN>(rS, boff(has_shift && m < g.M && f * 32 < kq, ((size_t)m * g.ld_shift + k) * 2));
+      sh[i][f] = ld_b8<PLAIN>(rS, boff(has_shift && m < g.M && f * 32 < kq, sh_off(g, m, k)));
     }
 #pragma unroll
   for (int i = 0; i < MT; ++i)
@@ -976,7 +984,7 @@ RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& 
         xn[2] = ex[2] + gt[2] * v[2];
         xn[3] = ex[3] + gt[3] * v[3];
         st_f4(rsrc(g.out_f), ((size_t)row * g.ldof + n) * 4, xn);
-        st_bf16x4(rsrc(g.p_out), ((size_t)row * g.ldp + n) * 2, (1.f + es[0]) * xn[0], (1.f + es[1]) * xn[1],
+        st_bf16x4(rsrc(g.p_out), p_off(g, row, n), (1.f + es[0]) * xn[0], (1.f + es[1]) * xn[1],
                   (1.f + es[2]) * xn[2], (1.f + es[3]) * xn[3]);
         sq = xn[0] * xn[0] + xn[1] * xn[1] + xn[2] * xn[2] + xn[3] * xn[3];
       }
@@ -1330,9 +1338,10 @@ RAVEL_DEV void rope_item(const PRope& r, int row) {
 // block that has no item in it touches one dword of every 128-byte line that the
 // items of phase p + 1 on its XCD (item j runs on block j, XCD j % 8) read from memory
 // written before the launch -- the item's weight rows, or the keys and values of a
-// prefix attention split -- so that those items' loads at the barrier find the lines
-// in the XCD's L2.  The idle blocks of an XCD share its items round-robin; a block
-// with an item of its own never issues these loads, so none of its waits include them.
+// prefix attention split, and the shift rows of a norm, which all of them read -- so
+// that those items' loads at the barrier find the lines in the XCD's L2.  The idle
+// blocks of an XCD share its items round-robin; a block with an item of its own never
+// issues these loads, so none of its waits include them.
 template <int HD>
 RAVEL_DEV void idle_warm(const Phase& nx, int items_now, const int* slots) {
   const int b = blockIdx.x, G = gridDim.x;
@@ -1345,6 +1354,20 @@ RAVEL_DEV void idle_warm(const Phase& nx, int items_now, const int* slots) {
   const int nitems = min(uni(nx.items), G);
   const int tid = local_tid();
   unsigned acc = 0;
+  if (ntype == PH_GEMM && nitems > x) {
+    // the norm's shift rows, which every item of the phase reads (K/64 lines per row)
+    const PGemm g = make_uniform(nx.g);
+    if (g.a_mode == PA_NORM && g.shift) {
+      // line l: rows 2j, 2j + 1 of 32-column tile c (tiles), or 64 columns of a row
+      const int lpr = g.sh_t32 ? (g.M + 1) >> 1 : g.K >> 6, lines = (g.sh_t32 ? g.K >> 5 : g.M) * lpr;
+      const rsrc_t rs = rsrc(g.shift);
+      for (int l = rank * 256 + tid; l < lines; l += count * 256) {
+        const size_t o = g.sh_t32 ? ((size_t)(l / lpr) * 2048 + (size_t)(l % lpr) * 64) * 2
+                                  : ((size_t)(l / lpr) * g.ld_shift + (l % lpr) * 64) * 2;
+        acc += __builtin_amdgcn_raw_buffer_load_b32(rs, o, 0, PLAIN);
+      }
+    }
+  }
   for (int j = x; j < nitems; j += 8) {
     if (((j >> 3) % count) != rank) continue;
     if (ntype == PH_GEMM) {
