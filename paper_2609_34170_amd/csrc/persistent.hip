@@ -1125,6 +1125,59 @@ RAVEL_DEV void attn_merge(const AttnArgs& a, int e, int j, int el0, int el1, PSm
   }
 }
 
+// The same merge in one round of loads, for a share of at most 128 elements and at
+// most kMaxAttnSplit splits: thread (h, j) = (tid / 128, tid % 128) takes element
+// el0 + j and the splits of parity h; it loads the (max, sum) of every split of
+// its query (one address per wave: the wave's elements share a query when HD >= 256,
+// a few queries otherwise) and its 16 partial outputs together, forms the weights
+// in registers, and the two halves are added through LDS (even splits, then odd).
+template <int HD>
+RAVEL_DEV void attn_merge_one_round(const AttnArgs& a, int e, int j, int el0, int el1, PSmem& sm) {
+  const int tid = local_tid(), h = tid >> 7, el = el0 + (tid & 127);
+  const int Hp = ((a.Hq + 15) / 16) * 16;
+  const size_t pbase = ((size_t)e * a.nq + j) * a.nsplit;
+  const rsrc_t rML = rsrc(a.part_ml), rO = rsrc(a.part_o);
+  const bool valid = el < el1;
+  const int qq = valid ? el / (HD / 4) : 0, d = (el % (HD / 4)) * 4;
+  float2 ml[kMaxAttnSplit];
+#pragma unroll
+  for (int sp = 0; sp < kMaxAttnSplit; ++sp)
+    ml[sp] = ld_f2<COH>(rML, boff(valid && sp < a.nsplit, ((pbase + sp) * Hp + qq) * 2 * 4));
+  f32x4_t pv[kMaxAttnSplit / 2];
+#pragma unroll
+  for (int i = 0; i < kMaxAttnSplit / 2; ++i) {
+    const int sp = 2 * i + h;
+    pv[i] = ld_f4<COH>(rO, boff(valid && sp < a.nsplit, (((pbase + sp) * Hp + qq) * HD + d) * 4));
+  }
+  // splits past nsplit read (0, 0): they are masked out of the max and get weight 0
+  float mmax = -INFINITY;
+#pragma unroll
+  for (int sp = 0; sp < kMaxAttnSplit; ++sp) mmax = fmaxf(mmax, sp < a.nsplit ? ml[sp].x : -INFINITY);
+  float den = 0.f;
+  f32x4_t num = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int sp = 0; sp < kMaxAttnSplit; ++sp) {
+    const bool use = sp < a.nsplit && ml[sp].x != -INFINITY;
+    const float wv = use ? exp2f(ml[sp].x - mmax) : 0.f;
+    den += wv * ml[sp].y;
+    const float wh = (sp & 1) == h ? wv : 0.f;
+    const f32x4_t p = pv[sp >> 1];
+    num[0] += wh * p[0];
+    num[1] += wh * p[1];
+    num[2] += wh * p[2];
+    num[3] += wh * p[3];
+  }
+  f32x4_t* x = reinterpret_cast<f32x4_t*>(&sm.red[0][0][0][0]);
+  if (h == 1) x[tid & 127] = num;
+  __syncthreads();
+  if (h == 0 && valid) {
+    const f32x4_t o = x[tid];
+    const float inv = 1.f / den;
+    st_bf16x4(rsrc(a.out), ((size_t)(e * a.Hq + qq) * a.ldo + j * HD + d) * 2, (num[0] + o[0]) * inv,
+              (num[1] + o[1]) * inv, (num[2] + o[2]) * inv, (num[3] + o[3]) * inv);
+  }
+}
+
 // One split: its keys and values (kv, fetched ahead when `have_kv`) are staged in
 // LDS, the four waves take 16 queries each, S^T = K Q^T with the split's softmax,
 // O^T = V^T P^T; a single split writes the output, otherwise the splits' partial
@@ -1282,7 +1335,10 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
       // shares of whole 128-byte lines of the bf16 output (16 elements of 4 dims)
       const int share = (((total + a.nsplit - 1) / a.nsplit) + 15) & ~15;
       const int el0 = split * share, el1 = min(total, el0 + share);
-      attn_merge<HD>(a, e, j, el0, el1, sm);
+      if (share <= 128)
+        attn_merge_one_round<HD>(a, e, j, el0, el1, sm);
+      else
+        attn_merge<HD>(a, e, j, el0, el1, sm);
     }
     group_leave(ctr, (unsigned)a.nsplit);
     __syncthreads();
