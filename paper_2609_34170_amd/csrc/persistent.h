@@ -113,8 +113,12 @@ struct alignas(16) Phase {
 // env_slot: [nenv] active context slot per env (read once per launch).
 // times: optional [nphase + 1] wall-clock stamps taken by block 0 at the start,
 // after each phase's barrier, and at its end (NULL: none).
+// counters: the ncounters split counters (one per kCounterStride words) that the
+// phases' tiles and heads use, each once per launch; zero at the launch, and zeroed
+// again by the last block to leave it.
 hipError_t launch_persistent(const Phase* phases, int nphase, const int* env_slot, int nenv, int mt, int hd, int blocks,
-                             unsigned* bar, int* err, unsigned long long* times, hipStream_t s);
+                             unsigned* bar, int* err, unsigned long long* times, unsigned* counters, int ncounters,
+                             hipStream_t s);
 // Blocks of the persistent kernel (row tiles mt, head dimension hd) that can be
 // co-resident (0 on error).
 int persistent_max_blocks(int mt, int hd);

@@ -145,16 +145,18 @@ RAVEL_DEV T make_uniform(const T& s) {
 }
 
 
+// Split tiles and split heads count their arrivals in counters of their own: every
+// phase has a range of counters used once per launch (zeroed by the last block to
+// leave the launch), so no block waits to re-arm one.
+//
 // Ticket of a split tile / split attention head: every wave drains its stores,
-// thread 0 takes the ticket; the last arrival re-arms it.
+// thread 0 takes the ticket.
 RAVEL_DEV bool last_arrival(unsigned* counter, unsigned arrivals, int* s_flag) {
   wait_memory();
   __syncthreads();
   if (threadIdx.x == 0) {
     const unsigned prev = __hip_atomic_fetch_add(gptr(counter), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const int last = prev == arrivals - 1;
-    if (last) __hip_atomic_store(gptr(counter), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    *s_flag = last;
+    *s_flag = prev == arrivals - 1;
   }
   __syncthreads();
   return *s_flag != 0;
@@ -188,18 +190,6 @@ RAVEL_DEV bool group_meet(unsigned* counter, unsigned arrivals, int* err, int* s
   }
   __syncthreads();
   return *s_flag != 0;
-}
-
-// After the group's work: the last block to leave re-arms the meeting word (every
-// block has passed its poll by then) and the leaving word, at counter + 32.
-RAVEL_DEV void group_leave(unsigned* counter, unsigned arrivals) {
-  if (threadIdx.x == 0) {
-    const unsigned prev = __hip_atomic_fetch_add(gptr(counter + 32), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (prev == arrivals - 1) {
-      __hip_atomic_store(gptr(counter), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(gptr(counter + 32), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-  }
 }
 
 // Hierarchical grid barrier, split in two so that loads can be issued between
@@ -609,7 +599,6 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int
     if (g.coop) {
       unsigned* ctr = &g.counters[tile * kCounterStride];
       if (group_meet(ctr, (unsigned)g.ksplit, err, &sm.flag)) coop_epilogue<MT>(g, tile, z, tiles, sm, ops);
-      group_leave(ctr, (unsigned)g.ksplit);
       __syncthreads();
       return;
     }
@@ -1340,7 +1329,6 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
       else
         attn_merge<HD>(a, e, j, el0, el1, sm);
     }
-    group_leave(ctr, (unsigned)a.nsplit);
     __syncthreads();
     return;
   }
@@ -1457,7 +1445,8 @@ RAVEL_DEV void idle_warm(const Phase& nx, int items_now, const int* slots) {
 template <int MT, int HD>
 __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __restrict__ phases, int nphase,
                                                               const int* __restrict__ env_slot, int nenv,
-                                                              unsigned* bar, int* err, unsigned long long* times) {
+                                                              unsigned* bar, int* err, unsigned long long* times,
+                                                              unsigned* counters, int ncounters) {
   __shared__ PSmem sm;
   __shared__ Phase desc[3];
   __shared__ int slots[64];
@@ -1558,12 +1547,18 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
   if (tid == 0) {
     unsigned* ex = bar + 64 * (2 + kBarrierGroups);
     const unsigned prev = __hip_atomic_fetch_add(gptr(ex), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (prev == gridDim.x - 1) {
+    ok = prev == gridDim.x - 1;
+    if (ok) {
       for (int i = 0; i < 2 + kBarrierGroups; ++i)
         __hip_atomic_store(gptr(bar + 64 * i), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(gptr(ex), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
+  __syncthreads();
+  // ... and the split counters of every phase
+  if (ok)
+    for (int i = tid; i < ncounters; i += 256)
+      __hip_atomic_store(gptr(counters + (size_t)i * kCounterStride), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <int MT>
@@ -1589,11 +1584,12 @@ const void* kernel_for(int mt, int hd) {
 }  // namespace
 
 hipError_t launch_persistent(const Phase* phases, int nphase, const int* env_slot, int nenv, int mt, int hd, int blocks,
-                             unsigned* bar, int* err, unsigned long long* times, hipStream_t s) {
+                             unsigned* bar, int* err, unsigned long long* times, unsigned* counters, int ncounters,
+                             hipStream_t s) {
   const void* fn = kernel_for(mt, hd);
-  if (!fn || nenv > 64 || nphase < 1) return hipErrorInvalidValue;
-  void* args[] = {(void*)&phases, (void*)&nphase, (void*)&env_slot, (void*)&nenv,
-                  (void*)&bar,    (void*)&err,    (void*)&times};
+  if (!fn || nenv > 64 || nphase < 1 || ncounters < 0) return hipErrorInvalidValue;
+  void* args[] = {(void*)&phases, (void*)&nphase, (void*)&env_slot, (void*)&nenv,     (void*)&bar,
+                  (void*)&err,    (void*)&times,  (void*)&counters, (void*)&ncounters};
   // An ordinary launch: the grid (one block per CU, at most the occupancy limit)
   // is co-resident as soon as the CUs are free, and every wait in the kernel is
   // bounded, so a block held back by other work only delays the first barrier; a

@@ -365,9 +365,9 @@ struct ravel_buffer {
   bf16_t* pnorm = nullptr;             // p = bf16((1 + scale) * x) of the first norm, [w/32][64][32]
   std::vector<void*> pallocs;          // device memory of the persistent path
   // split tickets of the persistent kernel (re-armed with the barrier after a failure)
-  unsigned* pgcnt = nullptr;
-  unsigned* pacnt = nullptr;
-  size_t pgcnt_bytes = 0, pacnt_bytes = 0;
+  unsigned* pgcnt = nullptr;  // split counters of the persistent step's phases (pcnt_n of them)
+  size_t pgcnt_bytes = 0;
+  int pcnt_n = 0;
   // pinned host word raised by the release kernel when the layers' kernel failed
   // (read by the next step call without synchronising), and its device address
   int* hflag = nullptr;
@@ -936,7 +936,6 @@ ravel_status build_persistent(ravel_buffer* b) {
   const bf16_t* pshift = b->pshift;
   auto shift_of = [&](int chunk) -> const bf16_t* { return pshift + (size_t)chunk * 64 * w; };
   size_t part = 0;
-  int max_tiles = 1;
   std::vector<Phase>& P = b->phases;
   P.clear();
   b->pnames.clear();
@@ -987,7 +986,6 @@ ravel_status build_persistent(ravel_buffer* b) {
     ph.items = tiles(N) * g.ksplit;
     g.coop = g.ksplit > 1 && ph.items <= b->pblocks;
     part = std::max(part, (size_t)g.ksplit * tiles(N) * mt * 4 * 64 * 4);
-    max_tiles = std::max(max_tiles, tiles(N));
     return ph;
   };
   auto resid = [&](Phase& ph, const float* gate, const float* gate_scalar, int ns_mode, const float* ns) {
@@ -1013,7 +1011,7 @@ ravel_status build_persistent(ravel_buffer* b) {
   };
   // the input projection writes the first norm's p and row sums of squares
   // (b->sumsq[0]) and the bf16 shifts before the launch
-  int max_attn_parts = 1, max_attn_heads = 1;
+  int max_attn_parts = 1;
   auto attn_phase = [&](AttnArgs a) {
     Phase ph;
     memset(&ph, 0, sizeof ph);
@@ -1034,7 +1032,6 @@ ravel_status build_persistent(ravel_buffer* b) {
     a.coop = a.nsplit > 1 && ph.items <= b->pblocks;
     ph.at = a;
     max_attn_parts = std::max(max_attn_parts, B * c.n_q_heads * a.nsplit);
-    max_attn_heads = std::max(max_attn_heads, B * c.n_q_heads);
     return ph;
   };
   const size_t ctx_layer = (size_t)c.prefix_len * kvd;
@@ -1187,17 +1184,23 @@ ravel_status build_persistent(ravel_buffer* b) {
     if (ph.type == PH_GEMM && ph.g.kw == 0) return fail(RAVEL_E_STATE, "persistent: K range too long");
   // workspaces, patched into the list
   float *gpart, *ao, *aml;
-  unsigned *gcnt, *acnt;
+  unsigned* cnt;
   const int Hp = ((H + 15) / 16) * 16;
   RV_TRY(palloc(b, &gpart, part * 4, false));
-  b->pgcnt_bytes = (size_t)max_tiles * 4 * kCounterStride;
-  RV_TRY(palloc(b, &gcnt, b->pgcnt_bytes, true));
   RV_TRY(palloc(b, &ao, (size_t)max_attn_parts * Hp * hd * 4, false));
   RV_TRY(palloc(b, &aml, (size_t)max_attn_parts * Hp * 2 * 4, false));
-  b->pacnt_bytes = (size_t)max_attn_heads * 4 * kCounterStride;
-  RV_TRY(palloc(b, &acnt, b->pacnt_bytes, true));
-  b->pgcnt = gcnt;
-  b->pacnt = acnt;
+  // split counters: a range per phase (its tiles, or its (env, head) pairs), each
+  // counter used once per launch
+  size_t ncnt = 0;
+  for (const auto& ph : P) {
+    if (ph.type == PH_GEMM && ph.g.ksplit > 1) ncnt += (size_t)tiles(ph.g.N);
+    if (ph.type == PH_ATTN && ph.at.nsplit > 1) ncnt += (size_t)B * c.n_q_heads;
+  }
+  ncnt = std::max(ncnt, (size_t)1);
+  b->pgcnt_bytes = ncnt * 4 * kCounterStride;
+  b->pcnt_n = (int)ncnt;
+  RV_TRY(palloc(b, &cnt, b->pgcnt_bytes, true));
+  b->pgcnt = cnt;
   if (!b->hflag) {
     void* h = nullptr;
     HIP_TRY(hipHostMalloc(&h, 64, hipHostMallocMapped));
@@ -1207,14 +1210,17 @@ ravel_status build_persistent(ravel_buffer* b) {
     HIP_TRY(hipHostGetDevicePointer(&d, h, 0));
     b->hflag_dev = (int*)d;
   }
+  size_t cbase = 0;
   for (auto& ph : P) {
     if (ph.type == PH_GEMM) {
       ph.g.partial = gpart;
-      ph.g.counters = gcnt;
+      ph.g.counters = cnt + cbase * kCounterStride;
+      if (ph.g.ksplit > 1) cbase += (size_t)tiles(ph.g.N);
     } else if (ph.type == PH_ATTN) {
       ph.at.part_o = ao;
       ph.at.part_ml = aml;
-      ph.at.counters = acnt;
+      ph.at.counters = cnt + cbase * kCounterStride;
+      if (ph.at.nsplit > 1) cbase += (size_t)B * c.n_q_heads;
     }
   }
   RV_TRY(palloc(b, &b->d_phases, P.size() * sizeof(Phase), false));
@@ -1324,7 +1330,7 @@ ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream
   }
   REC_BEGIN("persistent_layers", b->p_bytes, b->p_flops);
   HIP_TRY(launch_persistent(b->d_phases, (int)b->phases.size(), b->slot, B, b->pmt, c.head_dim, b->pblocks, b->pbar, b->perr,
-                            rec ? b->ptimes : nullptr, s));
+                            rec ? b->ptimes : nullptr, b->pgcnt, b->pcnt_n, s));
   REC_END();
   return RAVEL_OK;
 }
@@ -2043,7 +2049,6 @@ namespace {
 ravel_status persistent_rearm(ravel_buffer* b) {
   HIP_TRY(hipMemset(b->pbar, 0, kBarrierWords * 4));
   if (b->pgcnt) HIP_TRY(hipMemset(b->pgcnt, 0, b->pgcnt_bytes));
-  if (b->pacnt) HIP_TRY(hipMemset(b->pacnt, 0, b->pacnt_bytes));
   HIP_TRY(hipMemset(b->perr, 0, 64));
   HIP_TRY(hipDeviceSynchronize());
   if (b->hflag) __atomic_store_n(b->hflag, 0, __ATOMIC_RELEASE);
