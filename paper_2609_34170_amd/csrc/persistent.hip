@@ -590,12 +590,13 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int
     }
   };
   if (g.ksplit > 1) {
+    // split partial tiles [z][tile] are row-major [MT * 16 rows][64 columns] fp32
     const size_t tile_elems = (size_t)MT * 4 * 64 * 4;
     const rsrc_t rPw = rsrc(g.partial);
 #pragma unroll
     for (int q = 0; q < MT; ++q)
       if (row_of(q) < g.M)
-        st_f4(rPw, (((size_t)z * tiles + tile) * tile_elems + (size_t)(tid + q * 256) * 4) * 4, sum[q]);
+        st_f4(rPw, (((size_t)z * tiles + tile) * tile_elems + (size_t)row_of(q) * 64 + (col_of(q) - n0)) * 4, sum[q]);
     if (g.coop) {
       unsigned* ctr = &g.counters[tile * kCounterStride];
       if (group_meet(ctr, (unsigned)g.ksplit, err, &sm.flag)) coop_epilogue<MT>(g, tile, z, tiles, sm, ops);
@@ -616,7 +617,8 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int
 #pragma unroll
       for (int zz = 0; zz < kMaxKSplit; ++zz)
         pv[q][zz] = ld_f4<COH>(rP, boff(zz < g.ksplit && zz != z && row_of(q) < g.M,
-                                        (((size_t)zz * tiles + tile) * tile_elems + (size_t)(tid + q * 256) * 4) * 4));
+                                        (((size_t)zz * tiles + tile) * tile_elems + (size_t)row_of(q) * 64 +
+                                         (col_of(q) - n0)) * 4));
 #pragma unroll
     for (int q = 0; q < MT; ++q) {
       f32x4_t t = {0.f, 0.f, 0.f, 0.f};
@@ -870,7 +872,7 @@ RAVEL_DEV void gemm_item_wk(const PGemm& g, int item, const u32x4_t (&w16)[16], 
 // Slot s of the block's share: row r0 + s / per_row, 4-column group and 16-column
 // block (GEGLU: block pair) from s % per_row.
 struct CoopSlot {
-  int row, grp, cb, c, n, it, it_up;
+  int row, grp, cb, c, n;
   bool valid, ok;
 };
 template <int MT>
@@ -888,8 +890,6 @@ RAVEL_DEV CoopSlot coop_slot(const PGemm& g, int tile, int z, int slot) {
   q.cb = rem >> 2;
   q.c = geglu ? 2 * q.cb : q.cb;
   q.n = tile * 64 + q.c * 16 + q.grp * 4;
-  q.it = (q.c * MT + (q.row >> 4)) * 64 + q.grp * 16 + (q.row & 15);
-  q.it_up = ((q.c + 1) * MT + (q.row >> 4)) * 64 + q.grp * 16 + (q.row & 15);
   q.ok = q.valid && q.n + 4 <= g.N;
   return q;
 }
@@ -928,15 +928,22 @@ RAVEL_DEV void coop_epilogue(const PGemm& g, int tile, int z, int tiles, PSmem& 
   for (int s0 = 0; s0 < nslots; s0 += 256) {
     const CoopSlot q = coop_slot<MT>(g, tile, z, s0 + tid);
     const bool valid = q.valid;
-    const int row = q.row, grp = q.grp, cb = q.cb, c = q.c, n = q.n, it = q.it, it_up = q.it_up;
+    const int row = q.row, grp = q.grp, cb = q.cb, c = q.c, n = q.n;
     const CoopOps o = s0 == 0 ? first : coop_operands<MT>(g, tile, z, s0, true);
     const f32x4_t ex = o.ex, eg = o.eg, es = o.es, eb = o.eb;
+    // the slot's 4 columns in the row-major partial tiles (16 consecutive slots read
+    // one row), and for GeGLU those of the up block 16 columns on
+    const size_t el = (size_t)row * 64 + (n - n0);
     f32x4_t pv[kMaxKSplit], pu[kMaxKSplit];
 #pragma unroll
-    for (int zz = 0; zz < kMaxKSplit; ++zz) {
-      const size_t base = ((size_t)zz * tiles + tile) * tile_elems;
-      pv[zz] = ld_f4<COH>(rP, boff(valid && zz < g.ksplit, (base + (size_t)it * 4) * 4));
-      pu[zz] = ld_f4<COH>(rP, boff(geglu && valid && zz < g.ksplit, (base + (size_t)it_up * 4) * 4));
+    for (int zz = 0; zz < kMaxKSplit; ++zz)
+      pv[zz] = ld_f4<COH>(rP, boff(valid && zz < g.ksplit, (((size_t)zz * tiles + tile) * tile_elems + el) * 4));
+#pragma unroll
+    for (int zz = 0; zz < kMaxKSplit; ++zz) pu[zz] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    if (geglu) {
+#pragma unroll
+      for (int zz = 0; zz < kMaxKSplit; ++zz)
+        pu[zz] = ld_f4<COH>(rP, boff(valid && zz < g.ksplit, (((size_t)zz * tiles + tile) * tile_elems + el + 16) * 4));
     }
     f32x4_t v = {0.f, 0.f, 0.f, 0.f}, u = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
