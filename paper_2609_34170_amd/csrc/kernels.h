@@ -85,7 +85,7 @@ struct AttnArgs {
   float scale;
   void* out; int ldo;              // out[(e*Hq + i)*ldo + j*hd + d]
   int nsplit, keys_per_split;      // split of the key range (multiple of 32)
-  float* part_o;                   // [B*nq*nsplit][Hq_pad][hd]
+  float* part_o;                   // [B*nq*nsplit][Hq_pad][hd] (persistent kernel: fp16, normalised)
   float* part_ml;                  // [B*nq*nsplit][Hq_pad][2]
   unsigned* counters;              // [B*nq]
   int coop;                        // persistent kernel: the splits of a head merge together

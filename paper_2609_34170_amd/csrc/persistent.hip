@@ -122,6 +122,17 @@ RAVEL_DEV void st_bf16x4(rsrc_t r, size_t byte_off, float v0, float v1, float v2
   const u32x2_t w = {pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
   __builtin_amdgcn_raw_buffer_store_b64(w, r, (int)byte_off, 0, COH);
 }
+// four fp16 values (round to nearest even), and their load back to fp32
+typedef __attribute__((__vector_size__(4 * sizeof(_Float16)))) _Float16 f16x4_t;
+RAVEL_DEV void st_f16x4(rsrc_t r, size_t byte_off, f32x4_t v) {
+  const f16x4_t h = __builtin_convertvector(v, f16x4_t);
+  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2_t, h), r, (int)byte_off, 0, COH);
+}
+template <int AUX>
+RAVEL_DEV f32x4_t ld_f16x4(rsrc_t r, int off) {
+  const u32x2_t v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, AUX);
+  return __builtin_convertvector(__builtin_bit_cast(f16x4_t, v), f32x4_t);
+}
 
 // threadIdx.x behind an empty asm: index arithmetic derived from it stays inside
 // the work item that needs it instead of being hoisted out of the phase loop,
@@ -1054,8 +1065,9 @@ RAVEL_DEV void attn_load_kv(const AttnArgs& a, const SplitKeys& k, const int* sl
 }
 
 // Weighted sum of the splits' partial outputs for output elements [el0, el1) of
-// one (env, head) (element = 4 dims of one query), bf16 to a.out.  The weight of
-// split s for query q is exp2(m_s - m) / sum_s' exp2(m_s' - m) l_s' (fixed order).
+// one (env, head) (element = 4 dims of one query), bf16 to a.out.  Split s holds its
+// output normalised by its own sum l_s (fp16) and its maximum m_s; its weight for
+// query q is exp2(m_s - m) l_s / sum_s' exp2(m_s' - m) l_s' (fixed order).
 template <int HD>
 RAVEL_DEV void attn_merge(const AttnArgs& a, int e, int j, int el0, int el1, PSmem& sm) {
   const int tid = local_tid();
@@ -1076,7 +1088,7 @@ RAVEL_DEV void attn_merge(const AttnArgs& a, int e, int j, int el0, int el1, PSm
     const int qq = el / (HD / 4), d = (el % (HD / 4)) * 4;
 #pragma unroll
     for (int i = 0; i < SB; ++i)
-      pvl[i] = ld_f4<COH>(rO, boff(el < el1 && sp0 + i < a.nsplit, (((pbase + sp0 + i) * Hp + qq) * HD + d) * 4));
+      pvl[i] = ld_f16x4<COH>(rO, boff(el < el1 && sp0 + i < a.nsplit, (((pbase + sp0 + i) * Hp + qq) * HD + d) * 2));
   };
   load_parts(el0 + tid, 0);  // in flight with the (max, sum) loads
 #pragma unroll
@@ -1093,7 +1105,7 @@ RAVEL_DEV void attn_merge(const AttnArgs& a, int e, int j, int el0, int el1, PSm
     for (int sp = 0; sp < a.nsplit; ++sp) {
       const float ms = sm.mg.ml[sp][tid][0];
       const float wv = (ms == -INFINITY) ? 0.f : exp2f(ms - mmax);
-      sm.mg.wgt[sp][tid] = wv;
+      sm.mg.wgt[sp][tid] = wv * sm.mg.ml[sp][tid][1];
       den += wv * sm.mg.ml[sp][tid][1];
     }
     const float inv = 1.f / den;
@@ -1143,7 +1155,7 @@ RAVEL_DEV void attn_merge_one_round(const AttnArgs& a, int e, int j, int el0, in
 #pragma unroll
   for (int i = 0; i < kMaxAttnSplit / 2; ++i) {
     const int sp = 2 * i + h;
-    pv[i] = ld_f4<COH>(rO, boff(valid && sp < a.nsplit, (((pbase + sp) * Hp + qq) * HD + d) * 4));
+    pv[i] = ld_f16x4<COH>(rO, boff(valid && sp < a.nsplit, (((pbase + sp) * Hp + qq) * HD + d) * 2));
   }
   // splits past nsplit read (0, 0): they are masked out of the max and get weight 0
   float mmax = -INFINITY;
@@ -1154,8 +1166,8 @@ RAVEL_DEV void attn_merge_one_round(const AttnArgs& a, int e, int j, int el0, in
 #pragma unroll
   for (int sp = 0; sp < kMaxAttnSplit; ++sp) {
     const bool use = sp < a.nsplit && ml[sp].x != -INFINITY;
-    const float wv = use ? exp2f(ml[sp].x - mmax) : 0.f;
-    den += wv * ml[sp].y;
+    const float wv = use ? exp2f(ml[sp].x - mmax) * ml[sp].y : 0.f;
+    den += wv;
     const float wh = (sp & 1) == h ? wv : 0.f;
     const f32x4_t p = pv[sp >> 1];
     num[0] += wh * p[0];
@@ -1316,8 +1328,12 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
   if (active && query < a.Hq) {
     const rsrc_t rPo = rsrc(a.part_o), rPml = rsrc(a.part_ml);
     const size_t po = ((pbase + split) * Hp + query) * HD;
+    // the split's output normalised by its own softmax sum (|values| <= max |v|), fp16
+    const float inv = 1.f / lrow;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) st_f4(rPo, (po + dt * 16 + grp * 4) * 4, o[dt]);
+    for (int dt = 0; dt < DT; ++dt)
+      st_f16x4(rPo, (po + dt * 16 + grp * 4) * 2,
+               f32x4_t{o[dt][0] * inv, o[dt][1] * inv, o[dt][2] * inv, o[dt][3] * inv});
     if (grp == 0) {
       st_f1(rPml, (((pbase + split) * Hp + query) * 2 + 0) * 4, mrow);
       st_f1(rPml, (((pbase + split) * Hp + query) * 2 + 1) * 4, lrow);

@@ -1187,7 +1187,7 @@ ravel_status build_persistent(ravel_buffer* b) {
   unsigned* cnt;
   const int Hp = ((H + 15) / 16) * 16;
   RV_TRY(palloc(b, &gpart, part * 4, false));
-  RV_TRY(palloc(b, &ao, (size_t)max_attn_parts * Hp * hd * 4, false));
+  RV_TRY(palloc(b, &ao, (size_t)max_attn_parts * Hp * hd * 2, false));  // fp16 split outputs
   RV_TRY(palloc(b, &aml, (size_t)max_attn_parts * Hp * 2 * 4, false));
   // split counters: a range per phase (its tiles, or its (env, head) pairs), each
   // counter used once per launch
