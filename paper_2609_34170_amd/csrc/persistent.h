@@ -83,9 +83,9 @@ struct PGemm {
   // whole-K items (wk = column blocks of 16 per item, 1 or 2; 0: K ranges of 256 * kw
   // with split tiles): item t covers columns [16 wk t, 16 wk (t + 1)) over the whole K,
   // wave w its K quarter [w K/4, (w + 1) K/4) (K/4 a multiple of 32, at most 256); the
-  // quarters are added through LDS, so no tile is split across blocks.  PA_BF16 /
-  // PA_NORM operands, PE_BF16 / PE_GEGLU (wk = 2: a 16-column gate block and its up
-  // block) / PE_F32 epilogues.
+  // quarters are added through LDS, so no tile is split across blocks.  PA_NORM
+  // operands with p and shift in 32-column tiles (plain loads), PE_BF16 / PE_GEGLU
+  // (wk = 2: a 16-column gate block and its up block) / PE_F32 epilogues.
   int wk;
 };
 

@@ -318,6 +318,8 @@ RAVEL_DEV int coop_rows(const PGemm& g) {
 RAVEL_DEV size_t a_off(const PGemm& g, int m, int k) {
   return g.a_t32 ? ((size_t)(k >> 5) * 2048 + (size_t)m * 32 + (k & 31)) * 2 : ((size_t)m * g.lda + k) * 2;
 }
+// Byte offset of element (m, k) of a bf16 matrix in 32-column tiles [K/32][64 rows][32].
+RAVEL_DEV size_t t32_off(int m, int k) { return ((size_t)(k >> 5) * 2048 + (size_t)m * 32 + (k & 31)) * 2; }
 // Byte offset of shift[m][k] (bf16): row-major with stride ld_shift, or 32-column tiles.
 RAVEL_DEV size_t sh_off(const PGemm& g, int m, int k) {
   return g.sh_t32 ? ((size_t)(k >> 5) * 2048 + (size_t)m * 32 + (k & 31)) * 2 : ((size_t)m * g.ld_shift + k) * 2;
@@ -325,6 +327,19 @@ RAVEL_DEV size_t sh_off(const PGemm& g, int m, int k) {
 // Byte offset of p_out[m][n] (bf16) of a residual update.
 RAVEL_DEV size_t p_off(const PGemm& g, int m, int n) {
   return g.p_t32 ? ((size_t)(n >> 5) * 2048 + (size_t)m * 32 + (n & 31)) * 2 : ((size_t)m * g.ldp + n) * 2;
+}
+// Activation fragments af[i][f] of a split item (rows i*16 + (lane & 15), K range
+// kb + 32f + 8(lane >> 4) .. +7), with cache policy AUX.
+template <int AUX, int MT, int NF>
+RAVEL_DEV void load_a_frags(const PGemm& g, rsrc_t rA, int kb, bf16x8_t (&af)[MT][NF]) {
+  const int lane = local_tid() & 63, l16 = lane & 15, grp = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int f = 0; f < NF; ++f) {
+      const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
+      af[i][f] = ld_b8<AUX>(rA, boff(m < g.M && k < g.K, a_off(g, m, k)));
+    }
 }
 // Byte offset of output column c (of N / 2) of row m of a gated-GeLU phase.
 RAVEL_DEV size_t geglu_off(const PGemm& g, int m, int c) {
@@ -459,14 +474,12 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int
       const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
       sh[i][f] = ld_b8<PLAIN>(rS, boff(has_shift && m < g.M && k < g.K, sh_off(g, m, k)));
     }
-#pragma unroll
-  for (int i = 0; i < MT; ++i)
-#pragma unroll
-    for (int f = 0; f < NF; ++f) {
-      const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
-      const int o = boff(m < g.M && k < g.K, a_off(g, m, k));
-      af[i][f] = g.a_coh ? ld_b8<COH>(rA, o) : ld_b8<PLAIN>(rA, o);
-    }
+  // (the cache policy is part of the instruction: one batch per policy, chosen by a
+  // wave-uniform branch, rather than both loads and a select)
+  if (g.a_coh)
+    load_a_frags<COH, MT, NF>(g, rA, kb, af);
+  else
+    load_a_frags<PLAIN, MT, NF>(g, rA, kb, af);
   // PA_XATTN: the head's keys (this wave's 64 dims; lane: key l16) and its values
   // (16-byte chunks c = tid, tid + 256: key c / 32, dims (c % 32) * 8), plain loads
   const bool xattn = g.a_mode == PA_XATTN;
@@ -747,15 +760,14 @@ RAVEL_DEV void gemm_item_wk(const PGemm& g, int item, const u32x4_t (&w16)[16], 
 #pragma unroll
     for (int f = 0; f < 8; ++f) {
       const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
-      sh[i][f] = ld_b8<PLAIN>(rS, boff(has_shift && m < g.M && f * 32 < kq, sh_off(g, m, k)));
+      sh[i][f] = ld_b8<PLAIN>(rS, boff(has_shift && m < g.M && f * 32 < kq, t32_off(m, k)));
     }
 #pragma unroll
   for (int i = 0; i < MT; ++i)
 #pragma unroll
     for (int f = 0; f < 8; ++f) {
       const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
-      const int o = boff(m < g.M && f * 32 < kq, a_off(g, m, k));
-      af[i][f] = g.a_coh ? ld_b8<COH>(rA, o) : ld_b8<PLAIN>(rA, o);
+      af[i][f] = ld_b8<PLAIN>(rA, boff(m < g.M && f * 32 < kq, t32_off(m, k)));
     }
   float sq[16];
   const int row = tid & 63, part = tid >> 6, nt = g.K >> 6;
@@ -1036,8 +1048,8 @@ RAVEL_DEV SplitKeys split_keys(const AttnArgs& a, int item) {
 // chunks of keys 4 (tid / (HD/8)) + i, i < 4, at dims (tid % (HD/8)) * 8.  Prefix
 // rows were written before the launch (plain loads, and may be fetched before the
 // barrier that opens the phase); self rows by this launch (coherent loads).
-template <int HD>
-RAVEL_DEV void attn_load_kv(const AttnArgs& a, const SplitKeys& k, const int* slots, u32x4_t (&kv)[8]) {
+template <int HD, int AUX>
+RAVEL_DEV void attn_load_kv_aux(const AttnArgs& a, const SplitKeys& k, const int* slots, u32x4_t (&kv)[8]) {
   constexpr int CPR = HD / 8;
   const int tid = local_tid();
   const int slot = a.slot ? slots[k.e] : 0;
@@ -1047,7 +1059,6 @@ RAVEL_DEV void attn_load_kv(const AttnArgs& a, const SplitKeys& k, const int* sl
   const rsrc_t rV = k.self ? rsrc((const bf16_t*)a.sv + (size_t)k.e * a.S * a.s_ld) : rsrc(pv);
   const int ld_row = k.self ? a.s_ld : a.p_ld;
   const int k_row0 = k.self ? a.P : 0;
-  const bool coh = k.self && a.coh;
   auto off = [&](int kidx, int dc) {
     return boff(kidx < k.kend, ((size_t)(kidx - k_row0) * ld_row + k.g * HD + dc) * 2);
   };
@@ -1055,13 +1066,21 @@ RAVEL_DEV void attn_load_kv(const AttnArgs& a, const SplitKeys& k, const int* sl
   for (int r = 0; r < 4; ++r) {
     const int c = tid + r * 256;
     const int o = off(k.kbeg + c / CPR, (c % CPR) * 8);
-    kv[r] = coh ? ld16<COH>(rK, o) : ld16<PLAIN>(rK, o);
+    kv[r] = ld16<AUX>(rK, o);
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int o = off(k.kbeg + (tid / CPR) * 4 + i, (tid % CPR) * 8);
-    kv[4 + i] = coh ? ld16<COH>(rV, o) : ld16<PLAIN>(rV, o);
+    kv[4 + i] = ld16<AUX>(rV, o);
   }
+}
+// Self rows written in 16-column pieces (a.coh) are read device-coherent.
+template <int HD>
+RAVEL_DEV void attn_load_kv(const AttnArgs& a, const SplitKeys& k, const int* slots, u32x4_t (&kv)[8]) {
+  if (k.self && a.coh)
+    attn_load_kv_aux<HD, COH>(a, k, slots, kv);
+  else
+    attn_load_kv_aux<HD, PLAIN>(a, k, slots, kv);
 }
 
 // Weighted sum of the splits' partial outputs for output elements [el0, el1) of
@@ -1209,10 +1228,15 @@ RAVEL_DEV void attn_item(const AttnArgs& a, int item, const int* slots, int* err
   const int query = wave * 16 + l16;
   const bool active = wave < QB;
   bf16x8_t qf[KS];
+  auto q_off = [&](int ks) {
+    return boff(query < a.Hq, ((size_t)(e * a.Hq + query) * a.ldq + j * HD + ks * 32 + grp * 8) * 2);
+  };
+  if (a.coh) {
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    const int o = boff(query < a.Hq, ((size_t)(e * a.Hq + query) * a.ldq + j * HD + ks * 32 + grp * 8) * 2);
-    qf[ks] = a.coh ? ld_b8<COH>(rq, o) : ld_b8<PLAIN>(rq, o);
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = ld_b8<COH>(rq, q_off(ks));
+  } else {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = ld_b8<PLAIN>(rq, q_off(ks));
   }
   after_loads();
   __syncthreads();  // LDS may still be read by this block's previous item
@@ -1376,10 +1400,14 @@ RAVEL_DEV void rope_item(const PRope& r, int row) {
   for (int idx = local_tid(); idx < quads; idx += 256) {
     const int h = idx / (half >> 2), d = (idx - h * (half >> 2)) * 4;
     const int o0 = (h * r.hd + d) * 2, o1 = o0 + half * 2;
-    const auto a = r.coh ? __builtin_amdgcn_raw_buffer_load_b64(q, o0, 0, COH)
-                         : __builtin_amdgcn_raw_buffer_load_b64(q, o0, 0, PLAIN);
-    const auto b = r.coh ? __builtin_amdgcn_raw_buffer_load_b64(q, o1, 0, COH)
-                         : __builtin_amdgcn_raw_buffer_load_b64(q, o1, 0, PLAIN);
+    u32x2_t a, b;
+    if (r.coh) {
+      a = __builtin_amdgcn_raw_buffer_load_b64(q, o0, 0, COH);
+      b = __builtin_amdgcn_raw_buffer_load_b64(q, o1, 0, COH);
+    } else {
+      a = __builtin_amdgcn_raw_buffer_load_b64(q, o0, 0, PLAIN);
+      b = __builtin_amdgcn_raw_buffer_load_b64(q, o1, 0, PLAIN);
+    }
     const f32x4_t c01 = ld_f4<PLAIN>(t, d * 8), c23 = ld_f4<PLAIN>(t, d * 8 + 16);
     const float cs[8] = {c01[0], c01[1], c01[2], c01[3], c23[0], c23[1], c23[2], c23[3]};
     float x[4], y[4];
@@ -1488,32 +1516,24 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
   if (env_slot && tid < nenv && tid < 64) slots[tid] = *gptr(env_slot + tid);
   __syncthreads();
 
-  // What this block's first item of the coming phase reads from memory written
-  // before the launch -- GEMM weight fragments (16), or the keys and values (8) of
-  // a prefix attention split (kv_ready) -- is fetched while the block waits at the
-  // barrier that opens the phase.  (Issued any earlier, these loads would sit in
-  // front of the current phase's own loads and stores in the wave's in-order
-  // memory counter, and every wait of the phase would wait for them too.)
-  u32x4_t pre[16];
-  bool kv_ready = false;
-  auto prefetch = [&](const Phase& nx) {
-    kv_ready = false;
-    const int type = uni(nx.type);
-    if (type == PH_GEMM && (int)blockIdx.x < uni(nx.items)) {
-      load_weights(make_uniform(nx.g), blockIdx.x, pre);
-    } else if (type == PH_ATTN && (int)blockIdx.x < uni(nx.items)) {
-      const AttnArgs a = make_uniform(nx.at);
-      const SplitKeys k = split_keys(a, blockIdx.x);
-      if (!k.self) {
-        u32x4_t kv[8];
-        attn_load_kv<HD>(a, k, slots, kv);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) pre[i] = kv[i];
-        kv_ready = true;
-      }
-    }
+  // Phase p: this block's first item's reads of memory written before the launch --
+  // GEMM weight fragments (16), or the keys and values (8) of a prefix attention
+  // split -- are issued first, then the block waits at barrier p (between phases
+  // p - 1 and p), so the fetch overlaps the wait.  (Issued any earlier, these loads
+  // would sit in front of the previous phase's own loads and stores in the wave's
+  // in-order memory counter, and every wait of that phase would wait for them too.)
+  // The registers they land in belong to the phase's own branch of the loop.
+  u32x4_t dreg = {0, 0, 0, 0};  // descriptor p + 1, loaded after arriving at barrier p
+  auto wait_in = [&](int p) -> bool {
+    if (p == 0) return true;
+    if (tid == 0) ok = barrier_wait(bar, (unsigned)p, err);
+    __syncthreads();
+    if (!ok) return false;
+    if (p + 1 < nphase && tid < kDescChunks) reinterpret_cast<u32x4_t*>(&desc[(p + 1) % 3])[tid] = dreg;
+    if (stamp) *gptr(times + p) = wall_clock64();
+    __syncthreads();
+    return true;
   };
-  prefetch(desc[0]);
 
   auto none = [] {};
 
@@ -1522,6 +1542,9 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
     const int type = uni(ph.type), items = uni(ph.items);
     if (type == PH_GEMM) {
       const PGemm g = make_uniform(ph.g);
+      u32x4_t pre[16];
+      if ((int)blockIdx.x < items) load_weights(g, blockIdx.x, pre);
+      if (!wait_in(p)) return;
       for (int item = blockIdx.x; item < items; item += gridDim.x) {
         if (item != (int)blockIdx.x) load_weights(g, item, pre);
         if (g.wk == 2)
@@ -1535,32 +1558,33 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
       }
     } else if (type == PH_ATTN) {
       const AttnArgs a = make_uniform(ph.at);
-      for (int item = blockIdx.x; item < items; item += gridDim.x) {
-        u32x4_t kv[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) kv[i] = pre[i];
-        attn_item<HD>(a, item, slots, err, sm, kv, item == (int)blockIdx.x && kv_ready, none);
+      u32x4_t kv[8];
+      bool kv_ready = false;
+      if ((int)blockIdx.x < items) {
+        const SplitKeys k = split_keys(a, blockIdx.x);
+        if (!k.self) {
+          attn_load_kv_aux<HD, PLAIN>(a, k, slots, kv);
+          kv_ready = true;
+        }
       }
-    } else if (type == PH_ROPE) {
-      const PRope r = make_uniform(ph.r);
-      for (int item = blockIdx.x; item < items; item += gridDim.x) rope_item(r, item);
+      if (!wait_in(p)) return;
+      for (int item = blockIdx.x; item < items; item += gridDim.x)
+        attn_item<HD>(a, item, slots, err, sm, kv, item == (int)blockIdx.x && kv_ready, none);
+    } else {
+      if (!wait_in(p)) return;
+      if (type == PH_ROPE) {
+        const PRope r = make_uniform(ph.r);
+        for (int item = blockIdx.x; item < items; item += gridDim.x) rope_item(r, item);
+      }
     }
     if (p + 1 == nphase) break;
     idle_warm<HD>(desc[(p + 1) % 3], items, slots);
-    // barrier between phases p and p + 1; while waiting, fetch descriptor p + 2
-    // and what this block's item of phase p + 1 reads from before the launch
+    // arrive at barrier p + 1 once every wave's stores are done; fetch descriptor
+    // p + 2 (written to LDS after that barrier)
     wait_memory();
     __syncthreads();
-    const unsigned gen = (unsigned)(p + 1);
-    if (tid == 0) barrier_arrive(bar, gen);
-    u32x4_t dreg = {0, 0, 0, 0};
+    if (tid == 0) barrier_arrive(bar, (unsigned)(p + 1));
     if (p + 2 < nphase && tid < kDescChunks) dreg = *gptr(reinterpret_cast<const u32x4_t*>(&phases[p + 2]) + tid);
-    prefetch(desc[(p + 1) % 3]);
-    if (tid == 0) ok = barrier_wait(bar, gen, err);
-    __syncthreads();
-    if (!ok) return;
-    if (p + 2 < nphase && tid < kDescChunks) reinterpret_cast<u32x4_t*>(&desc[(p + 2) % 3])[tid] = dreg;
-    if (stamp) *gptr(times + p + 1) = wall_clock64();
   }
   if (stamp) *gptr(times + nphase) = wall_clock64();
   // re-arm the barrier: the last block to get here has seen every block pass

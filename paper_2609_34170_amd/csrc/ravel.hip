@@ -975,7 +975,7 @@ ravel_status build_persistent(ravel_buffer* b) {
     // a K that would be split over blocks and fits four waves' quarters of at most
     // 256: whole-K items of 16 columns (a gate block and its up block for GeGLU)
     const int wk = e_mode == PE_GEGLU ? 2 : 1;
-    if (whole_k && g.ksplit > 1 && K % 128 == 0 && K <= 1024 && N % (16 * wk) == 0 &&
+    if (whole_k && norm && g.ksplit > 1 && K % 128 == 0 && K <= 1024 && N % (16 * wk) == 0 &&
         (e_mode == PE_BF16 || e_mode == PE_F32 || e_mode == PE_GEGLU)) {
       g.wk = wk;
       g.kw = 1;
