@@ -754,29 +754,30 @@ RAVEL_DEV void gemm_item_wk(const PGemm& g, int item, const u32x4_t (&w16)[16], 
   const bool norm = g.a_mode == PA_NORM;
   const bool has_shift = norm && g.shift != nullptr;
   const rsrc_t rA = rsrc(g.A), rS = rsrc(g.shift);
-  bf16x8_t sh[MT][8], af[MT][8];
+  auto frag_off = [&](int i, int f, bool use) {
+    const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
+    return boff(use && m < g.M && f * 32 < kq, t32_off(m, k));
+  };
+  // The shift fragments are loaded first (written before the launch, and touched
+  // into the XCD's L2 by idle blocks); as the W shift MFMAs consume each one, the
+  // activation fragment of the same slot is loaded into its registers.  Holding
+  // both sets at once would exceed the wave's VGPRs, and the compiler's copies to
+  // accumulation registers would wait for loads still in flight.  No branches around
+  // loads (a phase without shift reads zeros: its W shift product is exactly 0), as a
+  // join after a branch that loads makes the compiler wait for every load in flight.
+  bf16x8_t x[MT][8];
 #pragma unroll
   for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int f = 0; f < 8; ++f) {
-      const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
-      sh[i][f] = ld_b8<PLAIN>(rS, boff(has_shift && m < g.M && f * 32 < kq, t32_off(m, k)));
-    }
-#pragma unroll
-  for (int i = 0; i < MT; ++i)
-#pragma unroll
-    for (int f = 0; f < 8; ++f) {
-      const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
-      af[i][f] = ld_b8<PLAIN>(rA, boff(m < g.M && f * 32 < kq, t32_off(m, k)));
-    }
+    for (int f = 0; f < 8; ++f) x[i][f] = ld_b8<PLAIN>(rS, frag_off(i, f, has_shift));
   float sq[16];
   const int row = tid & 63, part = tid >> 6, nt = g.K >> 6;
-  if (norm) {
+  {
     const rsrc_t rQ = rsrc(g.sumsq_in);
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const int t = part + 4 * j;
-      sq[j] = ld_f1<PLAIN>(rQ, boff(t < nt && row < g.M, (size_t)(t * 64 + row) * g.sq_in_ld * 4));
+      sq[j] = ld_f1<PLAIN>(rQ, boff(norm && t < nt && row < g.M, (size_t)(t * 64 + row) * g.sq_in_ld * 4));
     }
   }
   f32x4_t bias4 = {0.f, 0.f, 0.f, 0.f};
@@ -789,13 +790,15 @@ RAVEL_DEV void gemm_item_wk(const PGemm& g, int item, const u32x4_t (&w16)[16], 
 #pragma unroll
   for (int c = 0; c < WK; ++c)
 #pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      acc[c][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      if (has_shift) {
+    for (int i = 0; i < MT; ++i) acc[c][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int f = 0; f < 8; ++f)
-          acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[c][f], sh[i][f], acc[c][i], 0, 0, 0);
-      }
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+#pragma unroll
+      for (int c = 0; c < WK; ++c)
+        acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[c][f], x[i][f], acc[c][i], 0, 0, 0);
+      x[i][f] = ld_b8<PLAIN>(rA, frag_off(i, f, true));
     }
   if (norm) {
     float ssum = 0.f;
@@ -827,7 +830,7 @@ RAVEL_DEV void gemm_item_wk(const PGemm& g, int item, const u32x4_t (&w16)[16], 
     for (int i = 0; i < MT; ++i)
 #pragma unroll
       for (int f = 0; f < 8; ++f)
-        acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[c][f], af[i][f], acc[c][i], 0, 0, 0);
+        acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[c][f], x[i][f], acc[c][i], 0, 0, 0);
   if (norm) {
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
