@@ -1169,11 +1169,51 @@ RAVEL_DEV void attn_merge_one_round(const AttnArgs& a, int e, int j, int el0, in
   const rsrc_t rML = rsrc(a.part_ml), rO = rsrc(a.part_o);
   const bool valid = el < el1;
   const int qq = valid ? el / (HD / 4) : 0, d = (el % (HD / 4)) * 4;
+  f32x4_t pv[kMaxAttnSplit / 2];
+  if constexpr (HD == 256) {
+    // a wave's 64 elements are one query (shares start at multiples of 64 elements):
+    // lane s loads split s's (max, sum), the weights are reduced across the wave, and
+    // each thread takes the weights of its splits from their lanes
+    const int lane = tid & 63, e0 = el0 + (tid & 64);
+    const int qw = e0 / 64;
+    const float2 mls = ld_f2<COH>(rML, boff(e0 < el1 && lane < a.nsplit, ((pbase + lane) * Hp + qw) * 2 * 4));
+#pragma unroll
+    for (int i = 0; i < kMaxAttnSplit / 2; ++i) {
+      const int sp = 2 * i + h;
+      pv[i] = ld_f16x4<COH>(rO, boff(valid && sp < a.nsplit, (((pbase + sp) * Hp + qq) * HD + d) * 2));
+    }
+    const bool use = lane < a.nsplit && mls.x != -INFINITY;
+    float mmax = use ? mls.x : -INFINITY;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) mmax = fmaxf(mmax, __shfl_xor(mmax, o, 64));
+    const float ws = use ? exp2f(mls.x - mmax) * mls.y : 0.f;
+    float den = ws;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) den += __shfl_xor(den, o, 64);
+    f32x4_t num = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < kMaxAttnSplit / 2; ++i) {
+      const float w = __shfl(ws, 2 * i + h, 64);
+      num[0] += w * pv[i][0];
+      num[1] += w * pv[i][1];
+      num[2] += w * pv[i][2];
+      num[3] += w * pv[i][3];
+    }
+    f32x4_t* x = reinterpret_cast<f32x4_t*>(&sm.red[0][0][0][0]);
+    if (h == 1) x[tid & 127] = num;
+    __syncthreads();
+    if (h == 0 && valid) {
+      const f32x4_t o = x[tid];
+      const float inv = 1.f / den;
+      st_bf16x4(rsrc(a.out), ((size_t)(e * a.Hq + qq) * a.ldo + j * HD + d) * 2, (num[0] + o[0]) * inv,
+                (num[1] + o[1]) * inv, (num[2] + o[2]) * inv, (num[3] + o[3]) * inv);
+    }
+    return;
+  }
   float2 ml[kMaxAttnSplit];
 #pragma unroll
   for (int sp = 0; sp < kMaxAttnSplit; ++sp)
     ml[sp] = ld_f2<COH>(rML, boff(valid && sp < a.nsplit, ((pbase + sp) * Hp + qq) * 2 * 4));
-  f32x4_t pv[kMaxAttnSplit / 2];
 #pragma unroll
   for (int i = 0; i < kMaxAttnSplit / 2; ++i) {
     const int sp = 2 * i + h;
