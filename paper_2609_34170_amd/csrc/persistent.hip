@@ -63,6 +63,9 @@ struct PSmem {
       float ml[kMaxAttnSplit][64][2];  // attention merge: (max, sum) per split and query
       float wgt[kMaxAttnSplit][64];    // merge weights
     } mg;
+    // whole-K GEMM: the norm's shift fragments, staged by direct-to-LDS loads, wave w's
+    // fragment (i, f) at shs[w][i * 8 + f] in lane order
+    u32x4_t shs[4][32][64];
   };
   float rscale[64];
   float rowsq[64][17];
@@ -731,6 +734,29 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int
   __syncthreads();
 }
 
+// Stages a whole-K item's shift fragments (the same for every item of the phase) in
+// LDS with direct-to-LDS buffer loads: fragment (i, f) of wave w -- rows i*16 + (lane
+// & 15), K range w K/4 + 32f + 8(lane >> 4) .. +7, 32-column tiles -- lands at
+// shs[w][i * 8 + f][lane].  The shift rows were written before the launch, so this is
+// issued with the phase's weight prefetch, before the barrier wait.  The compiler
+// does not track these loads' writes to LDS: the reader waits for every load of the
+// wave (wait_memory) before it reads them.
+template <int MT>
+RAVEL_DEV void stage_shift(const PGemm& g, PSmem& sm) {
+  typedef __attribute__((address_space(3))) void lds_void_t;
+  const int tid = local_tid(), lane = tid & 63, wave = tid >> 6, l16 = lane & 15, grp = lane >> 4;
+  const int kq = g.K >> 2, kb = wave * kq;
+  const rsrc_t rS = rsrc(g.shift);
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+      const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rS, (lds_void_t*)&sm.shs[wave][i * 8 + f][0], 16,
+                                               boff(m < g.M && f * 32 < kq, t32_off(m, k)), 0, 0, 0);
+    }
+}
+
 // A whole-K item: 16 * WK output columns of every row over the whole K, so the
 // item owns its outputs and no other block meets it.  The four waves take K
 // quarters of the item (all their loads -- shift rows, activations, row sums --
@@ -742,7 +768,7 @@ RAVEL_DEV void gemm_item(const PGemm& g, int item, const u32x4_t (&w16)[16], int
 // are narrower than a 128-byte line, so the phases that read them use
 // device-coherent loads.
 template <int MT, int WK>
-RAVEL_DEV void gemm_item_wk(const PGemm& g, int item, const u32x4_t (&w16)[16], PSmem& sm) {
+RAVEL_DEV void gemm_item_wk(const PGemm& g, int item, const u32x4_t (&w16)[16], PSmem& sm, bool sh_staged) {
   bf16x8_t wf[WK][8];
 #pragma unroll
   for (int c = 0; c < WK; ++c)
@@ -753,23 +779,19 @@ RAVEL_DEV void gemm_item_wk(const PGemm& g, int item, const u32x4_t (&w16)[16], 
   const int n0 = item * 16 * WK, kq = g.K >> 2, kb = wave * kq;
   const bool norm = g.a_mode == PA_NORM;
   const bool has_shift = norm && g.shift != nullptr;
-  const rsrc_t rA = rsrc(g.A), rS = rsrc(g.shift);
-  auto frag_off = [&](int i, int f, bool use) {
-    const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
-    return boff(use && m < g.M && f * 32 < kq, t32_off(m, k));
-  };
-  // The shift fragments are loaded first (written before the launch, and touched
-  // into the XCD's L2 by idle blocks); as the W shift MFMAs consume each one, the
-  // activation fragment of the same slot is loaded into its registers.  Holding
-  // both sets at once would exceed the wave's VGPRs, and the compiler's copies to
-  // accumulation registers would wait for loads still in flight.  No branches around
-  // loads (a phase without shift reads zeros: its W shift product is exactly 0), as a
-  // join after a branch that loads makes the compiler wait for every load in flight.
+  const rsrc_t rA = rsrc(g.A);
+  // The shift fragments go to LDS (staged with the weight prefetch for the block's
+  // first item), the activation fragments to registers; every load of the item is
+  // in flight at once, and the MFMAs start when all have landed.
+  if (has_shift && !sh_staged) stage_shift<MT>(g, sm);
   bf16x8_t x[MT][8];
 #pragma unroll
   for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int f = 0; f < 8; ++f) x[i][f] = ld_b8<PLAIN>(rS, frag_off(i, f, has_shift));
+    for (int f = 0; f < 8; ++f) {
+      const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
+      x[i][f] = ld_b8<PLAIN>(rA, boff(m < g.M && f * 32 < kq, t32_off(m, k)));
+    }
   float sq[16];
   const int row = tid & 63, part = tid >> 6, nt = g.K >> 6;
   {
@@ -785,21 +807,23 @@ RAVEL_DEV void gemm_item_wk(const PGemm& g, int item, const u32x4_t (&w16)[16], 
     const int n = n0 + 4 * ((tid & 63) >> 4);
     bias4 = ld_f4<PLAIN>(rsrc(g.bias), boff(g.e_mode == PE_F32 && g.bias && n + 4 <= g.N, (size_t)n * 4));
   }
+  wait_memory();  // includes the direct-to-LDS shift loads
 
   f32x4_t acc[WK][MT];
 #pragma unroll
   for (int c = 0; c < WK; ++c)
 #pragma unroll
     for (int i = 0; i < MT; ++i) acc[c][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  if (has_shift) {
 #pragma unroll
-  for (int i = 0; i < MT; ++i)
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int f = 0; f < 8; ++f) {
+      for (int f = 0; f < 8; ++f) {
+        const bf16x8_t s = __builtin_bit_cast(bf16x8_t, sm.shs[wave][i * 8 + f][lane]);
 #pragma unroll
-      for (int c = 0; c < WK; ++c)
-        acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[c][f], x[i][f], acc[c][i], 0, 0, 0);
-      x[i][f] = ld_b8<PLAIN>(rA, frag_off(i, f, true));
-    }
+        for (int c = 0; c < WK; ++c) acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[c][f], s, acc[c][i], 0, 0, 0);
+      }
+  }
   if (norm) {
     float ssum = 0.f;
 #pragma unroll
@@ -1586,14 +1610,20 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
     if (type == PH_GEMM) {
       const PGemm g = make_uniform(ph.g);
       u32x4_t pre[16];
-      if ((int)blockIdx.x < items) load_weights(g, blockIdx.x, pre);
+      // whole-K norm phases: the shift fragments are staged in LDS with the prefetch
+      const bool stage = g.wk > 0 && g.a_mode == PA_NORM && g.shift != nullptr;
+      if ((int)blockIdx.x < items) {
+        load_weights(g, blockIdx.x, pre);
+        if (stage) stage_shift<MT>(g, sm);
+      }
       if (!wait_in(p)) return;
       for (int item = blockIdx.x; item < items; item += gridDim.x) {
         if (item != (int)blockIdx.x) load_weights(g, item, pre);
+        const bool staged = stage && item == (int)blockIdx.x;
         if (g.wk == 2)
-          gemm_item_wk<MT, 2>(g, item, pre, sm);
+          gemm_item_wk<MT, 2>(g, item, pre, sm, staged);
         else if (g.wk == 1)
-          gemm_item_wk<MT, 1>(g, item, pre, sm);
+          gemm_item_wk<MT, 1>(g, item, pre, sm, staged);
         else if (g.kw == 2)
           gemm_item<MT, 2>(g, item, pre, err, sm, none);
         else
