@@ -183,6 +183,18 @@ RAVEL_DEV int xcd_tile(int b, int T) {
   const int start = x * q + (x < r ? x : r);
   return start + local;
 }
+// Row and column of tile t of a tiles_m x tiles_n grid ordered in groups of up to 8
+// column tiles, row-major inside a group: an XCD's contiguous range of t covers a
+// compact rectangle (about 8 x 8 tiles), so its L2 holds the activation row panels and
+// the weight column panels it reads instead of every column panel of a wide output.
+RAVEL_DEV void tile_rc(int t, int tiles_m, int tiles_n, int& r, int& c) {
+  constexpr int GN = 8;
+  const int g = t / (tiles_m * GN);
+  const int gw = min(GN, tiles_n - g * GN);
+  const int ti = t - g * tiles_m * GN;
+  r = ti / gw;
+  c = g * GN + ti % gw;
+}
 
 template <int BM, int BN, int WM, int WN>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs a) {
@@ -206,8 +218,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs a) {
 
   const int tiles_n = (a.N + BN - 1) / BN;
   const int tile = xcd_tile(blockIdx.x, gridDim.x);
-  const int m0 = (tile / tiles_n) * BM;
-  const int n0 = (tile % tiles_n) * BN;
+  int tr, tc;
+  tile_rc(tile, gridDim.x / tiles_n, tiles_n, tr, tc);
+  const int m0 = tr * BM;
+  const int n0 = tc * BN;
   if (a.m_rows) a.M = min(a.M, *a.m_rows);
   if (m0 >= a.M) return;  // whole tile past a device-side row count (every K range alike)
   const int z = blockIdx.z;
@@ -375,8 +389,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_lds_kernel(GemmArgs a) {
     a.M = min(a.M, *a.m_rows);
   } else {
     tile = xcd_tile(blockIdx.x, gridDim.x);
-    m0 = (tile / tiles_n) * BM;
-    n0 = (tile % tiles_n) * BN;
+    int tr, tc;
+    tile_rc(tile, gridDim.x / tiles_n, tiles_n, tr, tc);
+    m0 = tr * BM;
+    n0 = tc * BN;
     if (a.m_rows) a.M = min(a.M, *a.m_rows);
   }
   if (m0 >= a.M) return;  // whole tile past a device-side row count (every K range alike)
