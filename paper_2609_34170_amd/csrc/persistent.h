@@ -101,6 +101,21 @@ struct PRope {
   const float* cs;
 };
 
+// Side work of a phase, run by its blocks that have no item of their own: items
+// item0 .. item0 + nitems - 1 of a modulation GEMM out = A W^T + bias over the whole
+// K (32 output columns per item, M <= 64 rows, A row-major bf16), fp32 out rows, and
+// for the columns of up to two shift ranges [shift_col[s], shift_col[s] + shift_w)
+// also bf16 copies in 32-column tiles [shift_w/32][64 rows][32] at shift_out[s].
+struct PSide {
+  const bf16_t* A; int lda;
+  const bf16_t* W; int ldw;
+  const float* bias;
+  float* out; int ldo;
+  bf16_t* shift_out[2]; int shift_col[2]; int shift_w;
+  int M, N, K;
+  int item0, nitems;
+};
+
 struct alignas(16) Phase {
   int type, items, pad0, pad1;
   union {
@@ -108,6 +123,7 @@ struct alignas(16) Phase {
     AttnArgs at;
     PRope r;
   };
+  PSide side;
 };
 
 // env_slot: [nenv] active context slot per env (read once per launch).

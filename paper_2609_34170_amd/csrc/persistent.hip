@@ -915,6 +915,82 @@ RAVEL_DEV void gemm_item_wk(const PGemm& g, int item, const u32x4_t (&w16)[16], 
   __syncthreads();
 }
 
+// One item of a phase's side work (PSide): 32 output columns n0 .. n0 + 31 of every
+// row over the whole K, the four waves taking K quarters (K/4 a multiple of 32, at
+// most 256) added in LDS; run by a block with no item of its own in the phase, off
+// the phase's critical path.
+template <int MT>
+RAVEL_DEV void side_item(const PSide& sd, int item, PSmem& sm) {
+  const int tid = local_tid(), lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, grp = lane >> 4;
+  const int n0 = item * 32, kq = sd.K >> 2, kb = wave * kq;
+  const rsrc_t rW = rsrc(sd.W), rA = rsrc(sd.A);
+  bf16x8_t wf[2][8], af[MT][8];
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+      const int n = n0 + c * 16 + l16, k = kb + f * 32 + grp * 8;
+      wf[c][f] = ld_b8<PLAIN>(rW, boff(f * 32 < kq && n < sd.N, ((size_t)n * sd.ldw + k) * 2));
+    }
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+      const int m = i * 16 + l16, k = kb + f * 32 + grp * 8;
+      af[i][f] = ld_b8<PLAIN>(rA, boff(f * 32 < kq && m < sd.M, ((size_t)m * sd.lda + k) * 2));
+    }
+  f32x4_t bias4[2];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const int n = n0 + c * 16 + 4 * ((tid & 63) >> 4);
+    bias4[c] = ld_f4<PLAIN>(rsrc(sd.bias), boff(n + 4 <= sd.N, (size_t)n * 4));
+  }
+  f32x4_t acc[2][MT];
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      acc[c][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int f = 0; f < 8; ++f) acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[c][f], af[i][f], acc[c][i], 0, 0, 0);
+    }
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+#pragma unroll
+    for (int i = 0; i < MT; ++i) *(f32x4_t*)&sm.red[wave][c * MT + i][lane][0] = acc[c][i];
+  __syncthreads();
+  if (tid < MT * 64) {
+    const int i = tid >> 6, ln = tid & 63;
+    const int m = i * 16 + (ln & 15), cg = 4 * (ln >> 4);
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      f32x4_t s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const f32x4_t v = *(const f32x4_t*)&sm.red[w][c * MT + i][ln][0];
+        s[0] += v[0];
+        s[1] += v[1];
+        s[2] += v[2];
+        s[3] += v[3];
+      }
+      const int n = n0 + c * 16 + cg;
+      if (m < sd.M && n + 4 <= sd.N) {
+        const f32x4_t o = {s[0] + bias4[c][0], s[1] + bias4[c][1], s[2] + bias4[c][2], s[3] + bias4[c][3]};
+        st_f4(rsrc(sd.out), ((size_t)m * sd.ldo + n) * 4, o);
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+          const int col = n - sd.shift_col[r];
+          if (sd.shift_out[r] && col >= 0 && col < sd.shift_w)
+            st_bf16x4(rsrc(sd.shift_out[r]), t32_off(m, col), o[0], o[1], o[2], o[3]);
+        }
+      }
+    }
+  }
+  __syncthreads();
+}
+
 // A split-K tile finished by its ksplit blocks together: block z takes rows
 // [z*rp, min(M, (z+1)*rp)), rp = ceil(M / ksplit), adds the partials of each of its
 // (row, 4-column) slots in split order and applies the epilogue; the new rows' sums
@@ -1650,8 +1726,15 @@ __global__ __launch_bounds__(256) void persistent_step_kernel(const Phase* __res
         for (int item = blockIdx.x; item < items; item += gridDim.x) rope_item(r, item);
       }
     }
+    // side work of the phase for the blocks without an item, then the L2 warm-up of
+    // the next phase by the blocks past those
+    const int nside = uni(ph.side.nitems);
+    if (nside > 0 && (int)blockIdx.x >= items && (int)blockIdx.x < items + nside) {
+      const PSide sd = make_uniform(ph.side);
+      side_item<MT>(sd, sd.item0 + (int)blockIdx.x - items, sm);
+    }
     if (p + 1 == nphase) break;
-    idle_warm<HD>(desc[(p + 1) % 3], items, slots);
+    idle_warm<HD>(desc[(p + 1) % 3], items + nside, slots);
     // arrive at barrier p + 1 once every wave's stores are done; fetch descriptor
     // p + 2 (written to LDS after that barrier)
     wait_memory();

@@ -350,6 +350,10 @@ struct ravel_buffer {
   int attn_nsplit = 1, attn_kps = 0;
   bool mod_all = false;
   int mod_ld = 0;
+  // persistent step: the modulation of layers 1 .. L - 1 and of the final norm (and
+  // their bf16 shift copies) is computed inside the layer kernel by otherwise idle
+  // blocks; before the launch only layer 0's
+  bool side_mod = false;
   // per-layer modulation on the rows of distinct offset conditionings only
   bool cgroups = false;
   int* cgrp = nullptr;     // [B] conditioning group of each env (negative: not the group's first env)
@@ -1043,8 +1047,12 @@ ravel_status build_persistent(ravel_buffer* b) {
   // outputs of whole-K items are written in 16-column pieces (several writers per
   // 128-byte line): their readers use device-coherent loads
   bool qkv_pieces = false, qa_pieces = false, u_pieces = false;
+  // per layer: its first phase and its gate/up phase (the side work of layer l, the
+  // modulation of layer l + 1 or of the final norm, runs in the phases between)
+  std::vector<int> layer_first(c.layers), layer_gu(c.layers);
   for (int l = 0; l < c.layers; ++l) {
     const LayerW& L = m->layers[l];
+    layer_first[l] = (int)P.size();
     const float* mod = b->mod + (size_t)l * 6 * w;
     const float* next_scale = b->mod + (size_t)(l + 1) * 6 * w;  // next layer's (or the final) chunk 0
     bf16_t* qkv = (bf16_t*)fresh((size_t)BH * qkvd * 2);
@@ -1161,6 +1169,7 @@ ravel_status build_persistent(ravel_buffer* b) {
       ph.g.ldo = F;
       ph.g.out_t32 = 1;
       u_pieces = ph.g.wk != 0;
+      layer_gu[l] = (int)P.size();
       push(ph, "gate_up");
     }
     {
@@ -1182,6 +1191,52 @@ ravel_status build_persistent(ravel_buffer* b) {
   }
   for (auto& ph : P)
     if (ph.type == PH_GEMM && ph.g.kw == 0) return fail(RAVEL_E_STATE, "persistent: K range too long");
+  // Modulation of layer l + 1 (or of the final norm) as side work of layer l's
+  // phases before gate/up, in 32-column whole-K items over the conditioning rows, on
+  // the blocks those phases leave idle (one item per idle block and phase); the
+  // launch before the kernel then computes layer 0's chunk only.  Off when some
+  // layer's phases lack the idle blocks, or the shapes do not fit the item.
+  {
+    bool ok = getenv("RAVEL_NO_SIDE_MOD") == nullptr || atoi(getenv("RAVEL_NO_SIDE_MOD")) == 0;
+    ok = ok && w % 128 == 0 && w <= 1024;
+    std::vector<PSide> sides(P.size());
+    for (auto& sd : sides) memset(&sd, 0, sizeof sd);
+    for (int l = 0; l < c.layers && ok; ++l) {
+      const bool last = l + 1 == c.layers;
+      const size_t col0 = (size_t)(l + 1) * 6 * w;  // the final norm's chunk follows the last layer's
+      const int N = last ? 2 * w : 6 * w;
+      int remaining = N / 32, next = 0;
+      for (int p = layer_first[l]; p < layer_gu[l] && remaining > 0; ++p) {
+        const int cap = std::max(0, b->pblocks - P[p].items);
+        const int take = std::min(cap, remaining);
+        if (take <= 0) continue;
+        PSide& sd = sides[p];
+        sd.A = (const bf16_t*)b->cond;
+        sd.lda = w;
+        sd.W = (const bf16_t*)((const char*)m->mod_all_w + col0 * w * 2);
+        sd.ldw = w;
+        sd.bias = m->mod_all_b + col0;
+        sd.out = b->mod + col0;
+        sd.ldo = b->mod_ld;
+        sd.shift_out[0] = (bf16_t*)shift_of(last ? 2 * c.layers : 2 * (l + 1));
+        sd.shift_col[0] = w;
+        sd.shift_out[1] = last ? nullptr : (bf16_t*)shift_of(2 * (l + 1) + 1);
+        sd.shift_col[1] = 4 * w;
+        sd.shift_w = w;
+        sd.M = BH;
+        sd.N = N;
+        sd.K = w;
+        sd.item0 = next;
+        sd.nitems = take;
+        next += take;
+        remaining -= take;
+      }
+      ok = remaining == 0;
+    }
+    b->side_mod = ok;
+    if (ok)
+      for (size_t p = 0; p < P.size(); ++p) P[p].side = sides[p];
+  }
   // workspaces, patched into the list
   float *gpart, *ao, *aml;
   unsigned* cnt;
@@ -1246,6 +1301,10 @@ ravel_status build_persistent(ravel_buffer* b) {
     } else if (ph.type == PH_ROPE) {  // the angle table (the rows stay in L2)
       b->ph_bytes[i] = (double)H * hd * 4;
     }
+    if (ph.side.nitems > 0) {  // side work: the modulation weights of its items
+      b->ph_bytes[i] += (double)ph.side.nitems * 32 * ph.side.K * 2;
+      b->ph_flops[i] += 2.0 * ph.side.M * ph.side.nitems * 32 * ph.side.K;
+    }
     by += b->ph_bytes[i];
     fl += b->ph_flops[i];
   }
@@ -1283,11 +1342,14 @@ ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream
     REC_END();
   }
   {
+    // every layer's modulation, or layer 0's only when the layer kernel computes the
+    // others in blocks its phases leave idle
     GemmArgs e = epi_args(EPI_F32);
     e.bias = m->mod_all_b;
     e.out_f = b->mod;
     e.ldo_f = b->mod_ld;
-    RV_TRY(run_gemm<bf16_t>(b, s, rec, "mod_all", b->cond, w, m->mod_all_w, w, BH, b->mod_ld, w, e));
+    RV_TRY(run_gemm<bf16_t>(b, s, rec, b->side_mod ? "mod_layer0" : "mod_all", b->cond, w, m->mod_all_w, w, BH,
+                            b->side_mod ? 6 * w : b->mod_ld, w, e));
   }
   {
     // input projection with the first layer's norm operands: p of the first norm,
@@ -1302,7 +1364,7 @@ ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream
     nrm.cvt_in = b->mod + w;
     nrm.cvt_ld = b->mod_ld;
     nrm.cvt_stride = 3 * w;
-    nrm.cvt_chunks = 2 * c.layers + 1;
+    nrm.cvt_chunks = b->side_mod ? 2 : 2 * c.layers + 1;
     nrm.cvt_out = b->pshift;
     if (adapter) {
       // the first norm's operands come from the offset form's tokens
