@@ -850,6 +850,103 @@ __global__ __launch_bounds__(64 * NW) void gemm_regstream_kernel(GemmArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Whole-K kernel for few rows (M <= 64) and K <= 1024 (K % 128 == 0): block = 32
+// output columns x all M rows x the whole K; wave w takes the K quarter
+// [w K/4, (w + 1) K/4) and loads all its weight and activation fragments at once.
+// The four partial tiles are added through LDS in fixed wave order, so no K range
+// is split across blocks: no partial tiles, no tickets, one memory latency.
+// ---------------------------------------------------------------------------
+template <int MT>
+__global__ __launch_bounds__(256) void gemm_wholek_kernel(GemmArgs a) {
+  constexpr int NC = 2;            // 16-column blocks per block
+  constexpr int FR = NC * MT;      // accumulator fragments per wave
+  __shared__ __attribute__((aligned(16))) float red[4][FR][64][4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, grp = lane >> 4;
+  const int n0 = blockIdx.x * 32;
+  const int kq = a.K >> 2, kb = wave * kq;  // kq: a multiple of 32, at most 256
+  const bf16_t* __restrict__ A = (const bf16_t*)a.A;
+  const bf16_t* __restrict__ B = (const bf16_t*)a.B;
+  const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(A), (short)0, 0x7fffffff,
+                                                                       0x00020000);
+  const __amdgpu_buffer_rsrc_t rB = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(B), (short)0, 0x7fffffff,
+                                                                       0x00020000);
+  constexpr int kOOR = (int)0x80000000u;
+  // fragments past the wave's K quarter, rows past M and columns past N read zeros
+  bf16x8_t wf[NC][8], xf[MT][8];
+#pragma unroll
+  for (int f = 0; f < 8; ++f) {
+    const int k = kb + f * 32 + grp * 8;
+    const bool kin = f * 32 < kq;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int n = n0 + c * 16 + l16;
+      const int off = (kin && n < a.N) ? (int)(((size_t)n * a.ldb + k) * 2) : kOOR;
+      wf[c][f] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rB, off, 0, 0));
+    }
+  }
+#pragma unroll
+  for (int f = 0; f < 8; ++f) {
+    const int k = kb + f * 32 + grp * 8;
+    const bool kin = f * 32 < kq;
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const int m = i * 16 + l16;
+      const int off = (kin && m < a.M) ? (int)(((size_t)m * a.lda + k) * 2) : kOOR;
+      xf[i][f] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rA, off, 0, 0));
+    }
+  }
+  f32x4_t acc[NC][MT];
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      acc[c][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int f = 0; f < 8; ++f)
+        acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[c][f], xf[i][f], acc[c][i], 0, 0, 0);
+    }
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int i = 0; i < MT; ++i) *(f32x4_t*)&red[wave][c * MT + i][lane][0] = acc[c][i];
+  __syncthreads();
+  // item = (c * MT + i) * 64 + lane: rows i*16 + (lane & 15), columns n0 + c*16 + 4*(lane >> 4)
+  const bool vec = epi_vec_ok(a);
+  for (int item = tid; item < FR * 64; item += 256) {
+    const int fr = item >> 6, ln = item & 63;
+    const int c = fr / MT, i = fr % MT;
+    f32x4_t s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const f32x4_t v = *(const f32x4_t*)&red[w][fr][ln][0];
+      s[0] += v[0];
+      s[1] += v[1];
+      s[2] += v[2];
+      s[3] += v[3];
+    }
+    const int m = i * 16 + (ln & 15), n = n0 + c * 16 + (ln >> 4) * 4;
+    if (m >= a.M || n >= a.N) continue;
+    switch (a.mode) {
+      case EPI_F32: epi4<EPI_F32>(a, m, n, s, vec); break;
+      case EPI_T: epi4<EPI_T>(a, m, n, s, vec); break;
+      case EPI_RESID: epi4<EPI_RESID>(a, m, n, s, vec); break;
+      case EPI_RESID_TANH: epi4<EPI_RESID_TANH>(a, m, n, s, vec); break;
+      case EPI_COND: epi4<EPI_COND>(a, m, n, s, vec); break;
+      case EPI_GELU_T: epi4<EPI_GELU_T>(a, m, n, s, vec); break;
+      case EPI_SILU_T: epi4<EPI_SILU_T>(a, m, n, s, vec); break;
+      default: break;
+    }
+  }
+}
+
+template <int MT>
+static hipError_t launch_wholek_t(const GemmArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL((gemm_wholek_kernel<MT>), dim3((a.N + 31) / 32), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 template <int MT, int NW>
 static hipError_t launch_regstream_t(const GemmArgs& a, hipStream_t s) {
   dim3 grid((a.N + 63) / 64, a.ksplit);
@@ -879,6 +976,16 @@ hipError_t launch_gemm_regstream(const GemmArgs& a, hipStream_t s) {
     case 2: return launch_regstream_m<2>(a, s);
     case 3: return launch_regstream_m<3>(a, s);
     default: return launch_regstream_m<4>(a, s);
+  }
+}
+
+hipError_t launch_gemm_wholek(const GemmArgs& a, hipStream_t s) {
+  if (a.M > 64 || a.K > 1024 || (a.K % 128) || a.mode == EPI_GEGLU || !fits_buffer(a)) return hipErrorInvalidValue;
+  switch ((a.M + 15) / 16) {
+    case 1: return launch_wholek_t<1>(a, s);
+    case 2: return launch_wholek_t<2>(a, s);
+    case 3: return launch_wholek_t<3>(a, s);
+    default: return launch_wholek_t<4>(a, s);
   }
 }
 

@@ -65,6 +65,9 @@ hipError_t launch_gemm_skinny(const GemmArgs& a, int nfr, hipStream_t s);
 // M <= 64, 64-column tiles, waves split the block's K range (kchunk 256 or 512 = 4 or 8
 // waves), ksplit ranges (grid.y).
 hipError_t launch_gemm_regstream(const GemmArgs& a, hipStream_t s);
+// M <= 64, K <= 1024 with K % 128 == 0, not EPI_GEGLU: 32-column blocks over the whole
+// K, waves split it in quarters (no split-K workspace).
+hipError_t launch_gemm_wholek(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------------------

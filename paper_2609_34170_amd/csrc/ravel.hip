@@ -226,6 +226,7 @@ ravel_status upload_all(const ravel_tensor* t, bool to_bf16, void* dst, const St
 struct GemmPlan {
   bool skinny;
   bool regstream;
+  bool wholek;  // skinny: 32-column blocks over the whole K (no split)
   int nfr;     // skinny: 16-column fragments per wave
   int tile;    // tiled: GemmTile
   int ksplit;
@@ -233,6 +234,16 @@ struct GemmPlan {
   int tiles;
   size_t part_elems;  // split-K workspace (floats)
 };
+
+// RAVEL_NO_WHOLE_K_GEMM=1: few-row GEMMs with K <= 1024 split K across blocks
+// (register streaming) instead of one block per 32 columns over the whole K
+bool no_wholek() {
+  static const bool v = [] {
+    const char* e = getenv("RAVEL_NO_WHOLE_K_GEMM");
+    return e && atoi(e) != 0;
+  }();
+  return v;
+}
 
 GemmPlan plan_gemm(int M, int N, int K, bool geglu) {
   GemmPlan p;
@@ -248,6 +259,15 @@ GemmPlan plan_gemm(int M, int N, int K, bool geglu) {
       p.nfr = 1;
       p.tiles = tiles64;
       p.kchunk = K <= 128 ? 128 : K <= 256 ? 256 : K <= 512 ? 512 : 1024;
+      p.ksplit = 1;
+      p.part_elems = 0;
+      return p;
+    }
+    if (!geglu && K <= 1024 && K % 128 == 0 && !no_wholek()) {
+      p.regstream = false;
+      p.wholek = true;
+      p.tiles = (N + 31) / 32;
+      p.kchunk = K;
       p.ksplit = 1;
       p.part_elems = 0;
       return p;
@@ -448,6 +468,8 @@ ravel_status run_gemm(ravel_buffer* b, hipStream_t s, KernelRecorder* rec, const
     char full[48];
     if (epi.m_rows)  // rows known on the device only: no byte / flop figures
       snprintf(full, sizeof full, "gemm_rows:%s", name);
+    else if (p.skinny && p.wholek)
+      snprintf(full, sizeof full, "gemm_wholek<%d>:%s", (M + 15) / 16, name);
     else if (p.skinny && p.regstream)
       snprintf(full, sizeof full, "gemm_regstream<%d>:%s", (M + 15) / 16, name);
     else if (p.skinny)
@@ -457,7 +479,9 @@ ravel_status run_gemm(ravel_buffer* b, hipStream_t s, KernelRecorder* rec, const
     rec->begin(full, epi.m_rows ? 0.0 : bytes, epi.m_rows ? 0.0 : flops);
   }
   if (p.skinny) {
-    if (p.regstream)
+    if (p.wholek)
+      HIP_TRY(launch_gemm_wholek(epi, s));
+    else if (p.regstream)
       HIP_TRY(launch_gemm_regstream(epi, s));
     else
       HIP_TRY(launch_gemm_skinny(epi, p.nfr, s));
