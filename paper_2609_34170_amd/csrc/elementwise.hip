@@ -299,18 +299,15 @@ template hipError_t launch_cond_expand<bf16_t>(const float*, int, int, int, cons
 constexpr int kCondCols = 16;
 constexpr int kCondMaxW = 2048;  // w <= 2048: 8 chunks of K per lane, 8 h1 values per thread
 constexpr int kCondMaxH = 128;   // H <= 128: 8 conditioning entries per thread
-__global__ __launch_bounds__(256) void offset_cond_kernel(const int64_t* t, const int64_t* t_obs,
-                                                          const int64_t* ages, int H, float delta_bias,
-                                                          const float* __restrict__ wd1,
-                                                          const float* __restrict__ bd1,
-                                                          const bf16_t* __restrict__ wd2,
-                                                          const float* __restrict__ bd2, int w,
-                                                          const float* __restrict__ ctau, int tau_row,
-                                                          bf16_t* __restrict__ cond) {
+// block (bx, by): columns [16 bx, 16 bx + 16) of env by
+RAVEL_DEV void offset_cond_block(int bx, int by, const int64_t* t, const int64_t* t_obs, const int64_t* ages, int H,
+                                 float delta_bias, const float* __restrict__ wd1, const float* __restrict__ bd1,
+                                 const bf16_t* __restrict__ wd2, const float* __restrict__ bd2, int w,
+                                 const float* __restrict__ ctau, int tau_row, bf16_t* __restrict__ cond) {
   __shared__ bf16_t h1[kCondMaxW];
   __shared__ float dcol[kCondCols];
   constexpr int MAXJ = kCondMaxW / 512, MAXK = kCondMaxW / 256, MAXC = kCondMaxH * kCondCols / 256;
-  const int e = blockIdx.y, n0 = blockIdx.x * kCondCols;
+  const int e = by, n0 = bx * kCondCols;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // every load of the block is issued before any is used: the offset MLP's first
   // layer, this wave's four rows of W_d2, the conditioning table entries and bias
@@ -371,6 +368,17 @@ __global__ __launch_bounds__(256) void offset_cond_kernel(const int64_t* t, cons
   }
 }
 
+__global__ __launch_bounds__(256) void offset_cond_kernel(const int64_t* t, const int64_t* t_obs,
+                                                          const int64_t* ages, int H, float delta_bias,
+                                                          const float* __restrict__ wd1,
+                                                          const float* __restrict__ bd1,
+                                                          const bf16_t* __restrict__ wd2,
+                                                          const float* __restrict__ bd2, int w,
+                                                          const float* __restrict__ ctau, int tau_row,
+                                                          bf16_t* __restrict__ cond) {
+  offset_cond_block(blockIdx.x, blockIdx.y, t, t_obs, ages, H, delta_bias, wd1, bd1, wd2, bd2, w, ctau, tau_row, cond);
+}
+
 hipError_t launch_offset_cond(const int64_t* t, const int64_t* t_obs, const int64_t* ages, int B, int H,
                               float delta_bias, const float* wd1, const float* bd1, const bf16_t* wd2,
                               const float* bd2, int w, const float* ctau, int tau_row, bf16_t* cond,
@@ -421,21 +429,22 @@ RAVEL_DEV void shift_copy_item(size_t idx, int M, int w, const InProjNorm& nrm) 
 // count.  Every output is bias + sum over d in increasing order.  Blocks past the
 // row blocks (blockIdx.y >= nrowblk) make the bf16 shift copies instead.
 constexpr int kInProjRows = 16;
-__global__ __launch_bounds__(256) void in_proj_kernel(const float* __restrict__ X, const int64_t* t, int B, int H, int D,
-                                                      const float* __restrict__ w_inT, const float* __restrict__ b_in,
-                                                      int w, float* __restrict__ x, InProjNorm nrm,
-                                                      const double* __restrict__ dval, int rpb, int nrowblk) {
+// block (bx, by) of a (gx, ...) grid
+RAVEL_DEV void in_proj_block(int bx, int by, int gx, const float* __restrict__ X, const int64_t* t, int B, int H, int D,
+                             const float* __restrict__ w_inT, const float* __restrict__ b_in, int w,
+                             float* __restrict__ x, const InProjNorm& nrm, const double* __restrict__ dval, int rpb,
+                             int nrowblk) {
   __shared__ float xs[kInProjRows][16];
   const int tid = threadIdx.x;
-  if ((int)blockIdx.y >= nrowblk) {
-    shift_copy_item(((size_t)(blockIdx.y - nrowblk) * gridDim.x + blockIdx.x) * 256 + tid, B * H, w, nrm);
+  if (by >= nrowblk) {
+    shift_copy_item(((size_t)(by - nrowblk) * gx + bx) * 256 + tid, B * H, w, nrm);
     return;
   }
-  const int n = blockIdx.x * 256 + tid;
+  const int n = bx * 256 + tid;
   const int lane = tid & 63;
   const int BH = B * H;
   const int h0 = t ? (int)(*t % H) : 0;  // no step counter: X is a chunk in logical order
-  const int row0 = blockIdx.y * rpb;
+  const int row0 = by * rpb;
   const int nrows = min(rpb, BH - row0);
   // the first norm's scales of this thread's column, requested up front
   float scv[kInProjRows];
@@ -480,14 +489,54 @@ __global__ __launch_bounds__(256) void in_proj_kernel(const float* __restrict__ 
     if (rr >= nrows) break;
     const int row = row0 + rr;
     if (n < w) x[(size_t)row * w + n] = acc[rr];
-    if (!nrm.p) continue;
-    // first adaptive norm of the persistent step: p = bf16((1 + scale) x), the
-    // 64-column tile's sum of squares of the row, and the bf16 shift copies
+    if (!nrm.sumsq) continue;
+    // first adaptive norm of the persistent step: p = bf16((1 + scale) x) (unless the
+    // modulation GEMM forms it), the 64-column tile's sum of squares of the row, and
+    // the bf16 shift copies
     const float v = n < w ? acc[rr] : 0.f;
-    if (n < w) nrm.p[t32_index(row, n)] = f32_to_bf16((1.f + scv[rr]) * v);
+    if (nrm.p && n < w) nrm.p[t32_index(row, n)] = f32_to_bf16((1.f + scv[rr]) * v);
     const float sq = wave_sum(v * v);
     if (lane == 0 && n < w) nrm.sumsq[(size_t)(n >> 6) * 64 + row] = sq;
   }
+}
+
+__global__ __launch_bounds__(256) void in_proj_kernel(const float* __restrict__ X, const int64_t* t, int B, int H, int D,
+                                                      const float* __restrict__ w_inT, const float* __restrict__ b_in,
+                                                      int w, float* __restrict__ x, InProjNorm nrm,
+                                                      const double* __restrict__ dval, int rpb, int nrowblk) {
+  in_proj_block(blockIdx.x, blockIdx.y, gridDim.x, X, t, B, H, D, w_inT, b_in, w, x, nrm, dval, rpb, nrowblk);
+}
+
+// The offset conditioning (blocks [0, ncx * B)) and the input projection with the
+// rows' sums of squares (the rest, one row per block) of a few-row step in one
+// launch: neither reads the other's output.
+__global__ __launch_bounds__(256) void offset_cond_in_proj_kernel(
+    const int64_t* t, const int64_t* t_obs, int H, float delta_bias, const float* __restrict__ wd1,
+    const float* __restrict__ bd1, const bf16_t* __restrict__ wd2, const float* __restrict__ bd2, int w,
+    const float* __restrict__ ctau, bf16_t* __restrict__ cond, int ncx, int nc, const float* __restrict__ X, int B,
+    int D, const float* __restrict__ w_inT, const float* __restrict__ b_in, float* __restrict__ x, InProjNorm nrm,
+    int ipx, int nrowblk) {
+  const int b = blockIdx.x;
+  if (b < nc) {
+    offset_cond_block(b % ncx, b / ncx, t, t_obs, nullptr, H, delta_bias, wd1, bd1, wd2, bd2, w, ctau, -1, cond);
+  } else {
+    const int i = b - nc;
+    in_proj_block(i % ipx, i / ipx, ipx, X, t, B, H, D, w_inT, b_in, w, x, nrm, nullptr, 1, nrowblk);
+  }
+}
+
+hipError_t launch_offset_cond_in_proj(const int64_t* t, const int64_t* t_obs, int B, int H, float delta_bias,
+                                      const float* wd1, const float* bd1, const bf16_t* wd2, const float* bd2, int w,
+                                      const float* ctau, bf16_t* cond, const float* X, int D, const float* w_inT,
+                                      const float* b_in, float* x, float* sumsq, hipStream_t s) {
+  if (w > kCondMaxW || w % 64 || B < 1 || H > kCondMaxH || B * H > 64 || !t || !sumsq) return hipErrorInvalidValue;
+  InProjNorm nrm{};
+  nrm.sumsq = sumsq;
+  const int ncx = (w + kCondCols - 1) / kCondCols, nc = ncx * B;
+  const int ipx = (w + 255) / 256, nrowblk = B * H;
+  hipLaunchKernelGGL(offset_cond_in_proj_kernel, dim3(nc + ipx * nrowblk), dim3(256), 0, s, t, t_obs, H, delta_bias,
+                     wd1, bd1, wd2, bd2, w, ctau, cond, ncx, nc, X, B, D, w_inT, b_in, x, nrm, ipx, nrowblk);
+  return hipGetLastError();
 }
 
 hipError_t launch_in_proj(const float* X, const int64_t* t, int B, int H, int D, const float* w_inT,

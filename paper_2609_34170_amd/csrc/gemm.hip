@@ -857,14 +857,35 @@ __global__ __launch_bounds__(64 * NW) void gemm_regstream_kernel(GemmArgs a) {
 // The four partial tiles are added through LDS in fixed wave order, so no K range
 // is split across blocks: no partial tiles, no tickets, one memory latency.
 // ---------------------------------------------------------------------------
+// The first adaptive norm's operands from modulation values v (columns n .. n+3 of
+// row m, see GemmArgs::nrm_p).
+RAVEL_DEV void norm_operands4(const GemmArgs& a, int m, int n, f32x4_t v) {
+  const int w = a.nrm_w;
+  const auto t32 = [](int row, int c) { return ((size_t)(c >> 5) * 64 + row) * 32 + (c & 31); };
+  if (n < w) {
+    const f32x4_t x = *(const f32x4_t*)(a.nrm_x + (size_t)m * w + n);
+    u32x2_t o;
+    o[0] = (uint32_t)f32_to_bf16((1.f + v[0]) * x[0]) | ((uint32_t)f32_to_bf16((1.f + v[1]) * x[1]) << 16);
+    o[1] = (uint32_t)f32_to_bf16((1.f + v[2]) * x[2]) | ((uint32_t)f32_to_bf16((1.f + v[3]) * x[3]) << 16);
+    *(u32x2_t*)(a.nrm_p + t32(m, n)) = o;
+    return;
+  }
+  const int c = (n >= w && n < 2 * w) ? 0 : ((n >= 4 * w && n < 5 * w) ? 1 : -1);
+  if (c < 0) return;
+  const int col = n - (c == 0 ? w : 4 * w);
+  const u32x2_t o = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+  *(u32x2_t*)(a.nrm_shift + (size_t)c * 64 * w + t32(m, col)) = o;
+}
+
+// block bx of a whole-K launch (32 output columns)
 template <int MT>
-__global__ __launch_bounds__(256) void gemm_wholek_kernel(GemmArgs a) {
+RAVEL_DEV void gemm_wholek_block(const GemmArgs& a, int bx) {
   constexpr int NC = 2;            // 16-column blocks per block
   constexpr int FR = NC * MT;      // accumulator fragments per wave
   __shared__ __attribute__((aligned(16))) float red[4][FR][64][4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, grp = lane >> 4;
-  const int n0 = blockIdx.x * 32;
+  const int n0 = bx * 32;
   const int kq = a.K >> 2, kb = wave * kq;  // kq: a multiple of 32, at most 256
   const bf16_t* __restrict__ A = (const bf16_t*)a.A;
   const bf16_t* __restrict__ B = (const bf16_t*)a.B;
@@ -928,6 +949,10 @@ __global__ __launch_bounds__(256) void gemm_wholek_kernel(GemmArgs a) {
     }
     const int m = i * 16 + (ln & 15), n = n0 + c * 16 + (ln >> 4) * 4;
     if (m >= a.M || n >= a.N) continue;
+    if (a.nrm_p && a.mode == EPI_F32 && n + 4 <= a.N) {
+      const f32x4_t b4 = a.bias ? *(const f32x4_t*)(a.bias + n) : f32x4_t{0.f, 0.f, 0.f, 0.f};
+      norm_operands4(a, m, n, f32x4_t{s[0] + b4[0], s[1] + b4[1], s[2] + b4[2], s[3] + b4[3]});
+    }
     switch (a.mode) {
       case EPI_F32: epi4<EPI_F32>(a, m, n, s, vec); break;
       case EPI_T: epi4<EPI_T>(a, m, n, s, vec); break;
@@ -939,6 +964,20 @@ __global__ __launch_bounds__(256) void gemm_wholek_kernel(GemmArgs a) {
       default: break;
     }
   }
+}
+
+template <int MT>
+__global__ __launch_bounds__(256) void gemm_wholek_kernel(GemmArgs a) {
+  gemm_wholek_block<MT>(a, blockIdx.x);
+}
+
+// two GEMMs: blocks [0, nb1) take a1, the rest a2
+template <int MT1, int MT2>
+__global__ __launch_bounds__(256) void gemm_wholek2_kernel(GemmArgs a1, int nb1, GemmArgs a2) {
+  if ((int)blockIdx.x < nb1)
+    gemm_wholek_block<MT1>(a1, blockIdx.x);
+  else
+    gemm_wholek_block<MT2>(a2, blockIdx.x - nb1);
 }
 
 template <int MT>
@@ -979,8 +1018,25 @@ hipError_t launch_gemm_regstream(const GemmArgs& a, hipStream_t s) {
   }
 }
 
+static bool wholek_ok(const GemmArgs& a) {
+  if (a.M > 64 || a.K > 1024 || (a.K % 128) || a.mode == EPI_GEGLU || !fits_buffer(a)) return false;
+  // the norm operands: modulation rows of 6 nrm_w columns, 4-column groups inside one chunk
+  if (a.nrm_p && (a.mode != EPI_F32 || !a.nrm_x || !a.nrm_shift || a.nrm_w % 32 || a.N != 6 * a.nrm_w)) return false;
+  return true;
+}
+
+hipError_t launch_gemm_wholek2(const GemmArgs& a1, const GemmArgs& a2, hipStream_t s) {
+  if (!wholek_ok(a1) || !wholek_ok(a2)) return hipErrorInvalidValue;
+  // the pairs used: a few rows' modulation (4 row fragments) with the FOP tokens' keys
+  // and values (1 row fragment)
+  if ((a1.M + 15) / 16 != 4 || (a2.M + 15) / 16 != 1) return hipErrorInvalidValue;
+  const int nb1 = (a1.N + 31) / 32, nb2 = (a2.N + 31) / 32;
+  hipLaunchKernelGGL((gemm_wholek2_kernel<4, 1>), dim3(nb1 + nb2), dim3(256), 0, s, a1, nb1, a2);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm_wholek(const GemmArgs& a, hipStream_t s) {
-  if (a.M > 64 || a.K > 1024 || (a.K % 128) || a.mode == EPI_GEGLU || !fits_buffer(a)) return hipErrorInvalidValue;
+  if (!wholek_ok(a)) return hipErrorInvalidValue;
   switch ((a.M + 15) / 16) {
     case 1: return launch_wholek_t<1>(a, s);
     case 2: return launch_wholek_t<2>(a, s);

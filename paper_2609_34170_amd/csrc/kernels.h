@@ -50,6 +50,15 @@ struct GemmArgs {
   const int* m_rows;     // device row count: rows >= min(M, *m_rows) are neither computed nor stored
   const int* gate_rows;  // [M]: EPI_RESID reads gate row gate_rows[m] instead of row m
   const int* cond_grp;   // [M], EPI_COND: output block cond_grp[m] (>= 0), or nothing (< 0)
+  // Whole-K few-row kernel, EPI_F32 on a layer's modulation rows (value v = acc + bias
+  // at columns [0, 6 nrm_w)): also the first adaptive norm's operands, p[m][n] =
+  // bf16((1 + v[m][n]) nrm_x[m][n]) for n < nrm_w, and bf16 copies of the two shifts
+  // (columns [nrm_w, 2 nrm_w) and [4 nrm_w, 5 nrm_w)) as chunks 0 and 1 of nrm_shift;
+  // p and the chunks (64 * nrm_w elements apart) in 32-column tiles [nrm_w/32][64][32].
+  bf16_t* nrm_p;
+  const float* nrm_x;
+  bf16_t* nrm_shift;
+  int nrm_w;
 };
 
 // Tile configurations of the bf16 MFMA GEMM.
@@ -68,6 +77,8 @@ hipError_t launch_gemm_regstream(const GemmArgs& a, hipStream_t s);
 // M <= 64, K <= 1024 with K % 128 == 0, not EPI_GEGLU: 32-column blocks over the whole
 // K, waves split it in quarters (no split-K workspace).
 hipError_t launch_gemm_wholek(const GemmArgs& a, hipStream_t s);
+// Two whole-K few-row GEMMs in one launch (blocks of a1 first, then those of a2).
+hipError_t launch_gemm_wholek2(const GemmArgs& a1, const GemmArgs& a2, hipStream_t s);
 hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------------------
@@ -169,6 +180,15 @@ hipError_t launch_offset_cond(const int64_t* t, const int64_t* t_obs, const int6
                               float delta_bias, const float* wd1, const float* bd1, const bf16_t* wd2,
                               const float* bd2, int w, const float* ctau, int tau_row, bf16_t* cond,
                               hipStream_t s);
+// launch_offset_cond (rolling step: ages and tau_row unused) and launch_in_proj (ring
+// in slot order from the step counter t, no offset input) in one launch, the input
+// projection writing x and the rows' per-64-column sums of squares (sumsq[tile][64])
+// only: the first norm's p and shift copies then come from the modulation GEMM
+// (GemmArgs nrm_*).  B * H <= 64, w a multiple of 64.
+hipError_t launch_offset_cond_in_proj(const int64_t* t, const int64_t* t_obs, int B, int H, float delta_bias,
+                                      const float* wd1, const float* bd1, const bf16_t* wd2, const float* bd2, int w,
+                                      const float* ctau, bf16_t* cond, const float* X, int D, const float* w_inT,
+                                      const float* b_in, float* x, float* sumsq, hipStream_t s);
 
 // dval: NULL, or [B] offsets delta_e concatenated to every slot's input: w_inT then has
 // D + 1 rows and row D multiplies delta_e.

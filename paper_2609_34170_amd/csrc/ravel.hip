@@ -1348,7 +1348,63 @@ ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream
   const bool concat = c.offset_mode == RAVEL_OFFSET_CONCAT;
   const bool adapter = c.offset_mode == RAVEL_OFFSET_ADAPTER;
   const float dbias = pin.lead_bias ? c.delta_bias : 0.f;
-  if (concat || adapter) {
+  // The rolling step of the MLP offset form in two launches before the layer kernel:
+  // (1) the offset conditioning with the input projection (x and its rows' sums of
+  // squares), (2) layer 0's modulation, whose epilogue also forms the first norm's p
+  // and shift copies, together with the FOP keys / values when they fit the same
+  // whole-K kernel.
+  const bool prologue2 = b->side_mod && !concat && !adapter && !pin.X && !pin.ages && !pin.ctau && pin.tau_row < 0 &&
+                         w % 64 == 0 && plan_gemm(BH, 6 * w, w, false).wholek;
+  bool kv_done = false;
+  if (prologue2) {
+    REC_BEGIN("offset_cond_in_proj", (double)w * w * elt + (double)H * w * 4 + (double)BH * w * elt +
+                                         (double)BH * (D + w) * 4 + (double)BH * w * 6,
+              2.0 * B * w * w + (double)BH * w * 4 + 2.0 * BH * w * D);
+    HIP_TRY(launch_offset_cond_in_proj(b->t, b->t_obs, B, H, dbias, m->d_w1, m->d_b1, (const bf16_t*)m->d_w2, m->d_b2,
+                                       w, m->ctau, (bf16_t*)b->cond, b->X, D, m->in_wT, m->in_b, b->x, b->sumsq[0],
+                                       s));
+    REC_END();
+    GemmArgs e = epi_args(EPI_F32);
+    e.bias = m->mod_all_b;
+    e.out_f = b->mod;
+    e.ldo_f = b->mod_ld;
+    e.nrm_p = b->pnorm;
+    e.nrm_x = b->x;
+    e.nrm_shift = b->pshift;
+    e.nrm_w = w;
+    const bool pair = m->n_ad > 0 && (BH + 15) / 16 == 4 && B * c.n_fop <= 16 &&
+                      plan_gemm(B * c.n_fop, m->n_ad * 2 * kvd, w, false).wholek;
+    if (pair) {
+      e.A = b->cond;
+      e.lda = w;
+      e.B = m->mod_all_w;
+      e.ldb = w;
+      e.M = BH;
+      e.N = 6 * w;
+      e.K = w;
+      e.kchunk = w;
+      GemmArgs f = epi_args(EPI_T);
+      f.out_t = b->kva;
+      f.ldo_t = m->n_ad * 2 * kvd;
+      f.A = fop;
+      f.lda = w;
+      f.B = m->kva_w;
+      f.ldb = w;
+      f.M = B * c.n_fop;
+      f.N = m->n_ad * 2 * kvd;
+      f.K = w;
+      f.kchunk = w;
+      REC_BEGIN("mod_layer0_fop_kv",
+                ((double)BH * w + 6.0 * w * w + (double)B * c.n_fop * w + (double)f.N * w) * elt +
+                    (double)BH * 6 * w * 4 + (double)BH * w * 6 + (double)f.M * f.N * elt,
+                2.0 * BH * 6 * w * w + 2.0 * f.M * f.N * w);
+      HIP_TRY(launch_gemm_wholek2(e, f, s));
+      REC_END();
+      kv_done = true;
+    } else {
+      RV_TRY(run_gemm<bf16_t>(b, s, rec, "mod_layer0", b->cond, w, m->mod_all_w, w, BH, 6 * w, w, e));
+    }
+  } else if (concat || adapter) {
     REC_BEGIN("offset_value", (double)B * 12, 0.0);
     HIP_TRY(launch_offset_value(pin.X ? nullptr : b->t, b->t_obs, pin.ages, B, H, dbias, b->dval, s));
     REC_END();
@@ -1365,7 +1421,7 @@ ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream
                                (bf16_t*)b->cond, s));
     REC_END();
   }
-  {
+  if (!prologue2) {
     // every layer's modulation, or layer 0's only when the layer kernel computes the
     // others in blocks its phases leave idle
     GemmArgs e = epi_args(EPI_F32);
@@ -1375,7 +1431,7 @@ ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream
     RV_TRY(run_gemm<bf16_t>(b, s, rec, b->side_mod ? "mod_layer0" : "mod_all", b->cond, w, m->mod_all_w, w, BH,
                             b->side_mod ? 6 * w : b->mod_ld, w, e));
   }
-  {
+  if (!prologue2) {
     // input projection with the first layer's norm operands: p of the first norm,
     // the rows' sums of squares, and the bf16 shifts of every norm (chunk 2l and
     // 2l + 1 of layer l, 2L the final norm: 3w apart in the modulation rows,
@@ -1408,7 +1464,7 @@ ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream
       REC_END();
     }
   }
-  if (m->n_ad > 0) {
+  if (m->n_ad > 0 && !kv_done) {
     GemmArgs e = epi_args(EPI_T);
     e.out_t = b->kva;
     e.ldo_t = m->n_ad * 2 * kvd;
