@@ -165,6 +165,16 @@ int64_t ravel_model_weight_bytes(const ravel_model* model);
  *   RAVEL_NO_FUSED_XATTN  a separate attention phase for the FOP adapters in the
  *                         persistent kernel (default for one env with 256-dim heads
  *                         and <= 16 FOP tokens: computed inside the output projection);
+ *   RAVEL_NO_SIDE_MOD     the modulation of every layer in one launch before the
+ *                         persistent kernel (default: layer 0's only, the others
+ *                         computed by blocks the kernel's phases leave idle);
+ *   RAVEL_NO_FUSED_PROLOGUE  the persistent step's offset conditioning, input
+ *                         projection, layer-0 modulation and FOP keys/values in
+ *                         separate launches (default: two launches, same results);
+ *   RAVEL_NO_WHOLE_K      split-K items instead of whole-K items for the persistent
+ *                         kernel's phases with K <= 1024;
+ *   RAVEL_NO_WHOLE_K_GEMM (read once per process) few-row GEMMs with K <= 1024 split
+ *                         K across blocks instead of one block per 32 columns;
  *   RAVEL_SYNC_CONTEXT    RAVEL_OPT_SYNC_CONTEXT on;  RAVEL_NO_GRAPH  RAVEL_OPT_USE_GRAPH off;
  *   RAVEL_COOPERATIVE     not supported: set to a nonzero value, buffer creation
  *                         fails with RAVEL_E_INVALID (the persistent kernel is

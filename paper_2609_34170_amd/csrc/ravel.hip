@@ -374,6 +374,7 @@ struct ravel_buffer {
   // their bf16 shift copies) is computed inside the layer kernel by otherwise idle
   // blocks; before the launch only layer 0's
   bool side_mod = false;
+  bool fused_prologue = true;  // the batch-1 step's two-launch prologue where it applies
   // per-layer modulation on the rows of distinct offset conditionings only
   bool cgroups = false;
   int* cgrp = nullptr;     // [B] conditioning group of each env (negative: not the group's first env)
@@ -1221,6 +1222,7 @@ ravel_status build_persistent(ravel_buffer* b) {
   // launch before the kernel then computes layer 0's chunk only.  Off when some
   // layer's phases lack the idle blocks, or the shapes do not fit the item.
   {
+    if (const char* ev = getenv("RAVEL_NO_FUSED_PROLOGUE")) b->fused_prologue = atoi(ev) == 0;
     bool ok = getenv("RAVEL_NO_SIDE_MOD") == nullptr || atoi(getenv("RAVEL_NO_SIDE_MOD")) == 0;
     ok = ok && w % 128 == 0 && w <= 1024;
     std::vector<PSide> sides(P.size());
@@ -1353,7 +1355,7 @@ ravel_status enqueue_persistent_pass(ravel_buffer* b, const void* fop, hipStream
   // squares), (2) layer 0's modulation, whose epilogue also forms the first norm's p
   // and shift copies, together with the FOP keys / values when they fit the same
   // whole-K kernel.
-  const bool prologue2 = b->side_mod && !concat && !adapter && !pin.X && !pin.ages && !pin.ctau && pin.tau_row < 0 &&
+  const bool prologue2 = b->fused_prologue && b->side_mod && !concat && !adapter && !pin.X && !pin.ages && !pin.ctau && pin.tau_row < 0 &&
                          w % 64 == 0 && plan_gemm(BH, 6 * w, w, false).wholek;
   bool kv_done = false;
   if (prologue2) {

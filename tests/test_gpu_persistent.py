@@ -96,3 +96,40 @@ def test_fused_cross_attention_matches_the_attention_phase_and_oracle(n_fop, mon
     assert rel_err(X_f, o.X) < 2e-2
     assert rel_err(a_u, a_o) < 2e-2
     assert rel_err(a_f, a_u) < 2e-2
+
+
+def _launch_names(shape, wts, batch):
+    from tests.harness import GpuRoll
+    g = GpuRoll(shape, wts, batch, seed=3)
+    for e in range(batch):
+        k, v = synth.draw_context(shape, 0, e, 0)
+        g.set_context(e, k, v, 0)
+    g.fop.copy_(g.to_dev(synth.draw_fop_tokens(shape, 0, 0, batch=batch)))
+    return {r[0] for r in g.buf.profile_step(g.fop, g.action) if not r[0].startswith(("persistent/", "phase/"))}
+
+
+@pytest.mark.parametrize("shape_kw,batch,paired", [
+    # 50 rows and 4 FOP tokens: layer 0's modulation and the FOP keys/values share a launch
+    (dict(layers=2, width=512, n_q_heads=2, n_kv_heads=1, head_dim=256, mlp_dim=1024, horizon=50,
+          action_dim=32, prefix_len=300, n_fop=4, fop_obs_dim=16), 1, True),
+    # 24 rows: the modulation launch forms the norm operands alone
+    (dict(layers=2, width=256, n_q_heads=4, n_kv_heads=2, head_dim=64, mlp_dim=512, horizon=12,
+          action_dim=7, prefix_len=40, n_fop=3, fop_obs_dim=16), 2, False),
+])
+def test_fused_prologue_is_bitwise_the_separate_launches(shape_kw, batch, paired, monkeypatch):
+    """The persistent step's two-launch prologue (offset conditioning with the input
+    projection; layer 0's modulation forming the first norm's p and shift copies) computes
+    every value with the same operations as the separate launches: actions and ring agree
+    bit for bit over several steps."""
+    s = synth.RavelShape(dtype=W.BF16, batch=batch, name="prologue", **shape_kw)
+    wts = synth.draw_weights(s, seed=8, stress=True)
+    names = _launch_names(s, wts, batch)
+    assert "offset_cond_in_proj" in names, names
+    assert ("mod_layer0_fop_kv" in names) == paired, names
+    a_f, X_f = _roll(s, wts, batch, 6, True)
+    monkeypatch.setenv("RAVEL_NO_FUSED_PROLOGUE", "1")
+    names_sep = _launch_names(s, wts, batch)
+    assert "offset_cond_in_proj" not in names_sep and "in_proj" in names_sep, names_sep
+    a_s, X_s = _roll(s, wts, batch, 6, True)
+    assert np.array_equal(a_f, a_s)
+    assert np.array_equal(X_f, X_s)
