@@ -798,10 +798,11 @@ hipError_t launch_train_loss(const float* v, const float* target, const float* n
   return hipGetLastError();
 }
 
-// One block per env: its threads first apply the Euler update to independent
-// ring elements, then the released slot is copied out and refilled with noise.  Every block reads the step counter at its start; the last
-// block to take the ticket (so every block has read it) re-arms the ticket and
-// advances the counter.
+// One block per env: each thread applies the Euler update to its ring elements and,
+// for logical slot 0, releases the updated value as the action and refills the
+// slot with the noise of the new tail step.  Every block reads the step counter at
+// its start; a single block advances it once its threads have read it, several
+// blocks take a ticket and the last one advances it (and re-arms the ticket).
 __global__ __launch_bounds__(256) void euler_release_kernel(float* __restrict__ X, const float* __restrict__ v,
                                                             int64_t* t, int H, int D, uint64_t seed,
                                                             float* __restrict__ action,
@@ -840,30 +841,33 @@ __global__ __launch_bounds__(256) void euler_release_kernel(float* __restrict__ 
       vv[u] = k < n ? ve[k] : 0.f;
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (off[u] >= 0) Xe[off[u]] = euler_sub(xv[u], dt, vv[u]);
-  }
-  __syncthreads();
-  const int NG = (D + 3) / 4;
-  float* xs = Xe + (size_t)h0 * D;
-  for (int c = threadIdx.x; c < NG; c += blockDim.x) {
-    float z[4];
-    ring_noise4(seed, e, tt + H, c, z);
-    for (int q = 0; q < 4; ++q) {
-      const int d = c * 4 + q;
-      if (d < D) {
-        // relative dimensions: the released action in absolute coordinates
-        action[(size_t)e * D + d] = state ? xs[d] + mask[d] * state[(size_t)e * D + d] : xs[d];
-        xs[d] = z[q];
+    for (int u = 0; u < 4; ++u) {
+      if (off[u] < 0) continue;
+      const float xn = euler_sub(xv[u], dt, vv[u]);
+      const int k = k0 + u * 256 + (int)threadIdx.x;
+      if (k >= D) {
+        Xe[off[u]] = xn;
+        continue;
       }
+      // logical slot 0 (k = d): released; its slot becomes the tail, refilled with the
+      // noise of step tt + H (4 dimensions per noise draw)
+      const int d = k;
+      action[(size_t)e * D + d] = state ? xn + mask[d] * state[(size_t)e * D + d] : xn;
+      float z[4];
+      ring_noise4(seed, e, tt + H, d >> 2, z);
+      Xe[off[u]] = z[d & 3];
     }
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    const unsigned prev = atomicAdd(ticket, 1u);
-    if (prev == gridDim.x - 1) {
-      *ticket = 0u;
+    if (gridDim.x == 1) {
       *t = tt + 1;
+    } else {
+      const unsigned prev = atomicAdd(ticket, 1u);
+      if (prev == gridDim.x - 1) {
+        *ticket = 0u;
+        *t = tt + 1;
+      }
     }
   }
 }
