@@ -19,9 +19,11 @@ Modules:
   training -- the streaming-aligned training objective (buffer at the rolling
               profile, offset p / K, flow-matching loss).
 
-Parity status: model output beyond the pins in tests/test_oracle_*.py is
-"parity unpinned" -- no trained weights or worked numeric example exist, so
-the oracle is the definition (see the pins for what is fixed independently).
+Pins: every function here is checked in tests/test_oracle_*.py against
+something other than itself (library routines, closed forms, special cases,
+invariants, known-answer vectors, planted mistakes that must fail).  The paper
+prints no numeric example of the expert's output (no trained weights exist), so
+values at random weights rest on those pins.
 """
 
 from .expert import Expert, fop_encode  # noqa: F401
