@@ -115,6 +115,9 @@ def _launch_names(shape, wts, batch):
     # 24 rows: the modulation launch forms the norm operands alone
     (dict(layers=2, width=256, n_q_heads=4, n_kv_heads=2, head_dim=64, mlp_dim=512, horizon=12,
           action_dim=7, prefix_len=40, n_fop=3, fop_obs_dim=16), 2, False),
+    # 64 rows of 4 envs and 16 FOP rows: both GEMMs of the paired launch at their full row fragments
+    (dict(layers=2, width=256, n_q_heads=4, n_kv_heads=2, head_dim=64, mlp_dim=512, horizon=16,
+          action_dim=5, prefix_len=33, n_fop=4, fop_obs_dim=16), 4, True),
 ])
 def test_fused_prologue_is_bitwise_the_separate_launches(shape_kw, batch, paired, monkeypatch):
     """The persistent step's two-launch prologue (offset conditioning with the input
