@@ -297,14 +297,13 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 // ---------------------------------------------------------------------------
 static constexpr float kLazy = 8.f;
 
-template <int HD, int NW>
+template <int HD, int NW, int TK>
 __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunks) {
   constexpr int NT = NW * 64;
-  constexpr int TK = 32;
   constexpr int KS = HD / 32;
   constexpr int DT = HD / 16;
   constexpr int KLD = HD + 8;
-  // V^T row stride 18 dwords (a stride of 20 measured slower)
+  // V^T row stride TK / 2 + 2 dwords (18 for 32-key tiles; 20 measured slower)
   constexpr int VLD = TK + 4;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2][TK][KLD];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[2][HD][VLD];
@@ -438,46 +437,48 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
     const int k0 = t * TK, buf = t & 1;
     if (t + 2 < ntile) load_tile(k0 + 2 * TK, s_next2);
     if (active) {
-    // S^T[key][row] for two 16-key sub-tiles, each summed in two independent
-    // MFMA chains (even / odd k-steps)
-    f32x4_t sa0 = {0.f, 0.f, 0.f, 0.f}, sa1 = sa0, sb0 = sa0, sb1 = sa0;
+    // S^T[key][row] for the tile's NS 16-key sub-tiles, each summed in two
+    // independent MFMA chains (even / odd k-steps)
+    constexpr int NS = TK / 16;
+    f32x4_t sa[NS], sb[NS];
+#pragma unroll
+    for (int u = 0; u < NS; ++u) sa[u] = sb[u] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     // the wave issuing MFMAs goes first; the SIMD's other wave fills the gaps
     // with its softmax or staging work
     __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int ks = 0; ks < KS; ks += 2) {
-      const bf16x8_t k0f = *(const bf16x8_t*)&Ks[buf][l16][ks * 32 + grp * 8];
-      const bf16x8_t k1f = *(const bf16x8_t*)&Ks[buf][16 + l16][ks * 32 + grp * 8];
-      sa0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0f, qf[ks], sa0, 0, 0, 0);
-      sa1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1f, qf[ks], sa1, 0, 0, 0);
+#pragma unroll
+      for (int u = 0; u < NS; ++u) {
+        const bf16x8_t kf = *(const bf16x8_t*)&Ks[buf][u * 16 + l16][ks * 32 + grp * 8];
+        sa[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], sa[u], 0, 0, 0);
+      }
       if (ks + 1 < KS) {
-        const bf16x8_t k2f = *(const bf16x8_t*)&Ks[buf][l16][(ks + 1) * 32 + grp * 8];
-        const bf16x8_t k3f = *(const bf16x8_t*)&Ks[buf][16 + l16][(ks + 1) * 32 + grp * 8];
-        sb0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k2f, qf[ks + 1], sb0, 0, 0, 0);
-        sb1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k3f, qf[ks + 1], sb1, 0, 0, 0);
+#pragma unroll
+        for (int u = 0; u < NS; ++u) {
+          const bf16x8_t kf = *(const bf16x8_t*)&Ks[buf][u * 16 + l16][(ks + 1) * 32 + grp * 8];
+          sb[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks + 1], sb[u], 0, 0, 0);
+        }
       }
     }
     __builtin_amdgcn_s_setprio(0);
-    float x[8];
+    float x[4 * NS];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      x[r] = (sa0[r] + sb0[r]) * sl2;
-      x[4 + r] = (sa1[r] + sb1[r]) * sl2;
-    }
+    for (int u = 0; u < NS; ++u)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) x[4 * u + r] = (sa[u][r] + sb[u][r]) * sl2;
     // valid keys of the tile (uniform): the last tile of each part is ragged
     const int nvalid = k0 < Ppad ? a.P - k0 : a.S - (k0 - Ppad);
     if (nvalid < TK) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        if (grp * 4 + r >= nvalid) x[r] = -INFINITY;
-        if (16 + grp * 4 + r >= nvalid) x[4 + r] = -INFINITY;
-      }
+      for (int u = 0; u < NS; ++u)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (u * 16 + grp * 4 + r >= nvalid) x[4 * u + r] = -INFINITY;
     }
-    // The row maximum needs the 4 lane groups only when some lane of the wave
-    // sees a score above mrow + kLazy; otherwise mrow (equal on the row's lanes)
-    // stays the reference.  Every tile holds a valid key, so the maximum is
-    // finite, and the first tile always moves.
-    const float lmx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+    float lmx = x[0];
+#pragma unroll
+    for (int r = 1; r < 4 * NS; ++r) lmx = fmaxf(lmx, x[r]);
     if (__any(lmx > mrow + kLazy)) {
       float mx = fmaxf(lmx, __shfl_xor(lmx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
@@ -493,26 +494,33 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(AttnArgs a, int chunk
         o[dt][3] *= corr;
       }
     }
-    // x - mrow <= kLazy: the hardware exp2 (no denormal range handling: results
-    // below 2^-126 flush to zero, far below the bf16 resolution of P)
-    float p[8];
+    float p[4 * NS];
 #pragma unroll
-    for (int r = 0; r < 8; ++r) p[r] = __builtin_amdgcn_exp2f(x[r] - mrow);
-    // the row sum stays split over the 4 lane groups until the end
-    lrow += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
-    // P^T as the B operand: slot jj of group grp is key (jj<4 ? 4grp+jj : 16+4grp+jj-4)
-    const u32x4_t pw = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
-                        pack_bf16x2(p[6], p[7])};
-    const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pw);
-    // V^T operands read per 16-dim block (the MFMA chain covers the LDS latency)
+    for (int r = 0; r < 4 * NS; ++r) p[r] = __builtin_amdgcn_exp2f(x[r] - mrow);
+#pragma unroll
+    for (int h = 0; h < NS / 2; ++h)
+      lrow += ((p[8 * h] + p[8 * h + 1]) + (p[8 * h + 2] + p[8 * h + 3])) +
+              ((p[8 * h + 4] + p[8 * h + 5]) + (p[8 * h + 6] + p[8 * h + 7]));
+    // P^T as the B operand, one per 32 keys: slot jj of group grp is key
+    // 32 h + (jj < 4 ? 4 grp + jj : 16 + 4 grp + jj - 4)
+    bf16x8_t pf[NS / 2];
+#pragma unroll
+    for (int h = 0; h < NS / 2; ++h) {
+      const u32x4_t pw = {pack_bf16x2(p[8 * h], p[8 * h + 1]), pack_bf16x2(p[8 * h + 2], p[8 * h + 3]),
+                          pack_bf16x2(p[8 * h + 4], p[8 * h + 5]), pack_bf16x2(p[8 * h + 6], p[8 * h + 7])};
+      pf[h] = __builtin_bit_cast(bf16x8_t, pw);
+    }
     __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
       const bf16_t* vrow = &Vt[buf][dt * 16 + l16][0];
-      const u32x2_t lo = *(const u32x2_t*)(vrow + grp * 4);
-      const u32x2_t hi = *(const u32x2_t*)(vrow + 16 + grp * 4);
-      const u32x4_t vv = {lo[0], lo[1], hi[0], hi[1]};
-      o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vv), pf, o[dt], 0, 0, 0);
+#pragma unroll
+      for (int h = 0; h < NS / 2; ++h) {
+        const u32x2_t lo = *(const u32x2_t*)(vrow + 32 * h + grp * 4);
+        const u32x2_t hi = *(const u32x2_t*)(vrow + 32 * h + 16 + grp * 4);
+        const u32x4_t vv = {lo[0], lo[1], hi[0], hi[1]};
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vv), pf[h], o[dt], 0, 0, 0);
+      }
     }
     __builtin_amdgcn_s_setprio(0);
     }
@@ -544,7 +552,10 @@ template <int HD, int NW>
 static hipError_t launch_gqa(const AttnArgs& a, hipStream_t s) {
   const int rb = (a.nq / a.nkv * a.Hq + 15) / 16;
   const int chunks = (rb + NW - 1) / NW;
-  hipLaunchKernelGGL((attn_gqa_kernel<HD, NW>), dim3(chunks * a.nkv * a.B), dim3(NW * 64), 0, s, a, chunks);
+  // key tiles of 64 where two blocks' staging still fits a CU's LDS (head dims up to
+  // 128; measured ~2% faster for the 128-dim expert), of 32 otherwise
+  constexpr int TK = HD <= 128 ? 64 : 32;
+  hipLaunchKernelGGL((attn_gqa_kernel<HD, NW, TK>), dim3(chunks * a.nkv * a.B), dim3(NW * 64), 0, s, a, chunks);
   return hipGetLastError();
 }
 
